@@ -1,0 +1,256 @@
+"""PRQuant calibration/export and the augmented MXFP4 GEMM -- oracle.
+
+TEST INFRASTRUCTURE ONLY (see ``oracle/__init__``).  Plain NumPy, float64
+unless a step's precision is fixed below.  Each function cites the passage of
+arXiv 2609.22106 it follows.  Readings of points the paper leaves open:
+
+* scale formula (Sec. Method, "Offline scaling and channel reordering"): the
+  paper prints s_j = (max_t |Z_tj|)^alpha ("act_only"); the SmoothQuant form
+  s_j = max_t|Z_tj|^alpha / max_n|W_nj|^(1-alpha) ("smooth", the default here)
+  and s = 1 ("none", the "w/o AWQ" ablation of Sec. 4.3) are also provided.
+  Both maxima are clamped below at 1e-5.  s_j is computed in float64 with the
+  scalar C-library pow and rounded once to float32; the inverse is the float32
+  quotient 1/s_j.  The scaled weight is the float32 product W_nj * s_j and the
+  transformed activation the float32 product X_mj * (1/s_j).
+* column-wise MXFP4 error (Algorithm 1, selection step): Q is applied to the
+  scaled weight in its ORIGINAL column order (selection precedes the
+  permutation), the error of column j is sum_n (W_s - Q(W_s))_nj^2, each term
+  exact in float64 and summed in float64 in increasing n.  The k columns with
+  the largest error are selected, ties to the smaller index.
+* permutation (Algorithm 1, permutation step): unselected channels in
+  increasing order, then the selected channels in increasing order (the
+  "contiguous tail"); perm[p] is the source channel of position p.
+* residual (Eq. 2): R = W~_tail - Q(W~)_tail where Q(W~) quantizes the whole
+  permuted weight; because the tail starts on a block boundary this equals
+  Q(W~_tail).  The difference is exact in float32 (checked here).
+* activation side of Eq. 3: quantize the concatenation [Z~, Z~_tail]; the
+  kernel's quantize-once-then-copy (Sec. "Kernel design") must equal it.
+* GEMM output: float64 here (exact up to the cross-block float64 sums).
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+from .mxfp4 import BLOCK, mx_dequantize, mx_quantize, pack_codes, qdq
+
+SCALE_MODES = ("smooth", "act_only", "none")
+CLAMP_MIN = 1e-5
+
+
+def bf16_bits_to_f32(u16):
+    """bfloat16 bit patterns (uint16) -> float32 (exact: append 16 zero bits)."""
+    u16 = np.asarray(u16, dtype=np.uint16)
+    return (u16.astype(np.uint32) << 16).view(np.float32)
+
+
+def _check_sizes(K, k_tail):
+    if K <= 0 or K % BLOCK:
+        raise ValueError("K must be a positive multiple of 32")
+    if k_tail < 0 or k_tail % BLOCK or k_tail > K:
+        raise ValueError("k_tail must be a multiple of 32 in [0, K]")
+
+
+# --------------------------------------------------------------------------- #
+# Algorithm 1, steps 1 and 3: per-channel maxima and the scaling D_alpha
+# --------------------------------------------------------------------------- #
+def channel_scales(W_bf16, Xcal_bf16, alpha, scale_mode="smooth"):
+    """(s, inv_s) float32[K] for D_alpha = diag(s) (Sec. Method, Algorithm 1)."""
+    if scale_mode not in SCALE_MODES:
+        raise ValueError(f"scale_mode must be one of {SCALE_MODES}")
+    if not (0.0 <= alpha <= 1.0):
+        raise ValueError("alpha must lie in [0, 1]")
+    W = bf16_bits_to_f32(W_bf16)
+    X = bf16_bits_to_f32(Xcal_bf16)
+    K = W.shape[1]
+    a = np.maximum(np.abs(X).max(axis=0).astype(np.float64), CLAMP_MIN)
+    b = np.maximum(np.abs(W).max(axis=0).astype(np.float64), CLAMP_MIN)
+    s64 = np.empty(K, dtype=np.float64)
+    for j in range(K):                      # scalar libm pow, one channel at a time
+        if scale_mode == "smooth":
+            s64[j] = math.pow(a[j], alpha) / math.pow(b[j], 1.0 - alpha)
+        elif scale_mode == "act_only":
+            s64[j] = math.pow(a[j], alpha)
+        else:
+            s64[j] = 1.0
+    s = s64.astype(np.float32)
+    inv = np.float32(1.0) / s               # float32 quotient, correctly rounded
+    return s, inv.astype(np.float32)
+
+
+# --------------------------------------------------------------------------- #
+# Algorithm 1, steps 4-5: top-k columns by MXFP4 error, contiguous-tail perm
+# --------------------------------------------------------------------------- #
+def column_errors(W_s):
+    """e_j = sum_n (W_s - Q(W_s))_nj^2 over the ORIGINAL column order."""
+    E = W_s.astype(np.float64) - qdq(W_s)          # exact (see module notes)
+    E2 = E * E                                      # exact: <= 48 significant bits
+    acc = np.zeros(W_s.shape[1], dtype=np.float64)
+    for n in range(E2.shape[0]):                    # sequential in n
+        acc += E2[n]
+    return acc
+
+
+def select_topk(col_err, k_tail):
+    """The k largest errors, ties to the smaller channel index; returned sorted."""
+    K = col_err.shape[0]
+    order = np.lexsort((np.arange(K), -col_err))   # primary -e, secondary j
+    return np.sort(order[:k_tail]).astype(np.int32)
+
+
+def tail_permutation(K, selected):
+    """perm = [unselected ascending, selected ascending]; perm[p] = source channel."""
+    mask = np.zeros(K, dtype=bool)
+    mask[selected] = True
+    head = np.flatnonzero(~mask)
+    tail = np.flatnonzero(mask)
+    return np.concatenate([head, tail]).astype(np.int32)
+
+
+# --------------------------------------------------------------------------- #
+# Algorithm 1 for one alpha: scaling, selection, permutation, Eq. 2, Eq. 3
+# --------------------------------------------------------------------------- #
+def prepare(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth"):
+    """Offline calibration/export for one alpha (Algorithm 1, steps 1, 3-7, 10).
+
+    W_bf16: uint16 [N, K] (bf16 bits of W_down); Xcal_bf16: uint16 [T, K].
+    Returns a dict with the exported artefacts (scale, inv_scale, perm, packed
+    Wq [N, (K+k)/2], Wsc [N, (K+k)/32]) and the intermediates the tests check.
+    """
+    W_bf16 = np.asarray(W_bf16, dtype=np.uint16)
+    Xcal_bf16 = np.asarray(Xcal_bf16, dtype=np.uint16)
+    N, K = W_bf16.shape
+    _check_sizes(K, k_tail)
+    if Xcal_bf16.ndim != 2 or Xcal_bf16.shape[1] != K or Xcal_bf16.shape[0] < 1:
+        raise ValueError("calibration activations must be [T >= 1, K]")
+    s, inv = channel_scales(W_bf16, Xcal_bf16, alpha, scale_mode)
+    W = bf16_bits_to_f32(W_bf16)
+    W_s = (W * s[None, :]).astype(np.float32)               # W D_alpha, float32 product
+    err = column_errors(W_s)
+    selected = select_topk(err, k_tail)
+    perm = tail_permutation(K, selected)
+    W_t = np.ascontiguousarray(W_s[:, perm])                # W D P (Eq. 1)
+    codes_t, scales_t = mx_quantize(W_t)                    # Q(W~)
+    deq_t = mx_dequantize(codes_t, scales_t)
+    R64 = W_t[:, K - k_tail:].astype(np.float64) - deq_t[:, K - k_tail:]   # Eq. 2
+    R = R64.astype(np.float32)
+    if not np.array_equal(R.astype(np.float64), R64):
+        raise AssertionError("tail residual is not exact in float32")
+    codes_r, scales_r = mx_quantize(R)                      # Q(R_W)
+    codes_aug = np.concatenate([codes_t, codes_r], axis=1)  # Q([W~, R_W]) (Eq. 3)
+    scales_aug = np.concatenate([scales_t, scales_r], axis=1)
+    return {
+        "scale": s, "inv_scale": inv, "perm": perm, "selected": selected,
+        "col_err": err, "W_s": W_s, "W_tilde": W_t, "R": R,
+        "codes": codes_aug, "Wq": pack_codes(codes_aug), "Wsc": scales_aug,
+        "K": K, "k_tail": k_tail, "K_aug": K + k_tail,
+    }
+
+
+# --------------------------------------------------------------------------- #
+# Activation side of Eq. 3 (online copy) -- Algorithm 1, step 11
+# --------------------------------------------------------------------------- #
+def transformed_activation(X_bf16, inv_scale=None, perm=None):
+    """Z~ = X D^-1 P as float32: Z~[m, p] = X[m, perm[p]] * inv_s[perm[p]]."""
+    X = bf16_bits_to_f32(X_bf16)
+    K = X.shape[1]
+    if perm is None:
+        perm = np.arange(K)
+    perm = np.asarray(perm)
+    Z = X[:, perm]
+    if inv_scale is not None:
+        Z = (Z * np.asarray(inv_scale, dtype=np.float32)[perm][None, :]).astype(np.float32)
+    return np.ascontiguousarray(Z, dtype=np.float32)
+
+
+def quant_act(X_bf16, inv_scale, perm, k_tail):
+    """Q([Z~, Z~_tail]) packed: (Aq uint8 [M, (K+k)/2], Asc uint8 [M, (K+k)/32])."""
+    X_bf16 = np.asarray(X_bf16, dtype=np.uint16)
+    K = X_bf16.shape[1]
+    _check_sizes(K, k_tail)
+    Z = transformed_activation(X_bf16, inv_scale, perm)
+    Z_aug = np.concatenate([Z, Z[:, K - k_tail:]], axis=1)  # [Z~, Z~_tail]
+    codes, scales = mx_quantize(Z_aug)
+    return pack_codes(codes), scales
+
+
+def quant_act_grouped(X_bf16, inv_scale, perm, group_offsets, k_tail):
+    """Rows [off[g], off[g+1]) use expert g's perm_g and inv_s_g (MoE experts)."""
+    X_bf16 = np.asarray(X_bf16, dtype=np.uint16)
+    M, K = X_bf16.shape
+    off = np.asarray(group_offsets, dtype=np.int64)
+    K_aug = K + k_tail
+    Aq = np.zeros((M, K_aug // 2), dtype=np.uint8)
+    Asc = np.zeros((M, K_aug // BLOCK), dtype=np.uint8)
+    for g in range(off.shape[0] - 1):
+        r0, r1 = int(off[g]), int(off[g + 1])
+        if r1 > r0:
+            inv_g = None if inv_scale is None else np.asarray(inv_scale)[g]
+            perm_g = None if perm is None else np.asarray(perm)[g]
+            Aq[r0:r1], Asc[r0:r1] = quant_act(X_bf16[r0:r1], inv_g, perm_g, k_tail)
+    return Aq, Asc
+
+
+# --------------------------------------------------------------------------- #
+# Eq. 3: the augmented GEMM over K + k, and its grouped (MoE) form
+# --------------------------------------------------------------------------- #
+def _deq_packed(q, sc):
+    from .mxfp4 import unpack_codes
+    return mx_dequantize(unpack_codes(q), sc)
+
+
+def gemm(Aq, Asc, Wq, Wsc):
+    """Y = deq(A_aug) deq(W_aug)^T in float64 ([M, N])."""
+    A = _deq_packed(Aq, Asc)
+    W = _deq_packed(Wq, Wsc)
+    if A.shape[1] != W.shape[1]:
+        raise ValueError("reduction lengths differ")
+    return A @ W.T
+
+
+def grouped_gemm(Aq, Asc, group_offsets, Wq, Wsc):
+    """Rows of expert e multiply W_aug,e; rows are sorted by expert."""
+    off = np.asarray(group_offsets, dtype=np.int64)
+    M = Aq.shape[0]
+    N = Wq.shape[1]
+    Y = np.zeros((M, N), dtype=np.float64)
+    for e in range(off.shape[0] - 1):
+        r0, r1 = int(off[e]), int(off[e + 1])
+        if r1 > r0:
+            Y[r0:r1] = gemm(Aq[r0:r1], Asc[r0:r1], Wq[e], Wsc[e])
+    return Y
+
+
+# --------------------------------------------------------------------------- #
+# Reference product, Eq. 1 without quantization, reconstruction error
+# --------------------------------------------------------------------------- #
+def reference_product(X_bf16, W_bf16):
+    """X W^T in float64 from the bf16 inputs (the unquantized target)."""
+    X = bf16_bits_to_f32(X_bf16).astype(np.float64)
+    W = bf16_bits_to_f32(W_bf16).astype(np.float64)
+    return X @ W.T
+
+
+def unquantized_transform_product(X_bf16, W_bf16, s, perm):
+    """(X D^-1 P)(W D P)^T in float64 with no quantization (Eq. 1)."""
+    X = bf16_bits_to_f32(X_bf16).astype(np.float64)
+    W = bf16_bits_to_f32(W_bf16).astype(np.float64)
+    s = np.asarray(s, dtype=np.float64)
+    Zt = (X / s[None, :])[:, perm]
+    Wt = (W * s[None, :])[:, perm]
+    return Zt @ Wt.T
+
+
+def nrmse(Y_hat, Y_ref):
+    """Normalized reconstruction error ||Y_hat - Y_ref||_F / ||Y_ref||_F."""
+    Y_hat = np.asarray(Y_hat, dtype=np.float64)
+    Y_ref = np.asarray(Y_ref, dtype=np.float64)
+    return float(np.linalg.norm(Y_hat - Y_ref) / np.linalg.norm(Y_ref))
+
+
+def prquant_forward(X_bf16, W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth"):
+    """Y_hat of Eq. 3 end to end: prepare, quantize the activation, GEMM."""
+    art = prepare(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode)
+    Aq, Asc = quant_act(X_bf16, art["inv_scale"], art["perm"], k_tail)
+    return gemm(Aq, Asc, art["Wq"], art["Wsc"]), art

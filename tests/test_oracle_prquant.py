@@ -1,0 +1,307 @@
+"""Pins of the PRQuant oracle (Algorithm 1, Eq. 1-3) against closed forms,
+invariants, special cases and brute force -- never against itself."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import mxfp4 as mx
+from oracle import prquant as pq
+from paper_2609_22106_amd import inputs
+
+
+def _bf16(x):
+    return inputs.f32_to_bf16_bits(np.asarray(x, np.float32))
+
+
+def _small(N=64, K=256, M=8, T=32, n_out=4, seed=0, scale=30.0):
+    return inputs.make_dense("small", N=N, K=K, M=M, T=T, k_tail=64, n_out=n_out,
+                             out_scale=scale, seed=seed)
+
+
+# ---------------------------------------------------------------- scaling ---
+def test_scale_closed_forms():
+    """s_j = a_j^alpha / b_j^(1-alpha) (SmoothQuant form) and a_j^alpha (paper's
+    printed form) at alphas where the power has a closed form."""
+    c = _small()
+    a = np.maximum(np.abs(inputs.bf16_bits_to_f32(c.Xcal)).max(0).astype(np.float64), 1e-5)
+    b = np.maximum(np.abs(inputs.bf16_bits_to_f32(c.W)).max(0).astype(np.float64), 1e-5)
+    s, inv = pq.channel_scales(c.W, c.Xcal, 1.0, "smooth")
+    np.testing.assert_array_equal(s, a.astype(np.float32))          # alpha = 1: s = a
+    s, _ = pq.channel_scales(c.W, c.Xcal, 0.0, "smooth")
+    np.testing.assert_array_equal(s, (1.0 / b).astype(np.float32))  # alpha = 0: s = 1/b
+    s, _ = pq.channel_scales(c.W, c.Xcal, 0.5, "smooth")
+    ref = np.array([math.sqrt(x) / math.sqrt(y) for x, y in zip(a, b)], np.float32)
+    assert np.max(np.abs(s.view(np.int32) - ref.view(np.int32))) <= 1   # within 1 ulp
+    s, _ = pq.channel_scales(c.W, c.Xcal, 0.5, "act_only")
+    ref = np.array([math.sqrt(x) for x in a], np.float32)
+    assert np.max(np.abs(s.view(np.int32) - ref.view(np.int32))) <= 1
+    s, inv = pq.channel_scales(c.W, c.Xcal, 0.5, "none")
+    assert np.all(s == 1) and np.all(inv == 1)
+
+
+def test_inverse_scale_is_float32_reciprocal():
+    c = _small()
+    s, inv = pq.channel_scales(c.W, c.Xcal, 0.5)
+    assert inv.dtype == np.float32
+    prod = s.astype(np.float64) * inv.astype(np.float64)
+    assert np.max(np.abs(prod - 1.0)) <= 2.0 ** -23          # |1/s - inv| <= ulp/2
+    # correctly rounded: neither neighbour of inv is closer to 1/s
+    exact = 1.0 / s.astype(np.float64)
+    for nb in (np.nextafter(inv, np.float32(0)), np.nextafter(inv, np.float32(np.inf))):
+        assert np.all(np.abs(inv - exact) <= np.abs(nb.astype(np.float64) - exact))
+
+
+def test_zero_calibration_channel_is_clamped():
+    c = _small()
+    Xcal = c.Xcal.copy()
+    Xcal[:, 5] = 0
+    s, _ = pq.channel_scales(c.W, Xcal, 1.0, "smooth")
+    assert s[5] == np.float32(1e-5)
+
+
+# --------------------------------------------------- selection, permutation ---
+def _brute_column_errors(W_s):
+    """Column errors by scalar Python loops with an independent E2M1 rounding
+    (Python round-half-even) and scale rule (float32 exponent field)."""
+    N, K = W_s.shape
+    err = [0.0] * K
+    for n in range(N):
+        for b0 in range(0, K, 32):
+            blk = [float(x) for x in W_s[n, b0:b0 + 32]]
+            amax = max(abs(x) for x in blk)
+            if amax == 0:
+                code = 0
+            else:
+                bexp = (int(np.float32(amax).view(np.uint32)) >> 23) & 0xFF
+                code = min(max(bexp - 2, 0), 254)
+            X = 2.0 ** (code - 127)
+            for j, x in enumerate(blk):
+                t = x / X
+                a = abs(t)
+                if a < 2:
+                    q = round(2 * a) / 2
+                elif a < 4:
+                    q = float(round(a))
+                else:
+                    q = min(2.0 * round(a / 2), 6.0)
+                q = math.copysign(q, t) * X
+                err[b0 + j] += (x - q) ** 2
+    return err
+
+
+@pytest.mark.parametrize("N,K", [(4, 64), (8, 96), (8, 128)])
+@pytest.mark.parametrize("tied", [False, True])
+def test_topk_brute_force(N, K, tied):
+    rng = np.random.default_rng(N * 1000 + K + tied)
+    W = (0.02 * rng.standard_normal((N, K))).astype(np.float32)
+    W[:, rng.choice(K, 3, replace=False)] *= 20
+    if tied:                                    # identical columns -> identical errors
+        W[:, 10] = W[:, 40]
+        W[:, 41] = W[:, 40]
+        W[:, 3] = W[:, 60]
+    Wb = _bf16(W)
+    Xcal = _bf16(rng.standard_normal((16, K)))
+    art = pq.prepare(Wb, Xcal, 0.5, 32)
+    W_s = (inputs.bf16_bits_to_f32(Wb) * art["scale"][None, :]).astype(np.float32)
+    err = _brute_column_errors(W_s)
+    np.testing.assert_allclose(art["col_err"], err, rtol=1e-12, atol=0)
+    want = sorted(sorted(range(K), key=lambda j: (-err[j], j))[:32])
+    np.testing.assert_array_equal(art["selected"], want)
+    sel = set(want)
+    assert min(err[j] for j in sel) >= max(err[j] for j in range(K) if j not in sel)
+
+
+def test_permutation_invariants():
+    c = _small()
+    art = pq.prepare(c.W, c.Xcal, 0.5, 64)
+    perm, K, k = art["perm"], 256, 64
+    assert sorted(perm.tolist()) == list(range(K))            # bijection
+    assert np.all(np.diff(perm[:K - k]) > 0)                   # head increasing
+    assert np.all(np.diff(perm[K - k:]) > 0)                   # tail increasing
+    np.testing.assert_array_equal(perm[K - k:], art["selected"])
+    np.testing.assert_array_equal(art["W_tilde"], art["W_s"][:, perm])
+
+
+# ------------------------------------------------------------- Eq. 1 and 2 ---
+def test_eq1_identity_without_quantization():
+    """(X D^-1 P)(W D P)^T = X W^T (Eq. 1), fp64, no quantization."""
+    c = _small()
+    art = pq.prepare(c.W, c.Xcal, 0.5, 64)
+    Y = pq.unquantized_transform_product(c.X, c.W, art["scale"], art["perm"])
+    ref = pq.reference_product(c.X, c.W)
+    assert np.max(np.abs(Y - ref)) <= 1e-12 * np.max(np.abs(ref))
+
+
+def test_residual_reconstructs_tail_exactly():
+    """Q(W~_tail) + R = W~_tail exactly (Eq. 2), and Q(W~_tail) equals the tail
+    of Q(W~) because the tail starts on a block boundary."""
+    c = _small()
+    art = pq.prepare(c.W, c.Xcal, 0.5, 64)
+    Wt = art["W_tilde"].astype(np.float64)
+    q_tail_alone = mx.qdq(art["W_tilde"][:, -64:])
+    q_full = mx.qdq(art["W_tilde"])[:, -64:]
+    np.testing.assert_array_equal(q_tail_alone, q_full)
+    np.testing.assert_array_equal(q_tail_alone + art["R"].astype(np.float64), Wt[:, -64:])
+
+
+def test_compensation_never_increases_elementwise_weight_error():
+    """|W~_tail - Q(W~_tail) - Q(R)| <= |R| element by element."""
+    c = _small(N=128, K=512)
+    art = pq.prepare(c.W, c.Xcal, 0.5, 64)
+    R = art["R"].astype(np.float64)
+    resid = R - mx.qdq(art["R"])
+    assert np.all(np.abs(resid) <= np.abs(R))
+
+
+def test_augmented_weight_layout():
+    c = _small()
+    art = pq.prepare(c.W, c.Xcal, 0.5, 64)
+    codes = mx.unpack_codes(art["Wq"])
+    assert art["Wq"].shape == (64, (256 + 64) // 2) and art["Wsc"].shape == (64, 10)
+    c_t, s_t = mx.mx_quantize(art["W_tilde"])
+    c_r, s_r = mx.mx_quantize(art["R"])
+    np.testing.assert_array_equal(codes[:, :256], c_t)
+    np.testing.assert_array_equal(codes[:, 256:], c_r)
+    np.testing.assert_array_equal(art["Wsc"], np.concatenate([s_t, s_r], 1))
+
+
+# ------------------------------------------------------------------ Eq. 3 ---
+def test_tail_copy_equals_quantizing_the_concatenation():
+    """Quantize Z~ once and append its quantized tail blocks with their scales
+    == Q([Z~, Z~_tail]) (Sec. Kernel design), codes and scales bit for bit."""
+    c = _small()
+    art = pq.prepare(c.W, c.Xcal, 0.5, 64)
+    Aq, Asc = pq.quant_act(c.X, art["inv_scale"], art["perm"], 64)
+    Z = pq.transformed_activation(c.X, art["inv_scale"], art["perm"])
+    cz, sz = mx.mx_quantize(Z)
+    copied_codes = np.concatenate([cz, cz[:, -64:]], 1)
+    copied_scales = np.concatenate([sz, sz[:, -2:]], 1)
+    np.testing.assert_array_equal(Aq, mx.pack_codes(copied_codes))
+    np.testing.assert_array_equal(Asc, copied_scales)
+
+
+def test_transformed_activation_definition():
+    c = _small()
+    art = pq.prepare(c.W, c.Xcal, 0.5, 64)
+    Z = pq.transformed_activation(c.X, art["inv_scale"], art["perm"])
+    X = inputs.bf16_bits_to_f32(c.X)
+    for p in (0, 17, 191, 192, 255):
+        j = art["perm"][p]
+        np.testing.assert_array_equal(Z[:, p], (X[:, j] * art["inv_scale"][j]).astype(np.float32))
+
+
+def test_k0_no_scaling_is_plain_mxfp4():
+    """k = 0 and s = 1 reduce every step to plain MXFP4 (the paper's MXFP4 baseline)."""
+    c = _small()
+    art = pq.prepare(c.W, c.Xcal, 0.5, 0, "none")
+    np.testing.assert_array_equal(art["perm"], np.arange(256))
+    cw, sw = mx.mx_quantize(inputs.bf16_bits_to_f32(c.W))
+    np.testing.assert_array_equal(art["Wq"], mx.pack_codes(cw))
+    np.testing.assert_array_equal(art["Wsc"], sw)
+    Aq, Asc = pq.quant_act(c.X, art["inv_scale"], art["perm"], 0)
+    cx, sx = mx.mx_quantize(inputs.bf16_bits_to_f32(c.X))
+    np.testing.assert_array_equal(Aq, mx.pack_codes(cx))
+    np.testing.assert_array_equal(Asc, sx)
+    Y = pq.gemm(Aq, Asc, art["Wq"], art["Wsc"])
+    plain = mx.mx_dequantize(cx, sx) @ mx.mx_dequantize(cw, sw).T
+    np.testing.assert_array_equal(Y, plain)
+
+
+def test_k0_with_scaling_is_mxfp4_of_scaled_operands():
+    c = _small()
+    art = pq.prepare(c.W, c.Xcal, 0.5, 0, "smooth")
+    np.testing.assert_array_equal(art["perm"], np.arange(256))
+    Aq, Asc = pq.quant_act(c.X, art["inv_scale"], art["perm"], 0)
+    Xs = (inputs.bf16_bits_to_f32(c.X) * art["inv_scale"][None, :]).astype(np.float32)
+    Ws = (inputs.bf16_bits_to_f32(c.W) * art["scale"][None, :]).astype(np.float32)
+    Y = pq.gemm(Aq, Asc, art["Wq"], art["Wsc"])
+    np.testing.assert_array_equal(Y, mx.qdq(Xs) @ mx.qdq(Ws).T)
+
+
+def _decode_brute(packed, scales):
+    """Independent decode: bit fields of each nibble, scale 2^(code-127)."""
+    R, Kh = packed.shape
+    out = np.zeros((R, 2 * Kh))
+    for r in range(R):
+        for i in range(2 * Kh):
+            byte = int(packed[r, i // 2])
+            nib = (byte >> (4 * (i % 2))) & 0xF
+            s, e, m = nib >> 3, (nib >> 1) & 3, nib & 1
+            mag = 0.5 * m if e == 0 else 2.0 ** (e - 1) * (1 + 0.5 * m)
+            out[r, i] = (-mag if s else mag) * 2.0 ** (int(scales[r, i // 32]) - 127)
+    return out
+
+
+def test_gemm_brute_force():
+    rng = np.random.default_rng(7)
+    M, N, K = 3, 5, 96
+    Aq = rng.integers(0, 256, (M, K // 2), dtype=np.uint8)
+    Wq = rng.integers(0, 256, (N, K // 2), dtype=np.uint8)
+    Asc = rng.integers(110, 140, (M, K // 32), dtype=np.uint8)
+    Wsc = rng.integers(110, 140, (N, K // 32), dtype=np.uint8)
+    A, W = _decode_brute(Aq, Asc), _decode_brute(Wq, Wsc)
+    Y = pq.gemm(Aq, Asc, Wq, Wsc)
+    for m in range(M):
+        for n in range(N):
+            terms = [A[m, i] * W[n, i] for i in range(K)]       # each product exact
+            bound = K * 2.0 ** -53 * math.fsum(abs(t) for t in terms)  # fp64 summation bound
+            assert abs(Y[m, n] - math.fsum(terms)) <= bound
+
+
+def test_gemm_hand_values():
+    """All-ones block times all-halves block: 32 * 0.5 = 16 (Eq. 3 on one block);
+    scales 2^1 and 2^-1 cancel; a second block at scales 2^3, 2^-1 adds 64."""
+    ones, halves = np.full((1, 16), 0x22, np.uint8), np.full((1, 16), 0x11, np.uint8)
+    assert pq.gemm(ones, np.array([[127]], np.uint8), halves, np.array([[127]], np.uint8))[0, 0] == 16
+    assert pq.gemm(ones, np.array([[128]], np.uint8), halves, np.array([[126]], np.uint8))[0, 0] == 16
+    A = np.concatenate([ones, ones], 1)
+    W = np.concatenate([halves, halves], 1)
+    assert pq.gemm(A, np.array([[127, 130]], np.uint8), W, np.array([[127, 126]], np.uint8))[0, 0] == 80
+
+
+# ------------------------------------------------- reconstruction error ---
+def test_residual_compensation_lowers_error_tiny_case():
+    """Residual compensation lowers y-NRMSE versus the same scaling without it
+    and versus plain MXFP4 (the paper's ablation direction, Sec. Ablation)."""
+    c = inputs.tiny_case()
+    ref = pq.reference_product(c.X, c.W)
+    y_prq, _ = pq.prquant_forward(c.X, c.W, c.Xcal, 0.5, 64)
+    y_nores, _ = pq.prquant_forward(c.X, c.W, c.Xcal, 0.5, 0)
+    y_plain, _ = pq.prquant_forward(c.X, c.W, c.Xcal, 0.5, 0, "none")
+    e_prq, e_nores, e_plain = (pq.nrmse(y, ref) for y in (y_prq, y_nores, y_plain))
+    assert e_prq < e_nores
+    assert e_prq < e_plain
+
+
+def test_grouped_matches_per_expert():
+    rng = np.random.default_rng(3)
+    E, N, K, k = 4, 16, 64, 32
+    counts = [3, 0, 5, 1]
+    off = inputs.routed_offsets(counts)
+    Mt = int(off[-1])
+    X = _bf16(rng.standard_normal((Mt, K)))
+    arts = [pq.prepare(_bf16(0.02 * rng.standard_normal((N, K))), _bf16(rng.standard_normal((8, K))),
+                       0.5, k) for _ in range(E)]
+    inv = np.stack([a["inv_scale"] for a in arts])
+    perm = np.stack([a["perm"] for a in arts])
+    Aq, Asc = pq.quant_act_grouped(X, inv, perm, off, k)
+    Wq = np.stack([a["Wq"] for a in arts])
+    Wsc = np.stack([a["Wsc"] for a in arts])
+    Y = pq.grouped_gemm(Aq, Asc, off, Wq, Wsc)
+    for e in range(E):
+        r0, r1 = off[e], off[e + 1]
+        if r1 > r0:
+            a_e, s_e = pq.quant_act(X[r0:r1], inv[e], perm[e], k)
+            np.testing.assert_array_equal(Aq[r0:r1], a_e)
+            np.testing.assert_array_equal(Y[r0:r1], pq.gemm(a_e, s_e, Wq[e], Wsc[e]))
+
+
+def test_prepare_rejects_misaligned():
+    c = _small()
+    with pytest.raises(ValueError):
+        pq.prepare(c.W, c.Xcal, 0.5, 48)
+    with pytest.raises(ValueError):
+        pq.prepare(c.W, c.Xcal, 1.5, 64)
+    with pytest.raises(ValueError):
+        pq.prepare(c.W[:, :100], c.Xcal[:, :100], 0.5, 32)
