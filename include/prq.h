@@ -1,0 +1,193 @@
+/*
+ * prq.h -- PRQuant (Permutation Residual Quantization, arXiv 2609.22106)
+ * MXFP4 + tail-residual hot path for AMD Instinct MI355X (gfx950).
+ *
+ * Plain C ABI of libprq.so.  Every array is row-major and contiguous unless a
+ * leading dimension is given; sizes are in elements unless stated.  Notation
+ * follows the paper: K (the paper's C) is the reduction dimension of the
+ * down-projection, k = k_tail is the number of "hardest" input channels moved
+ * to the contiguous tail, K_aug = K + k.  MXFP4 (the format the paper cites in
+ * Sec. 1): blocks of 32 elements along K share one E8M0 scale byte
+ * (value 2^(code-127)); elements are E2M1 nibbles (s<<3 | e<<1 | m,
+ * magnitudes 0, .5, 1, 1.5, 2, 3, 4, 6), two per byte, element 2i in bits 0-3
+ * and element 2i+1 in bits 4-7 of byte i.  Quantization rule: scale code =
+ * clamp(floor(log2(amax)) - 2 + 127, 0, 254) (0 for an all-zero block);
+ * elements divided by the scale, rounded to nearest E2M1 with ties to even
+ * code, saturating at 6; sign from the input's sign bit.
+ *
+ * Requirements common to every call: K and k_tail are multiples of 32 and
+ * 0 <= k_tail <= K.  Device pointers must be 16-byte aligned and every row
+ * start (ld_x * 2 bytes, K_aug/2 bytes) a multiple of 16 bytes, i.e.
+ * ld_x % 8 == 0 and K_aug % 32 == 0.  Device calls are asynchronous: they
+ * validate their arguments on the host, enqueue kernels on `stream` and return;
+ * they never allocate, never synchronize, and keep no mutable global state
+ * (apart from a per-device cache of the device's properties filled on first
+ * use).  They are safe to call from several host threads.  The caller owns
+ * every buffer.
+ */
+#ifndef PRQ_H
+#define PRQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PRQ_BLOCK 32
+#define PRQ_ABI_VERSION 1
+
+/* Status codes.  Negative values are errors; no kernel is enqueued when a call
+ * returns an error detected on the host. */
+enum {
+  PRQ_OK = 0,
+  PRQ_EINVAL = -1,       /* null pointer where data is needed, negative size,
+                            alpha outside [0, 1], unknown mode or variant      */
+  PRQ_EALIGN = -2,       /* K or k_tail not a multiple of 32, k_tail > K,
+                            K_aug != K + k_tail, misaligned pointer or stride  */
+  PRQ_EDEVICE = -3,      /* HIP reported an error (device query or launch)    */
+  PRQ_EUNSUPPORTED = -4, /* current device is not gfx950, or a size is beyond
+                            the limits stated below                             */
+  PRQ_EWORKSPACE = -5    /* workspace missing or smaller than required         */
+};
+
+/* Scaling rule of prq_prepare (Sec. Method, "Offline scaling"; the scaling
+ * step of Algorithm 1).  a_j = max_t |Xcal[t, j]|, b_j = max_n |W[n, j]|, both
+ * clamped below at 1e-5; s_j computed in double with the C library pow and
+ * rounded to float; inv_s_j = 1.0f / s_j in float. */
+enum {
+  PRQ_SCALE_SMOOTH = 0,   /* s_j = a_j^alpha / b_j^(1 - alpha) (default)      */
+  PRQ_SCALE_ACT_ONLY = 1, /* s_j = a_j^alpha (the form printed in the paper)  */
+  PRQ_SCALE_NONE = 2      /* s_j = 1 (no scaling: the "w/o AWQ" ablation)     */
+};
+
+/* GEMM kernel selection for the _ex calls. */
+enum {
+  PRQ_GEMM_AUTO = 0,   /* chosen from the shape                               */
+  PRQ_GEMM_TILE = 1,   /* LDS-tiled block-scaled MFMA kernel (prefill shapes) */
+  PRQ_GEMM_STREAM = 2  /* weight-streaming split-K kernel (decode shapes)     */
+};
+
+/* Human-readable text of a status code (static storage). */
+const char* prq_strerror(int status);
+
+/* PRQ_ABI_VERSION of the library. */
+int prq_abi_version(void);
+
+/*
+ * prq_prepare -- offline calibration and export for one alpha (Algorithm 1:
+ * per-channel maxima, scaling D_alpha, top-k columns of W D_alpha by MXFP4
+ * quantization error, permutation P_alpha to a contiguous tail, tail residual
+ * R_W of Eq. 2, augmented weight Q([W~, R_W]) of Eq. 3).  Host memory only,
+ * synchronous, deterministic; touches no GPU.
+ *
+ *   W_bf16     [N, K]  bf16 bit patterns of the down-projection weight
+ *   Xcal_bf16  [T, K]  bf16 calibration activations (T >= 1)
+ *   alpha      scaling strength in [0, 1]
+ *   k_tail     number of tail channels (multiple of 32, <= K)
+ *   scale_mode PRQ_SCALE_*
+ * Outputs (caller-allocated host buffers):
+ *   scale      [K] float   s_j
+ *   inv_scale  [K] float   1/s_j (the activation side multiplies by it)
+ *   perm       [K] int32   perm[p] = source channel of position p: channels
+ *                          not selected in increasing order, then the k
+ *                          selected ones in increasing order
+ *   Wq         [N, K_aug/2] uint8   packed E2M1 codes of [W~ | R_W]
+ *   Wsc        [N, K_aug/32] uint8  E8M0 scale codes
+ *   col_err    [K] double or NULL   per-channel squared MXFP4 error of
+ *                          W D_alpha (original channel order), summed in
+ *                          double over n in increasing order
+ * Selection: the k largest col_err, ties to the smaller channel index.
+ * Returns PRQ_OK, PRQ_EINVAL, PRQ_EALIGN; PRQ_EUNSUPPORTED if K > 65536.
+ */
+int prq_prepare(const uint16_t* W_bf16, int32_t N, int32_t K,
+                const uint16_t* Xcal_bf16, int32_t T,
+                double alpha, int32_t k_tail, int32_t scale_mode,
+                float* scale, float* inv_scale, int32_t* perm,
+                uint8_t* Wq, uint8_t* Wsc, double* col_err);
+
+/*
+ * prq_quant_act -- activation side of Eq. 3 with the online copy (Sec.
+ * "Activation tail construction" and "Kernel design"; Algorithm 1, step 11):
+ *   Z~[m, p] = X[m, perm[p]] * inv_scale[perm[p]]   (float32 product)
+ * quantized to MXFP4 once; the k/32 tail blocks are then written a second time,
+ * codes and scale bytes, after the K/32 main blocks, which equals quantizing
+ * [Z~, Z~[:, K-k:]].
+ *
+ *   X_bf16        device [M, ld_x] bf16 (K used columns), ld_x >= K, ld_x % 8 == 0
+ *   inv_scale     device [G, K] float, or NULL (no scaling: X is already scaled)
+ *   perm          device [G, K] int32, or NULL (identity: X is already permuted)
+ *                 values must lie in [0, K) (an entry outside it reads channel 0)
+ *   group_offsets device [G + 1] int32, or NULL when G == 1.  Rows
+ *                 [off[g], off[g+1]) use expert g's perm and inv_scale
+ *                 (MoE experts, each calibrated separately).  Offsets must be
+ *                 non-decreasing with off[0] = 0 and off[G] = M.
+ *   Aq            device [M, K_aug/2] uint8 output
+ *   Asc           device [M, K_aug/32] uint8 output
+ * Limits: K <= 16384, G <= 4096.  M == 0 is a no-op.
+ */
+int prq_quant_act(const void* X_bf16, int64_t ld_x, int32_t M, int32_t K, int32_t k_tail,
+                  const float* inv_scale, const int32_t* perm,
+                  const int32_t* group_offsets, int32_t G,
+                  uint8_t* Aq, uint8_t* Asc, hipStream_t stream);
+
+/*
+ * prq_gemm -- the augmented MXFP4 GEMM of Eq. 3, one GEMM over K_aug = K + k:
+ *   Y[m, n] = sum_b 2^(Asc[m,b]-127) 2^(Wsc[n,b]-127) sum_i e2m1(A[m,32b+i]) e2m1(W[n,32b+i])
+ * accumulated in float32 (block-scaled MFMA), Y float32 [M, N] (ld = N).
+ *
+ *   Aq [M, K_aug/2], Asc [M, K_aug/32]: from prq_quant_act
+ *   Wq [N, K_aug/2], Wsc [N, K_aug/32]: from prq_prepare
+ *   workspace: device buffer of at least prq_gemm_workspace_bytes(M, N, K_aug)
+ *   bytes (may be NULL when that is 0): split-K partial sums and one arrival
+ *   counter per 16-feature output tile.  It must be zero-filled once before its
+ *   first use; every call returns the counters to zero (the partial-sum area
+ *   keeps stale data, which is never read before being rewritten).  Calls
+ *   that share one workspace must be ordered (same stream).
+ * Limits: N % 16 == 0, K_aug <= 65536.  M == 0 is a no-op.
+ */
+size_t prq_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K_aug);
+int prq_gemm(const uint8_t* Aq, const uint8_t* Asc, int32_t M,
+             const uint8_t* Wq, const uint8_t* Wsc, int32_t N, int32_t K_aug,
+             float* Y, void* workspace, size_t workspace_bytes, hipStream_t stream);
+/* As prq_gemm with an explicit kernel (PRQ_GEMM_*) and, for PRQ_GEMM_STREAM,
+ * an explicit split count along K_aug (0 = chosen from the shape). */
+size_t prq_gemm_workspace_bytes_ex(int32_t M, int32_t N, int32_t K_aug, int32_t variant,
+                                   int32_t splits);
+int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M,
+                const uint8_t* Wq, const uint8_t* Wsc, int32_t N, int32_t K_aug,
+                float* Y, void* workspace, size_t workspace_bytes,
+                int32_t variant, int32_t splits, hipStream_t stream);
+
+/*
+ * prq_grouped_gemm -- Eq. 3 for E MoE experts in one launch (the paper applies
+ * PRQuant to every expert down-projection).  Rows are sorted by expert; rows
+ * [off[e], off[e+1]) multiply expert e's augmented weight.
+ *
+ *   Aq [M_total, K_aug/2], Asc [M_total, K_aug/32]
+ *   group_offsets device [E + 1] int32 (non-decreasing, off[0] = 0,
+ *                 off[E] = M_total); read on the device only, never copied
+ *                 to the host
+ *   Wq [E, N, K_aug/2], Wsc [E, N, K_aug/32] (experts contiguous)
+ *   Y  [M_total, N] float32
+ *   workspace: as for prq_gemm, sized by prq_grouped_gemm_workspace_bytes.
+ * Limits: N % 16 == 0, K_aug <= 65536, E <= 4096.
+ */
+size_t prq_grouped_gemm_workspace_bytes(int32_t M_total, int32_t E, int32_t N, int32_t K_aug);
+int prq_grouped_gemm(const uint8_t* Aq, const uint8_t* Asc,
+                     const int32_t* group_offsets, int32_t E, int32_t M_total,
+                     const uint8_t* Wq, const uint8_t* Wsc, int32_t N, int32_t K_aug,
+                     float* Y, void* workspace, size_t workspace_bytes, hipStream_t stream);
+int prq_grouped_gemm_ex(const uint8_t* Aq, const uint8_t* Asc,
+                        const int32_t* group_offsets, int32_t E, int32_t M_total,
+                        const uint8_t* Wq, const uint8_t* Wsc, int32_t N, int32_t K_aug,
+                        float* Y, void* workspace, size_t workspace_bytes,
+                        int32_t variant, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PRQ_H */

@@ -1,0 +1,80 @@
+// Test-only probes of gfx950 instruction semantics (libprq_probe.so; not part
+// of libprq.so).  Every kernel is in bounds by construction: one wave for the
+// MFMA probe, a fixed 2^32-pattern sweep with no memory traffic except an
+// atomic mismatch counter for the conversion probe.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "mx_device.hpp"
+
+namespace {
+
+using prq::dev::v4f;
+
+// One wave: lane l passes a[l] (16 bytes of FP4), b[l], sa[l], sb[l] to a single
+// block-scaled 16x16x128 FP4 MFMA and writes its 4 accumulator values.
+__global__ __launch_bounds__(64) void mfma16_probe(const uint4* a, const uint4* b,
+                                                   const uint32_t* sa, const uint32_t* sb,
+                                                   float* out) {
+  const int l = threadIdx.x;
+  v4f c = {0.f, 0.f, 0.f, 0.f};
+  c = prq::dev::mfma_fp4_16x16x128(a[l], b[l], sa[l], sb[l], c);
+  for (int q = 0; q < 4; ++q) out[l * 4 + q] = c[q];
+}
+
+// Exhaustive comparison of the hardware FP32 -> FP4 conversion (scale 1.0)
+// with the software rounding rule of mx_device.hpp over every finite float32
+// bit pattern.  result[0] counts mismatches, result[1..2*kRec] records the
+// first bit patterns and hardware bytes.
+constexpr int kRec = 8;
+
+__global__ __launch_bounds__(256) void cvt_sweep(uint32_t* result) {
+  const uint64_t t = static_cast<uint64_t>(blockIdx.x) * 256 + threadIdx.x;
+  for (uint32_t i = 0; i < 256; ++i) {
+    const uint32_t bits = static_cast<uint32_t>(t * 256 + i);
+    if (((bits >> 23) & 0xFFu) == 0xFFu) continue;  // Inf / NaN
+    const float x = __uint_as_float(bits);
+    const uint32_t hw = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, x, -x, 1.0f, 0) & 0xFFu;
+    const uint32_t sw = prq::dev::e2m1_code(x, x) | (prq::dev::e2m1_code(-x, -x) << 4);
+    if (hw != sw) {
+      const uint32_t k = atomicAdd(&result[0], 1u);
+      if (k < kRec) {
+        result[1 + 2 * k] = bits;
+        result[2 + 2 * k] = hw;
+      }
+    }
+  }
+}
+
+// Convert (x[i], y[i]) with scale s[i] into byte i (x in the low nibble slot).
+__global__ void cvt_pairs(const float* x, const float* y, const float* s, int n, uint8_t* out) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) out[i] = static_cast<uint8_t>(__builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, x[i], y[i], s[i], 0) & 0xFFu);
+}
+
+}  // namespace
+
+extern "C" {
+
+int prq_probe_mfma16(const void* a, const void* b, const uint32_t* sa, const uint32_t* sb,
+                     float* out, hipStream_t stream) {
+  mfma16_probe<<<1, 64, 0, stream>>>(static_cast<const uint4*>(a), static_cast<const uint4*>(b), sa,
+                                     sb, out);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+// result: device uint32[1 + 2*8], zero-filled by the caller.
+int prq_probe_cvt_sweep(uint32_t* result, hipStream_t stream) {
+  cvt_sweep<<<65536, 256, 0, stream>>>(result);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+int prq_probe_cvt_pairs(const float* x, const float* y, const float* s, int n, uint8_t* out,
+                        hipStream_t stream) {
+  if (n <= 0) return 0;
+  cvt_pairs<<<(n + 255) / 256, 256, 0, stream>>>(x, y, s, n, out);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+}  // extern "C"

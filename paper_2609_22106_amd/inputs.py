@@ -178,3 +178,12 @@ def routed_offsets(counts):
     off = np.zeros(len(counts) + 1, dtype=np.int32)
     off[1:] = np.cumsum(counts)
     return off
+
+
+def random_mxfp4(rng, shape_rows, K_aug, scale_lo=118, scale_hi=136):
+    """Random packed MXFP4 operand: uniform code bytes and E8M0 scale bytes in
+    [scale_lo, scale_hi] (any such pair is a valid GEMM input)."""
+    rows = tuple(np.atleast_1d(shape_rows).tolist())
+    q = rng.integers(0, 256, rows + (K_aug // 2,), dtype=np.uint8)
+    s = rng.integers(scale_lo, scale_hi + 1, rows + (K_aug // 32,), dtype=np.uint8)
+    return q, s

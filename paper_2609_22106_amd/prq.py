@@ -1,0 +1,181 @@
+"""ctypes binding of libprq.so (include/prq.h) -- argument marshalling only.
+
+Every step of the hot path runs in the library: ``prq_prepare`` in its native
+host code, ``prq_quant_act`` / ``prq_gemm`` / ``prq_grouped_gemm`` in its HIP
+kernels.  torch supplies device memory (``data_ptr()``) and the stream
+(``torch.cuda.current_stream().cuda_stream``); torch is imported before the
+library is loaded so both use one HIP runtime instance.  There is no fallback:
+a missing library raises ``ImportError`` at import time.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import torch  # noqa: F401  (loads the HIP runtime the library binds to)
+
+from . import build as _build
+
+PRQ_OK, PRQ_EINVAL, PRQ_EALIGN, PRQ_EDEVICE, PRQ_EUNSUPPORTED, PRQ_EWORKSPACE = 0, -1, -2, -3, -4, -5
+SCALE_MODES = {"smooth": 0, "act_only": 1, "none": 2}
+GEMM_AUTO, GEMM_TILE, GEMM_STREAM = 0, 1, 2
+HEADER = os.path.join(_build.INCLUDE, "prq.h")
+
+if not os.path.exists(_build.LIB):
+    raise ImportError(f"{_build.LIB} is not built; run `python -m paper_2609_22106_amd.build`")
+_lib = ctypes.CDLL(_build.LIB)
+
+_p = ctypes.c_void_p
+_i32 = ctypes.c_int32
+_i64 = ctypes.c_int64
+_sz = ctypes.c_size_t
+
+
+def _decl(name, restype, argtypes):
+    fn = getattr(_lib, name)
+    fn.restype = restype
+    fn.argtypes = argtypes
+    return fn
+
+
+_strerror = _decl("prq_strerror", ctypes.c_char_p, [ctypes.c_int])
+_abi_version = _decl("prq_abi_version", ctypes.c_int, [])
+_prepare = _decl("prq_prepare", ctypes.c_int,
+                 [_p, _i32, _i32, _p, _i32, ctypes.c_double, _i32, _i32, _p, _p, _p, _p, _p, _p])
+_quant_act = _decl("prq_quant_act", ctypes.c_int,
+                   [_p, _i64, _i32, _i32, _i32, _p, _p, _p, _i32, _p, _p, _p])
+_gemm_ws = _decl("prq_gemm_workspace_bytes", _sz, [_i32, _i32, _i32])
+_gemm_ws_ex = _decl("prq_gemm_workspace_bytes_ex", _sz, [_i32, _i32, _i32, _i32, _i32])
+_gemm = _decl("prq_gemm", ctypes.c_int, [_p, _p, _i32, _p, _p, _i32, _i32, _p, _p, _sz, _p])
+_gemm_ex = _decl("prq_gemm_ex", ctypes.c_int,
+                 [_p, _p, _i32, _p, _p, _i32, _i32, _p, _p, _sz, _i32, _i32, _p])
+_ggemm_ws = _decl("prq_grouped_gemm_workspace_bytes", _sz, [_i32, _i32, _i32, _i32])
+_ggemm = _decl("prq_grouped_gemm", ctypes.c_int,
+               [_p, _p, _p, _i32, _i32, _p, _p, _i32, _i32, _p, _p, _sz, _p])
+_ggemm_ex = _decl("prq_grouped_gemm_ex", ctypes.c_int,
+                  [_p, _p, _p, _i32, _i32, _p, _p, _i32, _i32, _p, _p, _sz, _i32, _p])
+
+
+class PRQError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__(f"{where}: {prq_strerror(status)} (status {status})")
+
+
+def _check(status, where):
+    if status != PRQ_OK:
+        raise PRQError(status, where)
+
+
+def prq_strerror(status):
+    return _strerror(int(status)).decode()
+
+
+def prq_abi_version():
+    return int(_abi_version())
+
+
+def exported_symbols():
+    """Names of the functions include/prq.h declares."""
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(prq_\w+)\s*\(", text)))
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, np.ndarray):
+        return t.ctypes.data
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+# --------------------------------------------------------------- prepare ---
+def prq_prepare(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth", with_col_err=False):
+    """Offline calibration/export (host).  W_bf16 [N, K] and Xcal_bf16 [T, K]
+    are uint16 numpy arrays of bf16 bit patterns.  Returns numpy arrays."""
+    W = np.ascontiguousarray(W_bf16, dtype=np.uint16)
+    X = np.ascontiguousarray(Xcal_bf16, dtype=np.uint16)
+    N, K = W.shape
+    T = X.shape[0]
+    if X.shape[1] != K:
+        raise ValueError("calibration activations must have K columns")
+    K_aug = K + int(k_tail)
+    out = {
+        "scale": np.empty(K, np.float32), "inv_scale": np.empty(K, np.float32),
+        "perm": np.empty(K, np.int32),
+        "Wq": np.empty((N, max(K_aug, 0) // 2), np.uint8),
+        "Wsc": np.empty((N, max(K_aug, 0) // 32), np.uint8),
+    }
+    col_err = np.empty(K, np.float64) if with_col_err else None
+    st = _prepare(_ptr(W), N, K, _ptr(X), T, float(alpha), int(k_tail), SCALE_MODES[scale_mode],
+                  _ptr(out["scale"]), _ptr(out["inv_scale"]), _ptr(out["perm"]), _ptr(out["Wq"]),
+                  _ptr(out["Wsc"]), _ptr(col_err))
+    _check(st, "prq_prepare")
+    if with_col_err:
+        out["col_err"] = col_err
+    return out
+
+
+# ------------------------------------------------------------- device ops ---
+def prq_quant_act(X, K, k_tail, inv_scale=None, perm=None, group_offsets=None, G=1,
+                  Aq=None, Asc=None, stream=None):
+    """Quantize bf16 activations X [M, ld] (device) -> (Aq [M, K_aug/2], Asc [M, K_aug/32])."""
+    M = X.shape[0]
+    K_aug = K + k_tail
+    if Aq is None:
+        Aq = torch.empty((M, K_aug // 2), dtype=torch.uint8, device=X.device)
+    if Asc is None:
+        Asc = torch.empty((M, K_aug // 32), dtype=torch.uint8, device=X.device)
+    ld = X.stride(0) if X.dim() == 2 else K
+    st = _quant_act(_ptr(X), ld, M, K, k_tail, _ptr(inv_scale), _ptr(perm), _ptr(group_offsets), G,
+                    _ptr(Aq), _ptr(Asc), _stream(stream))
+    _check(st, "prq_quant_act")
+    return Aq, Asc
+
+
+def prq_gemm_workspace_bytes(M, N, K_aug, variant=GEMM_AUTO, splits=0):
+    return int(_gemm_ws_ex(M, N, K_aug, variant, splits))
+
+
+def prq_gemm(Aq, Asc, Wq, Wsc, Y=None, workspace=None, variant=GEMM_AUTO, splits=0, stream=None):
+    """Y [M, N] float32 = deq(A_aug) deq(W_aug)^T over K_aug (device)."""
+    M = Aq.shape[0]
+    N = Wq.shape[0]
+    K_aug = Wq.shape[1] * 2
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float32, device=Wq.device)
+    need = prq_gemm_workspace_bytes(M, N, K_aug, variant, splits)
+    if workspace is None and need:
+        workspace = torch.zeros(need, dtype=torch.uint8, device=Wq.device)
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    st = _gemm_ex(_ptr(Aq), _ptr(Asc), M, _ptr(Wq), _ptr(Wsc), N, K_aug, _ptr(Y), _ptr(workspace),
+                  ws_bytes, variant, splits, _stream(stream))
+    _check(st, "prq_gemm")
+    return Y
+
+
+def prq_grouped_gemm_workspace_bytes(M_total, E, N, K_aug):
+    return int(_ggemm_ws(M_total, E, N, K_aug))
+
+
+def prq_grouped_gemm(Aq, Asc, group_offsets, Wq, Wsc, Y=None, workspace=None, variant=GEMM_AUTO,
+                     stream=None):
+    """Rows sorted by expert; Wq [E, N, K_aug/2]; Y [M_total, N] float32 (device)."""
+    M = Aq.shape[0]
+    E, N = Wq.shape[0], Wq.shape[1]
+    K_aug = Wq.shape[2] * 2
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float32, device=Wq.device)
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    st = _ggemm_ex(_ptr(Aq), _ptr(Asc), _ptr(group_offsets), E, M, _ptr(Wq), _ptr(Wsc), N, K_aug,
+                   _ptr(Y), _ptr(workspace), ws_bytes, variant, _stream(stream))
+    _check(st, "prq_grouped_gemm")
+    return Y

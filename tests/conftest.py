@@ -27,3 +27,13 @@ def pytest_collection_modifyitems(config, items):
     for item in items:
         if "gpu" in item.keywords:
             item.add_marker(skip)
+
+
+@pytest.fixture(scope="session")
+def c1_art():
+    """The 9728 -> 2560 down_proj workload (64 decode rows) and its oracle export
+    (about 20 s of CPU, computed once per session)."""
+    from oracle import prquant as pq
+    from paper_2609_22106_amd import inputs
+    c = inputs.down_proj_decode()
+    return c, pq.prepare(c.W, c.Xcal, 0.5, 256)

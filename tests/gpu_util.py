@@ -1,0 +1,40 @@
+"""Helpers shared by the GPU tests: host<->device copies and the tolerance
+of the GEMM parity checks."""
+import sys
+
+import numpy as np
+import torch
+
+# GEMM bar: float32 accumulation on the GPU against the float64 oracle,
+# max |dY| <= 1e-3 * max |Y_oracle|.
+GEMM_RTOL_OF_MAX = 1e-3
+
+
+def dev(a):
+    """numpy -> device tensor with the same bytes (uint16 travels as int16)."""
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    elif a.dtype == np.uint32:
+        a = a.view(np.int32)
+    return torch.from_numpy(a).cuda()
+
+
+def host(t, dtype=None):
+    a = t.detach().cpu().numpy()
+    return a.view(dtype) if dtype is not None else a
+
+
+def say(*msg):
+    print(*msg, file=sys.stderr, flush=True)
+
+
+def assert_gemm_close(Y_gpu, Y_ref, what=""):
+    Y_gpu = np.asarray(Y_gpu, dtype=np.float64)
+    Y_ref = np.asarray(Y_ref, dtype=np.float64)
+    assert Y_gpu.shape == Y_ref.shape, (Y_gpu.shape, Y_ref.shape)
+    assert np.all(np.isfinite(Y_gpu)), what
+    scale = np.max(np.abs(Y_ref)) if Y_ref.size else 0.0
+    err = np.max(np.abs(Y_gpu - Y_ref)) if Y_ref.size else 0.0
+    assert err <= GEMM_RTOL_OF_MAX * scale, f"{what}: max|dY| = {err:.3e}, max|Y| = {scale:.3e}"
+    return err / scale if scale else 0.0

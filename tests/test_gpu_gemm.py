@@ -1,0 +1,187 @@
+"""prq_gemm / prq_grouped_gemm (Eq. 3 over K + k) against the oracle's float64
+GEMM: max |dY| <= 1e-3 max |Y|.  Both kernels (LDS-tiled and weight-streaming
+split-K), ragged M, N and K_aug, the full decode/prefill down_proj shapes and
+the grouped expert shapes."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import prquant as pq                               # noqa: E402
+from paper_2609_22106_amd import inputs                        # noqa: E402
+from tests.gpu_util import assert_gemm_close, dev, host, say   # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+def _prq():
+    from paper_2609_22106_amd import prq
+    return prq
+
+
+def _gpu_gemm(Aq, Asc, Wq, Wsc, variant, splits=0, workspace=None):
+    prq = _prq()
+    Y = prq.prq_gemm(dev(Aq), dev(Asc), dev(Wq), dev(Wsc), variant=variant, splits=splits,
+                     workspace=workspace)
+    torch.cuda.synchronize()
+    return host(Y)
+
+
+SHAPES = [(1, 16, 32), (5, 48, 96), (16, 512, 1088), (100, 272, 1088), (64, 2560, 9984),
+          (200, 256, 2624), (130, 144, 4192), (257, 128, 832), (33, 2048, 832)]
+
+
+@pytest.mark.parametrize("M,N,K_aug", SHAPES)
+@pytest.mark.parametrize("variant", ["tile", "stream"])
+def test_random_operands(M, N, K_aug, variant):
+    prq = _prq()
+    rng = np.random.default_rng(M * 7 + N + K_aug)
+    Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+    Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
+    v = prq.GEMM_TILE if variant == "tile" else prq.GEMM_STREAM
+    say("gemm case:", variant, M, N, K_aug)
+    assert_gemm_close(_gpu_gemm(Aq, Asc, Wq, Wsc, v), pq.gemm(Aq, Asc, Wq, Wsc),
+                      f"{variant} {M}x{N}x{K_aug}")
+
+
+@pytest.mark.parametrize("splits", [1, 2, 3, 7, 19])
+def test_stream_split_counts(splits):
+    prq = _prq()
+    rng = np.random.default_rng(splits)
+    M, N, K_aug = 24, 320, 9984
+    Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+    Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
+    say("gemm case: stream splits", splits)
+    Y = _gpu_gemm(Aq, Asc, Wq, Wsc, prq.GEMM_STREAM, splits)
+    assert_gemm_close(Y, pq.gemm(Aq, Asc, Wq, Wsc), f"splits={splits}")
+
+
+def test_split_k_is_deterministic_and_resets_its_counters():
+    prq = _prq()
+    rng = np.random.default_rng(3)
+    M, N, K_aug = 64, 2560, 9984
+    Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+    Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
+    need = prq.prq_gemm_workspace_bytes(M, N, K_aug, prq.GEMM_STREAM, 4)
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+    ys = [_gpu_gemm(Aq, Asc, Wq, Wsc, prq.GEMM_STREAM, 4, ws) for _ in range(3)]
+    np.testing.assert_array_equal(ys[0].view(np.uint32), ys[1].view(np.uint32))
+    np.testing.assert_array_equal(ys[0].view(np.uint32), ys[2].view(np.uint32))
+    assert_gemm_close(ys[0], pq.gemm(Aq, Asc, Wq, Wsc), "split 4")
+
+
+def test_hand_values():
+    """All-ones A block x all-halves W block = 16 (one block); a second block at
+    scales (130, 126) adds 64 (Eq. 3 by hand)."""
+    prq = _prq()
+    A = np.full((1, 32), 0x22, np.uint8)
+    W = np.full((16, 32), 0x11, np.uint8)
+    Asc = np.array([[127, 130]], np.uint8)
+    Wsc = np.tile(np.array([[127, 126]], np.uint8), (16, 1))
+    for v in (prq.GEMM_TILE, prq.GEMM_STREAM):
+        Y = _gpu_gemm(A, Asc, W, Wsc, v)
+        np.testing.assert_array_equal(Y, np.full((1, 16), 80.0, np.float32))
+
+
+@pytest.mark.parametrize("M", [1, 8, 32, 64])
+def test_down_proj_decode_end_to_end(c1_art, M):
+    """9728 -> 2560, k = 256: oracle export, GPU act-quant + GEMM (auto kernel)
+    against the oracle's Eq. 3."""
+    prq = _prq()
+    c, art = c1_art
+    X = c.X[:M]
+    say("gemm case: down_proj decode M =", M)
+    Aq, Asc = prq.prq_quant_act(dev(X), 9728, 256, dev(art["inv_scale"]), dev(art["perm"]))
+    Y = prq.prq_gemm(Aq, Asc, dev(art["Wq"]), dev(art["Wsc"]))
+    torch.cuda.synchronize()
+    rq, rs = pq.quant_act(X, art["inv_scale"], art["perm"], 256)
+    assert_gemm_close(host(Y), pq.gemm(rq, rs, art["Wq"], art["Wsc"]), f"decode M={M}")
+
+
+@pytest.mark.parametrize("M", [512, 2048, 8192])
+def test_down_proj_prefill_sampled_rows(c1_art, M):
+    prq = _prq()
+    _, art = c1_art
+    c = inputs.down_proj_prefill()
+    X = c.X[:M]
+    say("gemm case: down_proj prefill M =", M)
+    Aq, Asc = prq.prq_quant_act(dev(X), 9728, 256, dev(art["inv_scale"]), dev(art["perm"]))
+    Y = host(prq.prq_gemm(Aq, Asc, dev(art["Wq"]), dev(art["Wsc"])))
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([np.random.default_rng(M).choice(M, 48, replace=False),
+                                     [0, M - 1]]))
+    rq, rs = pq.quant_act(X[rows], art["inv_scale"], art["perm"], 256)
+    assert_gemm_close(Y[rows], pq.gemm(rq, rs, art["Wq"], art["Wsc"]), f"prefill M={M}")
+
+
+# ------------------------------------------------------------- grouped ---
+def _grouped_case(counts, N, K_aug, seed):
+    rng = np.random.default_rng(seed)
+    off = inputs.routed_offsets(counts)
+    Aq, Asc = inputs.random_mxfp4(rng, int(off[-1]), K_aug)
+    Wq, Wsc = inputs.random_mxfp4(rng, (len(counts), N), K_aug)
+    return off, Aq, Asc, Wq, Wsc
+
+
+def _gpu_grouped(off, Aq, Asc, Wq, Wsc, variant):
+    prq = _prq()
+    Y = prq.prq_grouped_gemm(dev(Aq), dev(Asc), dev(off), dev(Wq), dev(Wsc), variant=variant)
+    torch.cuda.synchronize()
+    return host(Y)
+
+
+GROUPED = [([3, 0, 17, 1, 0], 48, 1088), ([0, 0, 40], 32, 832), ([1], 16, 64),
+           ([200, 3, 0, 65], 144, 832), ([0, 130, 0, 0, 7, 300], 256, 2624)]
+
+
+@pytest.mark.parametrize("counts,N,K_aug", GROUPED)
+@pytest.mark.parametrize("variant", ["tile", "stream"])
+def test_grouped_random(counts, N, K_aug, variant):
+    prq = _prq()
+    off, Aq, Asc, Wq, Wsc = _grouped_case(counts, N, K_aug, sum(counts) + N)
+    v = prq.GEMM_TILE if variant == "tile" else prq.GEMM_STREAM
+    say("grouped case:", variant, counts, N, K_aug)
+    Y = _gpu_grouped(off, Aq, Asc, Wq, Wsc, v)
+    assert_gemm_close(Y, pq.grouped_gemm(Aq, Asc, off, Wq, Wsc), f"grouped {variant} {counts}")
+
+
+@pytest.mark.parametrize("tokens", [64, 4096])
+def test_grouped_expert_shapes(tokens):
+    """128 experts of 2048 x 832 (768 + 64), rows routed top-8; all rows checked
+    at 512 routed rows, four experts' rows at 32768 routed rows."""
+    prq = _prq()
+    rng = np.random.default_rng(tokens)
+    E, N, K_aug = 128, 2048, 832
+    experts = np.stack([rng.choice(E, 8, replace=False) for _ in range(tokens)])
+    off = inputs.routed_offsets(np.bincount(experts.ravel(), minlength=E))
+    Aq, Asc = inputs.random_mxfp4(rng, int(off[-1]), K_aug)
+    Wq, Wsc = inputs.random_mxfp4(rng, (E, N), K_aug)
+    say("grouped case: experts", tokens, "tokens")
+    Y = _gpu_grouped(off, Aq, Asc, Wq, Wsc, prq.GEMM_AUTO)
+    if tokens <= 64:
+        assert_gemm_close(Y, pq.grouped_gemm(Aq, Asc, off, Wq, Wsc), "experts decode")
+    else:
+        for e in (0, 17, 64, 127):
+            r0, r1 = int(off[e]), int(off[e + 1])
+            assert_gemm_close(Y[r0:r1], pq.gemm(Aq[r0:r1], Asc[r0:r1], Wq[e], Wsc[e]), f"expert {e}")
+
+
+def test_grouped_end_to_end_prepared_experts():
+    """Eight experts of the 768 -> 2048 shape exported by the oracle, GPU grouped
+    act-quant + grouped GEMM against the oracle."""
+    prq = _prq()
+    c = inputs.make_moe("m", E=8, N=2048, K=768, tokens=40, topk=3, T=256, k_tail=64, seed=4)
+    arts = [pq.prepare(c.W[e], c.Xcal[e], 0.5, 64) for e in range(8)]
+    inv = np.stack([a["inv_scale"] for a in arts])
+    perm = np.stack([a["perm"] for a in arts])
+    Wq = np.stack([a["Wq"] for a in arts])
+    Wsc = np.stack([a["Wsc"] for a in arts])
+    off = c.group_offsets
+    say("grouped case: end to end, counts", np.diff(off).tolist())
+    Aq, Asc = prq.prq_quant_act(dev(c.X), 768, 64, dev(inv), dev(perm), dev(off), 8)
+    for v in (prq.GEMM_TILE, prq.GEMM_STREAM):
+        Y = prq.prq_grouped_gemm(Aq, Asc, dev(off), dev(Wq), dev(Wsc), variant=v)
+        torch.cuda.synchronize()
+        rq, rs = pq.quant_act_grouped(c.X, inv, perm, off, 64)
+        np.testing.assert_array_equal(host(Aq), rq)
+        assert_gemm_close(host(Y), pq.grouped_gemm(rq, rs, off, Wq, Wsc), f"e2e variant {v}")

@@ -1,0 +1,93 @@
+"""Single-instruction checks of the gfx950 semantics the kernels rely on:
+the operand/scale/output lane layout of the block-scaled FP4 MFMA, and the
+hardware FP32->FP4 conversion against the E2M1 rounding rule (all finite
+float32 inputs).  In-bounds by construction (one wave; a fixed sweep)."""
+import ctypes
+import itertools
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+
+def _probe_lib():
+    from paper_2609_22106_amd import build, prq  # noqa: F401  (prq loads torch first)
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    lib.prq_probe_mfma16.argtypes = [ctypes.c_void_p] * 6
+    lib.prq_probe_cvt_sweep.argtypes = [ctypes.c_void_p] * 2
+    lib.prq_probe_cvt_pairs.argtypes = [ctypes.c_void_p] * 3 + [ctypes.c_int] + [ctypes.c_void_p] * 2
+    return lib
+
+
+E2M1 = np.array([0, .5, 1, 1.5, 2, 3, 4, 6, -0., -.5, -1, -1.5, -2, -3, -4, -6])
+
+
+def _nibbles(lane_bytes, high_first):
+    lo, hi = lane_bytes & 15, lane_bytes >> 4
+    pair = (hi, lo) if high_first else (lo, hi)
+    return np.stack(pair, axis=-1).reshape(lane_bytes.shape[0], 32)
+
+
+def _operand(lane_bytes, lane_scales, layout, high_first):
+    """16 x 128 matrix of values under a lane-layout hypothesis."""
+    mat = np.zeros((16, 128))
+    vals = E2M1[_nibbles(lane_bytes, high_first)]
+    for l in range(64):
+        r, g = l % 16, l // 16
+        if layout == "contiguous32":
+            ks = np.arange(32 * g, 32 * g + 32)
+        else:  # two 16-element halves, 64 apart
+            ks = np.concatenate([np.arange(16 * g, 16 * g + 16), np.arange(64 + 16 * g, 80 + 16 * g)])
+        mat[r, ks] = vals[l] * 2.0 ** (int(lane_scales[l]) - 127)
+    return mat
+
+
+def test_block_scaled_fp4_mfma_layout():
+    lib = _probe_lib()
+    rng = np.random.default_rng(0)
+    a = rng.integers(0, 256, (64, 16), dtype=np.uint8)
+    b = rng.integers(0, 256, (64, 16), dtype=np.uint8)
+    sa = rng.integers(124, 131, 64).astype(np.uint32)
+    sb = rng.integers(124, 131, 64).astype(np.uint32)
+    dev = [torch.from_numpy(x.copy()).cuda() for x in (a, b, sa.view(np.int32), sb.view(np.int32))]
+    out = torch.zeros(64 * 4, dtype=torch.float32, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+    assert lib.prq_probe_mfma16(*[t.data_ptr() for t in dev], out.data_ptr(), s) == 0
+    got = out.cpu().numpy().reshape(64, 4).astype(np.float64)
+    matches = []
+    for layout, high_first, transposed in itertools.product(("contiguous32", "split16"), (False, True),
+                                                            (False, True)):
+        A = _operand(a, sa, layout, high_first)
+        B = _operand(b, sb, layout, high_first)
+        C = A @ B.T
+        pred = np.zeros((64, 4))
+        for l in range(64):
+            for q in range(4):
+                i, j = 4 * (l // 16) + q, l % 16
+                pred[l, q] = C[j, i] if transposed else C[i, j]
+        if np.allclose(pred, got, rtol=1e-6, atol=1e-6 * np.abs(C).max()):
+            matches.append((layout, high_first, transposed))
+    print("matching layouts:", matches, flush=True)
+    assert ("contiguous32", False, False) in matches, f"layout differs; matches={matches}\n{got[:4]}"
+
+
+def test_hw_fp4_convert_matches_rounding_rule():
+    lib = _probe_lib()
+    res = torch.zeros(17, dtype=torch.int32, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+    assert lib.prq_probe_cvt_sweep(res.data_ptr(), s) == 0
+    r = res.cpu().numpy().view(np.uint32)
+    first = [(hex(r[1 + 2 * k]), hex(r[2 + 2 * k])) for k in range(min(8, int(r[0])))]
+    print("cvt mismatches:", int(r[0]), first, flush=True)
+    # scale-operand semantics, reported for the record
+    x = torch.tensor([3.0, 3.0, 0.75, 5.0], device="cuda")
+    y = torch.tensor([1.0, 1.0, -0.1, 6.5], device="cuda")
+    sc = torch.tensor([1.0, 2.0, 1.0, 1.0], device="cuda")
+    o = torch.zeros(4, dtype=torch.uint8, device="cuda")
+    assert lib.prq_probe_cvt_pairs(x.data_ptr(), y.data_ptr(), sc.data_ptr(), 4, o.data_ptr(), s) == 0
+    print("cvt pairs (x=3,y=1,s=1), (x=3,y=1,s=2), (.75,-.1), (5,6.5):",
+          [hex(v) for v in o.cpu().numpy()], flush=True)
+    assert int(r[0]) == 0
