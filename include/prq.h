@@ -134,30 +134,51 @@ int prq_quant_act(const void* X_bf16, int64_t ld_x, int32_t M, int32_t K, int32_
                   uint8_t* Aq, uint8_t* Asc, hipStream_t stream);
 
 /*
+ * prq_packed_weight_bytes / prq_pack_weight -- the weight layout the GEMM
+ * kernels read: an invertible byte permutation of prq_prepare's canonical
+ * Wq [E][N][K_aug/2] / Wsc [E][N][K_aug/32], applied once per weight (offline).
+ * With S = ceil(K_aug / 128) K steps of 128 elements and T = N / 16 tiles:
+ *   Wp  [E][T][S][64][16] bytes: entry (e, t, s, l) holds the 16 code bytes of
+ *       row 16 t + l % 16, K elements [128 s + 32 (l / 16), +32) -- exactly
+ *       what lane l of the 16x16x128 block-scaled FP4 MFMA consumes -- and
+ *       zero bytes past K_aug;
+ *   Wps [E][T][ceil(S/4)][64] uint32: byte j of entry (e, t, q, l) is the
+ *       E8M0 scale of row 16 t + l % 16, 32-block 4 (4 q + j) + l / 16 (127
+ *       past K_aug).
+ * One wave thus reads one contiguous kilobyte per MFMA operand.  Both calls
+ * require N % 16 == 0 and K_aug % 32 == 0; prq_pack_weight runs on `stream`
+ * (device pointers; Wq and Wp 16-byte aligned, Wps 4-byte aligned).
+ */
+int prq_packed_weight_bytes(int32_t E, int32_t N, int32_t K_aug, size_t* code_bytes,
+                            size_t* scale_bytes);
+int prq_pack_weight(const uint8_t* Wq, const uint8_t* Wsc, int32_t E, int32_t N, int32_t K_aug,
+                    uint8_t* Wp, uint8_t* Wps, hipStream_t stream);
+
+/*
  * prq_gemm -- the augmented MXFP4 GEMM of Eq. 3, one GEMM over K_aug = K + k:
  *   Y[m, n] = sum_b 2^(Asc[m,b]-127) 2^(Wsc[n,b]-127) sum_i e2m1(A[m,32b+i]) e2m1(W[n,32b+i])
  * accumulated in float32 (block-scaled MFMA), Y float32 [M, N] (ld = N).
  *
- *   Aq [M, K_aug/2], Asc [M, K_aug/32]: from prq_quant_act
- *   Wq [N, K_aug/2], Wsc [N, K_aug/32]: from prq_prepare
+ *   Aq [M, K_aug/2], Asc [M, K_aug/32]: from prq_quant_act (row-major)
+ *   Wp, Wps: the weight in the packed layout above (E = 1), from
+ *            prq_pack_weight of prq_prepare's Wq / Wsc
  *   workspace: device buffer of at least prq_gemm_workspace_bytes(M, N, K_aug)
- *   bytes (may be NULL when that is 0): split-K partial sums and one arrival
- *   counter per 16-feature output tile.  It must be zero-filled once before its
- *   first use; every call returns the counters to zero (the partial-sum area
- *   keeps stale data, which is never read before being rewritten).  Calls
- *   that share one workspace must be ordered (same stream).
+ *   bytes (may be NULL when that is 0): a float accumulator [M][N] and one
+ *   arrival counter per output tile for split-K.  It must be zero-filled once
+ *   before its first use; every call leaves it zero-filled again.  Calls that
+ *   share one workspace must be ordered (same stream).
  * Limits: N % 16 == 0, K_aug <= 65536.  M == 0 is a no-op.
  */
 size_t prq_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K_aug);
 int prq_gemm(const uint8_t* Aq, const uint8_t* Asc, int32_t M,
-             const uint8_t* Wq, const uint8_t* Wsc, int32_t N, int32_t K_aug,
+             const uint8_t* Wp, const uint8_t* Wps, int32_t N, int32_t K_aug,
              float* Y, void* workspace, size_t workspace_bytes, hipStream_t stream);
 /* As prq_gemm with an explicit kernel (PRQ_GEMM_*) and, for PRQ_GEMM_STREAM,
  * an explicit split count along K_aug (0 = chosen from the shape). */
 size_t prq_gemm_workspace_bytes_ex(int32_t M, int32_t N, int32_t K_aug, int32_t variant,
                                    int32_t splits);
 int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M,
-                const uint8_t* Wq, const uint8_t* Wsc, int32_t N, int32_t K_aug,
+                const uint8_t* Wp, const uint8_t* Wps, int32_t N, int32_t K_aug,
                 float* Y, void* workspace, size_t workspace_bytes,
                 int32_t variant, int32_t splits, hipStream_t stream);
 
@@ -168,21 +189,22 @@ int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M,
  *
  *   Aq [M_total, K_aug/2], Asc [M_total, K_aug/32]
  *   group_offsets device [E + 1] int32 (non-decreasing, off[0] = 0,
- *                 off[E] = M_total); read on the device only, never copied
- *                 to the host
- *   Wq [E, N, K_aug/2], Wsc [E, N, K_aug/32] (experts contiguous)
+ *                 off[E] = M_total), read on the device only; offsets outside
+ *                 [0, M_total] are clamped into it
+ *   Wp, Wps  the E experts' weights in the packed layout (prq_pack_weight with E)
  *   Y  [M_total, N] float32
- *   workspace: as for prq_gemm, sized by prq_grouped_gemm_workspace_bytes.
+ *   workspace: as for prq_gemm, sized by prq_grouped_gemm_workspace_bytes
+ *   (currently 0: the grouped kernels do not split K).
  * Limits: N % 16 == 0, K_aug <= 65536, E <= 4096.
  */
 size_t prq_grouped_gemm_workspace_bytes(int32_t M_total, int32_t E, int32_t N, int32_t K_aug);
 int prq_grouped_gemm(const uint8_t* Aq, const uint8_t* Asc,
                      const int32_t* group_offsets, int32_t E, int32_t M_total,
-                     const uint8_t* Wq, const uint8_t* Wsc, int32_t N, int32_t K_aug,
+                     const uint8_t* Wp, const uint8_t* Wps, int32_t N, int32_t K_aug,
                      float* Y, void* workspace, size_t workspace_bytes, hipStream_t stream);
 int prq_grouped_gemm_ex(const uint8_t* Aq, const uint8_t* Asc,
                         const int32_t* group_offsets, int32_t E, int32_t M_total,
-                        const uint8_t* Wq, const uint8_t* Wsc, int32_t N, int32_t K_aug,
+                        const uint8_t* Wp, const uint8_t* Wps, int32_t N, int32_t K_aug,
                         float* Y, void* workspace, size_t workspace_bytes,
                         int32_t variant, hipStream_t stream);
 

@@ -28,12 +28,12 @@ HIP_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     "-mcode-object-version=5",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    "-Wall", "-Wno-unused-function",
+    "-munsafe-fp-atomics", "-Wall", "-Wno-unused-function",
 ]
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-ffp-contract=off", "-Wall",
               "-D__HIP_PLATFORM_AMD__", f"-I{ROCM}/include"]
 
-DEVICE_SOURCES = ["act_quant.hip", "gemm.hip"]
+DEVICE_SOURCES = ["act_quant.hip", "pack.hip", "gemm_tile.hip", "gemm_stream.hip"]
 HOST_SOURCES = ["prepare.cpp", "abi.cpp"]
 PROBE_SOURCES = ["probe.hip"]
 
@@ -72,7 +72,7 @@ def build(verbose=False):
         out = os.path.join(tmp, "libprq.so")
         _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", out, *objs, "-lpthread"])
         shutil.move(out, LIB)
-        pobjs = []
+        pobjs = [o for o in objs if o.endswith(".hip.o")]   # kernels, for the tuning entry
         for src in PROBE_SOURCES:
             obj = os.path.join(tmp, src + ".o")
             _run([HIPCC, *HIP_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", os.path.join(CSRC, src),

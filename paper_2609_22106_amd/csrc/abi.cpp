@@ -54,15 +54,16 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 int launch_status(hipError_t e) { return e == hipSuccess ? PRQ_OK : PRQ_EDEVICE; }
 
-int check_gemm_common(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t* Wq,
-                      const uint8_t* Wsc, int32_t N, int32_t K_aug, const float* Y) {
+int check_gemm_common(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t* Wp,
+                      const uint8_t* Wps, int32_t N, int32_t K_aug, const float* Y) {
   if (M < 0 || N <= 0 || K_aug <= 0) return PRQ_EINVAL;
-  if (!Wq || !Wsc) return PRQ_EINVAL;
+  if (!Wp || !Wps) return PRQ_EINVAL;
   if (M > 0 && (!Aq || !Asc || !Y)) return PRQ_EINVAL;
   if (K_aug % PRQ_BLOCK) return PRQ_EALIGN;
   if (N % 16) return PRQ_EALIGN;
   if (K_aug > kMaxKAug) return PRQ_EUNSUPPORTED;
-  if (!aligned16(Wq) || (M > 0 && (!aligned16(Aq) || (reinterpret_cast<uintptr_t>(Y) & 3u))))
+  if (!aligned16(Wp) || (reinterpret_cast<uintptr_t>(Wps) & 3u) ||
+      (M > 0 && (!aligned16(Aq) || (reinterpret_cast<uintptr_t>(Y) & 3u))))
     return PRQ_EALIGN;
   return PRQ_OK;
 }
@@ -86,6 +87,29 @@ const char* prq_strerror(int status) {
 
 int prq_abi_version(void) { return PRQ_ABI_VERSION; }
 
+int prq_packed_weight_bytes(int32_t E, int32_t N, int32_t K_aug, size_t* code_bytes,
+                            size_t* scale_bytes) {
+  if (E < 1 || N <= 0 || K_aug <= 0 || !code_bytes || !scale_bytes) return PRQ_EINVAL;
+  if (N % 16 || K_aug % PRQ_BLOCK) return PRQ_EALIGN;
+  if (K_aug > kMaxKAug || E > kMaxGroups) return PRQ_EUNSUPPORTED;
+  *code_bytes = prq::packed_code_bytes(N, K_aug, E);
+  *scale_bytes = prq::packed_scale_bytes(N, K_aug, E);
+  return PRQ_OK;
+}
+
+int prq_pack_weight(const uint8_t* Wq, const uint8_t* Wsc, int32_t E, int32_t N, int32_t K_aug,
+                    uint8_t* Wp, uint8_t* Wps, hipStream_t stream) {
+  size_t cb = 0, sb = 0;
+  int st = prq_packed_weight_bytes(E, N, K_aug, &cb, &sb);
+  if (st != PRQ_OK) return st;
+  if (!Wq || !Wsc || !Wp || !Wps) return PRQ_EINVAL;
+  if (!aligned16(Wq) || !aligned16(Wp) || (reinterpret_cast<uintptr_t>(Wps) & 3u)) return PRQ_EALIGN;
+  DeviceInfo dev;
+  st = current_device(&dev);
+  if (st != PRQ_OK) return st;
+  return launch_status(prq::launch_pack_weight(Wq, Wsc, N, K_aug, E, Wp, Wps, stream));
+}
+
 int prq_quant_act(const void* X_bf16, int64_t ld_x, int32_t M, int32_t K, int32_t k_tail,
                   const float* inv_scale, const int32_t* perm, const int32_t* group_offsets,
                   int32_t G, uint8_t* Aq, uint8_t* Asc, hipStream_t stream) {
@@ -107,27 +131,59 @@ int prq_quant_act(const void* X_bf16, int64_t ld_x, int32_t M, int32_t K, int32_
                                              dev.num_cus, stream));
 }
 
+}  // extern "C"
+
+namespace {
+
+// Stream-kernel configuration for a dense call; splits_req > 0 forces the
+// split count (the wave count and unroll are then re-derived for coverage).
+prq::StreamConfig dense_stream_config(int M, int N, int K_aug, int splits_req, int num_cus) {
+  prq::StreamConfig c = prq::choose_stream_config(M, N, K_aug, 0, num_cus);
+  if (splits_req > 0 && splits_req != c.splits) {
+    const int steps = (K_aug + 127) / 128;
+    c.splits = splits_req;
+    c.waves = 16;
+    const int per = (steps + c.splits - 1) / c.splits;
+    int u = (per + c.waves - 1) / c.waves;
+    static const int kU[] = {1, 2, 3, 4, 6, 8};
+    c.unroll = 0;
+    for (int x : kU)
+      if (x >= u) {
+        c.unroll = x;
+        break;
+      }
+    c.ok = c.unroll > 0 && splits_req <= steps;
+  }
+  if (c.ok) c.ok = prq::stream_config_covers(c, K_aug);
+  return c;
+}
+
+int device_cus() {
+  DeviceInfo dev;
+  return current_device(&dev) == PRQ_OK ? dev.num_cus : 256;
+}
+
+}  // namespace
+
+extern "C" {
+
 size_t prq_gemm_workspace_bytes_ex(int32_t M, int32_t N, int32_t K_aug, int32_t variant,
                                    int32_t splits) {
-  if (M <= 0 || N <= 0 || K_aug <= 0 || N % 16) return 0;
+  if (M <= 0 || N <= 0 || K_aug <= 0 || N % 16 || K_aug % PRQ_BLOCK || splits < 0) return 0;
   if (variant == PRQ_GEMM_AUTO) variant = prq::choose_variant(M, N, K_aug);
   if (variant != PRQ_GEMM_STREAM) return 0;
-  if (splits <= 0) {
-    DeviceInfo dev;
-    int cus = current_device(&dev) == PRQ_OK ? dev.num_cus : 256;
-    splits = prq::choose_stream_splits(M, N, K_aug, cus);
-  }
-  return prq::stream_workspace_bytes(M, 1, N, splits);
+  const prq::StreamConfig c = dense_stream_config(M, N, K_aug, splits, device_cus());
+  return c.ok ? prq::stream_workspace_bytes(M, 1, N, c.splits) : 0;
 }
 
 size_t prq_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K_aug) {
   return prq_gemm_workspace_bytes_ex(M, N, K_aug, PRQ_GEMM_AUTO, 0);
 }
 
-int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t* Wq,
-                const uint8_t* Wsc, int32_t N, int32_t K_aug, float* Y, void* workspace,
+int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t* Wp,
+                const uint8_t* Wps, int32_t N, int32_t K_aug, float* Y, void* workspace,
                 size_t workspace_bytes, int32_t variant, int32_t splits, hipStream_t stream) {
-  int st = check_gemm_common(Aq, Asc, M, Wq, Wsc, N, K_aug, Y);
+  int st = check_gemm_common(Aq, Asc, M, Wp, Wps, N, K_aug, Y);
   if (st != PRQ_OK) return st;
   if (variant < PRQ_GEMM_AUTO || variant > PRQ_GEMM_STREAM || splits < 0) return PRQ_EINVAL;
   if (M == 0) return PRQ_OK;
@@ -135,21 +191,26 @@ int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t*
   st = current_device(&dev);
   if (st != PRQ_OK) return st;
   if (variant == PRQ_GEMM_AUTO) variant = prq::choose_variant(M, N, K_aug);
-  if (variant == PRQ_GEMM_TILE)
-    return launch_status(prq::launch_gemm_tile(Aq, Asc, M, nullptr, 1, Wq, Wsc, N, K_aug, Y, stream));
-  if (splits == 0) splits = prq::choose_stream_splits(M, N, K_aug, dev.num_cus);
-  const int steps = (K_aug + 127) / 128;
-  if (splits > steps) return PRQ_EINVAL;
-  const size_t need = prq::stream_workspace_bytes(M, 1, N, splits);
-  if (need && (!workspace || workspace_bytes < need || !aligned16(workspace))) return PRQ_EWORKSPACE;
-  return launch_status(prq::launch_gemm_stream(Aq, Asc, M, nullptr, 1, Wq, Wsc, N, K_aug, Y, splits,
-                                               workspace, stream));
+  if (variant == PRQ_GEMM_STREAM) {
+    const prq::StreamConfig c = dense_stream_config(M, N, K_aug, splits, dev.num_cus);
+    if (!c.ok) {
+      if (splits > 0) return PRQ_EINVAL;   // the forced split count cannot cover K_aug
+      variant = PRQ_GEMM_TILE;
+    } else {
+      const size_t need = prq::stream_workspace_bytes(M, 1, N, c.splits);
+      if (need && (!workspace || workspace_bytes < need || !aligned16(workspace)))
+        return PRQ_EWORKSPACE;
+      return launch_status(prq::launch_gemm_stream(Aq, Asc, M, nullptr, 1, Wp, Wps, N, K_aug, Y, c,
+                                                   workspace, stream));
+    }
+  }
+  return launch_status(prq::launch_gemm_tile(Aq, Asc, M, nullptr, 1, Wp, Wps, N, K_aug, Y, stream));
 }
 
-int prq_gemm(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t* Wq,
-             const uint8_t* Wsc, int32_t N, int32_t K_aug, float* Y, void* workspace,
+int prq_gemm(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t* Wp,
+             const uint8_t* Wps, int32_t N, int32_t K_aug, float* Y, void* workspace,
              size_t workspace_bytes, hipStream_t stream) {
-  return prq_gemm_ex(Aq, Asc, M, Wq, Wsc, N, K_aug, Y, workspace, workspace_bytes, PRQ_GEMM_AUTO,
+  return prq_gemm_ex(Aq, Asc, M, Wp, Wps, N, K_aug, Y, workspace, workspace_bytes, PRQ_GEMM_AUTO,
                      0, stream);
 }
 
@@ -162,12 +223,12 @@ size_t prq_grouped_gemm_workspace_bytes(int32_t M_total, int32_t E, int32_t N, i
 }
 
 int prq_grouped_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, const int32_t* group_offsets,
-                        int32_t E, int32_t M_total, const uint8_t* Wq, const uint8_t* Wsc,
+                        int32_t E, int32_t M_total, const uint8_t* Wp, const uint8_t* Wps,
                         int32_t N, int32_t K_aug, float* Y, void* workspace,
                         size_t workspace_bytes, int32_t variant, hipStream_t stream) {
   (void)workspace;
   (void)workspace_bytes;
-  int st = check_gemm_common(Aq, Asc, M_total, Wq, Wsc, N, K_aug, Y);
+  int st = check_gemm_common(Aq, Asc, M_total, Wp, Wps, N, K_aug, Y);
   if (st != PRQ_OK) return st;
   if (E < 1 || !group_offsets) return PRQ_EINVAL;
   if (E > kMaxGroups) return PRQ_EUNSUPPORTED;
@@ -176,19 +237,23 @@ int prq_grouped_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, const int32_t* gr
   DeviceInfo dev;
   st = current_device(&dev);
   if (st != PRQ_OK) return st;
-  if (variant == PRQ_GEMM_AUTO) variant = prq::choose_variant((M_total + E - 1) / E, N, K_aug);
-  if (variant == PRQ_GEMM_TILE)
-    return launch_status(
-        prq::launch_gemm_tile(Aq, Asc, M_total, group_offsets, E, Wq, Wsc, N, K_aug, Y, stream));
-  return launch_status(prq::launch_gemm_stream(Aq, Asc, M_total, group_offsets, E, Wq, Wsc, N, K_aug,
-                                               Y, 1, nullptr, stream));
+  const int per_group = (M_total + E - 1) / E;
+  if (variant == PRQ_GEMM_AUTO) variant = prq::choose_variant(per_group, N, K_aug);
+  if (variant == PRQ_GEMM_STREAM) {
+    const prq::StreamConfig c = prq::choose_stream_config(per_group, N, K_aug, 1, dev.num_cus);
+    if (c.ok && prq::stream_config_covers(c, K_aug))
+      return launch_status(prq::launch_gemm_stream(Aq, Asc, M_total, group_offsets, E, Wp, Wps, N,
+                                                   K_aug, Y, c, nullptr, stream));
+  }
+  return launch_status(
+      prq::launch_gemm_tile(Aq, Asc, M_total, group_offsets, E, Wp, Wps, N, K_aug, Y, stream));
 }
 
 int prq_grouped_gemm(const uint8_t* Aq, const uint8_t* Asc, const int32_t* group_offsets, int32_t E,
-                     int32_t M_total, const uint8_t* Wq, const uint8_t* Wsc, int32_t N,
+                     int32_t M_total, const uint8_t* Wp, const uint8_t* Wps, int32_t N,
                      int32_t K_aug, float* Y, void* workspace, size_t workspace_bytes,
                      hipStream_t stream) {
-  return prq_grouped_gemm_ex(Aq, Asc, group_offsets, E, M_total, Wq, Wsc, N, K_aug, Y, workspace,
+  return prq_grouped_gemm_ex(Aq, Asc, group_offsets, E, M_total, Wp, Wps, N, K_aug, Y, workspace,
                              workspace_bytes, PRQ_GEMM_AUTO, stream);
 }
 

@@ -7,6 +7,7 @@
 #include <cstdint>
 
 #include "mx_device.hpp"
+#include "prq_internal.h"
 
 namespace {
 
@@ -53,6 +54,8 @@ __global__ void cvt_pairs(const float* x, const float* y, const float* s, int n,
   if (i < n) out[i] = static_cast<uint8_t>(__builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, x[i], y[i], s[i], 0) & 0xFFu);
 }
 
+__global__ void empty_kernel() {}
+
 }  // namespace
 
 extern "C" {
@@ -74,6 +77,32 @@ int prq_probe_cvt_pairs(const float* x, const float* y, const float* s, int n, u
                         hipStream_t stream) {
   if (n <= 0) return 0;
   cvt_pairs<<<(n + 255) / 256, 256, 0, stream>>>(x, y, s, n, out);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+// Tuning entry: the weight-streaming GEMM with an explicit configuration.
+// A bounded empty kernel for the launch-floor measurement follows.
+// Returns -1 when the configuration does not cover K_aug (nothing launched).
+int prq_tune_gemm_stream(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off, int E,
+                         const uint8_t* Wq, const uint8_t* Wsc, int N, int K_aug, float* Y,
+                         int splits, int waves, int unroll, int groups, int tiles,
+                         void* workspace, hipStream_t stream) {
+  prq::StreamConfig c;
+  c.tiles = tiles;
+  c.splits = splits;
+  c.waves = waves;
+  c.unroll = unroll;
+  c.groups = groups;
+  if (!prq::stream_config_covers(c, K_aug) || N % 16 || K_aug % 32 || M <= 0) return -1;
+  if (splits > 1 && !workspace) return -1;
+  return prq::launch_gemm_stream(Aq, Asc, M, off, E, Wq, Wsc, N, K_aug, Y, c, workspace, stream) ==
+                 hipSuccess
+             ? 0
+             : -3;
+}
+
+int prq_probe_empty(int blocks, int threads, hipStream_t stream) {
+  empty_kernel<<<blocks, threads, 0, stream>>>();
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

@@ -9,10 +9,16 @@
 
 namespace prq {
 
-// Launch parameters decided on the host from the shape.
-struct StreamPlan {
-  int splits;        // workgroups along K_aug per 16-row output tile
-  int ksteps;        // 128-element K steps in K_aug (last one may be partial)
+// Launch parameters of the weight-streaming GEMM, decided on the host from
+// the shape.  Coverage invariant: (waves / tiles) * unroll * splits >= K steps,
+// so every 128-element K step of every tile belongs to exactly one wave.
+struct StreamConfig {
+  int splits = 1;   // workgroups along K_aug per 16-feature output tile
+  int waves = 16;   // waves per workgroup (4, 8 or 16)
+  int unroll = 8;   // K steps per wave (1, 2, 3, 4, 6 or 8)
+  int groups = 1;   // 16-row activation column groups per pass (1, 2 or 4)
+  int tiles = 1;    // 16-feature tiles per workgroup (1 or 4; dense only)
+  bool ok = true;   // false: no configuration covers K_aug (use the tile kernel)
 };
 
 // act_quant.hip
@@ -21,19 +27,27 @@ hipError_t launch_act_quant(const uint16_t* X, int64_t ld_x, int M, int K, int k
                             const int32_t* group_offsets, int G, uint8_t* Aq, uint8_t* Asc,
                             int num_cus, hipStream_t stream);
 
-// gemm.hip.  group_offsets == nullptr means one group of M rows.
-hipError_t launch_gemm_tile(const uint8_t* Aq, const uint8_t* Asc, int M,
-                            const int32_t* group_offsets, int E, const uint8_t* Wq,
-                            const uint8_t* Wsc, int N, int K_aug, float* Y, hipStream_t stream);
-hipError_t launch_gemm_stream(const uint8_t* Aq, const uint8_t* Asc, int M,
-                              const int32_t* group_offsets, int E, const uint8_t* Wq,
-                              const uint8_t* Wsc, int N, int K_aug, float* Y, int splits,
-                              void* workspace, hipStream_t stream);
+// pack.hip: the packed weight layout the GEMM kernels read.
+size_t packed_code_bytes(int N, int K_aug, int E);
+size_t packed_scale_bytes(int N, int K_aug, int E);
+hipError_t launch_pack_weight(const uint8_t* Wq, const uint8_t* Wsc, int N, int K_aug, int E,
+                              uint8_t* Wp, uint8_t* Wps, hipStream_t stream);
 
-// Workspace of the split-K stream kernel: float partials [splits][M][N] plus
-// one uint32 arrival counter per 16-row output tile (and per expert).
+// gemm_tile.hip / gemm_stream.hip (packed weights Wp/Wps).  group_offsets ==
+// nullptr means one group of M rows.
+hipError_t launch_gemm_tile(const uint8_t* Aq, const uint8_t* Asc, int M,
+                            const int32_t* group_offsets, int E, const uint8_t* Wp,
+                            const uint8_t* Wps, int N, int K_aug, float* Y, hipStream_t stream);
+hipError_t launch_gemm_stream(const uint8_t* Aq, const uint8_t* Asc, int M,
+                              const int32_t* group_offsets, int E, const uint8_t* Wp,
+                              const uint8_t* Wps, int N, int K_aug, float* Y,
+                              const StreamConfig& cfg, void* workspace, hipStream_t stream);
+
+// Workspace of the split-K stream kernel: a float accumulator [M][N] plus one
+// uint32 arrival counter per 16-feature output tile (per expert); zero between calls.
 size_t stream_workspace_bytes(int M, int E, int N, int splits);
-int choose_stream_splits(int M, int N, int K_aug, int num_cus);
+StreamConfig choose_stream_config(int M_per_group, int N, int K_aug, int grouped, int num_cus);
+bool stream_config_covers(const StreamConfig& c, int K_aug);
 int choose_variant(int M_per_group, int N, int K_aug);
 
 }  // namespace prq

@@ -46,6 +46,9 @@ _prepare = _decl("prq_prepare", ctypes.c_int,
                  [_p, _i32, _i32, _p, _i32, ctypes.c_double, _i32, _i32, _p, _p, _p, _p, _p, _p])
 _quant_act = _decl("prq_quant_act", ctypes.c_int,
                    [_p, _i64, _i32, _i32, _i32, _p, _p, _p, _i32, _p, _p, _p])
+_packed_bytes = _decl("prq_packed_weight_bytes", ctypes.c_int,
+                      [_i32, _i32, _i32, ctypes.POINTER(_sz), ctypes.POINTER(_sz)])
+_pack = _decl("prq_pack_weight", ctypes.c_int, [_p, _p, _i32, _i32, _i32, _p, _p, _p])
 _gemm_ws = _decl("prq_gemm_workspace_bytes", _sz, [_i32, _i32, _i32])
 _gemm_ws_ex = _decl("prq_gemm_workspace_bytes_ex", _sz, [_i32, _i32, _i32, _i32, _i32])
 _gemm = _decl("prq_gemm", ctypes.c_int, [_p, _p, _i32, _p, _p, _i32, _i32, _p, _p, _sz, _p])
@@ -141,23 +144,50 @@ def prq_quant_act(X, K, k_tail, inv_scale=None, perm=None, group_offsets=None, G
     return Aq, Asc
 
 
+class PackedWeight:
+    """Device buffers of a weight in the GEMM's packed layout (include/prq.h)."""
+
+    def __init__(self, Wp, Wps, E, N, K_aug):
+        self.Wp, self.Wps, self.E, self.N, self.K_aug = Wp, Wps, E, N, K_aug
+
+
+def prq_packed_weight_bytes(E, N, K_aug):
+    cb, sb = _sz(0), _sz(0)
+    _check(_packed_bytes(E, N, K_aug, ctypes.byref(cb), ctypes.byref(sb)), "prq_packed_weight_bytes")
+    return int(cb.value), int(sb.value)
+
+
+def prq_pack_weight(Wq, Wsc, stream=None):
+    """Canonical device Wq [N, K_aug/2] / Wsc [N, K_aug/32] (or [E, N, ...]) ->
+    PackedWeight in the layout the GEMM kernels read."""
+    E = Wq.shape[0] if Wq.dim() == 3 else 1
+    N = Wq.shape[-2]
+    K_aug = Wq.shape[-1] * 2
+    cb, sb = prq_packed_weight_bytes(E, N, K_aug)
+    Wp = torch.empty(cb, dtype=torch.uint8, device=Wq.device)
+    Wps = torch.empty(sb, dtype=torch.uint8, device=Wq.device)
+    _check(_pack(_ptr(Wq), _ptr(Wsc), E, N, K_aug, _ptr(Wp), _ptr(Wps), _stream(stream)),
+           "prq_pack_weight")
+    return PackedWeight(Wp, Wps, E, N, K_aug)
+
+
 def prq_gemm_workspace_bytes(M, N, K_aug, variant=GEMM_AUTO, splits=0):
     return int(_gemm_ws_ex(M, N, K_aug, variant, splits))
 
 
-def prq_gemm(Aq, Asc, Wq, Wsc, Y=None, workspace=None, variant=GEMM_AUTO, splits=0, stream=None):
-    """Y [M, N] float32 = deq(A_aug) deq(W_aug)^T over K_aug (device)."""
+def prq_gemm(Aq, Asc, W, Y=None, workspace=None, variant=GEMM_AUTO, splits=0, stream=None):
+    """Y [M, N] float32 = deq(A_aug) deq(W_aug)^T over K_aug (device); W is a
+    PackedWeight (E = 1)."""
     M = Aq.shape[0]
-    N = Wq.shape[0]
-    K_aug = Wq.shape[1] * 2
+    N, K_aug = W.N, W.K_aug
     if Y is None:
-        Y = torch.empty((M, N), dtype=torch.float32, device=Wq.device)
+        Y = torch.empty((M, N), dtype=torch.float32, device=W.Wp.device)
     need = prq_gemm_workspace_bytes(M, N, K_aug, variant, splits)
     if workspace is None and need:
-        workspace = torch.zeros(need, dtype=torch.uint8, device=Wq.device)
+        workspace = torch.zeros(need, dtype=torch.uint8, device=W.Wp.device)
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
-    st = _gemm_ex(_ptr(Aq), _ptr(Asc), M, _ptr(Wq), _ptr(Wsc), N, K_aug, _ptr(Y), _ptr(workspace),
-                  ws_bytes, variant, splits, _stream(stream))
+    st = _gemm_ex(_ptr(Aq), _ptr(Asc), M, _ptr(W.Wp), _ptr(W.Wps), N, K_aug, _ptr(Y),
+                  _ptr(workspace), ws_bytes, variant, splits, _stream(stream))
     _check(st, "prq_gemm")
     return Y
 
@@ -166,16 +196,15 @@ def prq_grouped_gemm_workspace_bytes(M_total, E, N, K_aug):
     return int(_ggemm_ws(M_total, E, N, K_aug))
 
 
-def prq_grouped_gemm(Aq, Asc, group_offsets, Wq, Wsc, Y=None, workspace=None, variant=GEMM_AUTO,
+def prq_grouped_gemm(Aq, Asc, group_offsets, W, Y=None, workspace=None, variant=GEMM_AUTO,
                      stream=None):
-    """Rows sorted by expert; Wq [E, N, K_aug/2]; Y [M_total, N] float32 (device)."""
+    """Rows sorted by expert; W a PackedWeight of E experts; Y [M_total, N] float32."""
     M = Aq.shape[0]
-    E, N = Wq.shape[0], Wq.shape[1]
-    K_aug = Wq.shape[2] * 2
+    E, N, K_aug = W.E, W.N, W.K_aug
     if Y is None:
-        Y = torch.empty((M, N), dtype=torch.float32, device=Wq.device)
+        Y = torch.empty((M, N), dtype=torch.float32, device=W.Wp.device)
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
-    st = _ggemm_ex(_ptr(Aq), _ptr(Asc), _ptr(group_offsets), E, M, _ptr(Wq), _ptr(Wsc), N, K_aug,
-                   _ptr(Y), _ptr(workspace), ws_bytes, variant, _stream(stream))
+    st = _ggemm_ex(_ptr(Aq), _ptr(Asc), _ptr(group_offsets), E, M, _ptr(W.Wp), _ptr(W.Wps), N,
+                   K_aug, _ptr(Y), _ptr(workspace), ws_bytes, variant, _stream(stream))
     _check(st, "prq_grouped_gemm")
     return Y

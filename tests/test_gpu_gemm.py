@@ -19,9 +19,13 @@ def _prq():
     return prq
 
 
+def _packed(Wq, Wsc):
+    return _prq().prq_pack_weight(dev(Wq), dev(Wsc))
+
+
 def _gpu_gemm(Aq, Asc, Wq, Wsc, variant, splits=0, workspace=None):
     prq = _prq()
-    Y = prq.prq_gemm(dev(Aq), dev(Asc), dev(Wq), dev(Wsc), variant=variant, splits=splits,
+    Y = prq.prq_gemm(dev(Aq), dev(Asc), _packed(Wq, Wsc), variant=variant, splits=splits,
                      workspace=workspace)
     torch.cuda.synchronize()
     return host(Y)
@@ -56,18 +60,26 @@ def test_stream_split_counts(splits):
     assert_gemm_close(Y, pq.gemm(Aq, Asc, Wq, Wsc), f"splits={splits}")
 
 
-def test_split_k_is_deterministic_and_resets_its_counters():
+def test_split_k_workspace_returns_to_zero_and_two_splits_are_deterministic():
+    """Repeated calls on one workspace stay correct (the accumulator and the
+    arrival counters are cleared by each call); with two splits the float sum
+    0 + a + b is order-independent, so the bits repeat exactly."""
     prq = _prq()
     rng = np.random.default_rng(3)
     M, N, K_aug = 64, 2560, 9984
     Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
     Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
-    need = prq.prq_gemm_workspace_bytes(M, N, K_aug, prq.GEMM_STREAM, 4)
-    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
-    ys = [_gpu_gemm(Aq, Asc, Wq, Wsc, prq.GEMM_STREAM, 4, ws) for _ in range(3)]
-    np.testing.assert_array_equal(ys[0].view(np.uint32), ys[1].view(np.uint32))
-    np.testing.assert_array_equal(ys[0].view(np.uint32), ys[2].view(np.uint32))
-    assert_gemm_close(ys[0], pq.gemm(Aq, Asc, Wq, Wsc), "split 4")
+    ref = pq.gemm(Aq, Asc, Wq, Wsc)
+    for splits in (2, 4):
+        need = prq.prq_gemm_workspace_bytes(M, N, K_aug, prq.GEMM_STREAM, splits)
+        ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+        ys = [_gpu_gemm(Aq, Asc, Wq, Wsc, prq.GEMM_STREAM, splits, ws) for _ in range(3)]
+        for y in ys:
+            assert_gemm_close(y, ref, f"split {splits}")
+        assert int(torch.count_nonzero(ws)) == 0
+        if splits == 2:
+            np.testing.assert_array_equal(ys[0].view(np.uint32), ys[1].view(np.uint32))
+            np.testing.assert_array_equal(ys[0].view(np.uint32), ys[2].view(np.uint32))
 
 
 def test_hand_values():
@@ -92,7 +104,7 @@ def test_down_proj_decode_end_to_end(c1_art, M):
     X = c.X[:M]
     say("gemm case: down_proj decode M =", M)
     Aq, Asc = prq.prq_quant_act(dev(X), 9728, 256, dev(art["inv_scale"]), dev(art["perm"]))
-    Y = prq.prq_gemm(Aq, Asc, dev(art["Wq"]), dev(art["Wsc"]))
+    Y = prq.prq_gemm(Aq, Asc, _packed(art["Wq"], art["Wsc"]))
     torch.cuda.synchronize()
     rq, rs = pq.quant_act(X, art["inv_scale"], art["perm"], 256)
     assert_gemm_close(host(Y), pq.gemm(rq, rs, art["Wq"], art["Wsc"]), f"decode M={M}")
@@ -106,7 +118,7 @@ def test_down_proj_prefill_sampled_rows(c1_art, M):
     X = c.X[:M]
     say("gemm case: down_proj prefill M =", M)
     Aq, Asc = prq.prq_quant_act(dev(X), 9728, 256, dev(art["inv_scale"]), dev(art["perm"]))
-    Y = host(prq.prq_gemm(Aq, Asc, dev(art["Wq"]), dev(art["Wsc"])))
+    Y = host(prq.prq_gemm(Aq, Asc, _packed(art["Wq"], art["Wsc"])))
     torch.cuda.synchronize()
     rows = np.unique(np.concatenate([np.random.default_rng(M).choice(M, 48, replace=False),
                                      [0, M - 1]]))
@@ -125,7 +137,7 @@ def _grouped_case(counts, N, K_aug, seed):
 
 def _gpu_grouped(off, Aq, Asc, Wq, Wsc, variant):
     prq = _prq()
-    Y = prq.prq_grouped_gemm(dev(Aq), dev(Asc), dev(off), dev(Wq), dev(Wsc), variant=variant)
+    Y = prq.prq_grouped_gemm(dev(Aq), dev(Asc), dev(off), _packed(Wq, Wsc), variant=variant)
     torch.cuda.synchronize()
     return host(Y)
 
@@ -180,8 +192,44 @@ def test_grouped_end_to_end_prepared_experts():
     say("grouped case: end to end, counts", np.diff(off).tolist())
     Aq, Asc = prq.prq_quant_act(dev(c.X), 768, 64, dev(inv), dev(perm), dev(off), 8)
     for v in (prq.GEMM_TILE, prq.GEMM_STREAM):
-        Y = prq.prq_grouped_gemm(Aq, Asc, dev(off), dev(Wq), dev(Wsc), variant=v)
+        Y = prq.prq_grouped_gemm(Aq, Asc, dev(off), _packed(Wq, Wsc), variant=v)
         torch.cuda.synchronize()
         rq, rs = pq.quant_act_grouped(c.X, inv, perm, off, 64)
         np.testing.assert_array_equal(host(Aq), rq)
         assert_gemm_close(host(Y), pq.grouped_gemm(rq, rs, off, Wq, Wsc), f"e2e variant {v}")
+
+
+# ------------------------------------------------------------- packing ---
+def _pack_reference(Wq, Wsc):
+    """The packed layout written out from its definition in include/prq.h."""
+    E, N, Kh = Wq.shape
+    K_aug = 2 * Kh
+    S = -(-K_aug // 128)
+    Q = -(-S // 4)
+    nb = K_aug // 32
+    Wp = np.zeros((E, N // 16, S, 64, 16), np.uint8)
+    Wps = np.zeros((E, N // 16, Q, 64, 4), np.uint8)
+    for t in range(N // 16):
+        for l in range(64):
+            row = 16 * t + l % 16
+            for s in range(S):
+                k0 = (128 * s + 32 * (l // 16)) // 2
+                if k0 < Kh:
+                    Wp[:, t, s, l] = Wq[:, row, k0:k0 + 16]
+            for q in range(Q):
+                for j in range(4):
+                    b = 4 * (4 * q + j) + l // 16
+                    Wps[:, t, q, l, j] = Wsc[:, row, b] if b < nb else 127
+    return Wp.ravel(), Wps.ravel()
+
+
+@pytest.mark.parametrize("E,N,K_aug", [(1, 16, 32), (1, 48, 1088), (3, 32, 832), (2, 64, 544)])
+def test_pack_weight_layout(E, N, K_aug):
+    prq = _prq()
+    rng = np.random.default_rng(E * N + K_aug)
+    Wq, Wsc = inputs.random_mxfp4(rng, (E, N), K_aug)
+    W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
+    torch.cuda.synchronize()
+    ref_p, ref_s = _pack_reference(Wq, Wsc)
+    np.testing.assert_array_equal(host(W.Wp), ref_p)
+    np.testing.assert_array_equal(host(W.Wps), ref_s)
