@@ -131,5 +131,7 @@ def test_workspace_sizes():
     assert prq.prq_gemm_workspace_bytes(64, 2560, 9984, prq.GEMM_TILE) == 0
     assert prq.prq_gemm_workspace_bytes(64, 2560, 9984, prq.GEMM_STREAM, 1) == 0
     ws = prq.prq_gemm_workspace_bytes(64, 2560, 9984, prq.GEMM_STREAM, 4)
-    assert ws >= 4 * 64 * 2560 * 4 + (2560 // 16) * 4
+    assert ws >= 64 * 2560 * 4 + (2560 // 16) * 4     # float accumulator + arrival counters
+    assert prq.prq_packed_weight_bytes(1, 2560, 9984) == (160 * 78 * 1024, 160 * 20 * 256)
+    assert prq.prq_packed_weight_bytes(128, 2048, 832) == (128 * 128 * 7 * 1024, 128 * 128 * 2 * 256)
     assert prq.prq_grouped_gemm_workspace_bytes(512, 128, 2048, 832) == 0
