@@ -93,7 +93,7 @@ def build_dense_ops(torch, prq, layers, M_list, rotate_bytes, stream):
         R = max(1, math.ceil(rotate_bytes / w_bytes))
         Wc = prq.prq_pack_weight(torch.from_numpy(art["Wq"]).cuda(), torch.from_numpy(art["Wsc"]).cuda())
         Ws = [prq.PackedWeight(Wc.Wp.clone(), Wc.Wps.clone(), 1, N, K_aug) for _ in range(R)]
-        inv = torch.from_numpy(art["inv_scale"]).cuda()
+        inv = torch.from_numpy(art["inv_scale_pos"]).cuda()
         perm = torch.from_numpy(art["perm"]).cuda()
         X = torch.from_numpy(c.X.view("int16")).cuda()
         for M in M_list:
@@ -132,7 +132,7 @@ def build_expert_ops(torch, np, prq, inputs, tokens, rotate_bytes, stream):
     R = max(1, math.ceil(rotate_bytes / w_bytes))
     Wc = prq.prq_pack_weight(torch.from_numpy(Wq_h).cuda(), torch.from_numpy(Wsc_h).cuda())
     Ws = [prq.PackedWeight(Wc.Wp.clone(), Wc.Wps.clone(), E, N, K_aug) for _ in range(R)]
-    inv = torch.from_numpy(np.stack([a["inv_scale"] for a in arts])).cuda()
+    inv = torch.from_numpy(np.stack([a["inv_scale_pos"] for a in arts])).cuda()
     perm = torch.from_numpy(np.stack([a["perm"] for a in arts])).cuda()
     off = torch.from_numpy(c.group_offsets).cuda()
     M = int(c.group_offsets[-1])

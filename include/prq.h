@@ -94,6 +94,8 @@ int prq_abi_version(void);
  *   perm       [K] int32   perm[p] = source channel of position p: channels
  *                          not selected in increasing order, then the k
  *                          selected ones in increasing order
+ *   inv_scale_pos [K] float or NULL   inv_scale[perm[p]]: D^-1 at the
+ *                          permuted positions, the form prq_quant_act takes
  *   Wq         [N, K_aug/2] uint8   packed E2M1 codes of [W~ | R_W]
  *   Wsc        [N, K_aug/32] uint8  E8M0 scale codes
  *   col_err    [K] double or NULL   per-channel squared MXFP4 error of
@@ -105,20 +107,22 @@ int prq_abi_version(void);
 int prq_prepare(const uint16_t* W_bf16, int32_t N, int32_t K,
                 const uint16_t* Xcal_bf16, int32_t T,
                 double alpha, int32_t k_tail, int32_t scale_mode,
-                float* scale, float* inv_scale, int32_t* perm,
+                float* scale, float* inv_scale, int32_t* perm, float* inv_scale_pos,
                 uint8_t* Wq, uint8_t* Wsc, double* col_err);
 
 /*
  * prq_quant_act -- activation side of Eq. 3 with the online copy (Sec.
  * "Activation tail construction" and "Kernel design"; Algorithm 1, step 11):
- *   Z~[m, p] = X[m, perm[p]] * inv_scale[perm[p]]   (float32 product)
+ *   Z~[m, p] = X[m, perm[p]] * inv_scale_pos[p]     (float32 product,
+ *              inv_scale_pos[p] = 1/s_{perm[p]} from prq_prepare)
  * quantized to MXFP4 once; the k/32 tail blocks are then written a second time,
  * codes and scale bytes, after the K/32 main blocks, which equals quantizing
  * [Z~, Z~[:, K-k:]].
  *
  *   X_bf16        device [M, ld_x] bf16 (K used columns), ld_x >= K, ld_x % 8 == 0
- *   inv_scale     device [G, K] float, or NULL (no scaling: X is already scaled)
- *   perm          device [G, K] int32, or NULL (identity: X is already permuted)
+ *   inv_scale_pos device [G, K] float in position order, or NULL (no scaling)
+ *   perm          device [G, K] int32, or NULL (identity: X is already permuted);
+ *                 perm and inv_scale_pos must be 16-byte aligned
  *                 values must lie in [0, K) (an entry outside it reads channel 0)
  *   group_offsets device [G + 1] int32, or NULL when G == 1.  Rows
  *                 [off[g], off[g+1]) use expert g's perm and inv_scale
@@ -129,7 +133,7 @@ int prq_prepare(const uint16_t* W_bf16, int32_t N, int32_t K,
  * Limits: K <= 16384, G <= 4096.  M == 0 is a no-op.
  */
 int prq_quant_act(const void* X_bf16, int64_t ld_x, int32_t M, int32_t K, int32_t k_tail,
-                  const float* inv_scale, const int32_t* perm,
+                  const float* inv_scale_pos, const int32_t* perm,
                   const int32_t* group_offsets, int32_t G,
                   uint8_t* Aq, uint8_t* Asc, hipStream_t stream);
 

@@ -111,7 +111,7 @@ int prq_pack_weight(const uint8_t* Wq, const uint8_t* Wsc, int32_t E, int32_t N,
 }
 
 int prq_quant_act(const void* X_bf16, int64_t ld_x, int32_t M, int32_t K, int32_t k_tail,
-                  const float* inv_scale, const int32_t* perm, const int32_t* group_offsets,
+                  const float* inv_scale_pos, const int32_t* perm, const int32_t* group_offsets,
                   int32_t G, uint8_t* Aq, uint8_t* Asc, hipStream_t stream) {
   if (M < 0 || K <= 0 || G < 1 || ld_x < K) return PRQ_EINVAL;
   if (G > 1 && !group_offsets) return PRQ_EINVAL;
@@ -120,14 +120,13 @@ int prq_quant_act(const void* X_bf16, int64_t ld_x, int32_t M, int32_t K, int32_
   if (M == 0) return PRQ_OK;
   if (!X_bf16 || !Aq || !Asc) return PRQ_EINVAL;
   if (!aligned16(X_bf16) || ld_x % 8 || !aligned16(Aq)) return PRQ_EALIGN;
-  if ((inv_scale && (reinterpret_cast<uintptr_t>(inv_scale) & 3u)) ||
-      (perm && (reinterpret_cast<uintptr_t>(perm) & 3u)))
+  if ((inv_scale_pos && !aligned16(inv_scale_pos)) || (perm && !aligned16(perm)))
     return PRQ_EALIGN;
   DeviceInfo dev;
   int st = current_device(&dev);
   if (st != PRQ_OK) return st;
   return launch_status(prq::launch_act_quant(static_cast<const uint16_t*>(X_bf16), ld_x, M, K,
-                                             k_tail, inv_scale, perm, group_offsets, G, Aq, Asc,
+                                             k_tail, inv_scale_pos, perm, group_offsets, G, Aq, Asc,
                                              dev.num_cus, stream));
 }
 
@@ -142,19 +141,24 @@ prq::StreamConfig dense_stream_config(int M, int N, int K_aug, int splits_req, i
   if (splits_req > 0 && splits_req != c.splits) {
     const int steps = (K_aug + 127) / 128;
     c.splits = splits_req;
-    c.waves = 16;
-    const int per = (steps + c.splits - 1) / c.splits;
-    int u = (per + c.waves - 1) / c.waves;
     static const int kU[] = {1, 2, 3, 4, 6, 8};
-    c.unroll = 0;
-    for (int x : kU)
-      if (x >= u) {
-        c.unroll = x;
+    c.ok = false;
+    for (int tiles : {c.tiles, 1}) {   // keep the tile grouping if it still covers K_aug
+      c.tiles = tiles;
+      const int chunks = c.waves / c.tiles;
+      const int need = ((steps + c.splits - 1) / c.splits + chunks - 1) / chunks;
+      c.unroll = 0;
+      for (int x : kU)
+        if (x >= need) {
+          c.unroll = x;
+          break;
+        }
+      if (c.unroll > 0 && splits_req <= steps && prq::stream_config_covers(c, K_aug)) {
+        c.ok = true;
         break;
       }
-    c.ok = c.unroll > 0 && splits_req <= steps;
+    }
   }
-  if (c.ok) c.ok = prq::stream_config_covers(c, K_aug);
   return c;
 }
 
@@ -173,7 +177,7 @@ size_t prq_gemm_workspace_bytes_ex(int32_t M, int32_t N, int32_t K_aug, int32_t 
   if (variant == PRQ_GEMM_AUTO) variant = prq::choose_variant(M, N, K_aug);
   if (variant != PRQ_GEMM_STREAM) return 0;
   const prq::StreamConfig c = dense_stream_config(M, N, K_aug, splits, device_cus());
-  return c.ok ? prq::stream_workspace_bytes(M, 1, N, c.splits) : 0;
+  return c.ok ? prq::stream_workspace_bytes(M, 1, N, c.splits, c.reduce) : 0;
 }
 
 size_t prq_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K_aug) {
@@ -197,7 +201,7 @@ int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t*
       if (splits > 0) return PRQ_EINVAL;   // the forced split count cannot cover K_aug
       variant = PRQ_GEMM_TILE;
     } else {
-      const size_t need = prq::stream_workspace_bytes(M, 1, N, c.splits);
+      const size_t need = prq::stream_workspace_bytes(M, 1, N, c.splits, c.reduce);
       if (need && (!workspace || workspace_bytes < need || !aligned16(workspace)))
         return PRQ_EWORKSPACE;
       return launch_status(prq::launch_gemm_stream(Aq, Asc, M, nullptr, 1, Wp, Wps, N, K_aug, Y, c,

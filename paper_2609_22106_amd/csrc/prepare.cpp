@@ -101,8 +101,8 @@ void parallel_rows(int64_t rows, F&& body) {
 
 extern "C" int prq_prepare(const uint16_t* W_bf16, int32_t N, int32_t K, const uint16_t* Xcal_bf16,
                            int32_t T, double alpha, int32_t k_tail, int32_t scale_mode,
-                           float* scale, float* inv_scale, int32_t* perm, uint8_t* Wq,
-                           uint8_t* Wsc, double* col_err) {
+                           float* scale, float* inv_scale, int32_t* perm,
+                           float* inv_scale_pos, uint8_t* Wq, uint8_t* Wsc, double* col_err) {
   if (!W_bf16 || !Xcal_bf16 || !scale || !inv_scale || !perm || !Wq || !Wsc) return PRQ_EINVAL;
   if (N <= 0 || K <= 0 || T <= 0) return PRQ_EINVAL;
   if (!(alpha >= 0.0 && alpha <= 1.0)) return PRQ_EINVAL;
@@ -177,6 +177,8 @@ extern "C" int prq_prepare(const uint16_t* W_bf16, int32_t N, int32_t K, const u
     if (!sel[j]) perm[p++] = j;
   for (int j = 0; j < K; ++j)
     if (sel[j]) perm[p++] = j;
+  if (inv_scale_pos)
+    for (int q = 0; q < K; ++q) inv_scale_pos[q] = inv_scale[perm[q]];
 
   // Steps 6, 7, 10: W~ = W_s P, Q(W~), R = W~_tail - Q(W~)_tail, Q(R), packing.
   const int64_t row_bytes = Kaug / 2;

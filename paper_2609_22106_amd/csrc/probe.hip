@@ -56,6 +56,36 @@ __global__ void cvt_pairs(const float* x, const float* y, const float* s, int n,
 
 __global__ void empty_kernel() {}
 
+// Reads the packed weight with the stream GEMM's grid mapping (tile per
+// blockIdx.x, split per blockIdx.y, kU contiguous kilobytes per wave) and
+// writes one dword per workgroup: the memory side of that kernel alone.
+template <int kU>
+__global__ __launch_bounds__(1024) void stream_read_probe(const uint8_t* __restrict__ Wp, int steps,
+                                                          int splits, uint32_t* __restrict__ out) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tile = blockIdx.x, split = blockIdx.y;
+  const int s_begin = steps * split / splits, s_end = steps * (split + 1) / splits;
+  const int s0 = s_begin + wave * kU;
+  const uint8_t* base = Wp + static_cast<int64_t>(tile) * steps * 1024 + lane * 16;
+  uint4 v[kU];
+#pragma unroll
+  for (int j = 0; j < kU; ++j)
+    v[j] = (s0 + j < s_end) ? *reinterpret_cast<const uint4*>(base + static_cast<int64_t>(s0 + j) * 1024)
+                            : make_uint4(0, 0, 0, 0);
+  uint32_t x = 0;
+#pragma unroll
+  for (int j = 0; j < kU; ++j) x ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
+  __shared__ uint32_t s_x[16];
+  for (int o = 32; o > 0; o >>= 1) x ^= __shfl_xor(x, o);
+  if (lane == 0) s_x[wave] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t t = 0;
+    for (int w = 0; w < static_cast<int>(blockDim.x >> 6); ++w) t ^= s_x[w];
+    out[blockIdx.y * gridDim.x + blockIdx.x] = t;
+  }
+}
+
 }  // namespace
 
 extern "C" {
@@ -86,19 +116,37 @@ int prq_probe_cvt_pairs(const float* x, const float* y, const float* s, int n, u
 int prq_tune_gemm_stream(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off, int E,
                          const uint8_t* Wq, const uint8_t* Wsc, int N, int K_aug, float* Y,
                          int splits, int waves, int unroll, int groups, int tiles,
-                         void* workspace, hipStream_t stream) {
+                         int stage_lds, int reduce, void* workspace, hipStream_t stream) {
   prq::StreamConfig c;
   c.tiles = tiles;
+  c.stage_lds = stage_lds != 0;
+  c.reduce = reduce;
   c.splits = splits;
   c.waves = waves;
   c.unroll = unroll;
   c.groups = groups;
   if (!prq::stream_config_covers(c, K_aug) || N % 16 || K_aug % 32 || M <= 0) return -1;
-  if (splits > 1 && !workspace) return -1;
+  if (splits > 1 && reduce != 2 && !workspace) return -1;
+  if (reduce < 0 || reduce > 2) return -1;
   return prq::launch_gemm_stream(Aq, Asc, M, off, E, Wq, Wsc, N, K_aug, Y, c, workspace, stream) ==
                  hipSuccess
              ? 0
              : -3;
+}
+
+// out: uint32[tiles * splits]; Wp: tiles * steps kilobytes; waves * unroll * splits >= steps.
+int prq_probe_stream_read(const uint8_t* Wp, int tiles, int steps, int splits, int waves,
+                          int unroll, uint32_t* out, hipStream_t stream) {
+  if (waves < 1 || waves > 16 || static_cast<int64_t>(waves) * unroll * splits < steps) return -1;
+  const dim3 grid(tiles, splits);
+  switch (unroll) {
+    case 1: stream_read_probe<1><<<grid, waves * 64, 0, stream>>>(Wp, steps, splits, out); break;
+    case 2: stream_read_probe<2><<<grid, waves * 64, 0, stream>>>(Wp, steps, splits, out); break;
+    case 4: stream_read_probe<4><<<grid, waves * 64, 0, stream>>>(Wp, steps, splits, out); break;
+    case 8: stream_read_probe<8><<<grid, waves * 64, 0, stream>>>(Wp, steps, splits, out); break;
+    default: return -1;
+  }
+  return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
 int prq_probe_empty(int blocks, int threads, hipStream_t stream) {

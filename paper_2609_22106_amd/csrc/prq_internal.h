@@ -18,6 +18,9 @@ struct StreamConfig {
   int unroll = 8;   // K steps per wave (1, 2, 3, 4, 6 or 8)
   int groups = 1;   // 16-row activation column groups per pass (1, 2 or 4)
   int tiles = 1;    // 16-feature tiles per workgroup (1 or 4; dense only)
+  bool stage_lds = true;  // activation staged in LDS per workgroup (else per-wave loads)
+  int reduce = 0;   // split-K: 0 atomic accumulator + last arriver, 1 partial sums +
+                    // reduce kernel (deterministic), 2 atomics into Y zeroed first
   bool ok = true;   // false: no configuration covers K_aug (use the tile kernel)
 };
 
@@ -45,7 +48,7 @@ hipError_t launch_gemm_stream(const uint8_t* Aq, const uint8_t* Asc, int M,
 
 // Workspace of the split-K stream kernel: a float accumulator [M][N] plus one
 // uint32 arrival counter per 16-feature output tile (per expert); zero between calls.
-size_t stream_workspace_bytes(int M, int E, int N, int splits);
+size_t stream_workspace_bytes(int M, int E, int N, int splits, int reduce);
 StreamConfig choose_stream_config(int M_per_group, int N, int K_aug, int grouped, int num_cus);
 bool stream_config_covers(const StreamConfig& c, int K_aug);
 int choose_variant(int M_per_group, int N, int K_aug);

@@ -43,7 +43,7 @@ def _decl(name, restype, argtypes):
 _strerror = _decl("prq_strerror", ctypes.c_char_p, [ctypes.c_int])
 _abi_version = _decl("prq_abi_version", ctypes.c_int, [])
 _prepare = _decl("prq_prepare", ctypes.c_int,
-                 [_p, _i32, _i32, _p, _i32, ctypes.c_double, _i32, _i32, _p, _p, _p, _p, _p, _p])
+                 [_p, _i32, _i32, _p, _i32, ctypes.c_double, _i32, _i32, _p, _p, _p, _p, _p, _p, _p])
 _quant_act = _decl("prq_quant_act", ctypes.c_int,
                    [_p, _i64, _i32, _i32, _i32, _p, _p, _p, _i32, _p, _p, _p])
 _packed_bytes = _decl("prq_packed_weight_bytes", ctypes.c_int,
@@ -113,14 +113,14 @@ def prq_prepare(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth", with_col_
     K_aug = K + int(k_tail)
     out = {
         "scale": np.empty(K, np.float32), "inv_scale": np.empty(K, np.float32),
-        "perm": np.empty(K, np.int32),
+        "perm": np.empty(K, np.int32), "inv_scale_pos": np.empty(K, np.float32),
         "Wq": np.empty((N, max(K_aug, 0) // 2), np.uint8),
         "Wsc": np.empty((N, max(K_aug, 0) // 32), np.uint8),
     }
     col_err = np.empty(K, np.float64) if with_col_err else None
     st = _prepare(_ptr(W), N, K, _ptr(X), T, float(alpha), int(k_tail), SCALE_MODES[scale_mode],
-                  _ptr(out["scale"]), _ptr(out["inv_scale"]), _ptr(out["perm"]), _ptr(out["Wq"]),
-                  _ptr(out["Wsc"]), _ptr(col_err))
+                  _ptr(out["scale"]), _ptr(out["inv_scale"]), _ptr(out["perm"]),
+                  _ptr(out["inv_scale_pos"]), _ptr(out["Wq"]), _ptr(out["Wsc"]), _ptr(col_err))
     _check(st, "prq_prepare")
     if with_col_err:
         out["col_err"] = col_err
@@ -128,9 +128,10 @@ def prq_prepare(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth", with_col_
 
 
 # ------------------------------------------------------------- device ops ---
-def prq_quant_act(X, K, k_tail, inv_scale=None, perm=None, group_offsets=None, G=1,
+def prq_quant_act(X, K, k_tail, inv_scale_pos=None, perm=None, group_offsets=None, G=1,
                   Aq=None, Asc=None, stream=None):
-    """Quantize bf16 activations X [M, ld] (device) -> (Aq [M, K_aug/2], Asc [M, K_aug/32])."""
+    """Quantize bf16 activations X [M, ld] (device) -> (Aq [M, K_aug/2], Asc [M, K_aug/32]).
+    inv_scale_pos[p] = 1/s_{perm[p]} (prq_prepare's ``inv_scale_pos``)."""
     M = X.shape[0]
     K_aug = K + k_tail
     if Aq is None:
@@ -138,7 +139,7 @@ def prq_quant_act(X, K, k_tail, inv_scale=None, perm=None, group_offsets=None, G
     if Asc is None:
         Asc = torch.empty((M, K_aug // 32), dtype=torch.uint8, device=X.device)
     ld = X.stride(0) if X.dim() == 2 else K
-    st = _quant_act(_ptr(X), ld, M, K, k_tail, _ptr(inv_scale), _ptr(perm), _ptr(group_offsets), G,
+    st = _quant_act(_ptr(X), ld, M, K, k_tail, _ptr(inv_scale_pos), _ptr(perm), _ptr(group_offsets), G,
                     _ptr(Aq), _ptr(Asc), _stream(stream))
     _check(st, "prq_quant_act")
     return Aq, Asc

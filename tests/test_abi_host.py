@@ -28,6 +28,7 @@ def _assert_prepare_equal(ours, ref):
     np.testing.assert_array_equal(ours["scale"], ref["scale"])
     np.testing.assert_array_equal(ours["inv_scale"], ref["inv_scale"])
     np.testing.assert_array_equal(ours["perm"], ref["perm"])
+    np.testing.assert_array_equal(ours["inv_scale_pos"], ref["inv_scale"][ref["perm"]])
     np.testing.assert_array_equal(ours["Wsc"], ref["Wsc"])
     np.testing.assert_array_equal(ours["Wq"], ref["Wq"])
     if "col_err" in ours:
@@ -101,7 +102,7 @@ def test_prepare_rejects_bad_arguments():
     with pytest.raises(prq.PRQError) as ei:
         prq.prq_prepare(c.W[:, :48], c.Xcal[:, :48], 0.5, 32)  # K % 32
     assert ei.value.status == prq.PRQ_EALIGN
-    st = prq._prepare(None, 16, 64, None, 4, 0.5, 32, 0, None, None, None, None, None, None)
+    st = prq._prepare(None, 16, 64, None, 4, 0.5, 32, 0, None, None, None, None, None, None, None)
     assert st == prq.PRQ_EINVAL
 
 

@@ -13,6 +13,13 @@ from tests.gpu_util import dev, host, say              # noqa: E402
 pytestmark = pytest.mark.gpu
 
 
+def _pos(inv, perm):
+    """Inverse scales in position order, inv_s[perm[p]] (per group when 2-D)."""
+    if perm is None:
+        return inv
+    return np.take_along_axis(np.asarray(inv), np.asarray(perm).astype(np.int64), axis=-1)
+
+
 def _gpu_quant(X_bits, K, k, inv=None, perm=None, offsets=None, G=1, ld=None):
     from paper_2609_22106_amd import prq
     M = X_bits.shape[0]
@@ -22,7 +29,7 @@ def _gpu_quant(X_bits, K, k, inv=None, perm=None, offsets=None, G=1, ld=None):
         Xd = dev(Xp)
     else:
         Xd = dev(X_bits)
-    Aq, Asc = prq.prq_quant_act(Xd, K, k, None if inv is None else dev(inv),
+    Aq, Asc = prq.prq_quant_act(Xd, K, k, None if inv is None else dev(_pos(inv, perm)),
                                 None if perm is None else dev(perm),
                                 None if offsets is None else dev(offsets), G)
     torch.cuda.synchronize()

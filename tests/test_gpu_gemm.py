@@ -48,14 +48,26 @@ def test_random_operands(M, N, K_aug, variant):
                       f"{variant} {M}x{N}x{K_aug}")
 
 
-@pytest.mark.parametrize("splits", [1, 2, 3, 7, 19])
-def test_stream_split_counts(splits):
+def test_stream_forced_split_that_cannot_stage_is_rejected():
+    """One split over 9984 K elements would stage 24 rows x 78 steps of
+    activation in LDS (about 174 KB): the call is refused, nothing launched."""
+    prq = _prq()
+    rng = np.random.default_rng(0)
+    Aq, Asc = inputs.random_mxfp4(rng, 24, 9984)
+    Wq, Wsc = inputs.random_mxfp4(rng, 320, 9984)
+    with pytest.raises(prq.PRQError) as ei:
+        _gpu_gemm(Aq, Asc, Wq, Wsc, prq.GEMM_STREAM, 1)
+    assert ei.value.status == prq.PRQ_EINVAL
+
+
+@pytest.mark.parametrize("M,splits", [(8, 1), (24, 0), (24, 2), (24, 3), (24, 7), (24, 19), (64, 6)])
+def test_stream_split_counts(M, splits):
     prq = _prq()
     rng = np.random.default_rng(splits)
-    M, N, K_aug = 24, 320, 9984
+    N, K_aug = 320, 9984
     Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
     Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
-    say("gemm case: stream splits", splits)
+    say("gemm case: stream M", M, "splits", splits)
     Y = _gpu_gemm(Aq, Asc, Wq, Wsc, prq.GEMM_STREAM, splits)
     assert_gemm_close(Y, pq.gemm(Aq, Asc, Wq, Wsc), f"splits={splits}")
 
@@ -66,18 +78,19 @@ def test_split_k_workspace_returns_to_zero_and_two_splits_are_deterministic():
     0 + a + b is order-independent, so the bits repeat exactly."""
     prq = _prq()
     rng = np.random.default_rng(3)
-    M, N, K_aug = 64, 2560, 9984
-    Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+    N, K_aug = 2560, 9984
     Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
-    ref = pq.gemm(Aq, Asc, Wq, Wsc)
-    for splits in (2, 4):
+    for M, splits in ((16, 2), (64, 6), (64, 8)):
         need = prq.prq_gemm_workspace_bytes(M, N, K_aug, prq.GEMM_STREAM, splits)
         ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
-        ys = [_gpu_gemm(Aq, Asc, Wq, Wsc, prq.GEMM_STREAM, splits, ws) for _ in range(3)]
-        for y in ys:
-            assert_gemm_close(y, ref, f"split {splits}")
-        assert int(torch.count_nonzero(ws)) == 0
+        ys = []
+        for call in range(3):   # new activations each call: stale partial sums would show
+            Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+            y = _gpu_gemm(Aq, Asc, Wq, Wsc, prq.GEMM_STREAM, splits, ws)
+            assert_gemm_close(y, pq.gemm(Aq, Asc, Wq, Wsc), f"M={M} split {splits} call {call}")
+            assert int(torch.count_nonzero(ws)) == 0
         if splits == 2:
+            ys = [_gpu_gemm(Aq, Asc, Wq, Wsc, prq.GEMM_STREAM, 2, ws) for _ in range(3)]
             np.testing.assert_array_equal(ys[0].view(np.uint32), ys[1].view(np.uint32))
             np.testing.assert_array_equal(ys[0].view(np.uint32), ys[2].view(np.uint32))
 
@@ -103,7 +116,7 @@ def test_down_proj_decode_end_to_end(c1_art, M):
     c, art = c1_art
     X = c.X[:M]
     say("gemm case: down_proj decode M =", M)
-    Aq, Asc = prq.prq_quant_act(dev(X), 9728, 256, dev(art["inv_scale"]), dev(art["perm"]))
+    Aq, Asc = prq.prq_quant_act(dev(X), 9728, 256, dev(art["inv_scale"][art["perm"]]), dev(art["perm"]))
     Y = prq.prq_gemm(Aq, Asc, _packed(art["Wq"], art["Wsc"]))
     torch.cuda.synchronize()
     rq, rs = pq.quant_act(X, art["inv_scale"], art["perm"], 256)
@@ -117,7 +130,7 @@ def test_down_proj_prefill_sampled_rows(c1_art, M):
     c = inputs.down_proj_prefill()
     X = c.X[:M]
     say("gemm case: down_proj prefill M =", M)
-    Aq, Asc = prq.prq_quant_act(dev(X), 9728, 256, dev(art["inv_scale"]), dev(art["perm"]))
+    Aq, Asc = prq.prq_quant_act(dev(X), 9728, 256, dev(art["inv_scale"][art["perm"]]), dev(art["perm"]))
     Y = host(prq.prq_gemm(Aq, Asc, _packed(art["Wq"], art["Wsc"])))
     torch.cuda.synchronize()
     rows = np.unique(np.concatenate([np.random.default_rng(M).choice(M, 48, replace=False),
@@ -190,7 +203,8 @@ def test_grouped_end_to_end_prepared_experts():
     Wsc = np.stack([a["Wsc"] for a in arts])
     off = c.group_offsets
     say("grouped case: end to end, counts", np.diff(off).tolist())
-    Aq, Asc = prq.prq_quant_act(dev(c.X), 768, 64, dev(inv), dev(perm), dev(off), 8)
+    inv_pos = np.take_along_axis(inv, perm.astype(np.int64), axis=1)
+    Aq, Asc = prq.prq_quant_act(dev(c.X), 768, 64, dev(inv_pos), dev(perm), dev(off), 8)
     for v in (prq.GEMM_TILE, prq.GEMM_STREAM):
         Y = prq.prq_grouped_gemm(Aq, Asc, dev(off), _packed(Wq, Wsc), variant=v)
         torch.cuda.synchronize()
