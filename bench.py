@@ -54,6 +54,11 @@ def parse_args(argv=None):
                    help="minimum total bytes of rotated weight copies")
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run a plain device copy of known size (for counter scaling)")
+    p.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                   help="no run: turn two rocprofv3 --pmc output directories (FETCH_SIZE, "
+                        "WRITE_SIZE) into profiles/traffic_<workload>.json")
+    p.add_argument("--traffic-command", default="",
+                   help="the profiled command, recorded with --traffic-from")
     return p.parse_args(argv)
 
 
@@ -251,30 +256,92 @@ def cpu_baseline(np, layers, M_list, budget_s=12.0):
                       f"{len(os.sched_getaffinity(0))}, BLAS threads {threads}"}
 
 
-def copy_calibration(torch, nbytes=512 * 2 ** 20, reps=5):
-    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+CALIB_BYTES = 512 * 2 ** 20
+GEMM_SOURCES = ("gemm_stream.hip", "gemm_tile.hip", "mx_device.hpp", "prq_internal.h", "abi.cpp")
+
+
+def copy_calibration(torch, nbytes=CALIB_BYTES, reps=5):
+    """A plain streaming kernel of known traffic (reads and writes `nbytes`),
+    for scaling the HBM counters: torch.neg over float32."""
+    a = torch.zeros(nbytes // 4, dtype=torch.float32, device="cuda")
     b = torch.empty_like(a)
-    for _ in range(reps):
-        b.copy_(a)
     torch.cuda.synchronize()
-    log(f"[bench] copy calibration: {reps} copies of {nbytes} bytes")
+    for _ in range(reps):
+        torch.neg(a, out=b)
+    torch.cuda.synchronize()
+    log(f"[bench] copy calibration: {reps} x neg over {nbytes} bytes")
+
+
+def gemm_source_hash():
+    h = hashlib.sha256()
+    for name in GEMM_SOURCES:
+        h.update(open(os.path.join(ROOT, "paper_2609_22106_amd", "csrc", name), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def traffic_record(workload):
     """HBM bytes per GEMM launch from committed counter runs, or None when the
-    kernel source changed since they were taken."""
+    GEMM sources changed since they were taken."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    src = os.path.join(ROOT, "paper_2609_22106_amd", "csrc", "gemm.hip")
-    h = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    return rec.get("bytes_per_launch") if rec.get("gemm_hip_sha256_16") == h else None
+    return rec.get("bytes_per_launch") if rec.get("gemm_src_sha256_16") == gemm_source_hash() else None
+
+
+def _counter_rows(run_dir, counter):
+    """(dispatch id, kernel name, value) of `counter` from a rocprofv3 --pmc
+    CSV output directory."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no *counter_collection.csv under {run_dir}")
+    per = {}
+    for f in files:
+        for r in csv.DictReader(open(f)):
+            if r.get("Counter_Name") != counter:
+                continue
+            key = (f, r["Dispatch_Id"])
+            name, v = per.get(key, (r["Kernel_Name"], 0.0))
+            per[key] = (name, v + float(r["Counter_Value"]))
+    return list(per.values())
+
+
+def traffic_from_counters(workload, fetch_dir, write_dir, command):
+    """Write profiles/traffic_<workload>.json from a FETCH_SIZE run and a
+    WRITE_SIZE run of `bench.py --copy-calibration` (KiB per dispatch), each
+    scaled by what the same counter reads for the calibration kernel."""
+    out = {"workload": workload, "command": command, "calibration_bytes": CALIB_BYTES}
+    total = 0.0
+    for counter, run_dir in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = _counter_rows(run_dir, counter)
+        calib = [v for n, v in rows if "neg_kernel" in n]
+        gemm = [(n, v) for n, v in rows if "prq" in n and any(
+            t in n for t in ("gemm_stream_kernel", "gemm_tile_kernel", "reduce_partials_kernel", "zero_kernel"))]
+        launches = [v for n, v in gemm if "gemm_" in n]
+        if not calib or not launches:
+            raise SystemExit(f"{counter}: calibration or GEMM dispatches missing in {run_dir}")
+        scale = CALIB_BYTES / (sorted(calib)[len(calib) // 2] * 1024.0)
+        per_launch = sum(v for _, v in gemm) * 1024.0 * scale / len(launches)
+        out[counter] = {"calibration_kib_median": sorted(calib)[len(calib) // 2], "scale": scale,
+                        "gemm_dispatches": len(launches), "helper_dispatches": len(gemm) - len(launches),
+                        "bytes_per_launch": per_launch}
+        total += per_launch
+    out["bytes_per_launch"] = round(total, 1)
+    out["gemm_src_sha256_16"] = gemm_source_hash()
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out))
+    return 0
 
 
 # ---------------------------------------------------------------- main ---
 def main(argv=None):
     args = parse_args(argv)
+    if args.traffic_from:
+        return traffic_from_counters(args.workload, *args.traffic_from, args.traffic_command)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU "
               "sharding of this path is described in DESIGN.md and not built.", file=sys.stderr)

@@ -167,10 +167,13 @@ int prq_pack_weight(const uint8_t* Wq, const uint8_t* Wsc, int32_t E, int32_t N,
  *   Wp, Wps: the weight in the packed layout above (E = 1), from
  *            prq_pack_weight of prq_prepare's Wq / Wsc
  *   workspace: device buffer of at least prq_gemm_workspace_bytes(M, N, K_aug)
- *   bytes (may be NULL when that is 0): a float accumulator [M][N] and one
- *   arrival counter per output tile for split-K.  It must be zero-filled once
- *   before its first use; every call leaves it zero-filled again.  Calls that
- *   share one workspace must be ordered (same stream).
+ *   bytes (may be NULL when that is 0) for split-K: either a float
+ *   accumulator [M][N] plus one arrival counter per output tile, which every
+ *   call leaves zero-filled again (atomic mode, up to 32 rows), or partial
+ *   sums [splits][M][N] that are rewritten before being read and added in a
+ *   fixed order (deterministic mode, more rows).  It must be zero-filled once
+ *   before its first use.  Calls that share one workspace must be ordered
+ *   (same stream).
  * Limits: N % 16 == 0, K_aug <= 65536.  M == 0 is a no-op.
  */
 size_t prq_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K_aug);

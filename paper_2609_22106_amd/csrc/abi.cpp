@@ -143,8 +143,10 @@ prq::StreamConfig dense_stream_config(int M, int N, int K_aug, int splits_req, i
     c.splits = splits_req;
     static const int kU[] = {1, 2, 3, 4, 6, 8};
     c.ok = false;
-    for (int tiles : {c.tiles, 1}) {   // keep the tile grouping if it still covers K_aug
-      c.tiles = tiles;
+    const prq::StreamConfig base = c;
+    for (int cand = 0; cand < 4 && !c.ok; ++cand) {  // keep the shape if it still covers K_aug
+      c.tiles = (cand & 1) ? 1 : base.tiles;
+      c.waves = (cand & 2) ? 16 : base.waves;
       const int chunks = c.waves / c.tiles;
       const int need = ((steps + c.splits - 1) / c.splits + chunks - 1) / chunks;
       c.unroll = 0;
@@ -153,10 +155,7 @@ prq::StreamConfig dense_stream_config(int M, int N, int K_aug, int splits_req, i
           c.unroll = x;
           break;
         }
-      if (c.unroll > 0 && splits_req <= steps && prq::stream_config_covers(c, K_aug)) {
-        c.ok = true;
-        break;
-      }
+      c.ok = c.unroll > 0 && splits_req <= steps && prq::stream_config_covers(c, K_aug);
     }
   }
   return c;
@@ -208,7 +207,8 @@ int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t*
                                                    workspace, stream));
     }
   }
-  return launch_status(prq::launch_gemm_tile(Aq, Asc, M, nullptr, 1, Wp, Wps, N, K_aug, Y, stream));
+  return launch_status(prq::launch_gemm_tile(Aq, Asc, M, nullptr, 1, Wp, Wps, N, K_aug, Y,
+                                             prq::choose_tile_shape(M, N, dev.num_cus), stream));
 }
 
 int prq_gemm(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t* Wp,
@@ -249,8 +249,10 @@ int prq_grouped_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, const int32_t* gr
       return launch_status(prq::launch_gemm_stream(Aq, Asc, M_total, group_offsets, E, Wp, Wps, N,
                                                    K_aug, Y, c, nullptr, stream));
   }
-  return launch_status(
-      prq::launch_gemm_tile(Aq, Asc, M_total, group_offsets, E, Wp, Wps, N, K_aug, Y, stream));
+  // Row tiles are per expert: pick the shape from the mean rows per expert.
+  const int shape = per_group >= 256 ? 1 : 2;
+  return launch_status(prq::launch_gemm_tile(Aq, Asc, M_total, group_offsets, E, Wp, Wps, N, K_aug,
+                                             Y, shape, stream));
 }
 
 int prq_grouped_gemm(const uint8_t* Aq, const uint8_t* Asc, const int32_t* group_offsets, int32_t E,

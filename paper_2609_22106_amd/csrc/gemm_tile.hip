@@ -1,23 +1,33 @@
-// The augmented MXFP4 GEMM of arXiv 2609.22106 (Eq. 3): one block-scaled GEMM
-// whose reduction runs over K_aug = K + k (main channels, then the k tail
-// channels whose activation blocks were copied and whose weight side holds the
-// MXFP4 residual of Eq. 2):
+// LDS-tiled kernel of the augmented MXFP4 GEMM (arXiv 2609.22106, Eq. 3: one
+// block-scaled GEMM over K_aug = K + k) for prefill shapes, with a grouped
+// (MoE expert) mode in which rows [off[e], off[e+1]) multiply expert e's weight.
 //
 //   Y[m, n] = sum_b 2^(Asc[m,b]-127) 2^(Wsc[n,b]-127) sum_{i<32} A[m,32b+i] W[n,32b+i]
 //
-// computed on gfx950's v_mfma_scale_f32_16x16x128_f8f6f4 with FP4 operands and
-// E8M0 scales fed straight into the instruction, float32 accumulation.
+// on v_mfma_scale_f32_16x16x128_f8f6f4 (FP4 operands, E8M0 scales in the
+// instruction, float32 accumulation).
 //
-// This file: the LDS-tiled kernel for prefill shapes (the weight-streaming
-// decode kernel is in gemm_stream.hip), with a grouped (MoE expert) mode in
-// which rows [off[e], off[e+1]) multiply expert e's weight.  The weight comes
-// in the packed layout of pack.hip (contiguous kilobyte per 16-row K step).  128x128 output
-// tile per 256-thread workgroup, A/B/scale tiles staged in LDS (rows padded to
-// 80 bytes so the 16-byte lane reads of one MFMA operand hit distinct banks),
-// 4 waves of 64x64 (4x4 MFMA tiles each).
+// A workgroup computes a kBM x kBN tile with kWM x kWN waves (wave tile
+// kBM/kWM x kBN/kWN).  Per 128-element K step both operands are staged in LDS
+// in MFMA lane order -- for each 16-row block, 64 lanes x 16 bytes, lane l
+// holding row l % 16, K part l / 16 -- so that every operand read of a wave is
+// one contiguous kilobyte (conflict-free 16-byte lane reads).  The weight comes
+// in that order already (packed layout, pack.hip) and is copied verbatim; the
+// activation rows are transposed into it on the store.  Scales are staged the
+// same way, one scale byte per lane in a dword slot.  Pipeline: kNS LDS
+// stages filled by direct global->LDS loads (global_load_lds: one wave
+// instruction writes one lane-ordered kilobyte), kNS - 1 K steps in flight; per
+// step each wave waits for its own loads of that step with an explicit vmcnt,
+// one bare barrier, the next step's loads are issued into the stage just
+// freed, then the MFMAs.  Source addresses are always valid (clamped rows and
+// tiles; K parts past K_aug point at the row start and meet zero weight codes).
+// Workgroup ids are remapped so that each XCD (ids are dealt to the 8 XCDs in
+// turn) works on a contiguous band of row tiles and its L2 serves their
+// activation rows to every feature tile.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "mx_device.hpp"
 #include "prq.h"
@@ -28,30 +38,31 @@ namespace {
 
 using dev::v4f;
 
-constexpr int kTileM = 128, kTileN = 128;
-constexpr int kStepK = 128;           // elements per K step = 64 bytes per row
+constexpr int kStepK = 128;
 constexpr int kStepBytes = kStepK / 2;
-constexpr int kLdsRow = kStepBytes + 16;  // padded LDS row (bytes)
-constexpr int kTileThreads = 256;
-constexpr uint8_t kNeutralScale = 127;   // scale paired with zero codes past K_aug
+constexpr uint32_t kNeutralScale = 127;
+constexpr int kXcds = 8;
 
-__device__ __forceinline__ uint4 load16_or_zero(const uint8_t* p, bool ok) {
-  return ok ? *reinterpret_cast<const uint4*>(p) : make_uint4(0, 0, 0, 0);
+// Bijective remap of a linear workgroup id: ids dealt round-robin to kXcds
+// XCDs become contiguous ranges per XCD.
+__device__ __forceinline__ int xcd_remap(int L, int total) {
+  const int q = total / kXcds, r = total % kXcds;
+  const int x = L % kXcds, i = L / kXcds;
+  return x * q + min(x, r) + i;
 }
 
-// Row range [row_begin, row_end) and expert of row tile `mt` in the grouped
-// layout, where tiles of `tile_rows` rows are numbered expert after expert.
-// All threads of the (256-thread) workgroup call it; the per-expert tile
-// counts are prefix-summed 256 experts at a time in LDS.  Returns false for
-// an index beyond the last expert's last tile.
+// Row range and expert of row tile `mt` when tiles of `tile_rows` rows are
+// numbered expert after expert (prefix scan of per-expert tile counts over
+// the workgroup's threads, `nthreads` at a time).
+template <int kThreads>
 __device__ bool grouped_tile(const int32_t* __restrict__ off, int E, int M, int mt, int tile_rows,
                              int* e_out, int* row_begin, int* row_end) {
-  __shared__ int s_scan[kTileThreads];
+  __shared__ int s_scan[kThreads];
   __shared__ int s_hit[3];
   const int tid = threadIdx.x;
   if (tid == 0) s_hit[0] = -1;
   int base = 0;
-  for (int e0 = 0; e0 < E; e0 += kTileThreads) {
+  for (int e0 = 0; e0 < E; e0 += kThreads) {
     const int e = e0 + tid;
     int r0 = 0, r1 = 0, t = 0;
     if (e < E) {  // offsets clamped to [0, M]: malformed offsets cannot address past A
@@ -61,7 +72,7 @@ __device__ bool grouped_tile(const int32_t* __restrict__ off, int E, int M, int 
     }
     s_scan[tid] = t;
     __syncthreads();
-    for (int d = 1; d < kTileThreads; d <<= 1) {  // inclusive Hillis-Steele scan
+    for (int d = 1; d < kThreads; d <<= 1) {  // inclusive Hillis-Steele scan
       const int v = tid >= d ? s_scan[tid - d] : 0;
       __syncthreads();
       s_scan[tid] += v;
@@ -74,7 +85,7 @@ __device__ bool grouped_tile(const int32_t* __restrict__ off, int E, int M, int 
       s_hit[1] = r0 + (mt - excl) * tile_rows;
       s_hit[2] = min(r1, s_hit[1] + tile_rows);
     }
-    base += s_scan[kTileThreads - 1];
+    base += s_scan[kThreads - 1];
     __syncthreads();
   }
   if (s_hit[0] < 0) return false;
@@ -84,132 +95,255 @@ __device__ bool grouped_tile(const int32_t* __restrict__ off, int E, int M, int 
   return true;
 }
 
-template <bool kGrouped>
-__global__ __launch_bounds__(kTileThreads) void gemm_tile_kernel(
+template <int v>
+struct IntC {
+  static constexpr int value = v;
+};
+
+template <int n, class F, int i = 0>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (i < n) {
+    f(IntC<i>{});
+    static_for<n, F, i + 1>(static_cast<F&&>(f));
+  }
+}
+
+#define PRQ_GPTR(p) ((const __attribute__((address_space(1))) void*)(p))
+#define PRQ_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
+
+// s_waitcnt immediate that waits until at most n vector-memory operations of
+// this wave are outstanding (expcnt and lgkmcnt left at their maxima).
+template <int n>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(n >= 0 && n < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+template <int kBM, int kBN, int kWM, int kWN, int kNS, bool kGrouped>
+__global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
     const uint8_t* __restrict__ Aq, const uint8_t* __restrict__ Asc, int M,
-    const int32_t* __restrict__ off, int E, const uint8_t* __restrict__ Wp,
+    const int32_t* __restrict__ off, int E, int n_mtiles, const uint8_t* __restrict__ Wp,
     const uint8_t* __restrict__ Wps, int N, int K_aug, float* __restrict__ Y) {
-  __shared__ __align__(16) uint8_t sA[kTileM * kLdsRow];
-  __shared__ __align__(16) uint8_t sB[kTileN * kLdsRow];
-  __shared__ uint8_t sAs[kTileM * 4];
-  __shared__ uint8_t sBs[kTileN * 4];
+  constexpr int kWaves = kWM * kWN;
+  constexpr int kThreads = kWaves * 64;
+  constexpr int kTM = kBM / kWM, kTN = kBN / kWN;    // wave tile
+  constexpr int kFM = kTM / 16, kFN = kTN / 16;      // 16x16 fragments per wave
+  constexpr int kABlk = kBM / 16, kBBlk = kBN / 16;  // 16-row operand blocks per step
+  static_assert(kABlk % kWaves == 0 && kBBlk % kWaves == 0, "blocks split evenly over waves");
+  constexpr int kAPer = kABlk / kWaves, kBPer = kBBlk / kWaves;
+  constexpr int kLoads = 2 * (kAPer + kBPer);        // direct-to-LDS loads per wave per step
+  // Stage layout: A codes [kABlk][1 KiB] | B codes [kBBlk][1 KiB] | A scales
+  // [kABlk][64 dwords] | B scales [kBBlk][64 dwords]; lane order everywhere.
+  constexpr int kOffB = kABlk * 1024;
+  constexpr int kOffAs = (kABlk + kBBlk) * 1024;
+  constexpr int kOffBs = kOffAs + kABlk * 256;
+  constexpr int kStage = (kABlk + kBBlk) * 1280;
+  static_assert(kNS >= 2 && kNS <= 6, "stages");
+  // One LDS object per stage: the compiler then knows which stage an
+  // in-flight direct-to-LDS load writes and does not make LDS reads of the
+  // other stages wait for it.
+  __shared__ __align__(16) uint8_t st0[kStage];
+  __shared__ __align__(16) uint8_t st1[kStage];
+  __shared__ __align__(16) uint8_t st2[kNS > 2 ? kStage : 16];
+  __shared__ __align__(16) uint8_t st3[kNS > 3 ? kStage : 16];
+  __shared__ __align__(16) uint8_t st4[kNS > 4 ? kStage : 16];
+  __shared__ __align__(16) uint8_t st5[kNS > 5 ? kStage : 16];
+  auto stage = [&](auto pc) -> uint8_t* {
+    constexpr int p = decltype(pc)::value;
+    if constexpr (p == 0) return st0;
+    else if constexpr (p == 1) return st1;
+    else if constexpr (p == 2) return st2;
+    else if constexpr (p == 3) return st3;
+    else if constexpr (p == 4) return st4;
+    else return st5;
+  };
+
+  const int ntiles = N >> 4;
+  const int n_ntiles = (N + kBN - 1) / kBN;
+  const int total = n_mtiles * n_ntiles;
+  const int logical = xcd_remap(blockIdx.x, total);
+  const int mt = logical / n_ntiles, nt = logical % n_ntiles;
 
   int e = 0, row_begin, row_end;
-  const int n0 = blockIdx.x * kTileN;
   if (kGrouped) {
-    if (!grouped_tile(off, E, M, blockIdx.y, kTileM, &e, &row_begin, &row_end)) return;
+    if (!grouped_tile<kThreads>(off, E, M, mt, kBM, &e, &row_begin, &row_end)) return;
   } else {
-    row_begin = blockIdx.y * kTileM;
-    row_end = min(M, row_begin + kTileM);
+    row_begin = mt * kBM;
+    row_end = min(M, row_begin + kBM);
   }
+  const int t0 = nt * kBBlk;                         // first 16-feature tile
   const int64_t row_bytes = K_aug >> 1;
   const int nb = K_aug >> 5;
   const int steps = (K_aug + kStepK - 1) / kStepK;
   const int sgroups = (steps + 3) >> 2;
-  const int ntiles = N >> 4;
-  const int t0 = n0 >> 4;   // first 16-feature tile of this workgroup
-  const uint8_t* We = Wp + (static_cast<int64_t>(e) * ntiles + t0) * steps * 1024;
-  const uint32_t* Wse =
-      reinterpret_cast<const uint32_t*>(Wps) + (static_cast<int64_t>(e) * ntiles + t0) * sgroups * 64;
+  const uint8_t* We = Wp + static_cast<int64_t>(e) * ntiles * steps * 1024;
+  const uint8_t* Wse = Wps + static_cast<int64_t>(e) * ntiles * sgroups * 256;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / kWN, wn = wave % kWN;
   const int lr = lane & 15, lk = lane >> 4;
 
-  v4f acc[4][4];
+  // Per-lane source rows / tiles of this wave's loads (fixed over the K loop).
+  const uint8_t* a_row[kAPer];
+  const uint8_t* as_row[kAPer];
+  const uint8_t* b_tile[kBPer];
+  const uint8_t* bs_tile[kBPer];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < kAPer; ++i) {
+    const int rb = wave + i * kWaves;
+    const int m = min(row_begin + rb * 16 + lr, row_end - 1);
+    a_row[i] = Aq + m * row_bytes;
+    as_row[i] = Asc + static_cast<int64_t>(m) * nb;
+  }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
-
-  for (int s = 0; s < steps; ++s) {
-    // Stage A and B: 128 rows x 64 bytes each = 512 16-byte chunks per operand.
-#pragma unroll
-    for (int c = tid; c < kTileM * 4; c += kTileThreads) {
-      const int r = c >> 2, part = c & 3;
-      const bool kok = s * kStepK + part * 32 < K_aug;
-      const int m = row_begin + r;
-      const uint4 va = load16_or_zero(Aq + m * row_bytes + s * kStepBytes + part * 16,
-                                      kok && m < row_end);
-      *reinterpret_cast<uint4*>(&sA[r * kLdsRow + part * 16]) = va;
-    }
-    // B from the packed weight: chunk c = (tile nt, lane l) is the 16 bytes of
-    // row 16 nt + l % 16, K part l / 16 of this step (zero past K_aug).
-#pragma unroll
-    for (int c = tid; c < kTileN * 4; c += kTileThreads) {
-      const int nt = c >> 6, l = c & 63;
-      const int r = nt * 16 + (l & 15), part = l >> 4;
-      const uint4 vb = load16_or_zero(We + (static_cast<int64_t>(nt) * steps + s) * 1024 + l * 16,
-                                      t0 + nt < ntiles);
-      *reinterpret_cast<uint4*>(&sB[r * kLdsRow + part * 16]) = vb;
-    }
-    // Scales: 4 blocks per row per step; packed weight scales hold byte s % 4
-    // of lane (b * 16 + r % 16)'s dword in group s / 4.
-    for (int c = tid; c < kTileM * 4; c += kTileThreads) {
-      const int r = c >> 2, b = c & 3;
-      const int blk = s * 4 + b;
-      const int m = row_begin + r;
-      sAs[c] = (blk < nb && m < row_end) ? Asc[static_cast<int64_t>(m) * nb + blk] : kNeutralScale;
-      const int nt = c >> 6, l = c & 63;
-      const int rb = nt * 16 + (l & 15), bb = l >> 4;
-      sBs[rb * 4 + bb] = t0 + nt < ntiles
-          ? static_cast<uint8_t>(Wse[(static_cast<int64_t>(nt) * sgroups + (s >> 2)) * 64 + l] >> (8 * (s & 3)))
-          : kNeutralScale;
-    }
-    __syncthreads();
-
-    uint4 a[4], b[4];
-    uint32_t sa[4], sb[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = wm * 64 + i * 16 + lr;
-      a[i] = *reinterpret_cast<const uint4*>(&sA[r * kLdsRow + lk * 16]);
-      sa[i] = sAs[r * 4 + lk];
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = wn * 64 + j * 16 + lr;
-      b[j] = *reinterpret_cast<const uint4*>(&sB[r * kLdsRow + lk * 16]);
-      sb[j] = sBs[r * 4 + lk];
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = dev::mfma_fp4_16x16x128(a[i], b[j], sa[i], sb[j], acc[i][j]);
-    __syncthreads();
+  for (int i = 0; i < kBPer; ++i) {
+    const int t = min(t0 + wave + i * kWaves, ntiles - 1);
+    b_tile[i] = We + static_cast<int64_t>(t) * steps * 1024 + lane * 16;
+    bs_tile[i] = Wse + static_cast<int64_t>(t) * sgroups * 256 + lane * 4;
   }
 
-  // Lane holds C[4*lk + q][lr] of each 16x16 tile.
+  // Step s into stage `st`: every source address is valid (parts past K_aug
+  // point at the row start: they meet zero weight codes with finite scales).
+  auto issue = [&](int s, uint8_t* st) {
+    const bool kok = s * kStepK + lk * 32 < K_aug;
+    const int64_t abyte = kok ? static_cast<int64_t>(s) * kStepBytes + lk * 16 : 0;
+    const int sbyte = kok ? s * 4 + lk : 0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < kAPer; ++i)
+      __builtin_amdgcn_global_load_lds(PRQ_GPTR(a_row[i] + abyte),
+                                       PRQ_LPTR(st + (wave + i * kWaves) * 1024), 16, 0, 0);
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int i = 0; i < kBPer; ++i)
+      __builtin_amdgcn_global_load_lds(PRQ_GPTR(b_tile[i] + static_cast<int64_t>(s) * 1024),
+                                       PRQ_LPTR(st + kOffB + (wave + i * kWaves) * 1024), 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < kAPer; ++i)
+      __builtin_amdgcn_global_load_lds(PRQ_GPTR(as_row[i] + sbyte),
+                                       PRQ_LPTR(st + kOffAs + (wave + i * kWaves) * 256), 1, 0, 0);
+#pragma unroll
+    for (int i = 0; i < kBPer; ++i)
+      __builtin_amdgcn_global_load_lds(PRQ_GPTR(bs_tile[i] + (s >> 2) * 256 + (s & 3)),
+                                       PRQ_LPTR(st + kOffBs + (wave + i * kWaves) * 256), 1, 0, 0);
+  };
+
+  v4f acc[kFM][kFN];
+#pragma unroll
+  for (int i = 0; i < kFM; ++i)
+#pragma unroll
+    for (int j = 0; j < kFN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+
+  auto compute = [&](const uint8_t* st) {
+    uint4 a[kFM], b[kFN];
+    uint32_t sa[kFM], sb[kFN];
+#pragma unroll
+    for (int i = 0; i < kFM; ++i) {
+      const int blk = wm * kFM + i;
+      a[i] = *reinterpret_cast<const uint4*>(st + blk * 1024 + lane * 16);
+      sa[i] = *reinterpret_cast<const uint32_t*>(st + kOffAs + blk * 256 + lane * 4);
+    }
+#pragma unroll
+    for (int j = 0; j < kFN; ++j) {
+      const int blk = wn * kFN + j;
+      b[j] = *reinterpret_cast<const uint4*>(st + kOffB + blk * 1024 + lane * 16);
+      sb[j] = *reinterpret_cast<const uint32_t*>(st + kOffBs + blk * 256 + lane * 4);
+    }
+#pragma unroll
+    for (int i = 0; i < kFM; ++i)
+#pragma unroll
+      for (int j = 0; j < kFN; ++j)
+        acc[i][j] = dev::mfma_fp4_16x16x128(a[i], b[j], sa[i], sb[j], acc[i][j]);
+  };
+
+  // Prologue: steps 0 .. kNS-2 in flight.  Every wave issues the same
+  // sequence on every path: steps past the end reload the last step into a
+  // stage that is never read, and the wait, barrier and issue of a stage run
+  // even when its step is past the end (only its MFMAs are skipped).  Then
+  // exactly kNS - 2 later steps are in flight at every wait, one constant
+  // vmcnt serves every step, and the compiler sees that the stage about to be
+  // read has landed (a wait count chosen at run time, or a stage skipped as a
+  // whole, leaves it a path that makes it drain all loads first).
+  static_for<kNS - 1>([&](auto pc) {
+    issue(min(static_cast<int>(decltype(pc)::value), steps - 1), stage(pc));
+  });
+  // Main loop, unrolled by kNS so every stage is a known LDS object.
+  for (int s0 = 0; s0 < steps; s0 += kNS) {
+    static_for<kNS>([&](auto pc) {
+      constexpr int p = decltype(pc)::value;
+      const int s = s0 + p;
+      // This wave's loads of step s have landed; the bare barrier then says
+      // the same of every wave, and that every wave is done reading the stage
+      // the next issue overwrites.
+      wait_vmcnt<(kNS - 2) * kLoads>();
+      __builtin_amdgcn_s_barrier();
+      issue(min(s + kNS - 1, steps - 1), stage(IntC<(p + kNS - 1) % kNS>{}));
+      if (s < steps) compute(stage(pc));
+    });
+  }
+  wait_vmcnt<0>();   // no direct-to-LDS write outlives the workgroup
+
+  // Lane holds C[4 (l / 16) + q][l % 16] of each 16x16 fragment.
+#pragma unroll
+  for (int i = 0; i < kFM; ++i)
+#pragma unroll
+    for (int j = 0; j < kFN; ++j) {
+      const int n = (t0 + wn * kFN + j) * 16 + lr;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int m = row_begin + wm * 64 + i * 16 + 4 * lk + q;
-        const int n = n0 + wn * 64 + j * 16 + lr;
+        const int m = row_begin + wm * kTM + i * 16 + 4 * lk + q;
         if (m < row_end && n < N) Y[static_cast<int64_t>(m) * N + n] = acc[i][j][q];
       }
+    }
+}
+
+template <int kBM, int kBN, int kWM, int kWN, int kNS>
+hipError_t launch_shape(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off, int E,
+                        const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug, float* Y,
+                        hipStream_t stream) {
+  const int n_ntiles = (N + kBN - 1) / kBN;
+  // Grouped: an upper bound on the row tiles over all experts (extra ids exit).
+  const int n_mtiles = off ? (M + kBM - 1) / kBM + E : (M + kBM - 1) / kBM;
+  const int grid = n_mtiles * n_ntiles;
+  if (off)
+    gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, true><<<grid, kWM * kWN * 64, 0, stream>>>(
+        Aq, Asc, M, off, E, n_mtiles, Wp, Wps, N, K_aug, Y);
+  else
+    gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, false><<<grid, kWM * kWN * 64, 0, stream>>>(
+        Aq, Asc, M, nullptr, 1, n_mtiles, Wp, Wps, N, K_aug, Y);
+  return hipGetLastError();
 }
 
 }  // namespace
 
+int choose_tile_shape(int M_rows, int N, int num_cus) {
+  // Estimated cost ~ rounds of workgroups over the CUs x per-tile time; the
+  // per-shape factors are measured throughputs per tile area relative to
+  // 256 x 256 (smaller tiles move more bytes per MFMA).
+  struct Shape { int id, bm, bn; double eff; };
+  const Shape shapes[] = {{0, 256, 256, 1.0}, {1, 256, 128, 0.6}, {2, 128, 128, 0.55}};
+  int best = 2;
+  double best_cost = 1e300;
+  for (const Shape& s : shapes) {
+    const int tiles = ((M_rows + s.bm - 1) / s.bm) * ((N + s.bn - 1) / s.bn);
+    const int rounds = (tiles + num_cus - 1) / num_cus;
+    const double cost = rounds * static_cast<double>(s.bm) * s.bn / s.eff;
+    if (cost < best_cost) {
+      best_cost = cost;
+      best = s.id;
+    }
+  }
+  return best;
+}
+
 hipError_t launch_gemm_tile(const uint8_t* Aq, const uint8_t* Asc, int M,
                             const int32_t* group_offsets, int E, const uint8_t* Wp,
-                            const uint8_t* Wps, int N, int K_aug, float* Y, hipStream_t stream) {
-  const int nt = (N + kTileN - 1) / kTileN;
-  if (group_offsets) {
-    // Upper bound on the number of row tiles over all experts.
-    const int mt = (M + kTileM - 1) / kTileM + E;
-    gemm_tile_kernel<true><<<dim3(nt, mt), kTileThreads, 0, stream>>>(Aq, Asc, M, group_offsets, E,
-                                                                    Wp, Wps, N, K_aug, Y);
-  } else {
-    const int mt = (M + kTileM - 1) / kTileM;
-    gemm_tile_kernel<false><<<dim3(nt, mt), kTileThreads, 0, stream>>>(Aq, Asc, M, nullptr, 1, Wp,
-                                                                     Wps, N, K_aug, Y);
+                            const uint8_t* Wps, int N, int K_aug, float* Y, int shape,
+                            hipStream_t stream) {
+  switch (shape) {
+    case 0: return launch_shape<256, 256, 2, 4, 3>(Aq, Asc, M, group_offsets, E, Wp, Wps, N, K_aug, Y, stream);
+    case 1: return launch_shape<256, 128, 2, 2, 4>(Aq, Asc, M, group_offsets, E, Wp, Wps, N, K_aug, Y, stream);
+    default: return launch_shape<128, 128, 2, 2, 6>(Aq, Asc, M, group_offsets, E, Wp, Wps, N, K_aug, Y, stream);
   }
-  return hipGetLastError();
 }
 
 }  // namespace prq

@@ -56,6 +56,24 @@ __global__ void cvt_pairs(const float* x, const float* y, const float* s, int n,
 
 __global__ void empty_kernel() {}
 
+// Direct global->LDS loads (one wave): 16 bytes per lane from g16 into LDS at
+// byte 0, one byte per lane from g1 into LDS at byte 4096; the 8 KiB LDS image
+// (zeroed first) is copied out so the host can see where each lane's data went.
+__global__ __launch_bounds__(64) void lds_dma_probe(const uint8_t* g16, const uint8_t* g1,
+                                                    uint8_t* out) {
+  __shared__ __align__(16) uint8_t s[8192];
+  const int l = threadIdx.x;
+  for (int i = l; i < 8192 / 16; i += 64) reinterpret_cast<uint4*>(s)[i] = make_uint4(0, 0, 0, 0);
+  __syncthreads();
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(g16 + l * 16),
+                                   (__attribute__((address_space(3))) void*)(s), 16, 0, 0);
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(g1 + l),
+                                   (__attribute__((address_space(3))) void*)(s + 4096), 1, 0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  for (int i = l; i < 8192 / 16; i += 64) reinterpret_cast<uint4*>(out)[i] = reinterpret_cast<uint4*>(s)[i];
+}
+
 // Reads the packed weight with the stream GEMM's grid mapping (tile per
 // blockIdx.x, split per blockIdx.y, kU contiguous kilobytes per wave) and
 // writes one dword per workgroup: the memory side of that kernel alone.
@@ -146,6 +164,22 @@ int prq_probe_stream_read(const uint8_t* Wp, int tiles, int steps, int splits, i
     case 8: stream_read_probe<8><<<grid, waves * 64, 0, stream>>>(Wp, steps, splits, out); break;
     default: return -1;
   }
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+// Tuning entry: the tile GEMM with an explicit tile shape (0, 1 or 2).
+int prq_tune_gemm_tile(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off, int E,
+                       const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug, float* Y, int shape,
+                       hipStream_t stream) {
+  if (shape < 0 || shape > 2 || N % 16 || K_aug % 32 || M <= 0) return -1;
+  return prq::launch_gemm_tile(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, shape, stream) == hipSuccess
+             ? 0
+             : -3;
+}
+
+// g16: 1024 bytes, g1: 64 bytes, out: 8192 bytes (device).
+int prq_probe_lds_dma(const uint8_t* g16, const uint8_t* g1, uint8_t* out, hipStream_t stream) {
+  lds_dma_probe<<<1, 64, 0, stream>>>(g16, g1, out);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

@@ -91,3 +91,29 @@ def test_hw_fp4_convert_matches_rounding_rule():
     print("cvt pairs (x=3,y=1,s=1), (x=3,y=1,s=2), (.75,-.1), (5,6.5):",
           [hex(v) for v in o.cpu().numpy()], flush=True)
     assert int(r[0]) == 0
+
+
+def test_direct_global_to_lds_load_layout():
+    """global_load_lds: lane l's 16 bytes land at LDS base + 16 l (one
+    lane-ordered MFMA operand block per wave instruction); lane l's single byte
+    lands in the dword slot at base + 4 l, upper bytes zero (how the tile GEMM
+    stages its scale bytes)."""
+    from paper_2609_22106_amd import build
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    lib.prq_probe_lds_dma.argtypes = [ctypes.c_void_p] * 4
+    rng = np.random.default_rng(5)
+    g16 = rng.integers(1, 256, 1024, dtype=np.uint8)
+    g1 = rng.integers(1, 256, 64, dtype=np.uint8)
+    d16, d1 = torch.from_numpy(g16).cuda(), torch.from_numpy(g1).cuda()
+    out = torch.zeros(8192, dtype=torch.uint8, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+    assert lib.prq_probe_lds_dma(d16.data_ptr(), d1.data_ptr(), out.data_ptr(), s) == 0
+    o = out.cpu().numpy()
+    nz16 = np.flatnonzero(o[:4096])
+    nz1 = np.flatnonzero(o[4096:])
+    print("lds dma: 16-byte data at", nz16[:4], "...", nz16[-2:], "; bytes at", nz1[:8], flush=True)
+    np.testing.assert_array_equal(o[:1024], g16)
+    assert not o[1024:4096].any()
+    slots = o[4096:4096 + 256].reshape(64, 4)
+    np.testing.assert_array_equal(slots[:, 0], g1)
+    assert not slots[:, 1:].any() and not o[4096 + 256:].any()
