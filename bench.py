@@ -110,10 +110,12 @@ def build_dense_ops(torch, prq, layers, M_list, rotate_bytes, stream):
             Xm = X[:M]
             state = {"r": 0}
 
-            def act(Xm=Xm, Aq=Aq, Asc=Asc, K=K, k=k):
+            # every per-layer buffer is bound here: a name captured from the
+            # enclosing loop would see the last layer's buffers in every op
+            def act(Xm=Xm, Aq=Aq, Asc=Asc, K=K, k=k, inv=inv, perm=perm):
                 prq.prq_quant_act(Xm, K, k, inv, perm, Aq=Aq, Asc=Asc, stream=stream)
 
-            def gemm(Aq=Aq, Asc=Asc, Y=Y, ws=ws, state=state, R=R):
+            def gemm(Aq=Aq, Asc=Asc, Y=Y, ws=ws, state=state, R=R, Ws=Ws):
                 r = state["r"]
                 state["r"] = (r + 1) % R
                 prq.prq_gemm(Aq, Asc, Ws[r], Y=Y, workspace=ws, stream=stream)

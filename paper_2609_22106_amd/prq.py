@@ -128,17 +128,59 @@ def prq_prepare(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth", with_col_
 
 
 # ------------------------------------------------------------- device ops ---
+# The library receives bare pointers and cannot see buffer extents, so the
+# binding checks every tensor against the sizes it passes (shape, dtype,
+# contiguity) and that it lives on a GPU, before anything is launched.
+def _need(t, name, dtype, shape=None, min_numel=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype not in (dtype if isinstance(dtype, tuple) else (dtype,)):
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if min_numel is not None and t.numel() < min_numel:
+        raise ValueError(f"{name} has {t.numel()} elements, needs at least {min_numel}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _on_gpu(**tensors):
+    for name, t in tensors.items():
+        if t is not None and not t.is_cuda:
+            raise ValueError(f"{name} must be a GPU tensor")
+
+
+_BF16_LIKE = (torch.int16, torch.uint16, torch.bfloat16)
+
+
 def prq_quant_act(X, K, k_tail, inv_scale_pos=None, perm=None, group_offsets=None, G=1,
                   Aq=None, Asc=None, stream=None):
     """Quantize bf16 activations X [M, ld] (device) -> (Aq [M, K_aug/2], Asc [M, K_aug/32]).
     inv_scale_pos[p] = 1/s_{perm[p]} (prq_prepare's ``inv_scale_pos``)."""
+    if not isinstance(X, torch.Tensor) or X.dim() != 2 or X.dtype not in _BF16_LIKE:
+        raise ValueError("X must be a 2-D tensor of bf16 values (or their int16 bit patterns)")
     M = X.shape[0]
     K_aug = K + k_tail
+    if X.shape[1] < K or (M > 1 and X.stride(0) < K) or X.stride(1) != 1:
+        raise ValueError(f"X rows must hold K={K} contiguous values (shape {tuple(X.shape)}, "
+                         f"strides {X.stride()})")
     if Aq is None:
         Aq = torch.empty((M, K_aug // 2), dtype=torch.uint8, device=X.device)
     if Asc is None:
         Asc = torch.empty((M, K_aug // 32), dtype=torch.uint8, device=X.device)
-    ld = X.stride(0) if X.dim() == 2 else K
+    _need(Aq, "Aq", torch.uint8, (M, K_aug // 2))
+    _need(Asc, "Asc", torch.uint8, (M, K_aug // 32))
+    if inv_scale_pos is not None:
+        _need(inv_scale_pos, "inv_scale_pos", torch.float32, min_numel=G * K)
+    if perm is not None:
+        _need(perm, "perm", torch.int32, min_numel=G * K)
+    if G > 1:
+        if group_offsets is None:
+            raise ValueError("G > 1 needs group_offsets")
+        _need(group_offsets, "group_offsets", torch.int32, min_numel=G + 1)
+    _on_gpu(X=X, Aq=Aq, Asc=Asc, inv_scale_pos=inv_scale_pos, perm=perm,
+            group_offsets=group_offsets if G > 1 else None)
+    ld = X.stride(0) if M > 1 else K
     st = _quant_act(_ptr(X), ld, M, K, k_tail, _ptr(inv_scale_pos), _ptr(perm), _ptr(group_offsets), G,
                     _ptr(Aq), _ptr(Asc), _stream(stream))
     _check(st, "prq_quant_act")
@@ -151,6 +193,19 @@ class PackedWeight:
     def __init__(self, Wp, Wps, E, N, K_aug):
         self.Wp, self.Wps, self.E, self.N, self.K_aug = Wp, Wps, E, N, K_aug
 
+    def check_sizes(self):
+        cb, sb = prq_packed_weight_bytes(self.E, self.N, self.K_aug)
+        _need(self.Wp, "W.Wp", torch.uint8, min_numel=cb)
+        _need(self.Wps, "W.Wps", torch.uint8, min_numel=sb)
+
+
+def _check_gemm_operands(Aq, Asc, W, Y, M):
+    _need(Aq, "Aq", torch.uint8, (M, W.K_aug // 2))
+    _need(Asc, "Asc", torch.uint8, (M, W.K_aug // 32))
+    _need(Y, "Y", torch.float32, (M, W.N))
+    W.check_sizes()
+    _on_gpu(Aq=Aq, Asc=Asc, Y=Y, Wp=W.Wp, Wps=W.Wps)
+
 
 def prq_packed_weight_bytes(E, N, K_aug):
     cb, sb = _sz(0), _sz(0)
@@ -161,9 +216,14 @@ def prq_packed_weight_bytes(E, N, K_aug):
 def prq_pack_weight(Wq, Wsc, stream=None):
     """Canonical device Wq [N, K_aug/2] / Wsc [N, K_aug/32] (or [E, N, ...]) ->
     PackedWeight in the layout the GEMM kernels read."""
+    if not isinstance(Wq, torch.Tensor) or Wq.dim() not in (2, 3):
+        raise ValueError("Wq must be a [N, K_aug/2] or [E, N, K_aug/2] tensor")
     E = Wq.shape[0] if Wq.dim() == 3 else 1
     N = Wq.shape[-2]
     K_aug = Wq.shape[-1] * 2
+    _need(Wq, "Wq", torch.uint8)
+    _need(Wsc, "Wsc", torch.uint8, tuple(Wq.shape[:-1]) + (K_aug // 32,))
+    _on_gpu(Wq=Wq, Wsc=Wsc)
     cb, sb = prq_packed_weight_bytes(E, N, K_aug)
     Wp = torch.empty(cb, dtype=torch.uint8, device=Wq.device)
     Wps = torch.empty(sb, dtype=torch.uint8, device=Wq.device)
@@ -181,11 +241,17 @@ def prq_gemm(Aq, Asc, W, Y=None, workspace=None, variant=GEMM_AUTO, splits=0, st
     PackedWeight (E = 1)."""
     M = Aq.shape[0]
     N, K_aug = W.N, W.K_aug
+    if W.E != 1:
+        raise ValueError("prq_gemm takes a single weight (E = 1); use prq_grouped_gemm")
     if Y is None:
         Y = torch.empty((M, N), dtype=torch.float32, device=W.Wp.device)
+    _check_gemm_operands(Aq, Asc, W, Y, M)
     need = prq_gemm_workspace_bytes(M, N, K_aug, variant, splits)
     if workspace is None and need:
         workspace = torch.zeros(need, dtype=torch.uint8, device=W.Wp.device)
+    if workspace is not None:
+        _need(workspace, "workspace", torch.uint8)
+        _on_gpu(workspace=workspace)
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     st = _gemm_ex(_ptr(Aq), _ptr(Asc), M, _ptr(W.Wp), _ptr(W.Wps), N, K_aug, _ptr(Y),
                   _ptr(workspace), ws_bytes, variant, splits, _stream(stream))
@@ -204,6 +270,12 @@ def prq_grouped_gemm(Aq, Asc, group_offsets, W, Y=None, workspace=None, variant=
     E, N, K_aug = W.E, W.N, W.K_aug
     if Y is None:
         Y = torch.empty((M, N), dtype=torch.float32, device=W.Wp.device)
+    _need(group_offsets, "group_offsets", torch.int32, (E + 1,))
+    _check_gemm_operands(Aq, Asc, W, Y, M)
+    _on_gpu(group_offsets=group_offsets)
+    if workspace is not None:
+        _need(workspace, "workspace", torch.uint8)
+        _on_gpu(workspace=workspace)
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     st = _ggemm_ex(_ptr(Aq), _ptr(Asc), _ptr(group_offsets), E, M, _ptr(W.Wp), _ptr(W.Wps), N,
                    K_aug, _ptr(Y), _ptr(workspace), ws_bytes, variant, _stream(stream))

@@ -136,3 +136,62 @@ def test_workspace_sizes():
     assert prq.prq_packed_weight_bytes(1, 2560, 9984) == (160 * 78 * 1024, 160 * 20 * 256)
     assert prq.prq_packed_weight_bytes(128, 2048, 832) == (128 * 128 * 7 * 1024, 128 * 128 * 2 * 256)
     assert prq.prq_grouped_gemm_workspace_bytes(512, 128, 2048, 832) == 0
+
+
+def test_binding_rejects_operands_that_do_not_match_the_weight():
+    """The binding checks tensor extents the C ABI cannot see (it gets bare
+    pointers) before anything is launched: activations quantized for one
+    K_aug against a weight packed for another, wrong dtypes, wrong Y, host
+    tensors.  CPU tensors suffice: every check runs before the library call."""
+    import torch
+    M, N = 8, 64
+    cb, sb = prq.prq_packed_weight_bytes(1, N, 9952)
+    W = prq.PackedWeight(torch.zeros(cb, dtype=torch.uint8), torch.zeros(sb, dtype=torch.uint8),
+                         1, N, 9952)
+    Aq_small = torch.zeros((M, 2624 // 2), dtype=torch.uint8)
+    Asc_small = torch.zeros((M, 2624 // 32), dtype=torch.uint8)
+    with pytest.raises(ValueError, match="Aq has shape"):
+        prq.prq_gemm(Aq_small, Asc_small, W, Y=torch.zeros((M, N)))
+    Aq = torch.zeros((M, 9952 // 2), dtype=torch.uint8)
+    Asc = torch.zeros((M, 9952 // 32), dtype=torch.uint8)
+    with pytest.raises(ValueError, match="Asc has shape"):
+        prq.prq_gemm(Aq, Asc_small, W, Y=torch.zeros((M, N)))
+    with pytest.raises(ValueError, match="Y has shape"):
+        prq.prq_gemm(Aq, Asc, W, Y=torch.zeros((M, N + 16)))
+    with pytest.raises(ValueError, match="Y has dtype"):
+        prq.prq_gemm(Aq, Asc, W, Y=torch.zeros((M, N), dtype=torch.float64))
+    short = prq.PackedWeight(W.Wp[:-1], W.Wps, 1, N, 9952)
+    with pytest.raises(ValueError, match="W.Wp has"):
+        prq.prq_gemm(Aq, Asc, short, Y=torch.zeros((M, N)))
+    with pytest.raises(ValueError, match="GPU tensor"):
+        prq.prq_gemm(Aq, Asc, W, Y=torch.zeros((M, N)))
+    off = torch.tensor([0, 3, M], dtype=torch.int32)
+    W2 = prq.PackedWeight(torch.zeros(2 * cb, dtype=torch.uint8), torch.zeros(2 * sb, dtype=torch.uint8),
+                          2, N, 9952)
+    with pytest.raises(ValueError, match="group_offsets has shape"):
+        prq.prq_grouped_gemm(Aq, Asc, off[:2], W2, Y=torch.zeros((M, N)))
+    with pytest.raises(ValueError, match="group_offsets has dtype"):
+        prq.prq_grouped_gemm(Aq, Asc, off.long(), W2, Y=torch.zeros((M, N)))
+    with pytest.raises(ValueError, match="single weight"):
+        prq.prq_gemm(Aq, Asc, W2, Y=torch.zeros((M, N)))
+
+    K, k = 2560, 64
+    X = torch.zeros((M, K), dtype=torch.int16)
+    inv = torch.ones(K, dtype=torch.float32)
+    perm = torch.arange(K, dtype=torch.int32)
+    with pytest.raises(ValueError, match="X rows"):
+        prq.prq_quant_act(X[:, :K - 32], K, k, inv, perm)
+    with pytest.raises(ValueError, match="perm has dtype"):
+        prq.prq_quant_act(X, K, k, inv, perm.long())
+    with pytest.raises(ValueError, match="inv_scale_pos has"):
+        prq.prq_quant_act(X, K, k, inv[: K // 2], perm)
+    with pytest.raises(ValueError, match="perm has"):
+        prq.prq_quant_act(X, K, k, torch.ones(2 * K), torch.arange(K, dtype=torch.int32),
+                          group_offsets=torch.tensor([0, 4, M], dtype=torch.int32), G=2)
+    with pytest.raises(ValueError, match="Aq has shape"):
+        prq.prq_quant_act(X, K, k, inv, perm, Aq=torch.zeros((M, 9952 // 2), dtype=torch.uint8))
+    with pytest.raises(ValueError, match="GPU tensor"):
+        prq.prq_quant_act(X, K, k, inv, perm)
+    with pytest.raises(ValueError, match="Wsc has shape"):
+        prq.prq_pack_weight(torch.zeros((N, 1312), dtype=torch.uint8),
+                            torch.zeros((N, 80), dtype=torch.uint8))
