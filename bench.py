@@ -9,12 +9,17 @@ prq_prepare runs once before timing.  Weights are rotated through enough
 copies (>= 1 GiB) that every step streams them from HBM rather than from the
 256 MB Infinity Cache.
 
+Timed region: `--steps` whole steps launched eagerly but queued behind a GPU
+spin-sleep long enough for the host to enqueue all of them, with HIP events on
+the launch stream around every kernel; the GPU then runs the steps back to
+back, as it does when a serving loop replays them from a graph (the same steps
+replayed from one captured HIP graph are timed too: ``graph_ms_per_step``).
+
 Prints ONE JSON line on stdout (everything else goes to stderr):
   value = algorithmic bytes of one step / step time (GB/s), plus per-M
   kernel times, TFLOP/s, roofline fraction of the dominant kernel (the GEMM)
-  from HIP events recorded around each of its launches on its stream, a
-  same-shape BF16 torch.matmul for context, and the CPU oracle timed on a
-  bounded sample (``cpu_baseline``).
+  from the events around its launches, a same-shape BF16 torch.matmul for
+  context, and the CPU oracle timed on a bounded sample (``cpu_baseline``).
 
 Other workloads (--workload): prefill (M = 512, 2048, 8192), experts (128
 expert down_projs 768 -> 2048, k = 64, 64 or 4096 tokens routed top-8, one
@@ -50,6 +55,7 @@ def parse_args(argv=None):
                    choices=["decode", "prefill", "experts", "experts_prefill", "layers"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-bf16", action="store_true")
+    p.add_argument("--no-graph", action="store_true", help="skip the graph-replay cross-check")
     p.add_argument("--rotate-bytes", type=float, default=1.0 * 2 ** 30,
                    help="minimum total bytes of rotated weight copies")
     p.add_argument("--copy-calibration", action="store_true",
@@ -85,7 +91,7 @@ class Op:
         self.t_gemm, self.t_act = [], []
 
 
-def build_dense_ops(torch, prq, layers, M_list, rotate_bytes, stream):
+def build_dense_ops(torch, prq, layers, M_list, rotate_bytes):
     """layers: list of (name, DenseCase).  Weights rotated, activations per M."""
     ops = []
     for name, c in layers:
@@ -113,12 +119,12 @@ def build_dense_ops(torch, prq, layers, M_list, rotate_bytes, stream):
             # every per-layer buffer is bound here: a name captured from the
             # enclosing loop would see the last layer's buffers in every op
             def act(Xm=Xm, Aq=Aq, Asc=Asc, K=K, k=k, inv=inv, perm=perm):
-                prq.prq_quant_act(Xm, K, k, inv, perm, Aq=Aq, Asc=Asc, stream=stream)
+                prq.prq_quant_act(Xm, K, k, inv, perm, Aq=Aq, Asc=Asc)
 
             def gemm(Aq=Aq, Asc=Asc, Y=Y, ws=ws, state=state, R=R, Ws=Ws):
                 r = state["r"]
                 state["r"] = (r + 1) % R
-                prq.prq_gemm(Aq, Asc, Ws[r], Y=Y, workspace=ws, stream=stream)
+                prq.prq_gemm(Aq, Asc, Ws[r], Y=Y, workspace=ws)
 
             ops.append(Op(f"{name}/M={M}", M, N, K, k, act, gemm, gemm_bytes(M, N, K_aug),
                           act_bytes(M, K, K_aug), 2.0 * M * N * K_aug))
@@ -126,7 +132,7 @@ def build_dense_ops(torch, prq, layers, M_list, rotate_bytes, stream):
     return ops
 
 
-def build_expert_ops(torch, np, prq, inputs, tokens, rotate_bytes, stream):
+def build_expert_ops(torch, np, prq, inputs, tokens, rotate_bytes):
     c = inputs.moe_experts(tokens)
     E, N, K, k = c.E, c.N, c.K, c.k_tail
     K_aug = K + k
@@ -151,12 +157,12 @@ def build_expert_ops(torch, np, prq, inputs, tokens, rotate_bytes, stream):
     e_active = int(np.count_nonzero(np.diff(c.group_offsets)))
 
     def act():
-        prq.prq_quant_act(X, K, k, inv, perm, group_offsets=off, G=E, Aq=Aq, Asc=Asc, stream=stream)
+        prq.prq_quant_act(X, K, k, inv, perm, group_offsets=off, G=E, Aq=Aq, Asc=Asc)
 
     def gemm():
         r = state["r"]
         state["r"] = (r + 1) % R
-        prq.prq_grouped_gemm(Aq, Asc, off, Ws[r], Y=Y, stream=stream)
+        prq.prq_grouped_gemm(Aq, Asc, off, Ws[r], Y=Y)
 
     log(f"[bench] experts: {M} routed rows, {e_active} active experts, {R} weight copies")
     return [Op(f"experts/{tokens}tok", M, N, K, k, act, gemm,
@@ -165,38 +171,138 @@ def build_expert_ops(torch, np, prq, inputs, tokens, rotate_bytes, stream):
 
 
 # -------------------------------------------------------------- timing ---
-def run_steps(torch, ops, steps, warmup, stream, record):
-    """Run `steps` steps; with `record`, bracket every kernel with events."""
-    pairs = []
+def step_once(ops):
+    for op in ops:
+        op.act_fn()
+        op.gemm_fn()
+
+
+def sleep_rate(torch, stream):
+    """GPU spin-sleep cycles per second (torch.cuda._sleep), measured."""
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda._sleep(100_000)
+    a.record(stream)
+    torch.cuda._sleep(4_000_000)
+    b.record(stream)
+    torch.cuda.synchronize()
+    return 4_000_000 / (a.elapsed_time(b) * 1e-3)
+
+
+class HipTimer:
+    """Timing events made through the HIP runtime that torch has loaded (found
+    in /proc/self/maps, so it is the same runtime instance), created with
+    hipEventDisableSystemFence: recording such an event skips the system-scope
+    cache writeback/invalidate that a default event performs, which would
+    otherwise add microseconds to every bracketed kernel of a few
+    microseconds."""
+
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    def __init__(self):
+        import ctypes
+        path = next(line.split()[-1] for line in open("/proc/self/maps") if "libamdhip64" in line)
+        self.ct = ctypes
+        self.hip = ctypes.CDLL(path)
+        self.hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+        self.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.path = path
+
+    def _ok(self, err, what):
+        if err != 0:
+            raise RuntimeError(f"{what} failed with HIP error {err}")
+
+    def event(self):
+        e = self.ct.c_void_p()
+        self._ok(self.hip.hipEventCreateWithFlags(self.ct.byref(e), self.DISABLE_SYSTEM_FENCE),
+                 "hipEventCreateWithFlags")
+        return e
+
+    def record(self, e, stream):
+        self._ok(self.hip.hipEventRecord(e, self.ct.c_void_p(stream.cuda_stream)), "hipEventRecord")
+
+    def seconds(self, a, b):
+        ms = self.ct.c_float()
+        self._ok(self.hip.hipEventElapsedTime(self.ct.byref(ms), a, b), "hipEventElapsedTime")
+        return ms.value * 1e-3
+
+    def destroy(self, events):
+        for e in events:
+            self.hip.hipEventDestroy(e)
+
+
+def run_steps(torch, ops, steps, warmup, stream):
+    """Warmup, then the timed region: `steps` whole steps with HIP events on
+    the launch stream around every kernel.  The launches are queued behind a
+    GPU spin-sleep long enough for the host to enqueue all of them, so the
+    region measures the GPU executing the steps back to back, not the host's
+    per-launch cost (which a serving loop hides with a graph; see
+    graph_step_time)."""
     for _ in range(warmup):
-        for op in ops:
-            op.act_fn()
-            op.gemm_fn()
+        step_once(ops)
     torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    start.record(stream)
+    rate = sleep_rate(torch, stream)
     t0 = time.perf_counter()
-    for _ in range(steps):
-        for op in ops:
-            if record:
-                ea0, ea1, eg1 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
-                ea0.record(stream)
-                op.act_fn()
-                ea1.record(stream)
-                op.gemm_fn()
-                eg1.record(stream)
-                pairs.append((op, ea0, ea1, eg1))
-            else:
-                op.act_fn()
-                op.gemm_fn()
-    end.record(stream)
+    step_once(ops)                                   # host enqueue cost of a step
+    host_step = time.perf_counter() - t0
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+    # events add host time per launch too: budget 2x the measured step, +5 ms
+    hold_s = min(2.0, steps * host_step * 2.0 + 5e-3)
+    timer = HipTimer()
+    start, end = timer.event(), timer.event()
+    pairs = [(op, timer.event(), timer.event(), timer.event()) for _ in range(steps) for op in ops]
+    torch.cuda._sleep(int(hold_s * rate))
+    timer.record(start, stream)
+    t0 = time.perf_counter()
     for op, ea0, ea1, eg1 in pairs:
-        op.t_act.append(ea0.elapsed_time(ea1) * 1e-3)
-        op.t_gemm.append(ea1.elapsed_time(eg1) * 1e-3)
-    return start.elapsed_time(end) * 1e-3, wall
+        timer.record(ea0, stream)
+        op.act_fn()
+        timer.record(ea1, stream)
+        op.gemm_fn()
+        timer.record(eg1, stream)
+    timer.record(end, stream)
+    enqueue_s = time.perf_counter() - t0
+    torch.cuda.synchronize()
+    for op, ea0, ea1, eg1 in pairs:
+        op.t_act.append(timer.seconds(ea0, ea1))
+        op.t_gemm.append(timer.seconds(ea1, eg1))
+    gpu_s = timer.seconds(start, end)
+    timer.destroy([start, end] + [e for p in pairs for e in p[1:]])
+    return gpu_s, {"host_enqueue_s": round(enqueue_s, 5), "gpu_hold_s": round(hold_s, 5),
+                   "queued_ahead": bool(enqueue_s < hold_s)}
+
+
+def graph_step_time(torch, ops, steps):
+    """The same steps captured once into a HIP graph and replayed (how a
+    serving loop launches them): seconds per step."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step_once(ops)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    # all `steps` steps in one graph: each captured step binds the next
+    # rotated weight copy, so replays stream the same >= 1 GiB of weights as
+    # the eager region (a short graph would cycle through few enough copies to
+    # be served from the Infinity Cache)
+    per_graph = max(1, steps)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(per_graph):
+            step_once(ops)
+    g.replay()
+    torch.cuda.synchronize()
+    reps = 2
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    del g
+    return a.elapsed_time(b) * 1e-3 / (reps * per_graph)
 
 
 def bf16_context(torch, layers, M_list, rotate_bytes, steps):
@@ -362,19 +468,19 @@ def main(argv=None):
         c = inputs.down_proj_decode() if wl == "decode" else inputs.down_proj_prefill()
         layers = [("qwen3_4b_down_proj", c)]
         M_list = list(c.M_list)
-        ops = build_dense_ops(torch, prq, layers, M_list, args.rotate_bytes, stream)
+        ops = build_dense_ops(torch, prq, layers, M_list, args.rotate_bytes)
         config = {"workload": f"qwen3_4b_down_proj_{wl}", "N": 2560, "K": 9728, "k_tail": 256,
                   "alpha": 0.5, "M": M_list}
     elif wl in ("experts", "experts_prefill"):
         tokens = 64 if wl == "experts" else 4096
-        ops = build_expert_ops(torch, np, prq, inputs, tokens, args.rotate_bytes, stream)
+        ops = build_expert_ops(torch, np, prq, inputs, tokens, args.rotate_bytes)
         layers, M_list = [], []
         config = {"workload": f"qwen3_30b_a3b_expert_down_proj_{tokens}tok", "E": 128, "N": 2048,
                   "K": 768, "k_tail": 64, "alpha": 0.5, "topk": 8, "routed_rows": ops[0].M}
     else:
         layers = [(n, inputs.layer_case(n)) for n, _, _ in inputs.LAYER_SET]
         M_list = [4096]
-        ops = build_dense_ops(torch, prq, layers, M_list, args.rotate_bytes, stream)
+        ops = build_dense_ops(torch, prq, layers, M_list, args.rotate_bytes)
         config = {"workload": "qwen3_4b_decoder_linears_prefill", "M": 4096,
                   "layers": {n: {"N": c.N, "K": c.K, "k_tail": c.k_tail} for n, c in layers}}
 
@@ -382,8 +488,8 @@ def main(argv=None):
         copy_calibration(torch)
     # untimed warmup, then the timed region: whole steps, with HIP events on
     # the launch stream around every kernel for the per-kernel durations
-    run_steps(torch, ops, 0, args.warmup, stream, record=False)
-    t_gpu, t_wall = run_steps(torch, ops, args.steps, 0, stream, record=True)
+    t_gpu, queue_info = run_steps(torch, ops, args.steps, args.warmup, stream)
+    t_graph = graph_step_time(torch, ops, args.steps) if not args.no_graph else None
     ms_per_step = t_gpu / args.steps * 1e3
     step_bytes = sum(op.gemm_bytes + op.act_bytes for op in ops)
     step_flops = sum(op.flops for op in ops)
@@ -405,9 +511,9 @@ def main(argv=None):
             "gemm_mfma_frac": round(op.flops / tg / 1e12 / MXFP4_PEAK_TFLOPS, 4),
             "act_quant_GBs": round(op.act_bytes / ta / 1e9, 1),
         }
-    flops_per_byte = step_flops / max(step_bytes, 1)
-    bound = "mfma" if flops_per_byte > MXFP4_PEAK_TFLOPS / HBM_PEAK_GBS * 1e3 else "hbm"
+    # the GEMM's own arithmetic intensity decides which roof bounds it
     g_flops = sum(op.flops for op in ops)
+    bound = "mfma" if g_flops / max(g_bytes, 1) > MXFP4_PEAK_TFLOPS / HBM_PEAK_GBS * 1e3 else "hbm"
     if bound == "hbm":
         achieved, peak, unit = g_bytes / g_time / 1e9, HBM_PEAK_GBS, "GB/s"
     else:
@@ -437,7 +543,9 @@ def main(argv=None):
         "dtype": "mxfp4", "data": "synthetic", "config": config,
         "tflops": round(step_flops / (t_gpu / args.steps) / 1e12, 3),
         "roofline": roofline, "cpu_baseline": cpu, "detail": detail,
-        "wall_s_timed": round(t_wall, 4),
+        "timing": dict(queue_info, method="eager launches queued behind a GPU spin-sleep; HIP "
+                       "events (hipEventDisableSystemFence) on the launch stream around every kernel"),
+        "graph_ms_per_step": None if t_graph is None else round(t_graph * 1e3, 5),
     }
     print(json.dumps(line), flush=True)
     return 0
