@@ -17,14 +17,14 @@
 //     workgroups; perm and d of its 8 positions live in registers (no
 //     dependent gather: d is given in position order) and the row values are
 //     gathered straight from global memory (rows of a few KB stay in L2).
-//   * LDS kernel (many rows, prefill): a workgroup keeps the group's perm and d
-//     in LDS for a contiguous range of rows; each row is staged into LDS with
-//     coalesced 16-byte loads -- the next row is already being loaded into
-//     registers while the current one is quantized -- and gathered from LDS.
+//   * LDS kernel (many rows, prefill): a workgroup takes a contiguous range of
+//     rows; a thread keeps the perm and d of its units in registers; each row
+//     is staged into LDS with coalesced 16-byte loads (double-buffered, the
+//     next row already loading into registers) and gathered from LDS.
+// E2M1 encoding uses the hardware FP32->FP4 converter on exactly scaled values.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
-#include <mutex>
 
 #include "mx_device.hpp"
 #include "prq_internal.h"
@@ -68,7 +68,12 @@ __device__ __forceinline__ void load_unit(const int32_t* __restrict__ perm,
 }
 
 // Quantize 8 values of a quarter block (the quad holds the whole block) and
-// write the word, the scale and, for tail blocks, their copies.
+// write the word, the scale and, for tail blocks, their copies.  t = z * 2^-e
+// is exact (a power-of-two product whose magnitude stays below 8, or a
+// signed zero/denormal that encodes as a signed zero either way); its E2M1
+// code comes from the hardware converter at scale 1, which rounds to nearest
+// even and saturates at 6 exactly like the software rule on every float32
+// (checked exhaustively on the GPU).
 __device__ __forceinline__ void quantize_store(const float (&z)[8], int u, int tail_unit0,
                                                int copy_units, int copy_blocks, uint8_t* arow,
                                                uint8_t* srow) {
@@ -80,7 +85,9 @@ __device__ __forceinline__ void quantize_store(const float (&z)[8], int u, int t
   const float mul = dev::e8m0_reciprocal(code);
   uint32_t w = 0;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) w |= dev::e2m1_code(z[j] * mul, z[j]) << (4 * j);
+  for (int j = 0; j < 4; ++j)
+    w |= (__builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, z[2 * j] * mul, z[2 * j + 1] * mul, 1.0f, 0) &
+          0xFFu) << (8 * j);
   *reinterpret_cast<uint32_t*>(arow + 4 * u) = w;
   if ((u & 3) == 0) srow[u >> 2] = static_cast<uint8_t>(code);
   if (u >= tail_unit0) {  // online copy of the quantized tail and its scales
@@ -120,81 +127,144 @@ __global__ __launch_bounds__(kRowsThreads) void act_quant_rows_kernel(
   }
 }
 
-inline size_t lds_kernel_bytes(int K) {
-  // d (float) + one staged bf16 row + perm (uint16)
-  return static_cast<size_t>(K) * 4 + static_cast<size_t>(K) * 2 + static_cast<size_t>(K) * 2;
+// Positions of a unit with their source channels packed two per register
+// (K <= 16384 fits 16 bits) and their inverse scales.
+struct PackedUnit {
+  uint32_t src2[4];
+  float d[8];
+};
+
+__device__ __forceinline__ void load_packed_unit(const int32_t* __restrict__ perm,
+                                                 const float* __restrict__ inv, int g, int K,
+                                                 int u, PackedUnit* out) {
+  Unit t;
+  load_unit(perm, inv, g, K, u, &t);
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    out->src2[j] = static_cast<uint32_t>(t.src[2 * j]) | (static_cast<uint32_t>(t.src[2 * j + 1]) << 16);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) out->d[j] = t.d[j];
 }
 
-template <bool kGrouped>
+// Rows handled together by one pass of the LDS kernel: one when a row has at
+// least as many units as the workgroup has threads, else as many whole rows
+// as fit (a thread then owns one unit of one of them).
+__host__ __device__ inline int lds_rows_per_pass(int units) {
+  return units >= kLdsThreads ? 1 : kLdsThreads / units;
+}
+
+inline size_t lds_kernel_bytes(int K) {
+  const int units = K >> 3;
+  return static_cast<size_t>(lds_rows_per_pass(units)) * units * 16 * 2;   // two staged passes
+}
+
+// Many rows.  A workgroup takes a contiguous range of rows, a pass of
+// lds_rows_per_pass(K/8) rows at a time.  Thread t owns the units t + 512 j
+// of the pass (kUnits of them; with several rows per pass, one): flat index f
+// -> row f / units, unit f % units, the same row for all of a thread's units.
+// Their source channels and inverse scales stay in registers, reloaded only
+// when the thread's row enters another expert.  Passes are staged in LDS with
+// coalesced 16-byte loads into two alternating buffers: pass i+1 is loaded
+// into registers while pass i is quantized, and one barrier per pass suffices
+// -- a thread writes pass i into buffer i&1 only after the barrier of pass
+// i-1, which every thread passes only after it finished reading pass i-2 from
+// that buffer.
+template <bool kGrouped, int kUnits>
 __global__ __launch_bounds__(kLdsThreads) void act_quant_lds_kernel(
     const uint16_t* __restrict__ X, int64_t ld_x, int M, int K, int k_tail,
     const float* __restrict__ inv, const int32_t* __restrict__ perm,
     const int32_t* __restrict__ offsets, int G, int rows_per_wg, uint8_t* __restrict__ Aq,
     uint8_t* __restrict__ Asc) {
   extern __shared__ __align__(16) unsigned char smem[];
-  float* s_d = reinterpret_cast<float*>(smem);                                       // [K]
-  uint16_t* s_row = reinterpret_cast<uint16_t*>(smem + static_cast<size_t>(K) * 4);  // [K]
-  uint16_t* s_perm = s_row + K;                                                      // [K]
-
   const int tid = threadIdx.x;
+  const int units = K >> 3;                       // units (= uint4 vectors) per row
+  const int rpp = lds_rows_per_pass(units);
+  const int pass_vecs = rpp * units;              // <= max(units, 512) <= 2048
+  uint4* const buf0 = reinterpret_cast<uint4*>(smem);
+  uint4* const buf1 = buf0 + pass_vecs;
   const int r0 = blockIdx.x * rows_per_wg;
   const int r1 = min(M, r0 + rows_per_wg);
-  const int units = K >> 3;
-  const int vecs = K >> 3;    // uint4 per row
   const int k_aug = K + k_tail;
   const int64_t row_bytes = k_aug >> 1;
   const int nb = k_aug >> 5;
+  const int tail_unit0 = (K - k_tail) >> 3;
 
-  uint4 pre[kMaxRowVec];
-  auto prefetch = [&](int r) {
-    const uint4* xr = reinterpret_cast<const uint4*>(X + static_cast<int64_t>(r) * ld_x);
+  // Staged vectors of this thread: v = tid + 512 i -> (row offset, vector),
+  // as named registers (an array here ends up in scratch when its copy loop is
+  // not fully unrolled).
+  static_assert(kMaxRowVec == 4, "four named row vectors");
+  int vro[4];
+  int64_t voff[4];
 #pragma unroll
-    for (int i = 0; i < kMaxRowVec; ++i) {
-      const int v = tid + i * kLdsThreads;
-      if (v < vecs) pre[i] = xr[v];
-    }
+  for (int i = 0; i < 4; ++i) {
+    const int v = tid + i * kLdsThreads;
+    vro[i] = v < pass_vecs ? v / units : rpp;     // rpp: never a valid row offset
+    voff[i] = v < pass_vecs ? static_cast<int64_t>(vro[i]) * ld_x + (v - vro[i] * units) * 8 : 0;
+  }
+  uint4 p0 = {}, p1 = {}, p2 = {}, p3 = {};
+  auto prefetch = [&](int rb) {
+    const int lim = min(rpp, r1 - rb);           // rows of this pass
+    const uint16_t* xb = X + static_cast<int64_t>(rb) * ld_x;
+    if (vro[0] < lim) p0 = *reinterpret_cast<const uint4*>(xb + voff[0]);
+    if (vro[1] < lim) p1 = *reinterpret_cast<const uint4*>(xb + voff[1]);
+    if (vro[2] < lim) p2 = *reinterpret_cast<const uint4*>(xb + voff[2]);
+    if (vro[3] < lim) p3 = *reinterpret_cast<const uint4*>(xb + voff[3]);
   };
   if (r0 < r1) prefetch(r0);
 
+  const int ro = tid / units;                     // this thread's row within a pass
+  const int u0 = tid - ro * units;                // its first unit
+  PackedUnit un[kUnits];
   int cur_g = -1;
-  for (int r = r0; r < r1; ++r) {
-    const int g = kGrouped ? dev::find_group(offsets, G, r) : 0;
-    __syncthreads();  // the previous row's readers are done with s_row / s_perm / s_d
-    if (g != cur_g) {
-      const int32_t* pg = perm ? perm + static_cast<int64_t>(g) * K : nullptr;
-      const float* dg = inv ? inv + static_cast<int64_t>(g) * K : nullptr;
-      for (int p = tid; p < K; p += kLdsThreads) {
-        int src = pg ? pg[p] : p;
-        src = static_cast<unsigned>(src) < static_cast<unsigned>(K) ? src : 0;  // never past the row
-        s_perm[p] = static_cast<uint16_t>(src);
-        s_d[p] = dg ? dg[p] : 1.0f;
-      }
-      cur_g = g;
-    }
-    uint4* sr = reinterpret_cast<uint4*>(s_row);
-#pragma unroll
-    for (int i = 0; i < kMaxRowVec; ++i) {
-      const int v = tid + i * kLdsThreads;
-      if (v < vecs) sr[v] = pre[i];
-    }
-    if (r + 1 < r1) prefetch(r + 1);   // in flight while this row is quantized
+  int pass = 0;
+  for (int rb = r0; rb < r1; rb += rpp, ++pass) {
+    uint4* const sb = (pass & 1) ? buf1 : buf0;
+    if (tid < pass_vecs) sb[tid] = p0;
+    if (tid + kLdsThreads < pass_vecs) sb[tid + kLdsThreads] = p1;
+    if (tid + 2 * kLdsThreads < pass_vecs) sb[tid + 2 * kLdsThreads] = p2;
+    if (tid + 3 * kLdsThreads < pass_vecs) sb[tid + 3 * kLdsThreads] = p3;
+    if (rb + rpp < r1) prefetch(rb + rpp);       // in flight while this pass is quantized
     __syncthreads();
 
-    uint8_t* arow = Aq + static_cast<int64_t>(r) * row_bytes;
-    uint8_t* srow = Asc + static_cast<int64_t>(r) * nb;
-    for (int u = tid; u < units; u += kLdsThreads) {
-      float z[8];
+    const int r = rb + ro;
+    if (ro < rpp && r < r1) {                     // quad-uniform: units is a multiple of 4
+      const int g = kGrouped ? dev::find_group(offsets, G, r) : 0;
+      if (g != cur_g) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int p = (u << 3) + j;
-        z[j] = __uint_as_float(static_cast<uint32_t>(s_row[s_perm[p]]) << 16) * s_d[p];
+        for (int j = 0; j < kUnits; ++j) {
+          const int u = u0 + j * kLdsThreads;
+          if (u < units) load_packed_unit(perm, inv, g, K, u, &un[j]);
+        }
+        cur_g = g;
       }
-      quantize_store(z, u, (K - k_tail) >> 3, k_tail >> 3, k_tail >> 5, arow, srow);
+      const uint16_t* row = reinterpret_cast<const uint16_t*>(sb) + static_cast<int64_t>(ro) * K;
+      uint8_t* arow = Aq + static_cast<int64_t>(r) * row_bytes;
+      uint8_t* srow = Asc + static_cast<int64_t>(r) * nb;
+#pragma unroll
+      for (int j = 0; j < kUnits; ++j) {
+        const int u = u0 + j * kLdsThreads;
+        if (u < units) {
+          float z[8];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t sp = un[j].src2[e];
+            z[2 * e] = __uint_as_float(static_cast<uint32_t>(row[sp & 0xFFFFu]) << 16) * un[j].d[2 * e];
+            z[2 * e + 1] = __uint_as_float(static_cast<uint32_t>(row[sp >> 16]) << 16) * un[j].d[2 * e + 1];
+          }
+          quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, arow, srow);
+        }
+      }
     }
   }
 }
 
-std::once_flag g_attr_once;
+template <bool kGrouped, int kUnits>
+void launch_lds(dim3 grid, size_t lds, hipStream_t stream, const uint16_t* X, int64_t ld_x,
+                int M, int K, int k_tail, const float* inv, const int32_t* perm,
+                const int32_t* offsets, int G, int rows_per_wg, uint8_t* Aq, uint8_t* Asc) {
+  act_quant_lds_kernel<kGrouped, kUnits><<<grid, kLdsThreads, lds, stream>>>(
+      X, ld_x, M, K, k_tail, inv, perm, offsets, G, rows_per_wg, Aq, Asc);
+}
 
 }  // namespace
 
@@ -216,28 +286,35 @@ hipError_t launch_act_quant(const uint16_t* X, int64_t ld_x, int M, int K, int k
           X, ld_x, M, K, k_tail, inv_scale_pos, perm, nullptr, 1, rows_per_wg, Aq, Asc);
     return hipGetLastError();
   }
+  // At most 2 * 2048 * 16 bytes = 64 KiB of LDS: within the default limit.
   const size_t lds = lds_kernel_bytes(K);
-  // Raise the dynamic-LDS cap above the 64 KiB default once; a runtime that
-  // does not need or know the attribute is left to the launch check below.
-  std::call_once(g_attr_once, [] {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&act_quant_lds_kernel<false>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&act_quant_lds_kernel<true>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-    (void)hipGetLastError();
-  });
-  // Two workgroups per CU when the LDS allows it; contiguous row ranges keep
-  // a workgroup inside one expert for most of its rows.
-  const int wgs_per_cu = lds * 2 <= 160 * 1024 ? 2 : 1;
-  const int target = std::max(1, num_cus * wgs_per_cu);
-  const int rows_per_wg = std::max(1, (M + target - 1) / target);
-  const int grid = (M + rows_per_wg - 1) / rows_per_wg;
-  if (grouped)
-    act_quant_lds_kernel<true><<<grid, kLdsThreads, lds, stream>>>(
-        X, ld_x, M, K, k_tail, inv_scale_pos, perm, group_offsets, G, rows_per_wg, Aq, Asc);
-  else
-    act_quant_lds_kernel<false><<<grid, kLdsThreads, lds, stream>>>(
-        X, ld_x, M, K, k_tail, inv_scale_pos, perm, nullptr, 1, rows_per_wg, Aq, Asc);
+  const int rpp = lds_rows_per_pass(units);
+  const int per_thread = (units + kLdsThreads - 1) / kLdsThreads;   // 1..4 (K <= 16384)
+  // Two workgroups per CU; a workgroup's rows are a whole number of passes,
+  // and contiguous row ranges keep it inside one expert for most rows.
+  const int target = std::max(1, num_cus * 2);
+  int rows_per_wg = std::max(1, (M + target - 1) / target);
+  rows_per_wg = (rows_per_wg + rpp - 1) / rpp * rpp;
+  const dim3 grid((M + rows_per_wg - 1) / rows_per_wg);
+  const int32_t* off = grouped ? group_offsets : nullptr;
+  const int g = grouped ? G : 1;
+#define PRQ_LDS_CASE(n)                                                                     \
+  case n:                                                                                   \
+    if (grouped)                                                                            \
+      launch_lds<true, n>(grid, lds, stream, X, ld_x, M, K, k_tail, inv_scale_pos, perm, off, \
+                          g, rows_per_wg, Aq, Asc);                                         \
+    else                                                                                    \
+      launch_lds<false, n>(grid, lds, stream, X, ld_x, M, K, k_tail, inv_scale_pos, perm,   \
+                           off, g, rows_per_wg, Aq, Asc);                                   \
+    break;
+  switch (per_thread) {
+    PRQ_LDS_CASE(1)
+    PRQ_LDS_CASE(2)
+    PRQ_LDS_CASE(3)
+    default:
+      PRQ_LDS_CASE(4)
+  }
+#undef PRQ_LDS_CASE
   return hipGetLastError();
 }
 

@@ -58,6 +58,34 @@ def test_ragged_rows(M):
     _check(c.X, 1024, 64, art["inv_scale"], art["perm"], f"M={M}")
 
 
+@pytest.mark.parametrize("K,k,M", [(768, 64, 131), (4096, 96, 70), (4160, 160, 97), (9728, 224, 65),
+                                   (12320, 288, 66), (16384, 512, 67)])
+def test_many_row_kernel_shapes(K, k, M):
+    """The many-row kernel at every units-per-thread count (K/8 over 512
+    threads: 1 with several rows per pass, 1, 2, 3, 4 and the largest K),
+    ragged row counts, random permutation and scales."""
+    rng = np.random.default_rng(K + M)
+    X = inputs.f32_to_bf16_bits((rng.standard_normal((M, K)) * 3).astype(np.float32))
+    perm = rng.permutation(K).astype(np.int32)
+    inv = rng.uniform(0.05, 8.0, K).astype(np.float32)
+    _check(X, K, k, inv, perm, f"K={K} k={k} M={M}")
+
+
+def test_many_row_kernel_grouped_two_units_per_thread():
+    rng = np.random.default_rng(12)
+    E, K, k = 4, 4160, 160
+    counts = [40, 0, 90, 7]
+    off = inputs.routed_offsets(counts)
+    X = inputs.f32_to_bf16_bits((rng.standard_normal((int(off[-1]), K)) * 2).astype(np.float32))
+    perm = np.stack([rng.permutation(K) for _ in range(E)]).astype(np.int32)
+    inv = rng.uniform(0.1, 4.0, (E, K)).astype(np.float32)
+    say("act_quant case: grouped K=4160", counts)
+    Aq, Asc = _gpu_quant(X, K, k, inv, perm, offsets=off, G=E)
+    rq, rs = pq.quant_act_grouped(X, inv, perm, off, k)
+    np.testing.assert_array_equal(Asc, rs)
+    np.testing.assert_array_equal(Aq, rq)
+
+
 def test_no_scale_no_perm_k0():
     rng = np.random.default_rng(4)
     X = inputs.f32_to_bf16_bits(rng.standard_normal((33, 512)).astype(np.float32) * 3)
