@@ -175,6 +175,7 @@ size_t prq_gemm_workspace_bytes_ex(int32_t M, int32_t N, int32_t K_aug, int32_t 
   if (M <= 0 || N <= 0 || K_aug <= 0 || N % 16 || K_aug % PRQ_BLOCK || splits < 0) return 0;
   if (variant == PRQ_GEMM_AUTO) variant = prq::choose_variant(M, N, K_aug);
   if (variant != PRQ_GEMM_STREAM) return 0;
+  if (splits <= 1 && prq::choose_decode_config(M, N, K_aug, 0, 0, 0, device_cus()).ok) return 0;
   const prq::StreamConfig c = dense_stream_config(M, N, K_aug, splits, device_cus());
   return c.ok ? prq::stream_workspace_bytes(M, 1, N, c.splits, c.reduce) : 0;
 }
@@ -194,6 +195,13 @@ int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t*
   st = current_device(&dev);
   if (st != PRQ_OK) return st;
   if (variant == PRQ_GEMM_AUTO) variant = prq::choose_variant(M, N, K_aug);
+  if (variant == PRQ_GEMM_STREAM && splits <= 1) {
+    // no split-K: the decode kernel, unless K_aug exceeds what it stages
+    const prq::DecodeConfig d = prq::choose_decode_config(M, N, K_aug, 0, 0, 0, dev.num_cus);
+    if (d.ok)
+      return launch_status(prq::launch_gemm_decode(Aq, Asc, M, nullptr, 1, Wp, Wps, N, K_aug, Y, d,
+                                                   stream));
+  }
   if (variant == PRQ_GEMM_STREAM) {
     const prq::StreamConfig c = dense_stream_config(M, N, K_aug, splits, dev.num_cus);
     if (!c.ok) {
@@ -244,6 +252,8 @@ int prq_grouped_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, const int32_t* gr
   const int per_group = (M_total + E - 1) / E;
   if (variant == PRQ_GEMM_AUTO) variant = prq::choose_variant(per_group, N, K_aug);
   if (variant == PRQ_GEMM_STREAM) {
+    // (the decode kernel's grouped mode measured 2x slower on the expert
+    // shapes, whose few K steps leave most of its 16 waves idle)
     const prq::StreamConfig c = prq::choose_stream_config(per_group, N, K_aug, 1, dev.num_cus);
     if (c.ok && prq::stream_config_covers(c, K_aug))
       return launch_status(prq::launch_gemm_stream(Aq, Asc, M_total, group_offsets, E, Wp, Wps, N,

@@ -152,6 +152,20 @@ int prq_tune_gemm_stream(const uint8_t* Aq, const uint8_t* Asc, int M, const int
              : -3;
 }
 
+// The decode GEMM with forced tile / row-split counts (0 = automatic); -1 when the shape
+// is not covered.
+int prq_tune_gemm_decode(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off, int E,
+                         const uint8_t* Wq, const uint8_t* Wsc, int N, int K_aug, float* Y,
+                         int tiles, int row_splits, hipStream_t stream) {
+  if (N % 16 || K_aug % 32 || M <= 0) return -1;
+  const prq::DecodeConfig c = prq::choose_decode_config(off ? (M + E - 1) / E : M, N, K_aug,
+                                                        off ? 1 : 0, tiles, row_splits, 256);
+  if (!c.ok || (off && c.tiles != 1)) return -1;
+  return prq::launch_gemm_decode(Aq, Asc, M, off, E, Wq, Wsc, N, K_aug, Y, c, stream) == hipSuccess
+             ? 0
+             : -3;
+}
+
 // out: uint32[tiles * splits]; Wp: tiles * steps kilobytes; waves * unroll * splits >= steps.
 int prq_probe_stream_read(const uint8_t* Wp, int tiles, int steps, int splits, int waves,
                           int unroll, uint32_t* out, hipStream_t stream) {

@@ -24,6 +24,15 @@ struct StreamConfig {
   bool ok = true;   // false: no configuration covers K_aug (use the tile kernel)
 };
 
+// Launch parameters of the decode GEMM (gemm_decode.hip): a workgroup per
+// 16-row group and `tiles` 16-feature tiles over the whole K range.
+struct DecodeConfig {
+  int tiles = 1;    // feature tiles per workgroup (1, 2 or 4)
+  int row_splits = 1;  // workgroup rows the 16-row groups are dealt to (dense)
+  int unroll = 5;   // K steps per wave (2, 5 or 10), >= ceil(steps / (16 / tiles))
+  bool ok = true;   // false: K_aug needs more LDS or steps than the kernel takes
+};
+
 // act_quant.hip
 hipError_t launch_act_quant(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail,
                             const float* inv_scale, const int32_t* perm,
@@ -55,5 +64,13 @@ size_t stream_workspace_bytes(int M, int E, int N, int splits, int reduce);
 StreamConfig choose_stream_config(int M_per_group, int N, int K_aug, int grouped, int num_cus);
 bool stream_config_covers(const StreamConfig& c, int K_aug);
 int choose_variant(int M_per_group, int N, int K_aug);
+// gemm_decode.hip.  tiles / row_splits = 0 pick them from the rows.
+size_t decode_lds_bytes(int K_aug, int tiles);
+DecodeConfig choose_decode_config(int M_per_group, int N, int K_aug, int grouped, int tiles,
+                                  int row_splits, int num_cus);
+hipError_t launch_gemm_decode(const uint8_t* Aq, const uint8_t* Asc, int M,
+                              const int32_t* group_offsets, int E, const uint8_t* Wp,
+                              const uint8_t* Wps, int N, int K_aug, float* Y,
+                              const DecodeConfig& cfg, hipStream_t stream);
 
 }  // namespace prq

@@ -49,16 +49,56 @@ def test_random_operands(M, N, K_aug, variant):
 
 
 def test_stream_forced_split_that_cannot_stage_is_rejected():
-    """At 64 rows the stream kernel stages the activation in LDS; one split over
-    9984 K elements would need 64 rows x 78 steps (about 349 KB): the call is
-    refused and nothing is launched."""
+    """With a forced split count above one the split-K kernel runs; at 64 rows
+    it stages the activation of the split in LDS, and two splits over 9984 K
+    elements would need 64 rows x 39 steps (about 175 KB): the call is refused
+    and nothing is launched."""
     prq = _prq()
     rng = np.random.default_rng(0)
     Aq, Asc = inputs.random_mxfp4(rng, 64, 9984)
     Wq, Wsc = inputs.random_mxfp4(rng, 320, 9984)
     with pytest.raises(prq.PRQError) as ei:
-        _gpu_gemm(Aq, Asc, Wq, Wsc, prq.GEMM_STREAM, 1)
+        _gpu_gemm(Aq, Asc, Wq, Wsc, prq.GEMM_STREAM, 2)
     assert ei.value.status == prq.PRQ_EINVAL
+
+
+def _tune_decode(Aq, Asc, Wq, Wsc, tiles, row_splits, off=None, E=1):
+    """The decode kernel with explicit tiles per workgroup and row splits."""
+    import ctypes
+    from paper_2609_22106_amd import build
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    P, I = ctypes.c_void_p, ctypes.c_int
+    lib.prq_tune_gemm_decode.argtypes = [P, P, I, P, I, P, P, I, I, P, I, I, P]
+    W = _packed(Wq, Wsc)
+    A, S = dev(Aq), dev(Asc)
+    M = Aq.shape[0]
+    Y = torch.full((M, W.N), float("nan"), dtype=torch.float32, device="cuda")
+    o = dev(off) if off is not None else None
+    st = lib.prq_tune_gemm_decode(A.data_ptr(), S.data_ptr(), M, None if o is None else o.data_ptr(),
+                                  E, W.Wp.data_ptr(), W.Wps.data_ptr(), W.N, W.K_aug, Y.data_ptr(),
+                                  tiles, row_splits, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    return st, host(Y)
+
+
+@pytest.mark.parametrize("M,N,K_aug", [(1, 2560, 9984), (40, 320, 2624), (64, 272, 9984),
+                                       (17, 48, 1088), (100, 160, 832)])
+@pytest.mark.parametrize("tiles,row_splits", [(1, 1), (1, 4), (2, 2), (4, 1), (4, 3)])
+def test_decode_kernel_configs(M, N, K_aug, tiles, row_splits):
+    """Every tile count and row split (a workgroup looping over several row
+    groups, partial last tile group, ragged rows and K); shapes whose K needs
+    more weight steps per wave than the kernel holds are refused (-1)."""
+    rng = np.random.default_rng(M * 31 + tiles * 7 + row_splits)
+    Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+    Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
+    say("gemm case: decode", M, N, K_aug, "tiles", tiles, "row_splits", row_splits)
+    st, Y = _tune_decode(Aq, Asc, Wq, Wsc, tiles, row_splits)
+    steps = -(-K_aug // 128)
+    if -(-steps // (16 // tiles)) > 10:
+        assert st == -1
+        return
+    assert st == 0
+    assert_gemm_close(Y, pq.gemm(Aq, Asc, Wq, Wsc), f"decode {M}x{N}x{K_aug} t{tiles} r{row_splits}")
 
 
 @pytest.mark.parametrize("M,splits", [(8, 1), (24, 0), (24, 2), (24, 3), (24, 7), (24, 19), (64, 6)])
@@ -97,6 +137,17 @@ def test_split_k_workspace_reuse_and_two_splits_are_deterministic():
             ys = [_gpu_gemm(Aq, Asc, Wq, Wsc, prq.GEMM_STREAM, splits, ws) for _ in range(3)]
             np.testing.assert_array_equal(ys[0].view(np.uint32), ys[1].view(np.uint32))
             np.testing.assert_array_equal(ys[0].view(np.uint32), ys[2].view(np.uint32))
+
+
+def test_decode_kernel_grouped_mode():
+    """The decode kernel's grouped mode (one tile per workgroup, the expert's
+    16-row groups looped in one workgroup), empty experts included."""
+    counts = [0, 5, 40, 0, 17, 1]
+    off, Aq, Asc, Wq, Wsc = _grouped_case(counts, 64, 1088, 5)
+    say("gemm case: decode grouped", counts)
+    st, Y = _tune_decode(Aq, Asc, Wq, Wsc, 1, 1, off=off, E=len(counts))
+    assert st == 0
+    assert_gemm_close(Y, pq.grouped_gemm(Aq, Asc, off, Wq, Wsc), "decode grouped")
 
 
 def test_hand_values():
