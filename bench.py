@@ -365,7 +365,8 @@ def cpu_baseline(np, layers, M_list, budget_s=12.0):
 
 
 CALIB_BYTES = 512 * 2 ** 20
-GEMM_SOURCES = ("gemm_stream.hip", "gemm_tile.hip", "mx_device.hpp", "prq_internal.h", "abi.cpp")
+GEMM_SOURCES = ("gemm_decode.hip", "gemm_stream.hip", "gemm_tile.hip", "mx_device.hpp",
+                "prq_internal.h", "abi.cpp")
 
 
 def copy_calibration(torch, nbytes=CALIB_BYTES, reps=5):
@@ -426,7 +427,8 @@ def traffic_from_counters(workload, fetch_dir, write_dir, command):
         rows = _counter_rows(run_dir, counter)
         calib = [v for n, v in rows if "neg_kernel" in n]
         gemm = [(n, v) for n, v in rows if "prq" in n and any(
-            t in n for t in ("gemm_stream_kernel", "gemm_tile_kernel", "reduce_partials_kernel", "zero_kernel"))]
+            t in n for t in ("gemm_decode_kernel", "gemm_stream_kernel", "gemm_tile_kernel",
+                             "reduce_partials_kernel", "zero_kernel"))]
         launches = [v for n, v in gemm if "gemm_" in n]
         if not calib or not launches:
             raise SystemExit(f"{counter}: calibration or GEMM dispatches missing in {run_dir}")

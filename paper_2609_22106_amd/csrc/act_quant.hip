@@ -272,9 +272,17 @@ hipError_t launch_act_quant(const uint16_t* X, int64_t ld_x, int M, int K, int k
                             const float* inv_scale_pos, const int32_t* perm,
                             const int32_t* group_offsets, int G, uint8_t* Aq, uint8_t* Asc,
                             int num_cus, hipStream_t stream) {
+  return launch_act_quant_kernel(X, ld_x, M, K, k_tail, inv_scale_pos, perm, group_offsets, G, Aq,
+                                 Asc, num_cus, 0, stream);
+}
+
+hipError_t launch_act_quant_kernel(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail,
+                                   const float* inv_scale_pos, const int32_t* perm,
+                                   const int32_t* group_offsets, int G, uint8_t* Aq, uint8_t* Asc,
+                                   int num_cus, int kernel, hipStream_t stream) {
   const bool grouped = group_offsets && G > 1;
   const int units = K >> 3;
-  if (M <= 64) {
+  if (kernel == 1 || (kernel == 0 && M <= 64)) {
     // Few rows: spread the positions over workgroups, at most ~16 row chunks.
     const int rows_per_wg = std::max(1, (M + 15) / 16);
     const dim3 grid((units + kRowsThreads - 1) / kRowsThreads, (M + rows_per_wg - 1) / rows_per_wg);

@@ -152,6 +152,17 @@ int prq_tune_gemm_stream(const uint8_t* Aq, const uint8_t* Asc, int M, const int
              : -3;
 }
 
+// Activation quantization with a forced kernel (1 few-rows, 2 many-rows).
+int prq_tune_act_quant(const void* X, int64_t ld_x, int M, int K, int k_tail, const float* inv,
+                       const int32_t* perm, uint8_t* Aq, uint8_t* Asc, int kernel,
+                       hipStream_t stream) {
+  if (M <= 0 || K <= 0 || K % 32 || k_tail % 32 || k_tail > K || K > 16384 || ld_x < K) return -1;
+  return prq::launch_act_quant_kernel(static_cast<const uint16_t*>(X), ld_x, M, K, k_tail, inv, perm,
+                                      nullptr, 1, Aq, Asc, 256, kernel, stream) == hipSuccess
+             ? 0
+             : -3;
+}
+
 // The decode GEMM with forced tile / row-split counts (0 = automatic); -1 when the shape
 // is not covered.
 int prq_tune_gemm_decode(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off, int E,

@@ -71,6 +71,34 @@ def test_many_row_kernel_shapes(K, k, M):
     _check(X, K, k, inv, perm, f"K={K} k={k} M={M}")
 
 
+def test_few_row_kernel_grouped():
+    """Grouped rows through the few-rows kernel (at most 64 rows): a workgroup's
+    row range crosses experts, empty experts included."""
+    rng = np.random.default_rng(13)
+    E, K, k = 6, 768, 64
+    counts = [3, 0, 20, 1, 0, 9]
+    off = inputs.routed_offsets(counts)
+    X = inputs.f32_to_bf16_bits((rng.standard_normal((int(off[-1]), K)) * 3).astype(np.float32))
+    perm = np.stack([rng.permutation(K) for _ in range(E)]).astype(np.int32)
+    inv = rng.uniform(0.1, 4.0, (E, K)).astype(np.float32)
+    say("act_quant case: grouped few rows", counts)
+    Aq, Asc = _gpu_quant(X, K, k, inv, perm, offsets=off, G=E)
+    rq, rs = pq.quant_act_grouped(X, inv, perm, off, k)
+    np.testing.assert_array_equal(Asc, rs)
+    np.testing.assert_array_equal(Aq, rq)
+
+
+@pytest.mark.parametrize("M", [1, 5, 48, 64])
+def test_few_row_kernel_largest_rows(M):
+    """K = 16384 (four staged rows of 32 KiB per workgroup at 64 rows)."""
+    rng = np.random.default_rng(M)
+    K, k = 16384, 512
+    X = inputs.f32_to_bf16_bits((rng.standard_normal((M, K)) * 3).astype(np.float32))
+    perm = rng.permutation(K).astype(np.int32)
+    inv = rng.uniform(0.05, 8.0, K).astype(np.float32)
+    _check(X, K, k, inv, perm, f"K=16384 M={M}")
+
+
 def test_many_row_kernel_grouped_two_units_per_thread():
     rng = np.random.default_rng(12)
     E, K, k = 4, 4160, 160
