@@ -4,8 +4,9 @@
 //
 //   Y[m, n] = sum_b 2^(Asc[m,b]-127) 2^(Wsc[n,b]-127) sum_{i<32} A[m,32b+i] W[n,32b+i]
 //
-// on v_mfma_scale_f32_16x16x128_f8f6f4 (FP4 operands, E8M0 scales in the
-// instruction, float32 accumulation).
+// on v_mfma_scale_f32_32x32x64_f8f6f4 (FP4 operands, E8M0 scales in the
+// instruction, float32 accumulation; this form issues twice the products per
+// cycle of the 16x16x128 one).
 //
 // A workgroup computes a kBM x kBN tile with kWM x kWN waves (wave tile
 // kBM/kWM x kBN/kWN).  Per 128-element K step both operands are staged in LDS
@@ -36,11 +37,10 @@
 namespace prq {
 namespace {
 
-using dev::v4f;
+using dev::v16f;
 
 constexpr int kStepK = 128;
 constexpr int kStepBytes = kStepK / 2;
-constexpr uint32_t kNeutralScale = 127;
 constexpr int kXcds = 8;
 
 // Bijective remap of a linear workgroup id: ids dealt round-robin to kXcds
@@ -112,11 +112,13 @@ __device__ __forceinline__ void static_for(F&& f) {
 #define PRQ_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
 
 // s_waitcnt immediate that waits until at most n vector-memory operations of
-// this wave are outstanding (expcnt and lgkmcnt left at their maxima).
+// this wave are outstanding and all its LDS reads are complete (expcnt left at
+// its maximum).  Before a bare barrier this makes the wave's reads of the
+// stage that the next direct-to-LDS loads overwrite finished, not just issued.
 template <int n>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(n >= 0 && n < 64, "vmcnt");
-  __builtin_amdgcn_s_waitcnt((n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+  __builtin_amdgcn_s_waitcnt((n & 0xF) | ((n >> 4) << 14) | (0x7 << 4));
 }
 
 template <int kBM, int kBN, int kWM, int kWN, int kNS, bool kGrouped>
@@ -127,7 +129,8 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   constexpr int kWaves = kWM * kWN;
   constexpr int kThreads = kWaves * 64;
   constexpr int kTM = kBM / kWM, kTN = kBN / kWN;    // wave tile
-  constexpr int kFM = kTM / 16, kFN = kTN / 16;      // 16x16 fragments per wave
+  constexpr int kFM = kTM / 32, kFN = kTN / 32;      // 32x32 fragments per wave
+  static_assert(kTM % 32 == 0 && kTN % 32 == 0, "wave tile of whole 32x32 fragments");
   constexpr int kABlk = kBM / 16, kBBlk = kBN / 16;  // 16-row operand blocks per step
   static_assert(kABlk % kWaves == 0 && kBBlk % kWaves == 0, "blocks split evenly over waves");
   constexpr int kAPer = kABlk / kWaves, kBPer = kBBlk / kWaves;
@@ -227,32 +230,63 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
                                        PRQ_LPTR(st + kOffBs + (wave + i * kWaves) * 256), 1, 0, 0);
   };
 
-  v4f acc[kFM][kFN];
+  v16f acc[kFM][kFN];
 #pragma unroll
   for (int i = 0; i < kFM; ++i)
 #pragma unroll
-    for (int j = 0; j < kFN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < kFN; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  auto compute = [&](const uint8_t* st) {
-    uint4 a[kFM], b[kFN];
-    uint32_t sa[kFM], sb[kFN];
+  // A 32-row x 64-element operand of the 32x32x64 MFMA read from the staged
+  // 16-row x 128-element blocks: lane l takes row l % 32 (block 2f + bit 4 of
+  // l), K part 2h + l / 32 of the step -- in-block lane (l % 16) + 16 (2h + l / 32),
+  // so each 16 lanes read 256 contiguous bytes (conflict-free).
+  const int blk_sel = (lane >> 4) & 1;
+  const int lib0 = (lane & 15) + 16 * (lane >> 5);
+  auto load_half = [&](const uint8_t* st, int h, uint4 (&a)[kFM], uint4 (&b)[kFN],
+                       uint32_t (&sa)[kFM], uint32_t (&sb)[kFN]) {
+    const int lib = lib0 + 32 * h;
 #pragma unroll
     for (int i = 0; i < kFM; ++i) {
-      const int blk = wm * kFM + i;
-      a[i] = *reinterpret_cast<const uint4*>(st + blk * 1024 + lane * 16);
-      sa[i] = *reinterpret_cast<const uint32_t*>(st + kOffAs + blk * 256 + lane * 4);
+      const int blk = wm * (kTM / 16) + 2 * i + blk_sel;
+      a[i] = *reinterpret_cast<const uint4*>(st + blk * 1024 + lib * 16);
+      sa[i] = *reinterpret_cast<const uint32_t*>(st + kOffAs + blk * 256 + lib * 4);
     }
 #pragma unroll
     for (int j = 0; j < kFN; ++j) {
-      const int blk = wn * kFN + j;
-      b[j] = *reinterpret_cast<const uint4*>(st + kOffB + blk * 1024 + lane * 16);
-      sb[j] = *reinterpret_cast<const uint32_t*>(st + kOffBs + blk * 256 + lane * 4);
+      const int blk = wn * (kTN / 16) + 2 * j + blk_sel;
+      b[j] = *reinterpret_cast<const uint4*>(st + kOffB + blk * 1024 + lib * 16);
+      sb[j] = *reinterpret_cast<const uint32_t*>(st + kOffBs + blk * 256 + lib * 4);
     }
+  };
+  auto mfma_half = [&](const uint4 (&a)[kFM], const uint4 (&b)[kFN], const uint32_t (&sa)[kFM],
+                       const uint32_t (&sb)[kFN]) {
 #pragma unroll
     for (int i = 0; i < kFM; ++i)
 #pragma unroll
       for (int j = 0; j < kFN; ++j)
-        acc[i][j] = dev::mfma_fp4_16x16x128(a[i], b[j], sa[i], sb[j], acc[i][j]);
+        acc[i][j] = dev::mfma_fp4_32x32x64(a[i], b[j], sa[i], sb[j], acc[i][j]);
+  };
+  // With one wave per SIMD (4-wave workgroups) the register budget holds both
+  // K halves' operands, so all LDS reads of a step are issued before its
+  // MFMAs; with two waves per SIMD the halves go one after the other.
+  constexpr bool kBothHalves = kWaves <= 4;
+  auto compute = [&](const uint8_t* st) {
+    uint4 a0[kFM], b0[kFN];
+    uint32_t sa0[kFM], sb0[kFN];
+    load_half(st, 0, a0, b0, sa0, sb0);
+    if constexpr (kBothHalves) {
+      uint4 a1[kFM], b1[kFN];
+      uint32_t sa1[kFM], sb1[kFN];
+      load_half(st, 1, a1, b1, sa1, sb1);
+      mfma_half(a0, b0, sa0, sb0);
+      mfma_half(a1, b1, sa1, sb1);
+    } else {
+      mfma_half(a0, b0, sa0, sb0);
+      load_half(st, 1, a0, b0, sa0, sb0);
+      mfma_half(a0, b0, sa0, sb0);
+    }
   };
 
   // Prologue: steps 0 .. kNS-2 in flight.  Every wave issues the same
@@ -282,16 +316,17 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   }
   wait_vmcnt<0>();   // no direct-to-LDS write outlives the workgroup
 
-  // Lane holds C[4 (l / 16) + q][l % 16] of each 16x16 fragment.
+  // Element e of a lane's fragment is C[8 (e / 4) + 4 (l / 32) + e % 4][l % 32]:
+  // activation row, feature column (32 lanes store 128 contiguous bytes).
 #pragma unroll
   for (int i = 0; i < kFM; ++i)
 #pragma unroll
     for (int j = 0; j < kFN; ++j) {
-      const int n = (t0 + wn * kFN + j) * 16 + lr;
+      const int n = t0 * 16 + wn * kTN + j * 32 + (lane & 31);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int m = row_begin + wm * kTM + i * 16 + 4 * lk + q;
-        if (m < row_end && n < N) Y[static_cast<int64_t>(m) * N + n] = acc[i][j][q];
+      for (int e = 0; e < 16; ++e) {
+        const int m = row_begin + wm * kTM + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        if (m < row_end && n < N) Y[static_cast<int64_t>(m) * N + n] = acc[i][j][e];
       }
     }
 }

@@ -71,6 +71,23 @@ __device__ __forceinline__ v4f mfma_fp4_16x16x128(const uint4& a, const uint4& b
                                                           static_cast<int>(sb));
 }
 
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+// 32x32x64 block-scaled FP4 MFMA (the full-rate form: twice the products of
+// the 16x16x128 form per issue slot): lane l supplies row l % 32, K elements
+// [32 (l / 32), +32) of each operand with that block's E8M0 scale, and holds
+// C[8 (j / 4) + 4 (l / 32) + j % 4][l % 32] in element j of the result.
+__device__ __forceinline__ v16f mfma_fp4_32x32x64(const uint4& a, const uint4& b, uint32_t sa,
+                                                  uint32_t sb, v16f c) {
+  v8i av = {static_cast<int>(a.x), static_cast<int>(a.y), static_cast<int>(a.z),
+            static_cast<int>(a.w), 0, 0, 0, 0};
+  v8i bv = {static_cast<int>(b.x), static_cast<int>(b.y), static_cast<int>(b.z),
+            static_cast<int>(b.w), 0, 0, 0, 0};
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, c, 4, 4, 0,
+                                                         static_cast<int>(sa), 0,
+                                                         static_cast<int>(sb));
+}
+
 // Group g with off[g] <= row < off[g+1] for non-decreasing offsets
 // (empty groups are skipped): the largest g in [0, G) with off[g] <= row.
 __device__ __forceinline__ int find_group(const int32_t* __restrict__ off, int G, int row) {

@@ -56,6 +56,25 @@ __global__ void cvt_pairs(const float* x, const float* y, const float* s, int n,
 
 __global__ void empty_kernel() {}
 
+// MFMA issue rate: every wave runs `iters` rounds of 8 independent
+// block-scaled FP4 MFMAs on register operands (no memory traffic in the loop).
+__global__ __launch_bounds__(256) void mfma_rate_probe(int iters, float* out) {
+  const uint32_t l = threadIdx.x;
+  const uint4 a = make_uint4(0x22222222u ^ l, 0x12121212u, 0x21212121u, 0x11111111u);
+  const uint4 b = make_uint4(0x11111111u, 0x22222222u ^ l, 0x12121212u, 0x21212121u);
+  prq::dev::v4f acc[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc[i] = prq::dev::v4f{0.f, 0.f, 0.f, 0.f};
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = prq::dev::mfma_fp4_16x16x128(a, b, 120u + i, 121u, acc[i]);
+  }
+  float sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) sum += acc[i][0] + acc[i][1] + acc[i][2] + acc[i][3];
+  out[blockIdx.x * blockDim.x + threadIdx.x] = sum;
+}
+
 // Direct global->LDS loads (one wave): 16 bytes per lane from g16 into LDS at
 // byte 0, one byte per lane from g1 into LDS at byte 4096; the 8 KiB LDS image
 // (zeroed first) is copied out so the host can see where each lane's data went.
@@ -150,6 +169,73 @@ int prq_tune_gemm_stream(const uint8_t* Aq, const uint8_t* Asc, int M, const int
                  hipSuccess
              ? 0
              : -3;
+}
+
+typedef float v16f_t __attribute__((ext_vector_type(16)));
+
+// The same for the 32x32x64 block-scaled FP4 MFMA (4 independent chains).
+__global__ __launch_bounds__(256) void mfma32_rate_probe(int iters, float* out) {
+  const int l = static_cast<int>(threadIdx.x);
+  const prq::dev::v8i a = {0x22222222 ^ l, 0x12121212, 0x21212121, 0x11111111, 0, 0, 0, 0};
+  const prq::dev::v8i b = {0x11111111, 0x22222222 ^ l, 0x12121212, 0x21212121, 0, 0, 0, 0};
+  v16f_t acc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) acc[i][j] = 0.f;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      acc[i] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, acc[i], 4, 4, 0, 120 + i, 0, 121);
+  }
+  float sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) sum += acc[i][j];
+  out[blockIdx.x * blockDim.x + threadIdx.x] = sum;
+}
+
+// One 32x32x64 block-scaled FP4 MFMA on lane-supplied operands: a, b are
+// [64 lanes][16 bytes], sa, sb one E8M0 byte per lane; out [64 lanes][16].
+__global__ __launch_bounds__(64) void mfma32_probe(const uint4* a, const uint4* b,
+                                                   const uint32_t* sa, const uint32_t* sb,
+                                                   float* out) {
+  const int l = threadIdx.x;
+  const uint4 x = a[l], y = b[l];
+  const prq::dev::v8i av = {static_cast<int>(x.x), static_cast<int>(x.y), static_cast<int>(x.z),
+                            static_cast<int>(x.w), 0, 0, 0, 0};
+  const prq::dev::v8i bv = {static_cast<int>(y.x), static_cast<int>(y.y), static_cast<int>(y.z),
+                            static_cast<int>(y.w), 0, 0, 0, 0};
+  v16f_t c;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) c[j] = 0.f;
+  c = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, c, 4, 4, 0, static_cast<int>(sa[l]), 0,
+                                                      static_cast<int>(sb[l]));
+#pragma unroll
+  for (int j = 0; j < 16; ++j) out[l * 16 + j] = c[j];
+}
+
+int prq_probe_mfma32(const void* a, const void* b, const void* sa, const void* sb, float* out,
+                     hipStream_t stream) {
+  mfma32_probe<<<1, 64, 0, stream>>>(static_cast<const uint4*>(a), static_cast<const uint4*>(b),
+                                     static_cast<const uint32_t*>(sa),
+                                     static_cast<const uint32_t*>(sb), out);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+// 4 waves per block, 4 * iters 32x32x64 MFMAs per wave.
+int prq_probe_mfma32_rate(int blocks, int iters, float* out, hipStream_t stream) {
+  if (blocks <= 0 || iters <= 0) return -1;
+  mfma32_rate_probe<<<blocks, 256, 0, stream>>>(iters, out);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+// out: float[blocks * 256]; 4 waves per block, 8 * iters MFMAs per wave.
+int prq_probe_mfma_rate(int blocks, int iters, float* out, hipStream_t stream) {
+  if (blocks <= 0 || iters <= 0) return -1;
+  mfma_rate_probe<<<blocks, 256, 0, stream>>>(iters, out);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
 // Activation quantization with a forced kernel (1 few-rows, 2 many-rows).

@@ -74,6 +74,46 @@ def test_block_scaled_fp4_mfma_layout():
     assert ("contiguous32", False, False) in matches, f"layout differs; matches={matches}\n{got[:4]}"
 
 
+def test_block_scaled_fp4_mfma_32x32x64_layout():
+    """The 32x32x64 form: lane l supplies row l % 32 and K elements
+    [32 (l / 32), +32) of its operand (low nibble first), with that block's
+    scale; it receives C[8 (j / 4) + 4 (l / 32) + j % 4][l % 32] in element j."""
+    lib = _probe_lib()
+    lib.prq_probe_mfma32.argtypes = [ctypes.c_void_p] * 6
+    rng = np.random.default_rng(1)
+    a = rng.integers(0, 256, (64, 16), dtype=np.uint8)
+    b = rng.integers(0, 256, (64, 16), dtype=np.uint8)
+    sa = rng.integers(124, 131, 64).astype(np.uint32)
+    sb = rng.integers(124, 131, 64).astype(np.uint32)
+    dev = [torch.from_numpy(x.copy()).cuda() for x in (a, b, sa.view(np.int32), sb.view(np.int32))]
+    out = torch.zeros(64 * 16, dtype=torch.float32, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+    assert lib.prq_probe_mfma32(*[t.data_ptr() for t in dev], out.data_ptr(), s) == 0
+    got = out.cpu().numpy().reshape(64, 16).astype(np.float64)
+
+    def operand(lane_bytes, lane_scales):
+        mat = np.zeros((32, 64))
+        vals = E2M1[_nibbles(lane_bytes, False)]
+        for l in range(64):
+            r, g = l % 32, l // 32
+            mat[r, 32 * g:32 * g + 32] = vals[l] * 2.0 ** (int(lane_scales[l]) - 127)
+        return mat
+
+    C = operand(a, sa) @ operand(b, sb).T
+    hyps = {
+        "8(j/4)+4(l/32)+j%4": lambda l, j: (8 * (j // 4) + 4 * (l // 32) + j % 4, l % 32),
+        "16(l/32)+j": lambda l, j: (16 * (l // 32) + j, l % 32),
+        "transposed": lambda l, j: (l % 32, 8 * (j // 4) + 4 * (l // 32) + j % 4),
+    }
+    matches = []
+    for name, f in hyps.items():
+        pred = np.array([[C[f(l, j)] for j in range(16)] for l in range(64)])
+        if np.allclose(pred, got, rtol=1e-6, atol=1e-6 * np.abs(C).max()):
+            matches.append(name)
+    print("32x32x64 matching layouts:", matches, flush=True)
+    assert matches == ["8(j/4)+4(l/32)+j%4"], f"layout differs; matches={matches}\n{got[:2]}"
+
+
 def test_hw_fp4_convert_matches_rounding_rule():
     lib = _probe_lib()
     res = torch.zeros(17, dtype=torch.int32, device="cuda")
