@@ -67,7 +67,8 @@ enum {
 enum {
   PRQ_GEMM_AUTO = 0,   /* chosen from the shape                               */
   PRQ_GEMM_TILE = 1,   /* LDS-tiled block-scaled MFMA kernel (prefill shapes) */
-  PRQ_GEMM_STREAM = 2  /* weight-streaming split-K kernel (decode shapes)     */
+  PRQ_GEMM_STREAM = 2  /* weight-streaming decode kernels: whole-K workgroups
+                          (splits 0 or 1), split-K for a forced split count > 1 */
 };
 
 /* Human-readable text of a status code (static storage). */
@@ -109,6 +110,30 @@ int prq_prepare(const uint16_t* W_bf16, int32_t N, int32_t K,
                 double alpha, int32_t k_tail, int32_t scale_mode,
                 float* scale, float* inv_scale, int32_t* perm, float* inv_scale_pos,
                 uint8_t* Wq, uint8_t* Wsc, double* col_err);
+
+/* Options of prq_prepare_ex. */
+enum {
+  PRQ_PREPARE_E8M0_SEARCH = 1  /* weight-side E8M0 block-scale search (below)  */
+};
+
+/*
+ * prq_prepare_ex -- prq_prepare with options; flags = 0 is prq_prepare.
+ *   PRQ_PREPARE_E8M0_SEARCH: the "E8M0-W" variant of Sec. Ablation Studies, a
+ *   local search of the weight block scales.  The paper gives no rule; the one
+ *   used here: every 32-element block of Q(W~) and of Q(R_W) takes the first of
+ *   the E8M0 codes c0, c0 - 1, c0 + 1 (c0 the OCP code of the block, each
+ *   clamped to [0, 254]) whose sum of squared errors sum_i (w_i - deq_i)^2 --
+ *   accumulated in double, one element at a time in index order -- is smallest,
+ *   so no block is worse than under plain Q(.).  R_W is taken against the
+ *   searched Q(W~); col_err and the tail selection use plain Q(.) (Algorithm 1
+ *   unchanged).  The activation side is not affected.
+ * Returns as prq_prepare, and PRQ_EINVAL for unknown flag bits.
+ */
+int prq_prepare_ex(const uint16_t* W_bf16, int32_t N, int32_t K,
+                   const uint16_t* Xcal_bf16, int32_t T,
+                   double alpha, int32_t k_tail, int32_t scale_mode, int32_t flags,
+                   float* scale, float* inv_scale, int32_t* perm, float* inv_scale_pos,
+                   uint8_t* Wq, uint8_t* Wsc, double* col_err);
 
 /*
  * prq_quant_act -- activation side of Eq. 3 with the online copy (Sec.

@@ -113,6 +113,56 @@ def mx_quantize(v):
     return codes.reshape(*lead, K), scales.reshape(*lead, K // BLOCK)
 
 
+def mx_quantize_with_scales(v, scales):
+    """Elements of float32 ``v`` rounded to E2M1 under given E8M0 block codes
+    (the element rule of Q(.) with the shared exponent replaced): codes uint8."""
+    v = np.asarray(v)
+    if v.dtype != np.float32:
+        raise TypeError("Q(.) takes float32 input (the precision of its decisions)")
+    K = v.shape[-1]
+    blk = v.astype(np.float64).reshape(*v.shape[:-1], K // BLOCK, BLOCK)
+    sc = np.asarray(scales, dtype=np.int64)
+    t = np.ldexp(blk, E8M0_BIAS - sc[..., None])     # v / 2**(code - 127), exact
+    idx = _round_to_e2m1_index(t)
+    sign = np.signbit(blk).astype(np.uint8) << 3
+    return (idx | sign).reshape(v.shape)
+
+
+SEARCH_OFFSETS = (0, -1, 1)   # candidate codes around the OCP code, in preference order
+
+
+def block_squared_errors(v, codes, scales):
+    """sum_i (v_i - deq_i)^2 per 32-block, float64, summed in element order."""
+    K = v.shape[-1]
+    d = (v.astype(np.float64) - mx_dequantize(codes, scales)).reshape(*v.shape[:-1], K // BLOCK, BLOCK)
+    err = np.zeros(d.shape[:-1])
+    for i in range(BLOCK):               # one element at a time: a fixed summation order
+        err = err + d[..., i] * d[..., i]
+    return err
+
+
+def mx_quantize_searched(v):
+    """Q(.) with a local E8M0 search per block (the weight-side block-scale
+    search of Sec. Ablation Studies, whose rule the paper does not give; the
+    reading here): among the codes c0, c0 - 1, c0 + 1 (c0 the OCP code,
+    clamped to [0, 254]) keep the first with the smallest squared block error
+    sum_i (v_i - deq_i)^2, so no block is worse than under Q(.)."""
+    v = np.asarray(v)
+    codes0, sc0 = mx_quantize(v)
+    best_codes, best_sc = codes0, sc0.copy()
+    best_err = block_squared_errors(v, codes0, sc0)
+    for off in SEARCH_OFFSETS[1:]:
+        sc = np.clip(sc0.astype(np.int64) + off, 0, 254).astype(np.uint8)
+        codes = mx_quantize_with_scales(v, sc)
+        err = block_squared_errors(v, codes, sc)
+        better = err < best_err
+        best_err = np.where(better, err, best_err)
+        best_sc = np.where(better, sc, best_sc)
+        better_el = np.repeat(better, BLOCK, axis=-1).reshape(v.shape)
+        best_codes = np.where(better_el, codes, best_codes)
+    return best_codes.astype(np.uint8), best_sc.astype(np.uint8)
+
+
 def mx_dequantize(codes, scales):
     """deq(code, scale) = e2m1(code) * 2**(scale - 127), float64."""
     codes = np.asarray(codes, dtype=np.uint8)

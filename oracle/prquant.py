@@ -33,7 +33,7 @@ import math
 
 import numpy as np
 
-from .mxfp4 import BLOCK, mx_dequantize, mx_quantize, pack_codes, qdq
+from .mxfp4 import BLOCK, mx_dequantize, mx_quantize, mx_quantize_searched, pack_codes, qdq
 
 SCALE_MODES = ("smooth", "act_only", "none")
 CLAMP_MIN = 1e-5
@@ -111,12 +111,16 @@ def tail_permutation(K, selected):
 # --------------------------------------------------------------------------- #
 # Algorithm 1 for one alpha: scaling, selection, permutation, Eq. 2, Eq. 3
 # --------------------------------------------------------------------------- #
-def prepare(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth"):
+def prepare(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth", scale_search=False):
     """Offline calibration/export for one alpha (Algorithm 1, steps 1, 3-7, 10).
 
     W_bf16: uint16 [N, K] (bf16 bits of W_down); Xcal_bf16: uint16 [T, K].
     Returns a dict with the exported artefacts (scale, inv_scale, perm, packed
     Wq [N, (K+k)/2], Wsc [N, (K+k)/32]) and the intermediates the tests check.
+    scale_search: the E8M0-W variant of Sec. Ablation Studies -- Q(W~) and
+    Q(R_W) with the local block-scale search (mx_quantize_searched); the
+    residual is taken against the searched Q(W~); the column errors that pick
+    the tail keep the plain Q(.) (Algorithm 1, step 4, unchanged).
     """
     W_bf16 = np.asarray(W_bf16, dtype=np.uint16)
     Xcal_bf16 = np.asarray(Xcal_bf16, dtype=np.uint16)
@@ -131,13 +135,14 @@ def prepare(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth"):
     selected = select_topk(err, k_tail)
     perm = tail_permutation(K, selected)
     W_t = np.ascontiguousarray(W_s[:, perm])                # W D P (Eq. 1)
-    codes_t, scales_t = mx_quantize(W_t)                    # Q(W~)
+    quantize = mx_quantize_searched if scale_search else mx_quantize
+    codes_t, scales_t = quantize(W_t)                       # Q(W~)
     deq_t = mx_dequantize(codes_t, scales_t)
     R64 = W_t[:, K - k_tail:].astype(np.float64) - deq_t[:, K - k_tail:]   # Eq. 2
     R = R64.astype(np.float32)
     if not np.array_equal(R.astype(np.float64), R64):
         raise AssertionError("tail residual is not exact in float32")
-    codes_r, scales_r = mx_quantize(R)                      # Q(R_W)
+    codes_r, scales_r = quantize(R)                         # Q(R_W)
     codes_aug = np.concatenate([codes_t, codes_r], axis=1)  # Q([W~, R_W]) (Eq. 3)
     scales_aug = np.concatenate([scales_t, scales_r], axis=1)
     return {
@@ -249,8 +254,9 @@ def nrmse(Y_hat, Y_ref):
     return float(np.linalg.norm(Y_hat - Y_ref) / np.linalg.norm(Y_ref))
 
 
-def prquant_forward(X_bf16, W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth"):
+def prquant_forward(X_bf16, W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth",
+                    scale_search=False):
     """Y_hat of Eq. 3 end to end: prepare, quantize the activation, GEMM."""
-    art = prepare(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode)
+    art = prepare(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode, scale_search)
     Aq, Asc = quant_act(X_bf16, art["inv_scale"], art["perm"], k_tail)
     return gemm(Aq, Asc, art["Wq"], art["Wsc"]), art

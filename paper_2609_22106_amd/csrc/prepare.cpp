@@ -79,6 +79,46 @@ inline uint8_t mx_quantize_block(const float* v, uint8_t* codes) {
   return sc;
 }
 
+// Quantize one block with a given E8M0 code (code <= 253 keeps 2^(127 - code)
+// a normal float); t may reach 16 for code = c0 - 1 and saturates at 6.
+inline void mx_quantize_block_with(const float* v, uint8_t sc, uint8_t* codes) {
+  float mul = mx_inv_scale(sc);
+  for (int i = 0; i < PRQ_BLOCK; ++i) codes[i] = e2m1_code(v[i] * mul, v[i]);
+}
+
+// sum_i (v_i - deq_i)^2 in double, one element at a time in index order (each
+// difference and square is exact; the order fixes the rounding of the sum).
+inline double block_squared_error(const float* v, const uint8_t* codes, uint8_t sc) {
+  double err = 0.0;
+  for (int i = 0; i < PRQ_BLOCK; ++i) {
+    double d = static_cast<double>(v[i]) - static_cast<double>(e2m1_value(codes[i], sc));
+    err += d * d;
+  }
+  return err;
+}
+
+// Q(.) with the local E8M0 search of the E8M0-W variant: the first of the
+// codes c0, c0 - 1, c0 + 1 (clamped to [0, 254]) with the smallest block error.
+inline uint8_t mx_quantize_block_searched(const float* v, uint8_t* codes) {
+  uint8_t best = mx_quantize_block(v, codes);
+  double best_err = block_squared_error(v, codes, best);
+  const int c0 = best;
+  uint8_t trial[PRQ_BLOCK];
+  for (int off : {-1, 1}) {
+    int c = c0 + off;
+    c = c < 0 ? 0 : (c > 254 ? 254 : c);
+    const uint8_t sc = static_cast<uint8_t>(c);
+    mx_quantize_block_with(v, sc, trial);
+    const double e = block_squared_error(v, trial, sc);
+    if (e < best_err) {
+      best_err = e;
+      best = sc;
+      std::copy(trial, trial + PRQ_BLOCK, codes);
+    }
+  }
+  return best;
+}
+
 template <class F>
 void parallel_rows(int64_t rows, F&& body) {
   unsigned hw = std::thread::hardware_concurrency();
@@ -99,11 +139,14 @@ void parallel_rows(int64_t rows, F&& body) {
 
 }  // namespace
 
-extern "C" int prq_prepare(const uint16_t* W_bf16, int32_t N, int32_t K, const uint16_t* Xcal_bf16,
-                           int32_t T, double alpha, int32_t k_tail, int32_t scale_mode,
-                           float* scale, float* inv_scale, int32_t* perm,
-                           float* inv_scale_pos, uint8_t* Wq, uint8_t* Wsc, double* col_err) {
+extern "C" int prq_prepare_ex(const uint16_t* W_bf16, int32_t N, int32_t K,
+                              const uint16_t* Xcal_bf16, int32_t T, double alpha, int32_t k_tail,
+                              int32_t scale_mode, int32_t flags, float* scale, float* inv_scale,
+                              int32_t* perm, float* inv_scale_pos, uint8_t* Wq, uint8_t* Wsc,
+                              double* col_err) {
   if (!W_bf16 || !Xcal_bf16 || !scale || !inv_scale || !perm || !Wq || !Wsc) return PRQ_EINVAL;
+  if (flags & ~PRQ_PREPARE_E8M0_SEARCH) return PRQ_EINVAL;
+  const bool search = (flags & PRQ_PREPARE_E8M0_SEARCH) != 0;
   if (N <= 0 || K <= 0 || T <= 0) return PRQ_EINVAL;
   if (!(alpha >= 0.0 && alpha <= 1.0)) return PRQ_EINVAL;
   if (scale_mode != PRQ_SCALE_SMOOTH && scale_mode != PRQ_SCALE_ACT_ONLY &&
@@ -190,17 +233,28 @@ extern "C" int prq_prepare(const uint16_t* W_bf16, int32_t N, int32_t K, const u
       for (int q = 0; q < K; ++q) wt[q] = ws[perm[q]];
       uint8_t* sc = Wsc + n * nb_aug;
       for (int blk = 0; blk < nb_main; ++blk)
-        sc[blk] = mx_quantize_block(&wt[blk * PRQ_BLOCK], &codes[blk * PRQ_BLOCK]);
+        sc[blk] = search ? mx_quantize_block_searched(&wt[blk * PRQ_BLOCK], &codes[blk * PRQ_BLOCK])
+                         : mx_quantize_block(&wt[blk * PRQ_BLOCK], &codes[blk * PRQ_BLOCK]);
       for (int i = 0; i < k_tail; ++i) {
         int q = K - k_tail + i;
         res[i] = wt[q] - e2m1_value(codes[q], sc[q / PRQ_BLOCK]);  // exact (Eq. 2)
       }
       for (int blk = 0; blk < k_tail / PRQ_BLOCK; ++blk)
-        sc[nb_main + blk] = mx_quantize_block(&res[blk * PRQ_BLOCK], &codes[K + blk * PRQ_BLOCK]);
+        sc[nb_main + blk] =
+            search ? mx_quantize_block_searched(&res[blk * PRQ_BLOCK], &codes[K + blk * PRQ_BLOCK])
+                   : mx_quantize_block(&res[blk * PRQ_BLOCK], &codes[K + blk * PRQ_BLOCK]);
       uint8_t* out = Wq + n * row_bytes;
       for (int64_t i = 0; i < row_bytes; ++i)
         out[i] = static_cast<uint8_t>(codes[2 * i] | (codes[2 * i + 1] << 4));
     }
   });
   return PRQ_OK;
+}
+
+extern "C" int prq_prepare(const uint16_t* W_bf16, int32_t N, int32_t K, const uint16_t* Xcal_bf16,
+                           int32_t T, double alpha, int32_t k_tail, int32_t scale_mode,
+                           float* scale, float* inv_scale, int32_t* perm,
+                           float* inv_scale_pos, uint8_t* Wq, uint8_t* Wsc, double* col_err) {
+  return prq_prepare_ex(W_bf16, N, K, Xcal_bf16, T, alpha, k_tail, scale_mode, 0, scale, inv_scale,
+                        perm, inv_scale_pos, Wq, Wsc, col_err);
 }

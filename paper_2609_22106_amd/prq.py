@@ -44,6 +44,10 @@ _strerror = _decl("prq_strerror", ctypes.c_char_p, [ctypes.c_int])
 _abi_version = _decl("prq_abi_version", ctypes.c_int, [])
 _prepare = _decl("prq_prepare", ctypes.c_int,
                  [_p, _i32, _i32, _p, _i32, ctypes.c_double, _i32, _i32, _p, _p, _p, _p, _p, _p, _p])
+_prepare_ex = _decl("prq_prepare_ex", ctypes.c_int,
+                    [_p, _i32, _i32, _p, _i32, ctypes.c_double, _i32, _i32, _i32, _p, _p, _p, _p, _p,
+                     _p, _p])
+PREPARE_E8M0_SEARCH = 1
 _quant_act = _decl("prq_quant_act", ctypes.c_int,
                    [_p, _i64, _i32, _i32, _i32, _p, _p, _p, _i32, _p, _p, _p])
 _packed_bytes = _decl("prq_packed_weight_bytes", ctypes.c_int,
@@ -101,9 +105,11 @@ def _stream(stream):
 
 
 # --------------------------------------------------------------- prepare ---
-def prq_prepare(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth", with_col_err=False):
+def prq_prepare(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth", with_col_err=False,
+                scale_search=False):
     """Offline calibration/export (host).  W_bf16 [N, K] and Xcal_bf16 [T, K]
-    are uint16 numpy arrays of bf16 bit patterns.  Returns numpy arrays."""
+    are uint16 numpy arrays of bf16 bit patterns.  Returns numpy arrays.
+    scale_search: the weight-side E8M0 block-scale search (prq_prepare_ex)."""
     W = np.ascontiguousarray(W_bf16, dtype=np.uint16)
     X = np.ascontiguousarray(Xcal_bf16, dtype=np.uint16)
     N, K = W.shape
@@ -118,9 +124,10 @@ def prq_prepare(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth", with_col_
         "Wsc": np.empty((N, max(K_aug, 0) // 32), np.uint8),
     }
     col_err = np.empty(K, np.float64) if with_col_err else None
-    st = _prepare(_ptr(W), N, K, _ptr(X), T, float(alpha), int(k_tail), SCALE_MODES[scale_mode],
-                  _ptr(out["scale"]), _ptr(out["inv_scale"]), _ptr(out["perm"]),
-                  _ptr(out["inv_scale_pos"]), _ptr(out["Wq"]), _ptr(out["Wsc"]), _ptr(col_err))
+    st = _prepare_ex(_ptr(W), N, K, _ptr(X), T, float(alpha), int(k_tail), SCALE_MODES[scale_mode],
+                     PREPARE_E8M0_SEARCH if scale_search else 0,
+                     _ptr(out["scale"]), _ptr(out["inv_scale"]), _ptr(out["perm"]),
+                     _ptr(out["inv_scale_pos"]), _ptr(out["Wq"]), _ptr(out["Wsc"]), _ptr(col_err))
     _check(st, "prq_prepare")
     if with_col_err:
         out["col_err"] = col_err

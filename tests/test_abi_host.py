@@ -88,6 +88,34 @@ def test_prepare_matches_oracle_down_proj_full():
                           pq.prepare(c.W, c.Xcal, 0.5, 256))
 
 
+@pytest.mark.parametrize("mode", ["smooth", "none"])
+@pytest.mark.parametrize("k", [0, 64])
+def test_prepare_e8m0_search_matches_oracle(mode, k):
+    """prq_prepare_ex with the weight-side E8M0 search, bit for bit."""
+    c = inputs.make_dense("s", N=96, K=256, M=4, T=48, k_tail=k, n_out=5, seed=12)
+    ours = prq.prq_prepare(c.W, c.Xcal, 0.5, k, mode, with_col_err=True, scale_search=True)
+    _assert_prepare_equal(ours, pq.prepare(c.W, c.Xcal, 0.5, k, mode, scale_search=True))
+
+
+def test_prepare_e8m0_search_matches_oracle_workloads():
+    c = inputs.tiny_case()
+    _assert_prepare_equal(prq.prq_prepare(c.W, c.Xcal, 0.5, 64, scale_search=True),
+                          pq.prepare(c.W, c.Xcal, 0.5, 64, scale_search=True))
+    m = inputs.make_moe("m", E=1, N=2048, K=768, tokens=4, topk=1, T=256, k_tail=64, seed=3)
+    _assert_prepare_equal(prq.prq_prepare(m.W[0], m.Xcal[0], 0.5, 64, scale_search=True),
+                          pq.prepare(m.W[0], m.Xcal[0], 0.5, 64, scale_search=True))
+
+
+def test_prepare_ex_rejects_unknown_flags():
+    c = inputs.make_dense("s", N=16, K=64, M=1, T=4, k_tail=32, n_out=1)
+    K = 64
+    bufs = [np.empty(K, np.float32), np.empty(K, np.float32), np.empty(K, np.int32),
+            np.empty(K, np.float32), np.empty((16, 48), np.uint8), np.empty((16, 3), np.uint8)]
+    st = prq._prepare_ex(c.W.ctypes.data, 16, K, c.Xcal.ctypes.data, 4, 0.5, 32, 0, 2,
+                         *[b.ctypes.data for b in bufs], None)
+    assert st == prq.PRQ_EINVAL
+
+
 def test_prepare_rejects_bad_arguments():
     c = inputs.make_dense("s", N=16, K=64, M=1, T=4, k_tail=32, n_out=1)
     with pytest.raises(prq.PRQError) as ei:

@@ -150,6 +150,23 @@ def test_decode_kernel_grouped_mode():
     assert_gemm_close(Y, pq.grouped_gemm(Aq, Asc, off, Wq, Wsc), "decode grouped")
 
 
+@pytest.mark.parametrize("M", [1, 16, 300])
+def test_e8m0_search_export_end_to_end(M):
+    """Weights exported with the weight-side E8M0 block-scale search through
+    the GPU act-quant and GEMM (decode and tile kernels) against the oracle."""
+    prq = _prq()
+    c = inputs.make_dense("e", N=256, K=1024, M=M, T=64, k_tail=64, n_out=8, out_scale=40.0,
+                          heavy_tail=False, seed=M)
+    art = prq.prq_prepare(c.W, c.Xcal, 0.5, 64, scale_search=True)
+    ref = pq.prepare(c.W, c.Xcal, 0.5, 64, scale_search=True)
+    np.testing.assert_array_equal(art["Wsc"], ref["Wsc"])
+    say("gemm case: E8M0-W export M", M)
+    Aq, Asc = prq.prq_quant_act(dev(c.X), 1024, 64, dev(art["inv_scale_pos"]), dev(art["perm"]))
+    Y = host(prq.prq_gemm(Aq, Asc, _packed(art["Wq"], art["Wsc"])))
+    rq, rs = pq.quant_act(c.X, ref["inv_scale"], ref["perm"], 64)
+    assert_gemm_close(Y, pq.gemm(rq, rs, ref["Wq"], ref["Wsc"]), f"E8M0-W M={M}")
+
+
 def test_hand_values():
     """All-ones A block x all-halves W block = 16 (one block); a second block at
     scales (130, 126) adds 64 (Eq. 3 by hand)."""

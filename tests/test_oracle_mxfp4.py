@@ -149,3 +149,79 @@ def test_rejects_bad_input():
         mx.mx_quantize(np.zeros((1, 32), np.float64))
     with pytest.raises(ValueError):
         mx.mx_quantize(np.full((1, 32), np.inf, np.float32))
+
+
+# ------------------------------------------- E8M0 block-scale search ---
+_E2M1_GRID = [0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0]
+
+
+def _scalar_block_error(block, code):
+    """Exact squared error of a block under one E8M0 code, by a scalar loop
+    independent of the oracle: each element is rounded to the nearest E2M1
+    magnitude of |v| / 2**(code - 127) (ties to the even grid index,
+    saturating at 6) and compared with the exact rational value."""
+    from fractions import Fraction
+    scale = Fraction(2) ** (int(code) - 127)
+    err = Fraction(0)
+    for v in block:
+        fv = Fraction(float(v))
+        t = abs(fv) / scale
+        dists = [abs(t - Fraction(g)) for g in _E2M1_GRID]
+        dmin = min(dists)
+        cands = [i for i, d in enumerate(dists) if d == dmin]
+        idx = next((i for i in cands if i % 2 == 0), cands[0])
+        q = Fraction(_E2M1_GRID[idx]) * scale * (-1 if fv < 0 else 1)
+        err += (fv - q) ** 2
+    return err
+
+
+def test_searched_scale_hand_blocks():
+    """7.5 alone: the OCP code (127) saturates it to 6 (error 1.5^2); code 128
+    rounds 3.75 to 4 -> 8 (error 0.5^2).  4.0 with 31 x 0.3: code 126 gives 4 ->
+    3 (error 1) but 0.3 -> 0.25 (31 x 0.05^2), better than 127's 31 x 0.2^2."""
+    b1 = np.zeros(32, np.float32)
+    b1[0] = 7.5
+    b2 = np.full(32, 0.3, np.float32)
+    b2[0] = 4.0
+    v = np.stack([b1, b2])
+    _, s0 = mx.mx_quantize(v)
+    codes, sc = mx.mx_quantize_searched(v)
+    assert list(s0.ravel()) == [127, 127]
+    assert list(sc.ravel()) == [128, 126]
+    deq = mx.mx_dequantize(codes, sc)
+    assert deq[0, 0] == 8.0 and deq[1, 0] == 3.0 and deq[1, 1] == 0.25
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_searched_scale_is_the_exact_minimizer(seed):
+    """Against exact rational errors of every candidate code: the chosen code
+    is a minimizer among c0, c0 - 1, c0 + 1 (first in that order on exact ties)
+    and never worse than the OCP code; codes are Q(.)'s element rule under
+    the chosen scale."""
+    rng = np.random.default_rng(seed)
+    kinds = [rng.standard_normal(32), rng.standard_t(2, 32) * 3, rng.uniform(-7.9, 7.9, 32),
+             np.concatenate([[rng.uniform(4, 8)], rng.uniform(-0.4, 0.4, 31)])]
+    blocks = np.stack([(k * 2.0 ** rng.integers(-20, 20)).astype(np.float32) for k in kinds
+                       for _ in range(3)])
+    codes, sc = mx.mx_quantize_searched(blocks)
+    _, s0 = mx.mx_quantize(blocks)
+    for b in range(blocks.shape[0]):
+        c0 = int(s0[b, 0])
+        cands = [min(max(c0 + off, 0), 254) for off in (0, -1, 1)]
+        errs = [_scalar_block_error(blocks[b], c) for c in cands]
+        chosen = int(sc[b, 0])
+        assert chosen in cands
+        e_chosen = _scalar_block_error(blocks[b], chosen)
+        assert e_chosen == min(errs), (b, cands, [float(e) for e in errs], chosen)
+        assert e_chosen <= errs[0]
+        np.testing.assert_array_equal(codes[b], mx.mx_quantize_with_scales(blocks[b:b + 1], sc[b:b + 1])[0])
+
+
+def test_searched_scale_edge_blocks():
+    zeros = np.zeros((1, 32), np.float32)
+    codes, sc = mx.mx_quantize_searched(zeros)
+    assert sc[0, 0] == 0 and not codes.any()
+    big = np.full((1, 32), 3.0e38, np.float32)           # c0 = 252: c0 + 1 = 253 is still normal
+    codes, sc = mx.mx_quantize_searched(big)
+    assert int(sc[0, 0]) in (251, 252, 253)
+    assert np.isfinite(mx.mx_dequantize(codes, sc)).all()

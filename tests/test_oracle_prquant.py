@@ -274,6 +274,33 @@ def test_residual_compensation_lowers_error_tiny_case():
     assert e_prq < e_plain
 
 
+def test_e8m0_search_prepare_never_worse_per_block():
+    """The E8M0-W export: same selection and permutation as plain, every
+    32-block of Q(W~) and of Q(R_W) no worse than under plain Q(.) (exact
+    squared errors), the residual still exact, and the compensated tail still
+    no worse than the uncompensated one element by element."""
+    c = inputs.tiny_case()
+    plain = pq.prepare(c.W, c.Xcal, 0.5, 64)
+    srch = pq.prepare(c.W, c.Xcal, 0.5, 64, scale_search=True)
+    np.testing.assert_array_equal(plain["perm"], srch["perm"])
+    K = plain["K"]
+    Wt = srch["W_tilde"]
+    codes_p, codes_s = plain["codes"], srch["codes"]
+    sc_p, sc_s = plain["Wsc"], srch["Wsc"]
+    e_p = mx.block_squared_errors(Wt, codes_p[:, :K], sc_p[:, :K // 32])
+    e_s = mx.block_squared_errors(Wt, codes_s[:, :K], sc_s[:, :K // 32])
+    assert np.all(e_s <= e_p) and np.any(e_s < e_p)
+    R = srch["R"]
+    deq_s = mx.mx_dequantize(codes_s, sc_s)
+    np.testing.assert_array_equal(Wt[:, K - 64:].astype(np.float64) - deq_s[:, K - 64:K], R)
+    comp = np.abs(Wt[:, K - 64:] - deq_s[:, K - 64:K] - deq_s[:, K:])
+    assert np.all(comp <= np.abs(R))
+    ref = pq.reference_product(c.X, c.W)
+    y_s, _ = pq.prquant_forward(c.X, c.W, c.Xcal, 0.5, 64, scale_search=True)
+    y_p, _ = pq.prquant_forward(c.X, c.W, c.Xcal, 0.5, 64)
+    print(f"tiny y-NRMSE: PRQuant {pq.nrmse(y_p, ref):.5f}, E8M0-W {pq.nrmse(y_s, ref):.5f}")
+
+
 def test_grouped_matches_per_expert():
     rng = np.random.default_rng(3)
     E, N, K, k = 4, 16, 64, 32
