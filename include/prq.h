@@ -240,6 +240,41 @@ int prq_grouped_gemm_ex(const uint8_t* Aq, const uint8_t* Asc,
                         float* Y, void* workspace, size_t workspace_bytes,
                         int32_t variant, hipStream_t stream);
 
+/*
+ * prq_evaluate_nrmse -- offline: the normalized reconstruction error of one
+ * configuration, ||Y_hat - X W^T||_F / ||X W^T||_F, where Y_hat is Eq. 3
+ * evaluated on the rows X with the device path (prq_prepare_ex on the
+ * calibration rows Xcal with alpha, k_tail, scale_mode and flags, then
+ * prq_pack_weight, prq_quant_act, prq_gemm) and X W^T is computed on the device
+ * from the bf16 inputs with float32 accumulation.
+ *   W_bf16 [N, K], Xcal_bf16 [T, K], X_bf16 [M, K]: host arrays (bf16 bits)
+ *   nrmse: host double
+ * Allocates and frees its own device buffers, runs on `stream` and
+ * synchronizes it before returning.  N % 16 == 0 and K <= 16384 (the device
+ * kernels' limits) besides prq_prepare's conditions.
+ */
+int prq_evaluate_nrmse(const uint16_t* W_bf16, int32_t N, int32_t K,
+                       const uint16_t* Xcal_bf16, int32_t T,
+                       const uint16_t* X_bf16, int32_t M,
+                       double alpha, int32_t k_tail, int32_t scale_mode, int32_t flags,
+                       double* nrmse, hipStream_t stream);
+
+/*
+ * prq_search_alpha -- offline: the alpha search of Algorithm 1.  For every
+ * candidate alphas[a] (in [0, 1]) the export is built as by prq_prepare_ex and
+ * Eq. 3 is evaluated on the calibration rows themselves; nrmse[a] receives the
+ * normalized reconstruction error (as in prq_evaluate_nrmse with X = Xcal) and
+ * *best the index of the smallest (the first on equal errors).  Export the
+ * chosen configuration with prq_prepare_ex(alphas[*best], ...).
+ *   alphas [n_alpha] host doubles; nrmse [n_alpha] host doubles; best host int32.
+ * Device buffers, stream and limits as for prq_evaluate_nrmse.
+ */
+int prq_search_alpha(const uint16_t* W_bf16, int32_t N, int32_t K,
+                     const uint16_t* Xcal_bf16, int32_t T,
+                     const double* alphas, int32_t n_alpha, int32_t k_tail,
+                     int32_t scale_mode, int32_t flags,
+                     double* nrmse, int32_t* best, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -260,3 +260,20 @@ def prquant_forward(X_bf16, W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth
     art = prepare(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode, scale_search)
     Aq, Asc = quant_act(X_bf16, art["inv_scale"], art["perm"], k_tail)
     return gemm(Aq, Asc, art["Wq"], art["Wsc"]), art
+
+
+# --------------------------------------------------------------------------- #
+# Algorithm 1, steps 2-9: the alpha search
+# --------------------------------------------------------------------------- #
+def search_alpha(W_bf16, Xcal_bf16, alphas, k_tail, scale_mode="smooth", scale_search=False):
+    """For each candidate alpha build the export and evaluate Eq. 3 on the
+    calibration rows; return (index of the smallest reconstruction error --
+    the first on equal errors --, the errors).  The error is nrmse against the
+    unquantized product of the bf16 inputs."""
+    ref = reference_product(Xcal_bf16, W_bf16)
+    errs = []
+    for a in alphas:
+        y, _ = prquant_forward(Xcal_bf16, W_bf16, Xcal_bf16, a, k_tail, scale_mode, scale_search)
+        errs.append(nrmse(y, ref))
+    best = min(range(len(errs)), key=lambda i: (errs[i], i))
+    return best, np.array(errs)

@@ -48,6 +48,10 @@ _prepare_ex = _decl("prq_prepare_ex", ctypes.c_int,
                     [_p, _i32, _i32, _p, _i32, ctypes.c_double, _i32, _i32, _i32, _p, _p, _p, _p, _p,
                      _p, _p])
 PREPARE_E8M0_SEARCH = 1
+_evaluate = _decl("prq_evaluate_nrmse", ctypes.c_int,
+                  [_p, _i32, _i32, _p, _i32, _p, _i32, ctypes.c_double, _i32, _i32, _i32, _p, _p])
+_search = _decl("prq_search_alpha", ctypes.c_int,
+                [_p, _i32, _i32, _p, _i32, _p, _i32, _i32, _i32, _i32, _p, _p, _p])
 _quant_act = _decl("prq_quant_act", ctypes.c_int,
                    [_p, _i64, _i32, _i32, _i32, _p, _p, _p, _i32, _p, _p, _p])
 _packed_bytes = _decl("prq_packed_weight_bytes", ctypes.c_int,
@@ -132,6 +136,46 @@ def prq_prepare(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth", with_col_
     if with_col_err:
         out["col_err"] = col_err
     return out
+
+
+# ------------------------------------------------------------ evaluation ---
+def _bf16_host(a, name):
+    a = np.ascontiguousarray(a)
+    if a.dtype not in (np.uint16, np.int16) or a.ndim != 2:
+        raise ValueError(f"{name} must be a 2-D array of bf16 bit patterns (uint16)")
+    return a
+
+
+def prq_evaluate_nrmse(W_bf16, Xcal_bf16, X_bf16, alpha, k_tail, scale_mode="smooth",
+                       scale_search=False, stream=None):
+    """y-NRMSE of one configuration on the rows X (offline; host arrays)."""
+    W, Xc, X = _bf16_host(W_bf16, "W"), _bf16_host(Xcal_bf16, "Xcal"), _bf16_host(X_bf16, "X")
+    N, K = W.shape
+    if Xc.shape[1] != K or X.shape[1] != K:
+        raise ValueError("activations must have K columns")
+    out = ctypes.c_double()
+    st = _evaluate(_ptr(W), N, K, _ptr(Xc), Xc.shape[0], _ptr(X), X.shape[0], float(alpha),
+                   int(k_tail), SCALE_MODES[scale_mode], PREPARE_E8M0_SEARCH if scale_search else 0,
+                   ctypes.byref(out), _stream(stream))
+    _check(st, "prq_evaluate_nrmse")
+    return float(out.value)
+
+
+def prq_search_alpha(W_bf16, Xcal_bf16, alphas, k_tail, scale_mode="smooth", scale_search=False,
+                     stream=None):
+    """Algorithm 1's alpha search (offline): (best alpha, y-NRMSE per alpha)."""
+    W, Xc = _bf16_host(W_bf16, "W"), _bf16_host(Xcal_bf16, "Xcal")
+    N, K = W.shape
+    if Xc.shape[1] != K:
+        raise ValueError("calibration activations must have K columns")
+    a = np.ascontiguousarray(alphas, dtype=np.float64)
+    err = np.empty(a.size, np.float64)
+    best = ctypes.c_int32()
+    st = _search(_ptr(W), N, K, _ptr(Xc), Xc.shape[0], _ptr(a), a.size, int(k_tail),
+                 SCALE_MODES[scale_mode], PREPARE_E8M0_SEARCH if scale_search else 0, _ptr(err),
+                 ctypes.byref(best), _stream(stream))
+    _check(st, "prq_search_alpha")
+    return float(a[best.value]), err
 
 
 # ------------------------------------------------------------- device ops ---

@@ -223,3 +223,25 @@ def test_binding_rejects_operands_that_do_not_match_the_weight():
     with pytest.raises(ValueError, match="Wsc has shape"):
         prq.prq_pack_weight(torch.zeros((N, 1312), dtype=torch.uint8),
                             torch.zeros((N, 80), dtype=torch.uint8))
+
+
+def test_evaluation_calls_reject_bad_arguments_before_the_gpu():
+    """Argument errors of the offline evaluation calls are reported before any
+    device work (these run on hosts without a GPU)."""
+    import ctypes
+    c = inputs.make_dense("s", N=32, K=64, M=4, T=4, k_tail=32, n_out=1)
+    a = np.array([0.5, 1.5], np.float64)
+    err = np.empty(2, np.float64)
+    best = ctypes.c_int32()
+    st = prq._search(c.W.ctypes.data, 32, 64, c.Xcal.ctypes.data, 4, a.ctypes.data, 2, 32, 0, 0,
+                     err.ctypes.data, ctypes.byref(best), None)
+    assert st == prq.PRQ_EINVAL                      # alpha outside [0, 1]
+    st = prq._search(c.W.ctypes.data, 32, 64, c.Xcal.ctypes.data, 4, a.ctypes.data, 0, 32, 0, 0,
+                     err.ctypes.data, ctypes.byref(best), None)
+    assert st == prq.PRQ_EINVAL                      # no candidates
+    st = prq._evaluate(c.W.ctypes.data, 30, 64, c.Xcal.ctypes.data, 4, c.X.ctypes.data, 4, 0.5, 32,
+                       0, 0, err.ctypes.data, None)
+    assert st == prq.PRQ_EALIGN                      # N not a multiple of 16
+    st = prq._evaluate(None, 32, 64, c.Xcal.ctypes.data, 4, c.X.ctypes.data, 4, 0.5, 32, 0, 0,
+                       err.ctypes.data, None)
+    assert st == prq.PRQ_EINVAL

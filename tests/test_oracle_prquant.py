@@ -301,6 +301,24 @@ def test_e8m0_search_prepare_never_worse_per_block():
     print(f"tiny y-NRMSE: PRQuant {pq.nrmse(y_p, ref):.5f}, E8M0-W {pq.nrmse(y_s, ref):.5f}")
 
 
+def test_alpha_search_selects_the_smallest_error():
+    """Algorithm 1's loop: each candidate's error equals the y-NRMSE of that
+    alpha's export evaluated on the calibration rows, and the selection is the
+    first minimizer; without scaling every alpha is the same export (equal
+    errors: the first is kept)."""
+    c = inputs.tiny_case()
+    alphas = [0.0, 0.5, 1.0]
+    best, errs = pq.search_alpha(c.W, c.Xcal, alphas, 64)
+    ref = pq.reference_product(c.Xcal, c.W)
+    for a, e in zip(alphas, errs):
+        art = pq.prepare(c.W, c.Xcal, a, 64)
+        Aq, Asc = pq.quant_act(c.Xcal, art["inv_scale"], art["perm"], 64)
+        assert e == pq.nrmse(pq.gemm(Aq, Asc, art["Wq"], art["Wsc"]), ref)
+    assert errs[best] == errs.min() and all(errs[i] > errs[best] for i in range(best))
+    b2, e2 = pq.search_alpha(c.W, c.Xcal, [0.2, 0.7], 64, scale_mode="none")
+    assert b2 == 0 and e2[0] == e2[1]
+
+
 def test_grouped_matches_per_expert():
     rng = np.random.default_rng(3)
     E, N, K, k = 4, 16, 64, 32
