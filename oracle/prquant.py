@@ -277,3 +277,59 @@ def search_alpha(W_bf16, Xcal_bf16, alphas, k_tail, scale_mode="smooth", scale_s
         errs.append(nrmse(y, ref))
     best = min(range(len(errs)), key=lambda i: (errs[i], i))
     return best, np.array(errs)
+
+
+# --------------------------------------------------------------------------- #
+# Sec. Ablation Studies: the "w/o Perm" variant (numerics only)
+# --------------------------------------------------------------------------- #
+def prepare_no_perm(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth"):
+    """The selected channels stay in place: W_aug = [Q(W D) | Q(R_S)] with
+    R_S = (W D)[:, S] - deq Q(W D)[:, S] (S ascending; Q(W D) in the original
+    channel order), so the residual columns are gathered from scattered
+    blocks.  Returns scale, inv_scale, selected and the unpacked codes / scales."""
+    W_bf16 = np.asarray(W_bf16, dtype=np.uint16)
+    N, K = W_bf16.shape
+    _check_sizes(K, k_tail)
+    s, inv = channel_scales(W_bf16, np.asarray(Xcal_bf16, dtype=np.uint16), alpha, scale_mode)
+    W_s = (bf16_bits_to_f32(W_bf16) * s[None, :]).astype(np.float32)
+    selected = select_topk(column_errors(W_s), k_tail)
+    codes, scales = mx_quantize(W_s)
+    deq = mx_dequantize(codes, scales)
+    R = (W_s[:, selected].astype(np.float64) - deq[:, selected]).astype(np.float32)
+    codes_r, scales_r = mx_quantize(R)
+    return {"scale": s, "inv_scale": inv, "selected": selected,
+            "codes": np.concatenate([codes, codes_r], axis=1),
+            "Wsc": np.concatenate([scales, scales_r], axis=1)}
+
+
+def no_perm_forward(X_bf16, W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth"):
+    """Y_hat of the w/o Perm variant: A_aug = Q([Z, Z[:, S]]) with Z = X D^-1 in
+    the original channel order, times the augmented weight."""
+    art = prepare_no_perm(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode)
+    Z = transformed_activation(X_bf16, art["inv_scale"], None)
+    Z_aug = np.concatenate([Z, Z[:, art["selected"]]], axis=1)
+    a_codes, a_scales = mx_quantize(np.ascontiguousarray(Z_aug))
+    A = mx_dequantize(a_codes, a_scales)
+    Wd = mx_dequantize(art["codes"], art["Wsc"])
+    return A @ Wd.T, art
+
+
+ABLATION_VARIANTS = {   # name -> (scale_mode, uses k_tail, E8M0 search)
+    "plain MXFP4": ("none", False, False),
+    "PRQuant": ("smooth", True, False),
+    "w/o AWQ": ("none", True, False),
+    "w/o Res": ("smooth", False, False),
+    "E8M0-W": ("smooth", True, True),
+}
+
+
+def ablation_grid(X_bf16, W_bf16, Xcal_bf16, alpha, k_tail):
+    """y-NRMSE of every variant of Sec. Ablation Studies on the rows X."""
+    ref = reference_product(X_bf16, W_bf16)
+    out = {}
+    for name, (mode, use_k, search) in ABLATION_VARIANTS.items():
+        y, _ = prquant_forward(X_bf16, W_bf16, Xcal_bf16, alpha, k_tail if use_k else 0, mode, search)
+        out[name] = nrmse(y, ref)
+    y, _ = no_perm_forward(X_bf16, W_bf16, Xcal_bf16, alpha, k_tail)
+    out["w/o Perm"] = nrmse(y, ref)
+    return out

@@ -40,3 +40,30 @@ def test_evaluate_on_held_out_rows_matches_oracle():
         y, _ = pq.prquant_forward(c.X, c.W, c.Xcal, 0.5, k, mode)
         want = pq.nrmse(y, pq.reference_product(c.X, c.W))
         assert abs(got - want) <= RTOL * want, (mode, k, got, want)
+
+
+def test_ablation_grid_matches_oracle():
+    """The device-path ablation grid against the oracle's on a small shape."""
+    from paper_2609_22106_amd import ablation
+    c = inputs.make_dense("a", N=128, K=1024, M=64, T=64, k_tail=64, n_out=8, seed=31)
+    got = ablation.run_grid(c.X, c.W, c.Xcal, 0.5, 64)
+    want = pq.ablation_grid(c.X, c.W, c.Xcal, 0.5, 64)
+    say("ablation grid", {k: round(v, 5) for k, v in got.items()}, "w/o Perm (oracle)",
+        round(want["w/o Perm"], 5))
+    for name, v in got.items():
+        assert abs(v - want[name]) <= RTOL * want[name], (name, v, want[name])
+
+
+def test_ablation_grid_full_down_proj_matches_stored_oracle():
+    """The full 9728 -> 2560 workload (512 evaluation rows) against the oracle
+    values written by tests/golden/make_ablation_down_proj.py."""
+    import json
+    import os
+    from paper_2609_22106_amd import ablation
+    with open(os.path.join(os.path.dirname(__file__), "golden", "ablation_down_proj.json")) as f:
+        want = json.load(f)["y_nrmse"]
+    c = inputs.down_proj_prefill()
+    say("evaluate case: ablation grid, full down_proj")
+    got = ablation.run_grid(c.X[:512], c.W, c.Xcal, c.alpha, c.k_tail)
+    for name, v in got.items():
+        assert abs(v - want[name]) <= RTOL * want[name], (name, v, want[name])

@@ -319,6 +319,48 @@ def test_alpha_search_selects_the_smallest_error():
     assert b2 == 0 and e2[0] == e2[1]
 
 
+def test_no_perm_variant_reductions():
+    """w/o Perm: when the selected channels already are the last k (the
+    permutation is the identity) it is PRQuant itself; with k = 0 it is the
+    scaled MXFP4 product; the compensated weight columns are never worse than
+    the uncompensated ones element by element."""
+    rng = np.random.default_rng(8)
+    K, k = 128, 32
+    W = 0.02 * rng.standard_normal((24, K))
+    W[:, K - k:] *= 40                                  # the largest errors sit in the last k channels
+    Wb = _bf16(W)
+    Xc = _bf16(rng.standard_normal((16, K)))
+    X = _bf16(rng.standard_normal((5, K)))
+    art = pq.prepare(Wb, Xc, 0.5, k)
+    np.testing.assert_array_equal(art["perm"], np.arange(K))
+    y_np, _ = pq.no_perm_forward(X, Wb, Xc, 0.5, k)
+    y_prq, _ = pq.prquant_forward(X, Wb, Xc, 0.5, k)
+    np.testing.assert_array_equal(y_np, y_prq)
+    y0, _ = pq.no_perm_forward(X, Wb, Xc, 0.5, 0)
+    y00, _ = pq.prquant_forward(X, Wb, Xc, 0.5, 0)
+    np.testing.assert_array_equal(y0, y00)
+    c = inputs.tiny_case()
+    a2 = pq.prepare_no_perm(c.W, c.Xcal, 0.5, 64)
+    W_s = (pq.bf16_bits_to_f32(c.W) * a2["scale"][None, :]).astype(np.float32)
+    deq = mx.mx_dequantize(a2["codes"], a2["Wsc"])
+    S = a2["selected"]
+    Kt = W_s.shape[1]
+    comp = np.abs(W_s[:, S] - deq[:, S] - deq[:, Kt:])
+    assert np.all(comp <= np.abs(W_s[:, S] - deq[:, S]))
+
+
+def test_ablation_grid_directions_tiny():
+    """The paper's ablation directions on the tiny workload: PRQuant beats
+    plain MXFP4 and the same scaling without the residual; E8M0-W is no worse
+    than PRQuant here.  (Whether scaling alone beats plain MXFP4 is reported,
+    not asserted.)"""
+    c = inputs.tiny_case()
+    g = pq.ablation_grid(c.X, c.W, c.Xcal, 0.5, 64)
+    print({k: round(v, 5) for k, v in g.items()})
+    assert g["PRQuant"] < g["w/o Res"] and g["PRQuant"] < g["plain MXFP4"]
+    assert g["E8M0-W"] <= g["PRQuant"]
+
+
 def test_grouped_matches_per_expert():
     rng = np.random.default_rng(3)
     E, N, K, k = 4, 16, 64, 32
