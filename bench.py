@@ -305,6 +305,42 @@ def graph_step_time(torch, ops, steps):
     return a.elapsed_time(b) * 1e-3 / (reps * per_graph)
 
 
+def copy_context(torch, prq, layers, M_list, reps=50):
+    """Activation side, online copy (gather by perm, scale, quantize, copy the
+    tail blocks) against offline copy (the expanded producer already emitted
+    [Z~, Z~_tail]: a plain quantizer over K + k), both launched back to back
+    on warm inputs (seconds per launch)."""
+    out = {}
+    for name, c in layers:
+        K, k = c.K, c.k_tail
+        art = prq.prq_prepare(c.W, c.Xcal, c.alpha, k)
+        inv = torch.from_numpy(art["inv_scale_pos"]).cuda()
+        perm = torch.from_numpy(art["perm"]).cuda()
+        X = torch.from_numpy(c.X.view("int16")).cuda()
+        g = torch.Generator(device="cpu").manual_seed(0)
+        Zaug = (torch.randn((max(M_list), K + k), generator=g) * 2).to(torch.bfloat16).cuda()
+        for M in M_list:
+            Aq = torch.empty((M, (K + k) // 2), dtype=torch.uint8, device="cuda")
+            Asc = torch.empty((M, (K + k) // 32), dtype=torch.uint8, device="cuda")
+            res = {}
+            for label, fn in (
+                    ("online", lambda: prq.prq_quant_act(X[:M], K, k, inv, perm, Aq=Aq, Asc=Asc)),
+                    ("offline", lambda: prq.prq_quant_act(Zaug[:M], K + k, 0, Aq=Aq, Asc=Asc))):
+                for _ in range(3):
+                    fn()
+                torch.cuda.synchronize()
+                torch.cuda._sleep(20_000_000)
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                for _ in range(reps):
+                    fn()
+                b.record()
+                torch.cuda.synchronize()
+                res[label] = a.elapsed_time(b) * 1e-3 / reps
+            out[f"{name}/M={M}"] = res
+    return out
+
+
 def bf16_context(torch, layers, M_list, rotate_bytes, steps):
     """Same-shape BF16 torch.matmul (hipBLASLt/rocBLAS), weights rotated."""
     out = {}
@@ -533,6 +569,12 @@ def main(argv=None):
                 detail[key]["bf16_matmul_us"] = round(t * 1e6, 3)
                 detail[key]["speedup_op_vs_bf16"] = round(t / (detail[key]["op_us"] * 1e-6), 3)
                 detail[key]["speedup_gemm_vs_bf16"] = round(t / (detail[key]["gemm_us"] * 1e-6), 3)
+
+    if layers and wl in ("decode", "prefill"):
+        for key, r in copy_context(torch, prq, layers, M_list).items():
+            if key in detail:
+                detail[key]["act_quant_online_copy_warm_us"] = round(r["online"] * 1e6, 3)
+                detail[key]["act_quant_offline_copy_warm_us"] = round(r["offline"] * 1e6, 3)
 
     cpu = None
     if not args.no_cpu_baseline and wl in ("decode",):

@@ -241,6 +241,28 @@ int prq_grouped_gemm_ex(const uint8_t* Aq, const uint8_t* Asc,
                         int32_t variant, hipStream_t stream);
 
 /*
+ * prq_expand_producer -- offline copy (Sec. Method, "Activation tail
+ * construction", and Eq. 1): fold D^-1 into the up-projection and P into the
+ * up- and gate-projections, and duplicate their last k output channels, so
+ * that the gated FFN emits [Z~, Z~_tail] (C + k channels) directly and the
+ * down-projection's activation needs a plain MXFP4 quantizer only
+ * (prq_quant_act with K = C + k, k_tail = 0, no perm, no scales).
+ *   W_up_bf16, W_gate_bf16 [C, H]  bf16 bit patterns; row = output channel
+ *                                  (the down-projection's input channel);
+ *                                  W_gate_bf16 may be NULL (no gate)
+ *   inv_scale [C], perm [C]        from prq_prepare (channel order / position)
+ * Outputs (caller-allocated host buffers) [C + k, H]:
+ *   W_up_aug[r]   = bf16_rne(W_up[perm[p]] * inv_scale[perm[p]]), p = r for
+ *                   r < C, p = r - k for r >= C (the tail copies)
+ *   W_gate_aug[r] = W_gate[perm[p]] (same p)
+ * The scaled up-projection is rounded once to bf16 (nearest, ties to even).
+ * Host memory only, synchronous.  Returns PRQ_OK or PRQ_EINVAL.
+ */
+int prq_expand_producer(const uint16_t* W_up_bf16, const uint16_t* W_gate_bf16,
+                        int32_t C, int32_t H, const float* inv_scale, const int32_t* perm,
+                        int32_t k_tail, uint16_t* W_up_aug, uint16_t* W_gate_aug);
+
+/*
  * prq_evaluate_nrmse -- offline: the normalized reconstruction error of one
  * configuration, ||Y_hat - X W^T||_F / ||X W^T||_F, where Y_hat is Eq. 3
  * evaluated on the rows X with the device path (prq_prepare_ex on the

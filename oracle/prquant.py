@@ -333,3 +333,37 @@ def ablation_grid(X_bf16, W_bf16, Xcal_bf16, alpha, k_tail):
     y, _ = no_perm_forward(X_bf16, W_bf16, Xcal_bf16, alpha, k_tail)
     out["w/o Perm"] = nrmse(y, ref)
     return out
+
+
+# --------------------------------------------------------------------------- #
+# Offline copy (Sec. Method, "Activation tail construction"; Eq. 1)
+# --------------------------------------------------------------------------- #
+def bf16_round_bits(x):
+    """float32 -> bf16 bit patterns, nearest with ties to even (finite input)."""
+    u = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    u = u + 0x7FFF + ((u >> 16) & 1)
+    return (u >> 16).astype(np.uint16)
+
+
+def expand_producer(W_up_bf16, W_gate_bf16, inv_scale, perm, k_tail):
+    """D^-1 folded into the up-projection rows, P into the up- and
+    gate-projection rows, the last k output channels duplicated: row r of the
+    result is channel perm[p] with p = r (r < C) or r - k (r >= C); the scaled
+    up-projection is rounded once to bf16.  Returns bf16 bit patterns."""
+    C = len(perm)
+    p = np.concatenate([np.arange(C), np.arange(C - k_tail, C)])
+    src = np.asarray(perm)[p]
+    up = bf16_bits_to_f32(np.asarray(W_up_bf16, dtype=np.uint16))[src]
+    d = np.asarray(inv_scale, dtype=np.float32)[src][:, None]
+    up_aug = bf16_round_bits((up * d).astype(np.float32))
+    gate_aug = None if W_gate_bf16 is None else np.asarray(W_gate_bf16, dtype=np.uint16)[src]
+    return up_aug, gate_aug
+
+
+def gated_ffn(X_hidden_bf16, W_up_bf16, W_gate_bf16):
+    """(X W_up^T) * silu(X W_gate^T) in float64 (the producer of the
+    down-projection's input; Eq. 1 with sigma = SiLU)."""
+    X = bf16_bits_to_f32(np.asarray(X_hidden_bf16, dtype=np.uint16)).astype(np.float64)
+    up = X @ bf16_bits_to_f32(np.asarray(W_up_bf16, dtype=np.uint16)).astype(np.float64).T
+    g = X @ bf16_bits_to_f32(np.asarray(W_gate_bf16, dtype=np.uint16)).astype(np.float64).T
+    return up * (g / (1.0 + np.exp(-g)))

@@ -28,6 +28,14 @@ inline float bf16_to_float(uint16_t h) {
   return f;
 }
 
+// Round a finite float to bf16, nearest with ties to even.
+inline uint16_t float_to_bf16(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
 inline uint32_t float_bits(float f) {
   uint32_t u;
   std::memcpy(&u, &f, 4);
@@ -257,4 +265,32 @@ extern "C" int prq_prepare(const uint16_t* W_bf16, int32_t N, int32_t K, const u
                            float* inv_scale_pos, uint8_t* Wq, uint8_t* Wsc, double* col_err) {
   return prq_prepare_ex(W_bf16, N, K, Xcal_bf16, T, alpha, k_tail, scale_mode, 0, scale, inv_scale,
                         perm, inv_scale_pos, Wq, Wsc, col_err);
+}
+
+extern "C" int prq_expand_producer(const uint16_t* W_up_bf16, const uint16_t* W_gate_bf16, int32_t C,
+                                   int32_t H, const float* inv_scale, const int32_t* perm,
+                                   int32_t k_tail, uint16_t* W_up_aug, uint16_t* W_gate_aug) {
+  if (!W_up_bf16 || !inv_scale || !perm || !W_up_aug || C <= 0 || H <= 0) return PRQ_EINVAL;
+  if (W_gate_bf16 && !W_gate_aug) return PRQ_EINVAL;
+  if (k_tail < 0 || k_tail > C) return PRQ_EINVAL;
+  for (int p = 0; p < C; ++p)
+    if (perm[p] < 0 || perm[p] >= C) return PRQ_EINVAL;
+  for (int p = 0; p < C; ++p)
+    if (!std::isfinite(inv_scale[perm[p]])) return PRQ_EINVAL;
+  const int64_t rows = static_cast<int64_t>(C) + k_tail;
+  parallel_rows(rows, [&](int64_t r0, int64_t r1) {
+    for (int64_t r = r0; r < r1; ++r) {
+      // output channel r of the expanded producer: position r (r < C), or the
+      // copy of tail position r - k_tail (r >= C)
+      const int64_t p = r < C ? r : r - k_tail;
+      const int64_t src = perm[p];
+      const float d = inv_scale[src];
+      const uint16_t* up = W_up_bf16 + src * H;
+      uint16_t* out = W_up_aug + r * H;
+      for (int h = 0; h < H; ++h) out[h] = float_to_bf16(bf16_to_float(up[h]) * d);
+      if (W_gate_bf16)
+        std::memcpy(W_gate_aug + r * H, W_gate_bf16 + src * H, static_cast<size_t>(H) * 2);
+    }
+  });
+  return PRQ_OK;
 }

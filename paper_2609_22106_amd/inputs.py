@@ -187,3 +187,32 @@ def random_mxfp4(rng, shape_rows, K_aug, scale_lo=118, scale_hi=136):
     q = rng.integers(0, 256, rows + (K_aug // 2,), dtype=np.uint8)
     s = rng.integers(scale_lo, scale_hi + 1, rows + (K_aug // 32,), dtype=np.uint8)
     return q, s
+
+
+@dataclass
+class FFNCase:
+    """A gated FFN (the down-projection's producer) with random weights."""
+    name: str
+    H: int            # hidden size
+    C: int            # intermediate size = the down-projection's K
+    W_up: np.ndarray  # bf16 [C, H]
+    W_gate: np.ndarray
+    W_down: np.ndarray   # bf16 [H, C]
+    X_hidden: np.ndarray  # bf16 [M, H]
+    X_cal: np.ndarray     # bf16 [T, H]
+    out_idx: np.ndarray   # intermediate channels with 30x up-projection rows
+
+
+def make_ffn(name, H, C, M, T, n_out=8, out_scale=30.0, seed=0):
+    """W_up, W_gate, W_down ~ 0.02 N(0,1); n_out up-projection rows scaled by
+    out_scale (outlier intermediate channels); hidden states ~ N(0,1)."""
+    rng = np.random.default_rng(seed)
+    out_idx = np.sort(rng.choice(C, n_out, replace=False))
+    W_up = 0.02 * rng.standard_normal((C, H))
+    W_up[out_idx] *= out_scale
+    W_gate = 0.02 * rng.standard_normal((C, H))
+    W_down = 0.02 * rng.standard_normal((H, C))
+    Xc = rng.standard_normal((T, H))
+    X = rng.standard_normal((M, H))
+    b = lambda a: f32_to_bf16_bits(a.astype(np.float32))
+    return FFNCase(name, H, C, b(W_up), b(W_gate), b(W_down), b(X), b(Xc), out_idx)

@@ -48,6 +48,7 @@ _prepare_ex = _decl("prq_prepare_ex", ctypes.c_int,
                     [_p, _i32, _i32, _p, _i32, ctypes.c_double, _i32, _i32, _i32, _p, _p, _p, _p, _p,
                      _p, _p])
 PREPARE_E8M0_SEARCH = 1
+_expand = _decl("prq_expand_producer", ctypes.c_int, [_p, _p, _i32, _i32, _p, _p, _i32, _p, _p])
 _evaluate = _decl("prq_evaluate_nrmse", ctypes.c_int,
                   [_p, _i32, _i32, _p, _i32, _p, _i32, ctypes.c_double, _i32, _i32, _i32, _p, _p])
 _search = _decl("prq_search_alpha", ctypes.c_int,
@@ -136,6 +137,25 @@ def prq_prepare(W_bf16, Xcal_bf16, alpha, k_tail, scale_mode="smooth", with_col_
     if with_col_err:
         out["col_err"] = col_err
     return out
+
+
+def prq_expand_producer(W_up_bf16, W_gate_bf16, inv_scale, perm, k_tail):
+    """Offline copy (host): (W_up_aug, W_gate_aug or None), each [C + k, H]
+    bf16 bit patterns (uint16)."""
+    up = _bf16_host(W_up_bf16, "W_up")
+    gate = None if W_gate_bf16 is None else _bf16_host(W_gate_bf16, "W_gate")
+    C, H = up.shape
+    if gate is not None and gate.shape != up.shape:
+        raise ValueError("W_gate must have W_up's shape")
+    inv = np.ascontiguousarray(inv_scale, dtype=np.float32)
+    p = np.ascontiguousarray(perm, dtype=np.int32)
+    if inv.shape != (C,) or p.shape != (C,):
+        raise ValueError("inv_scale and perm must have C entries")
+    up_aug = np.empty((C + int(k_tail), H), np.uint16)
+    gate_aug = None if gate is None else np.empty((C + int(k_tail), H), np.uint16)
+    _check(_expand(_ptr(up), _ptr(gate), C, H, _ptr(inv), _ptr(p), int(k_tail), _ptr(up_aug),
+                   _ptr(gate_aug)), "prq_expand_producer")
+    return up_aug, gate_aug
 
 
 # ------------------------------------------------------------ evaluation ---

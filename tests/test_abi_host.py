@@ -245,3 +245,22 @@ def test_evaluation_calls_reject_bad_arguments_before_the_gpu():
     st = prq._evaluate(None, 32, 64, c.Xcal.ctypes.data, 4, c.X.ctypes.data, 4, 0.5, 32, 0, 0,
                        err.ctypes.data, None)
     assert st == prq.PRQ_EINVAL
+
+
+@pytest.mark.parametrize("gate", [True, False])
+def test_expand_producer_matches_oracle(gate):
+    rng = np.random.default_rng(4)
+    f = inputs.make_ffn("f", H=96, C=320, M=2, T=2, seed=4)
+    perm = rng.permutation(f.C).astype(np.int32)
+    inv = rng.uniform(0.01, 30.0, f.C).astype(np.float32)
+    up, gt = prq.prq_expand_producer(f.W_up, f.W_gate if gate else None, inv, perm, 96)
+    rup, rgt = pq.expand_producer(f.W_up, f.W_gate if gate else None, inv, perm, 96)
+    np.testing.assert_array_equal(up, rup)
+    if gate:
+        np.testing.assert_array_equal(gt, rgt)
+    else:
+        assert gt is None
+    with pytest.raises(prq.PRQError):
+        bad = perm.copy()
+        bad[0] = f.C
+        prq.prq_expand_producer(f.W_up, None, inv, bad, 96)

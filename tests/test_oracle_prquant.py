@@ -361,6 +361,58 @@ def test_ablation_grid_directions_tiny():
     assert g["E8M0-W"] <= g["PRQuant"]
 
 
+def _pow2_inverse_scales(rng, C):
+    return (2.0 ** rng.integers(-3, 4, C)).astype(np.float32)
+
+
+def test_offline_copy_expanded_ffn_emits_the_augmented_activation():
+    """Eq. 1 with exact arithmetic: with power-of-two inverse scales (exact in
+    bf16) the expanded producer's FFN output is [Z~, Z~_tail] of the original
+    FFN output, Z~[:, p] = Z[:, perm[p]] / s_{perm[p]}, bit for bit."""
+    rng = np.random.default_rng(2)
+    f = inputs.make_ffn("f", H=64, C=256, M=7, T=4, seed=2)
+    k = 64
+    perm = rng.permutation(f.C).astype(np.int32)
+    inv = _pow2_inverse_scales(rng, f.C)
+    up_aug, gate_aug = pq.expand_producer(f.W_up, f.W_gate, inv, perm, k)
+    assert up_aug.shape == (f.C + k, f.H) and gate_aug.shape == (f.C + k, f.H)
+    Z = pq.gated_ffn(f.X_hidden, f.W_up, f.W_gate)
+    Zt = Z[:, perm] * inv[perm].astype(np.float64)
+    want = np.concatenate([Zt, Zt[:, f.C - k:]], axis=1)
+    got = pq.gated_ffn(f.X_hidden, up_aug, gate_aug)
+    np.testing.assert_array_equal(got, want)
+
+
+def test_offline_copy_quantizes_like_the_online_copy():
+    """With power-of-two scales the plain quantizer over C + k on the expanded
+    producer's (bf16) output gives the online copy's codes and scales."""
+    rng = np.random.default_rng(3)
+    f = inputs.make_ffn("f", H=64, C=256, M=9, T=4, seed=3)
+    k = 64
+    perm = rng.permutation(f.C).astype(np.int32)
+    inv = _pow2_inverse_scales(rng, f.C)
+    up_aug, gate_aug = pq.expand_producer(f.W_up, f.W_gate, inv, perm, k)
+    z_aug = pq.bf16_round_bits(pq.gated_ffn(f.X_hidden, up_aug, gate_aug).astype(np.float32))
+    off_q, off_s = pq.quant_act(z_aug, None, None, 0)
+    z = pq.bf16_round_bits(pq.gated_ffn(f.X_hidden, f.W_up, f.W_gate).astype(np.float32))
+    on_q, on_s = pq.quant_act(z, inv, perm, k)
+    np.testing.assert_array_equal(off_s, on_s)
+    np.testing.assert_array_equal(off_q, on_q)
+
+
+def test_bf16_rounding_is_nearest_even():
+    x = np.array([1.0, 1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8, 1.0 + 2.0 ** -9, -2.5e-40, 3.0e38],
+                 np.float32)
+    b = pq.bf16_round_bits(x)
+    back = pq.bf16_bits_to_f32(b)
+    assert back[0] == 1.0 and back[1] == 1.0              # tie -> even mantissa
+    assert back[2] == np.float32(1.0 + 4 * 2.0 ** -8)     # tie -> even (up)
+    assert back[3] == 1.0
+    for v, r in zip(x, back):                               # nearest: |v - r| <= half an ulp
+        ulp = np.spacing(np.float32(abs(r))) * 2 ** 16 if r != 0 else 2.0 ** -133
+        assert abs(float(v) - float(r)) <= ulp / 2
+
+
 def test_grouped_matches_per_expert():
     rng = np.random.default_rng(3)
     E, N, K, k = 4, 16, 64, 32
