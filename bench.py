@@ -56,6 +56,7 @@ def parse_args(argv=None):
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-bf16", action="store_true")
     p.add_argument("--no-graph", action="store_true", help="skip the graph-replay cross-check")
+    p.add_argument("--no-plain", action="store_true", help="skip the plain MXFP4 (k = 0) context")
     p.add_argument("--rotate-bytes", type=float, default=1.0 * 2 ** 30,
                    help="minimum total bytes of rotated weight copies")
     p.add_argument("--copy-calibration", action="store_true",
@@ -91,14 +92,15 @@ class Op:
         self.t_gemm, self.t_act = [], []
 
 
-def build_dense_ops(torch, prq, layers, M_list, rotate_bytes):
-    """layers: list of (name, DenseCase).  Weights rotated, activations per M."""
+def build_dense_ops(torch, prq, layers, M_list, rotate_bytes, plain=False):
+    """layers: list of (name, DenseCase).  Weights rotated, activations per M.
+    plain: the plain MXFP4 baseline (no scaling, no tail: k = 0)."""
     ops = []
     for name, c in layers:
-        K, k, N = c.K, c.k_tail, c.N
+        K, k, N = c.K, (0 if plain else c.k_tail), c.N
         K_aug = K + k
         t0 = time.perf_counter()
-        art = prq.prq_prepare(c.W, c.Xcal, c.alpha, k)
+        art = prq.prq_prepare(c.W, c.Xcal, c.alpha, k, "none" if plain else "smooth")
         log(f"[bench] prq_prepare {name}: {time.perf_counter() - t0:.2f} s")
         w_bytes = art["Wq"].nbytes + art["Wsc"].nbytes
         R = max(1, math.ceil(rotate_bytes / w_bytes))
@@ -570,6 +572,18 @@ def main(argv=None):
                 detail[key]["speedup_op_vs_bf16"] = round(t / (detail[key]["op_us"] * 1e-6), 3)
                 detail[key]["speedup_gemm_vs_bf16"] = round(t / (detail[key]["gemm_us"] * 1e-6), 3)
 
+    if layers and not args.no_plain:
+        # plain MXFP4 (k = 0, no scaling) through the same kernels and timing
+        plain_ops = build_dense_ops(torch, prq, layers, M_list, args.rotate_bytes, plain=True)
+        t_plain, _ = run_steps(torch, plain_ops, args.steps, args.warmup, stream)
+        for op in plain_ops:
+            if op.name in detail:
+                tg, ta = float(np.mean(op.t_gemm)), float(np.mean(op.t_act))
+                d = detail[op.name]
+                d["plain_mxfp4_gemm_us"] = round(tg * 1e6, 3)
+                d["plain_mxfp4_op_us"] = round((tg + ta) * 1e6, 3)
+                d["op_over_plain_mxfp4"] = round(d["op_us"] / ((tg + ta) * 1e6), 3)
+        del plain_ops
     if layers and wl in ("decode", "prefill"):
         for key, r in copy_context(torch, prq, layers, M_list).items():
             if key in detail:
