@@ -92,6 +92,9 @@ class Op:
         self.t_gemm, self.t_act = [], []
 
 
+PACKED_MIN_ROWS = 64   # more rows than this: the packed prefill pair
+
+
 def build_dense_ops(torch, prq, layers, M_list, rotate_bytes, plain=False):
     """layers: list of (name, DenseCase).  Weights rotated, activations per M.
     plain: the plain MXFP4 baseline (no scaling, no tail: k = 0)."""
@@ -110,23 +113,36 @@ def build_dense_ops(torch, prq, layers, M_list, rotate_bytes, plain=False):
         perm = torch.from_numpy(art["perm"]).cuda()
         X = torch.from_numpy(c.X.view("int16")).cuda()
         for M in M_list:
-            Aq = torch.empty((M, K_aug // 2), dtype=torch.uint8, device="cuda")
-            Asc = torch.empty((M, K_aug // 32), dtype=torch.uint8, device="cuda")
             Y = torch.empty((M, N), dtype=torch.float32, device="cuda")
-            ws_n = prq.prq_gemm_workspace_bytes(M, N, K_aug)
-            ws = torch.zeros(max(ws_n, 1), dtype=torch.uint8, device="cuda") if ws_n else None
             Xm = X[:M]
             state = {"r": 0}
-
             # every per-layer buffer is bound here: a name captured from the
             # enclosing loop would see the last layer's buffers in every op
-            def act(Xm=Xm, Aq=Aq, Asc=Asc, K=K, k=k, inv=inv, perm=perm):
-                prq.prq_quant_act(Xm, K, k, inv, perm, Aq=Aq, Asc=Asc)
+            if M > PACKED_MIN_ROWS:
+                # prefill: the packed pair (activation written in the layout the
+                # tile GEMM copies in whole kilobytes)
+                A = prq.prq_quant_act_packed(Xm, K, k, inv, perm)
 
-            def gemm(Aq=Aq, Asc=Asc, Y=Y, ws=ws, state=state, R=R, Ws=Ws):
-                r = state["r"]
-                state["r"] = (r + 1) % R
-                prq.prq_gemm(Aq, Asc, Ws[r], Y=Y, workspace=ws)
+                def act(Xm=Xm, A=A, K=K, k=k, inv=inv, perm=perm):
+                    prq.prq_quant_act_packed(Xm, K, k, inv, perm, out=A)
+
+                def gemm(A=A, Y=Y, state=state, R=R, Ws=Ws):
+                    r = state["r"]
+                    state["r"] = (r + 1) % R
+                    prq.prq_gemm_packed(A, Ws[r], Y=Y)
+            else:
+                Aq = torch.empty((M, K_aug // 2), dtype=torch.uint8, device="cuda")
+                Asc = torch.empty((M, K_aug // 32), dtype=torch.uint8, device="cuda")
+                ws_n = prq.prq_gemm_workspace_bytes(M, N, K_aug)
+                ws = torch.zeros(max(ws_n, 1), dtype=torch.uint8, device="cuda") if ws_n else None
+
+                def act(Xm=Xm, Aq=Aq, Asc=Asc, K=K, k=k, inv=inv, perm=perm):
+                    prq.prq_quant_act(Xm, K, k, inv, perm, Aq=Aq, Asc=Asc)
+
+                def gemm(Aq=Aq, Asc=Asc, Y=Y, ws=ws, state=state, R=R, Ws=Ws):
+                    r = state["r"]
+                    state["r"] = (r + 1) % R
+                    prq.prq_gemm(Aq, Asc, Ws[r], Y=Y, workspace=ws)
 
             ops.append(Op(f"{name}/M={M}", M, N, K, k, act, gemm, gemm_bytes(M, N, K_aug),
                           act_bytes(M, K, K_aug), 2.0 * M * N * K_aug))
@@ -322,12 +338,17 @@ def copy_context(torch, prq, layers, M_list, reps=50):
         g = torch.Generator(device="cpu").manual_seed(0)
         Zaug = (torch.randn((max(M_list), K + k), generator=g) * 2).to(torch.bfloat16).cuda()
         for M in M_list:
-            Aq = torch.empty((M, (K + k) // 2), dtype=torch.uint8, device="cuda")
-            Asc = torch.empty((M, (K + k) // 32), dtype=torch.uint8, device="cuda")
             res = {}
-            for label, fn in (
-                    ("online", lambda: prq.prq_quant_act(X[:M], K, k, inv, perm, Aq=Aq, Asc=Asc)),
-                    ("offline", lambda: prq.prq_quant_act(Zaug[:M], K + k, 0, Aq=Aq, Asc=Asc))):
+            if M > PACKED_MIN_ROWS:     # the quantizer the step uses: packed output
+                A = prq.prq_quant_act_packed(X[:M], K, k, inv, perm)
+                fns = (("online", lambda: prq.prq_quant_act_packed(X[:M], K, k, inv, perm, out=A)),
+                       ("offline", lambda: prq.prq_quant_act_packed(Zaug[:M], K + k, 0, out=A)))
+            else:
+                Aq = torch.empty((M, (K + k) // 2), dtype=torch.uint8, device="cuda")
+                Asc = torch.empty((M, (K + k) // 32), dtype=torch.uint8, device="cuda")
+                fns = (("online", lambda: prq.prq_quant_act(X[:M], K, k, inv, perm, Aq=Aq, Asc=Asc)),
+                       ("offline", lambda: prq.prq_quant_act(Zaug[:M], K + k, 0, Aq=Aq, Asc=Asc)))
+            for label, fn in fns:
                 for _ in range(3):
                     fn()
                 torch.cuda.synchronize()

@@ -176,7 +176,7 @@ int prq_quant_act(const void* X_bf16, int64_t ld_x, int32_t M, int32_t K, int32_
  *       past K_aug).
  * One wave thus reads one contiguous kilobyte per MFMA operand.  Both calls
  * require N % 16 == 0 and K_aug % 32 == 0; prq_pack_weight runs on `stream`
- * (device pointers; Wq and Wp 16-byte aligned, Wps 4-byte aligned).
+ * (device pointers; Wq, Wp and Wps 16-byte aligned).
  */
 int prq_packed_weight_bytes(int32_t E, int32_t N, int32_t K_aug, size_t* code_bytes,
                             size_t* scale_bytes);
@@ -213,6 +213,36 @@ int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M,
                 const uint8_t* Wp, const uint8_t* Wps, int32_t N, int32_t K_aug,
                 float* Y, void* workspace, size_t workspace_bytes,
                 int32_t variant, int32_t splits, hipStream_t stream);
+
+/*
+ * Packed activations (prefill): the activation side of Eq. 3 written by the
+ * quantizer directly in the packed layout of the weights (prq_pack_weight's
+ * layout with the M rows in the place of the N output features), so that the
+ * LDS-tiled GEMM copies both operands in whole contiguous kilobytes.  With
+ * S = ceil(K_aug / 128) and B = ceil(M / 16) row blocks:
+ *   Ap  [B][S][64][16] bytes: entry (b, s, l) the 16 code bytes of row
+ *       16 b + l % 16, K elements [128 s + 32 (l / 16), +32);
+ *   Aps [B][ceil(S/4)][64] uint32: byte j of entry (b, q, l) the E8M0 scale of
+ *       row 16 b + l % 16, 32-block 4 (4 q + j) + l / 16.
+ * Rows past M and K positions past K_aug hold zero codes and scale byte 127.
+ * The codes and scales are those of prq_quant_act, byte for byte.
+ *
+ * prq_packed_act_bytes -- sizes of Ap and Aps for M rows.  Returns PRQ_OK,
+ *   PRQ_EINVAL, PRQ_EALIGN (K_aug % 32), PRQ_EUNSUPPORTED (K_aug > 65536).
+ * prq_quant_act_packed -- prq_quant_act (dense: one perm and inv_scale_pos,
+ *   G = 1) into Ap / Aps (device, 16-byte aligned, of the sizes above).
+ *   Limits as prq_quant_act.  M == 0 is a no-op.
+ * prq_gemm_packed -- prq_gemm on a packed activation (the LDS-tiled kernel):
+ *   Y [M, N] float32 = Eq. 3 over K_aug; Ap / Aps from prq_quant_act_packed,
+ *   Wp / Wps from prq_pack_weight (E = 1).  No workspace.  Limits as prq_gemm.
+ */
+int prq_packed_act_bytes(int32_t M, int32_t K_aug, size_t* code_bytes, size_t* scale_bytes);
+int prq_quant_act_packed(const void* X_bf16, int64_t ld_x, int32_t M, int32_t K, int32_t k_tail,
+                         const float* inv_scale_pos, const int32_t* perm,
+                         uint8_t* Ap, uint8_t* Aps, hipStream_t stream);
+int prq_gemm_packed(const uint8_t* Ap, const uint8_t* Aps, int32_t M,
+                    const uint8_t* Wp, const uint8_t* Wps, int32_t N, int32_t K_aug,
+                    float* Y, hipStream_t stream);
 
 /*
  * prq_grouped_gemm -- Eq. 3 for E MoE experts in one launch (the paper applies

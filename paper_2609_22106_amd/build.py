@@ -73,7 +73,9 @@ def build(verbose=False):
         out = os.path.join(tmp, "libprq.so")
         _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", out, *objs, "-lpthread"])
         shutil.move(out, LIB)
-        pobjs = [o for o in objs if o.endswith(".hip.o")]   # kernels, for the tuning entry
+        # kernels for the tuning entry points (evaluate.hip calls into the host
+        # library and stays out)
+        pobjs = [o for o in objs if o.endswith(".hip.o") and not o.endswith("evaluate.hip.o")]
         for src in PROBE_SOURCES:
             obj = os.path.join(tmp, src + ".o")
             _run([HIPCC, *HIP_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", os.path.join(CSRC, src),

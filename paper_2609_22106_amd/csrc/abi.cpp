@@ -62,7 +62,7 @@ int check_gemm_common(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const ui
   if (K_aug % PRQ_BLOCK) return PRQ_EALIGN;
   if (N % 16) return PRQ_EALIGN;
   if (K_aug > kMaxKAug) return PRQ_EUNSUPPORTED;
-  if (!aligned16(Wp) || (reinterpret_cast<uintptr_t>(Wps) & 3u) ||
+  if (!aligned16(Wp) || !aligned16(Wps) ||
       (M > 0 && (!aligned16(Aq) || (reinterpret_cast<uintptr_t>(Y) & 3u))))
     return PRQ_EALIGN;
   return PRQ_OK;
@@ -103,7 +103,7 @@ int prq_pack_weight(const uint8_t* Wq, const uint8_t* Wsc, int32_t E, int32_t N,
   int st = prq_packed_weight_bytes(E, N, K_aug, &cb, &sb);
   if (st != PRQ_OK) return st;
   if (!Wq || !Wsc || !Wp || !Wps) return PRQ_EINVAL;
-  if (!aligned16(Wq) || !aligned16(Wp) || (reinterpret_cast<uintptr_t>(Wps) & 3u)) return PRQ_EALIGN;
+  if (!aligned16(Wq) || !aligned16(Wp) || !aligned16(Wps)) return PRQ_EALIGN;
   DeviceInfo dev;
   st = current_device(&dev);
   if (st != PRQ_OK) return st;
@@ -216,7 +216,7 @@ int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t*
     }
   }
   return launch_status(prq::launch_gemm_tile(Aq, Asc, M, nullptr, 1, Wp, Wps, N, K_aug, Y,
-                                             prq::choose_tile_shape(M, N, dev.num_cus), stream));
+                                             prq::choose_tile_shape(M, N, dev.num_cus, false), stream));
 }
 
 int prq_gemm(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t* Wp,
@@ -224,6 +224,50 @@ int prq_gemm(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t* Wp
              size_t workspace_bytes, hipStream_t stream) {
   return prq_gemm_ex(Aq, Asc, M, Wp, Wps, N, K_aug, Y, workspace, workspace_bytes, PRQ_GEMM_AUTO,
                      0, stream);
+}
+
+int prq_packed_act_bytes(int32_t M, int32_t K_aug, size_t* code_bytes, size_t* scale_bytes) {
+  if (M < 0 || K_aug <= 0 || !code_bytes || !scale_bytes) return PRQ_EINVAL;
+  if (K_aug % PRQ_BLOCK) return PRQ_EALIGN;
+  if (K_aug > kMaxKAug) return PRQ_EUNSUPPORTED;
+  const size_t blocks = (static_cast<size_t>(M) + 15) / 16;
+  const size_t steps = (static_cast<size_t>(K_aug) + 127) / 128;
+  *code_bytes = blocks * steps * 1024;
+  *scale_bytes = blocks * ((steps + 3) / 4) * 256;
+  return PRQ_OK;
+}
+
+int prq_quant_act_packed(const void* X_bf16, int64_t ld_x, int32_t M, int32_t K, int32_t k_tail,
+                         const float* inv_scale_pos, const int32_t* perm, uint8_t* Ap,
+                         uint8_t* Aps, hipStream_t stream) {
+  if (M < 0 || K <= 0 || ld_x < K) return PRQ_EINVAL;
+  if (K % PRQ_BLOCK || k_tail < 0 || k_tail % PRQ_BLOCK || k_tail > K) return PRQ_EALIGN;
+  if (K > kMaxK) return PRQ_EUNSUPPORTED;
+  if (M == 0) return PRQ_OK;
+  if (!X_bf16 || !Ap || !Aps) return PRQ_EINVAL;
+  if (!aligned16(X_bf16) || ld_x % 8 || !aligned16(Ap) || !aligned16(Aps)) return PRQ_EALIGN;
+  if ((inv_scale_pos && !aligned16(inv_scale_pos)) || (perm && !aligned16(perm)))
+    return PRQ_EALIGN;
+  DeviceInfo dev;
+  int st = current_device(&dev);
+  if (st != PRQ_OK) return st;
+  return launch_status(prq::launch_act_quant_packed(static_cast<const uint16_t*>(X_bf16), ld_x, M,
+                                                    K, k_tail, inv_scale_pos, perm, Ap, Aps,
+                                                    dev.num_cus, stream));
+}
+
+int prq_gemm_packed(const uint8_t* Ap, const uint8_t* Aps, int32_t M, const uint8_t* Wp,
+                    const uint8_t* Wps, int32_t N, int32_t K_aug, float* Y, hipStream_t stream) {
+  int st = check_gemm_common(Ap, Aps, M, Wp, Wps, N, K_aug, Y);
+  if (st != PRQ_OK) return st;
+  if (M == 0) return PRQ_OK;
+  if (!aligned16(Aps)) return PRQ_EALIGN;
+  DeviceInfo dev;
+  st = current_device(&dev);
+  if (st != PRQ_OK) return st;
+  return launch_status(prq::launch_gemm_tile_packed(Ap, Aps, M, Wp, Wps, N, K_aug, Y,
+                                                    prq::choose_tile_shape(M, N, dev.num_cus, true),
+                                                    stream));
 }
 
 size_t prq_grouped_gemm_workspace_bytes(int32_t M_total, int32_t E, int32_t N, int32_t K_aug) {

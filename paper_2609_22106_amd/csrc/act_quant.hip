@@ -67,6 +67,37 @@ __device__ __forceinline__ void load_unit(const int32_t* __restrict__ perm,
   }
 }
 
+// Where a row's codes and scales go.  Row-major: Aq [M][K_aug/2], Asc
+// [M][K_aug/32].  Packed: the MFMA-ordered layout of the packed weights with the
+// rows in the place of the output features -- Ap [ceil(M/16)][S][64][16] bytes,
+// entry (row block, step s, lane l) the 16 code bytes of row 16 rb + l % 16,
+// K elements [128 s + 32 (l / 16), +32); Aps [ceil(M/16)][ceil(S/4)][64] uint32,
+// byte j of entry (rb, q, l) the scale of the same row, 32-block
+// 4 (4 q + j) + l / 16 -- so the GEMM copies both operands in whole kilobytes.
+struct RowSink {
+  uint8_t* arow;
+  uint8_t* srow;
+  __device__ void word(int v, uint32_t w) const { *reinterpret_cast<uint32_t*>(arow + 4 * v) = w; }
+  __device__ void scale(int b, uint32_t c) const { srow[b] = static_cast<uint8_t>(c); }
+};
+
+struct PackedSink {
+  uint8_t* code;    // Ap + (r / 16) S 1024 + (r % 16) 16
+  uint8_t* sc;      // Aps + (r / 16) ceil(S/4) 256 + (r % 16) 4
+  __device__ PackedSink(uint8_t* Ap, uint8_t* Aps, int r, int steps, int sgroups)
+      : code(Ap + static_cast<int64_t>(r >> 4) * steps * 1024 + (r & 15) * 16),
+        sc(Aps + static_cast<int64_t>(r >> 4) * sgroups * 256 + (r & 15) * 4) {}
+  // unit v = 8 positions: block v / 4 (step b / 4, K part b % 4), quarter v % 4
+  __device__ void word(int v, uint32_t w) const {
+    const int b = v >> 2;
+    *reinterpret_cast<uint32_t*>(code + (b >> 2) * 1024 + (b & 3) * 256 + (v & 3) * 4) = w;
+  }
+  __device__ void scale(int b, uint32_t c) const {
+    const int s = b >> 2;
+    sc[(s >> 2) * 256 + (b & 3) * 64 + (s & 3)] = static_cast<uint8_t>(c);
+  }
+};
+
 // Quantize 8 values of a quarter block (the quad holds the whole block) and
 // write the word, the scale and, for tail blocks, their copies.  t = z * 2^-e
 // is exact (a power-of-two product whose magnitude stays below 8, or a
@@ -74,9 +105,9 @@ __device__ __forceinline__ void load_unit(const int32_t* __restrict__ perm,
 // code comes from the hardware converter at scale 1, which rounds to nearest
 // even and saturates at 6 exactly like the software rule on every float32
 // (checked exhaustively on the GPU).
+template <class Sink>
 __device__ __forceinline__ void quantize_store(const float (&z)[8], int u, int tail_unit0,
-                                               int copy_units, int copy_blocks, uint8_t* arow,
-                                               uint8_t* srow) {
+                                               int copy_units, int copy_blocks, const Sink& out) {
   float amax = 0.0f;
 #pragma unroll
   for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(z[j]));
@@ -88,11 +119,28 @@ __device__ __forceinline__ void quantize_store(const float (&z)[8], int u, int t
   for (int j = 0; j < 4; ++j)
     w |= (__builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, z[2 * j] * mul, z[2 * j + 1] * mul, 1.0f, 0) &
           0xFFu) << (8 * j);
-  *reinterpret_cast<uint32_t*>(arow + 4 * u) = w;
-  if ((u & 3) == 0) srow[u >> 2] = static_cast<uint8_t>(code);
+  out.word(u, w);
+  if ((u & 3) == 0) out.scale(u >> 2, code);
   if (u >= tail_unit0) {  // online copy of the quantized tail and its scales
-    *reinterpret_cast<uint32_t*>(arow + 4 * (u + copy_units)) = w;
-    if ((u & 3) == 0) srow[(u >> 2) + copy_blocks] = static_cast<uint8_t>(code);
+    out.word(u + copy_units, w);
+    if ((u & 3) == 0) out.scale((u >> 2) + copy_blocks, code);
+  }
+}
+
+// Packed layout padding of one row past K_aug: zero codes up to the end of
+// the last K step, scale byte 127 up to the end of the last group of four
+// steps (fewer than 16 blocks; the row's thread with unit u0 writes blocks
+// nb + u0, nb + u0 + units, ...).
+__device__ __forceinline__ void pad_row_tail(const PackedSink& out, int u0, int units, int nb,
+                                             int steps, int sgroups) {
+  for (int t = u0; t < 16; t += units) {
+    const int b = nb + t;
+    if (b < sgroups * 16) {
+      out.scale(b, 127u);
+      if (b < steps * 4)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) out.word(4 * b + q, 0u);
+    }
   }
 }
 
@@ -123,7 +171,7 @@ __global__ __launch_bounds__(kRowsThreads) void act_quant_rows_kernel(
     for (int j = 0; j < 8; ++j)
       z[j] = __uint_as_float(static_cast<uint32_t>(xr[un.src[j]]) << 16) * un.d[j];
     quantize_store(z, u, (K - k_tail) >> 3, k_tail >> 3, k_tail >> 5,
-                   Aq + static_cast<int64_t>(r) * row_bytes, Asc + static_cast<int64_t>(r) * nb);
+                   RowSink{Aq + static_cast<int64_t>(r) * row_bytes, Asc + static_cast<int64_t>(r) * nb});
   }
 }
 
@@ -169,7 +217,7 @@ inline size_t lds_kernel_bytes(int K) {
 // -- a thread writes pass i into buffer i&1 only after the barrier of pass
 // i-1, which every thread passes only after it finished reading pass i-2 from
 // that buffer.
-template <bool kGrouped, int kUnits>
+template <bool kGrouped, int kUnits, bool kPacked>
 __global__ __launch_bounds__(kLdsThreads) void act_quant_lds_kernel(
     const uint16_t* __restrict__ X, int64_t ld_x, int M, int K, int k_tail,
     const float* __restrict__ inv, const int32_t* __restrict__ perm,
@@ -188,6 +236,8 @@ __global__ __launch_bounds__(kLdsThreads) void act_quant_lds_kernel(
   const int64_t row_bytes = k_aug >> 1;
   const int nb = k_aug >> 5;
   const int tail_unit0 = (K - k_tail) >> 3;
+  const int steps = (k_aug + 127) >> 7;
+  const int sgroups = (steps + 3) >> 2;
 
   // Staged vectors of this thread: v = tid + 512 i -> (row offset, vector),
   // as named registers (an array here ends up in scratch when its copy loop is
@@ -238,8 +288,9 @@ __global__ __launch_bounds__(kLdsThreads) void act_quant_lds_kernel(
         cur_g = g;
       }
       const uint16_t* row = reinterpret_cast<const uint16_t*>(sb) + static_cast<int64_t>(ro) * K;
-      uint8_t* arow = Aq + static_cast<int64_t>(r) * row_bytes;
-      uint8_t* srow = Asc + static_cast<int64_t>(r) * nb;
+      const RowSink rsink{Aq + static_cast<int64_t>(r) * row_bytes, Asc + static_cast<int64_t>(r) * nb};
+      const PackedSink psink(Aq, Asc, r, steps, sgroups);
+      if constexpr (kPacked) pad_row_tail(psink, u0, units, nb, steps, sgroups);
 #pragma unroll
       for (int j = 0; j < kUnits; ++j) {
         const int u = u0 + j * kLdsThreads;
@@ -251,19 +302,42 @@ __global__ __launch_bounds__(kLdsThreads) void act_quant_lds_kernel(
             z[2 * e] = __uint_as_float(static_cast<uint32_t>(row[sp & 0xFFFFu]) << 16) * un[j].d[2 * e];
             z[2 * e + 1] = __uint_as_float(static_cast<uint32_t>(row[sp >> 16]) << 16) * un[j].d[2 * e + 1];
           }
-          quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, arow, srow);
+          if constexpr (kPacked)
+            quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, psink);
+          else
+            quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, rsink);
         }
+      }
+    }
+  }
+  // Packed layout: the workgroup with the last row also fills the rows of the
+  // last 16-row block past M (zero codes, scale byte 127).
+  if constexpr (kPacked) {
+    if (r0 < r1 && r1 == M) {
+      for (int r = M; r < ((M + 15) & ~15); ++r) {
+        const PackedSink psink(Aq, Asc, r, steps, sgroups);
+        for (int v = tid; v < steps * 16; v += kLdsThreads) psink.word(v, 0u);
+        for (int b = tid; b < sgroups * 16; b += kLdsThreads) psink.scale(b, 127u);
       }
     }
   }
 }
 
-template <bool kGrouped, int kUnits>
+template <bool kGrouped, int kUnits, bool kPacked = false>
 void launch_lds(dim3 grid, size_t lds, hipStream_t stream, const uint16_t* X, int64_t ld_x,
                 int M, int K, int k_tail, const float* inv, const int32_t* perm,
                 const int32_t* offsets, int G, int rows_per_wg, uint8_t* Aq, uint8_t* Asc) {
-  act_quant_lds_kernel<kGrouped, kUnits><<<grid, kLdsThreads, lds, stream>>>(
+  act_quant_lds_kernel<kGrouped, kUnits, kPacked><<<grid, kLdsThreads, lds, stream>>>(
       X, ld_x, M, K, k_tail, inv, perm, offsets, G, rows_per_wg, Aq, Asc);
+}
+
+// Rows per workgroup of the LDS kernel: two workgroups per CU, a whole number
+// of passes each, contiguous row ranges (inside one expert for most rows).
+int lds_rows_per_wg(int M, int units, int num_cus) {
+  const int rpp = lds_rows_per_pass(units);
+  const int target = std::max(1, num_cus * 2);
+  int rows_per_wg = std::max(1, (M + target - 1) / target);
+  return (rows_per_wg + rpp - 1) / rpp * rpp;
 }
 
 }  // namespace
@@ -296,13 +370,8 @@ hipError_t launch_act_quant_kernel(const uint16_t* X, int64_t ld_x, int M, int K
   }
   // At most 2 * 2048 * 16 bytes = 64 KiB of LDS: within the default limit.
   const size_t lds = lds_kernel_bytes(K);
-  const int rpp = lds_rows_per_pass(units);
   const int per_thread = (units + kLdsThreads - 1) / kLdsThreads;   // 1..4 (K <= 16384)
-  // Two workgroups per CU; a workgroup's rows are a whole number of passes,
-  // and contiguous row ranges keep it inside one expert for most rows.
-  const int target = std::max(1, num_cus * 2);
-  int rows_per_wg = std::max(1, (M + target - 1) / target);
-  rows_per_wg = (rows_per_wg + rpp - 1) / rpp * rpp;
+  const int rows_per_wg = lds_rows_per_wg(M, units, num_cus);
   const dim3 grid((M + rows_per_wg - 1) / rows_per_wg);
   const int32_t* off = grouped ? group_offsets : nullptr;
   const int g = grouped ? G : 1;
@@ -323,6 +392,23 @@ hipError_t launch_act_quant_kernel(const uint16_t* X, int64_t ld_x, int M, int K
       PRQ_LDS_CASE(4)
   }
 #undef PRQ_LDS_CASE
+  return hipGetLastError();
+}
+
+hipError_t launch_act_quant_packed(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail,
+                                   const float* inv_scale_pos, const int32_t* perm, uint8_t* Ap,
+                                   uint8_t* Aps, int num_cus, hipStream_t stream) {
+  const int units = K >> 3;
+  const size_t lds = lds_kernel_bytes(K);
+  const int per_thread = (units + kLdsThreads - 1) / kLdsThreads;
+  const int rows_per_wg = lds_rows_per_wg(M, units, num_cus);
+  const dim3 grid((M + rows_per_wg - 1) / rows_per_wg);
+  switch (per_thread) {
+    case 1: launch_lds<false, 1, true>(grid, lds, stream, X, ld_x, M, K, k_tail, inv_scale_pos, perm, nullptr, 1, rows_per_wg, Ap, Aps); break;
+    case 2: launch_lds<false, 2, true>(grid, lds, stream, X, ld_x, M, K, k_tail, inv_scale_pos, perm, nullptr, 1, rows_per_wg, Ap, Aps); break;
+    case 3: launch_lds<false, 3, true>(grid, lds, stream, X, ld_x, M, K, k_tail, inv_scale_pos, perm, nullptr, 1, rows_per_wg, Ap, Aps); break;
+    default: launch_lds<false, 4, true>(grid, lds, stream, X, ld_x, M, K, k_tail, inv_scale_pos, perm, nullptr, 1, rows_per_wg, Ap, Aps); break;
+  }
   return hipGetLastError();
 }
 

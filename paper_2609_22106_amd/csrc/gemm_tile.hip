@@ -121,44 +121,90 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((n & 0xF) | ((n >> 4) << 14) | (0x7 << 4));
 }
 
-template <int kBM, int kBN, int kWM, int kWN, int kNS, bool kGrouped>
+// Instruction order of one pipelined step: the MFMAs one after another, the
+// step's direct-to-LDS loads after the first kLd of them and its LDS reads of
+// the next step spread between all of them, so both are issued while the
+// matrix unit is busy.
+template <int kMf, int kLd, int kRd>
+__device__ __forceinline__ void interleave() {
+  static_for<kMf>([&](auto ic) {
+    constexpr int i = decltype(ic)::value;
+    constexpr int r0 = i * kRd / kMf, r1 = (i + 1) * kRd / kMf;
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);              // MFMA
+    if constexpr (i < kLd) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // VMEM read
+    if constexpr (r1 > r0) __builtin_amdgcn_sched_group_barrier(0x100, r1 - r0, 0);  // DS read
+  });
+}
+
+// How the activation operand is laid out in memory: row-major Aq/Asc with the
+// scales staged a byte at a time or, when K_aug % 128 == 0, one aligned dword
+// per row and step; or the packed (weight) layout, staged like the weight.
+enum AMode { kARowByte = 0, kARowDword = 1, kAPacked = 2 };
+
+// LDS stage of one 128-element K step: A codes [kBM/16 blocks][1 KiB] | B codes
+// [kBN/16 blocks][1 KiB] | A scales | B scales [kBN/16 tiles][64 dwords].  Codes
+// are in MFMA lane order (block b, lane l: row 16b + l % 16, K part l / 16, 16
+// bytes).  A scales: row dwords -- one dword per row (the row's four scale bytes
+// of the step); row bytes -- one byte per lane-order slot of each 16-row block
+// (dword slots); packed -- as B.  B scales are the packed weight's dwords of the
+// step's group of four steps (byte j = step 4q+j).
+template <int kBM, int kBN, int kAMode>
+struct TileStage {
+  static constexpr int kABlk = kBM / 16, kBBlk = kBN / 16;
+  static constexpr int kOffB = kABlk * 1024;
+  static constexpr int kOffAs = (kABlk + kBBlk) * 1024;
+  static constexpr int kAsBytes = kAMode == kARowDword ? kBM * 4 : kABlk * 256;
+  static constexpr int kOffBs = kOffAs + kAsBytes;
+  static constexpr int kBytes = kOffBs + kBBlk * 256;
+};
+
+constexpr int lcm4(int n) { return n % 4 == 0 ? n : (n % 2 == 0 ? 2 * n : 4 * n); }
+
+template <int kBM, int kBN, int kWM, int kWN, int kNS, bool kGrouped, int kAMode>
 __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
     const uint8_t* __restrict__ Aq, const uint8_t* __restrict__ Asc, int M,
     const int32_t* __restrict__ off, int E, int n_mtiles, const uint8_t* __restrict__ Wp,
     const uint8_t* __restrict__ Wps, int N, int K_aug, float* __restrict__ Y) {
+  using L = TileStage<kBM, kBN, kAMode>;
+  constexpr bool kScaleDword = kAMode == kARowDword;
+  constexpr bool kPackedA = kAMode == kAPacked;
+  static_assert(!(kPackedA && kGrouped), "packed activations: dense calls");
   constexpr int kWaves = kWM * kWN;
   constexpr int kThreads = kWaves * 64;
   constexpr int kTM = kBM / kWM, kTN = kBN / kWN;    // wave tile
   constexpr int kFM = kTM / 32, kFN = kTN / 32;      // 32x32 fragments per wave
   static_assert(kTM % 32 == 0 && kTN % 32 == 0, "wave tile of whole 32x32 fragments");
-  constexpr int kABlk = kBM / 16, kBBlk = kBN / 16;  // 16-row operand blocks per step
-  static_assert(kABlk % kWaves == 0 && kBBlk % kWaves == 0, "blocks split evenly over waves");
+  constexpr int kABlk = L::kABlk, kBBlk = L::kBBlk;
+  static_assert(kABlk % kWaves == 0 && kBBlk % kWaves == 0, "code blocks split evenly over waves");
+  static_assert(kBBlk % 4 == 0, "B scales move four tile entries per instruction");
   constexpr int kAPer = kABlk / kWaves, kBPer = kBBlk / kWaves;
-  constexpr int kLoads = 2 * (kAPer + kBPer);        // direct-to-LDS loads per wave per step
-  // Stage layout: A codes [kABlk][1 KiB] | B codes [kBBlk][1 KiB] | A scales
-  // [kABlk][64 dwords] | B scales [kBBlk][64 dwords]; lane order everywhere.
-  constexpr int kOffB = kABlk * 1024;
-  constexpr int kOffAs = (kABlk + kBBlk) * 1024;
-  constexpr int kOffBs = kOffAs + kABlk * 256;
-  constexpr int kStage = (kABlk + kBBlk) * 1280;
-  static_assert(kNS >= 2 && kNS <= 6, "stages");
-  // One LDS object per stage: the compiler then knows which stage an
-  // in-flight direct-to-LDS load writes and does not make LDS reads of the
-  // other stages wait for it.
-  __shared__ __align__(16) uint8_t st0[kStage];
-  __shared__ __align__(16) uint8_t st1[kStage];
-  __shared__ __align__(16) uint8_t st2[kNS > 2 ? kStage : 16];
-  __shared__ __align__(16) uint8_t st3[kNS > 3 ? kStage : 16];
-  __shared__ __align__(16) uint8_t st4[kNS > 4 ? kStage : 16];
-  __shared__ __align__(16) uint8_t st5[kNS > 5 ? kStage : 16];
+  // Scale instructions per step: A as 64 row dwords, one per 16-row block
+  // (bytes), or four block entries of 256 bytes (packed); B as four tile
+  // entries.  When there are fewer than waves, several waves load the same
+  // chunk (identical bytes).
+  constexpr int kAsChunks = kScaleDword ? kBM / 64 : (kPackedA ? kABlk / 4 : kABlk);
+  constexpr int kBsChunks = kBBlk / 4;
+  constexpr int kAsPer = (kAsChunks + kWaves - 1) / kWaves;
+  constexpr int kBsPer = (kBsChunks + kWaves - 1) / kWaves;
+  constexpr int kLoads = kAPer + kBPer + kAsPer + kBsPer;   // direct-to-LDS loads per wave per step
+  static_assert(kNS >= 2 && kNS <= 4, "stages");
+  static_assert(kNS * L::kBytes + (kGrouped ? kThreads * 4 + 16 : 0) <= 160 * 1024, "LDS");
+  constexpr int kU = lcm4(kNS);   // main-loop unroll: stage index and step mod 4 both known
+  constexpr int kMfmas = 2 * kFM * kFN;                                  // per step
+  constexpr int kReads = 4 * (kFM + kFN);                                // LDS reads per step
+  // One LDS object per stage: the compiler then knows which stage an in-flight
+  // direct-to-LDS load writes and does not make LDS reads of the other stages
+  // wait for it.
+  __shared__ __align__(16) uint8_t st0[L::kBytes];
+  __shared__ __align__(16) uint8_t st1[L::kBytes];
+  __shared__ __align__(16) uint8_t st2[kNS > 2 ? L::kBytes : 16];
+  __shared__ __align__(16) uint8_t st3[kNS > 3 ? L::kBytes : 16];
   auto stage = [&](auto pc) -> uint8_t* {
-    constexpr int p = decltype(pc)::value;
+    constexpr int p = decltype(pc)::value % kNS;
     if constexpr (p == 0) return st0;
     else if constexpr (p == 1) return st1;
     else if constexpr (p == 2) return st2;
-    else if constexpr (p == 3) return st3;
-    else if constexpr (p == 4) return st4;
-    else return st5;
+    else return st3;
   };
 
   const int ntiles = N >> 4;
@@ -179,55 +225,94 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   const int nb = K_aug >> 5;
   const int steps = (K_aug + kStepK - 1) / kStepK;
   const int sgroups = (steps + 3) >> 2;
+  const int nblk = (M + 15) >> 4;                    // packed activation row blocks
   const uint8_t* We = Wp + static_cast<int64_t>(e) * ntiles * steps * 1024;
   const uint8_t* Wse = Wps + static_cast<int64_t>(e) * ntiles * sgroups * 256;
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar registers
   const int wm = wave / kWN, wn = wave % kWN;
   const int lr = lane & 15, lk = lane >> 4;
 
-  // Per-lane source rows / tiles of this wave's loads (fixed over the K loop).
-  const uint8_t* a_row[kAPer];
-  const uint8_t* as_row[kAPer];
-  const uint8_t* b_tile[kBPer];
-  const uint8_t* bs_tile[kBPer];
+  // Per-lane byte offsets of this wave's loads from uniform bases (fixed over
+  // the K loop; rows and tiles clamped into the operands; the host checks that
+  // the operands fit 32-bit offsets).
+  uint32_t a_off[kAPer], as_off[kAsPer], b_off[kBPer], bs_off[kBsPer];
 #pragma unroll
   for (int i = 0; i < kAPer; ++i) {
-    const int rb = wave + i * kWaves;
-    const int m = min(row_begin + rb * 16 + lr, row_end - 1);
-    a_row[i] = Aq + m * row_bytes;
-    as_row[i] = Asc + static_cast<int64_t>(m) * nb;
+    if constexpr (kPackedA) {
+      const int rb = min((row_begin >> 4) + wave + i * kWaves, nblk - 1);
+      a_off[i] = static_cast<uint32_t>(rb) * steps * 1024 + lane * 16;
+    } else {
+      const int m = min(row_begin + (wave + i * kWaves) * 16 + lr, row_end - 1);
+      a_off[i] = static_cast<uint32_t>(m) * static_cast<uint32_t>(row_bytes) + lk * 16;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < kAsPer; ++i) {
+    const int c = (wave + i * kWaves) % kAsChunks;
+    if constexpr (kPackedA) {
+      const int rb = min((row_begin >> 4) + c * 4 + (lane >> 4), nblk - 1);
+      as_off[i] = static_cast<uint32_t>(rb) * sgroups * 256 + (lane & 15) * 16;
+    } else {
+      const int m = kScaleDword ? min(row_begin + c * 64 + lane, row_end - 1)
+                                : min(row_begin + c * 16 + lr, row_end - 1);
+      as_off[i] = static_cast<uint32_t>(m) * nb + (kScaleDword ? 0 : lk);
+    }
   }
 #pragma unroll
   for (int i = 0; i < kBPer; ++i) {
     const int t = min(t0 + wave + i * kWaves, ntiles - 1);
-    b_tile[i] = We + static_cast<int64_t>(t) * steps * 1024 + lane * 16;
-    bs_tile[i] = Wse + static_cast<int64_t>(t) * sgroups * 256 + lane * 4;
+    b_off[i] = static_cast<uint32_t>(t) * steps * 1024 + lane * 16;
+  }
+#pragma unroll
+  for (int i = 0; i < kBsPer; ++i) {
+    const int c = (wave + i * kWaves) % kBsChunks;
+    const int t = min(t0 + c * 4 + (lane >> 4), ntiles - 1);
+    bs_off[i] = static_cast<uint32_t>(t) * sgroups * 256 + (lane & 15) * 16;
   }
 
-  // Step s into stage `st`: every source address is valid (parts past K_aug
-  // point at the row start: they meet zero weight codes with finite scales).
+  // Step s into stage `st`.  Every source address is valid: with K_aug not a
+  // multiple of 128, K parts of the last step past K_aug point at the row start
+  // (they meet zero weight codes with finite scales).
   auto issue = [&](int s, uint8_t* st) {
-    const bool kok = s * kStepK + lk * 32 < K_aug;
-    const int64_t abyte = kok ? static_cast<int64_t>(s) * kStepBytes + lk * 16 : 0;
-    const int sbyte = kok ? s * 4 + lk : 0;
+    const bool kok = kScaleDword || s * kStepK + lk * 32 < K_aug;
 #pragma unroll
-    for (int i = 0; i < kAPer; ++i)
-      __builtin_amdgcn_global_load_lds(PRQ_GPTR(a_row[i] + abyte),
-                                       PRQ_LPTR(st + (wave + i * kWaves) * 1024), 16, 0, 0);
-#pragma unroll
-    for (int i = 0; i < kBPer; ++i)
-      __builtin_amdgcn_global_load_lds(PRQ_GPTR(b_tile[i] + static_cast<int64_t>(s) * 1024),
-                                       PRQ_LPTR(st + kOffB + (wave + i * kWaves) * 1024), 16, 0, 0);
-#pragma unroll
-    for (int i = 0; i < kAPer; ++i)
-      __builtin_amdgcn_global_load_lds(PRQ_GPTR(as_row[i] + sbyte),
-                                       PRQ_LPTR(st + kOffAs + (wave + i * kWaves) * 256), 1, 0, 0);
+    for (int i = 0; i < kAPer; ++i) {
+      if constexpr (kPackedA)   // padded past K_aug and M: whole steps, whole blocks
+        __builtin_amdgcn_global_load_lds(PRQ_GPTR(Aq + (a_off[i] + s * 1024u)),
+                                         PRQ_LPTR(st + (wave + i * kWaves) * 1024), 16, 0, 0);
+      else
+        __builtin_amdgcn_global_load_lds(
+            PRQ_GPTR(Aq + (kok ? a_off[i] + s * kStepBytes : a_off[i] - lk * 16)),
+            PRQ_LPTR(st + (wave + i * kWaves) * 1024), 16, 0, 0);
+    }
 #pragma unroll
     for (int i = 0; i < kBPer; ++i)
-      __builtin_amdgcn_global_load_lds(PRQ_GPTR(bs_tile[i] + (s >> 2) * 256 + (s & 3)),
-                                       PRQ_LPTR(st + kOffBs + (wave + i * kWaves) * 256), 1, 0, 0);
+      __builtin_amdgcn_global_load_lds(PRQ_GPTR(We + (b_off[i] + s * 1024u)),
+                                       PRQ_LPTR(st + L::kOffB + (wave + i * kWaves) * 1024), 16,
+                                       0, 0);
+#pragma unroll
+    for (int i = 0; i < kAsPer; ++i) {
+      const int c = (wave + i * kWaves) % kAsChunks;
+      if constexpr (kPackedA)      // four blocks' entries of the step's group
+        __builtin_amdgcn_global_load_lds(PRQ_GPTR(Asc + (as_off[i] + (s >> 2) * 256u)),
+                                         PRQ_LPTR(st + L::kOffAs + c * 1024), 16, 0, 0);
+      else if constexpr (kScaleDword)   // K_aug % 128 == 0: the row's 4 bytes of step s, aligned
+        __builtin_amdgcn_global_load_lds(PRQ_GPTR(Asc + (as_off[i] + s * 4)),
+                                         PRQ_LPTR(st + L::kOffAs + c * 256), 4, 0, 0);
+      else
+        __builtin_amdgcn_global_load_lds(
+            PRQ_GPTR(Asc + (kok ? as_off[i] + s * 4 : as_off[i] - lk)),
+            PRQ_LPTR(st + L::kOffAs + c * 256), 1, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < kBsPer; ++i) {
+      const int c = (wave + i * kWaves) % kBsChunks;
+      __builtin_amdgcn_global_load_lds(PRQ_GPTR(Wse + (bs_off[i] + (s >> 2) * 256u)),
+                                       PRQ_LPTR(st + L::kOffBs + c * 1024), 16, 0, 0);
+    }
   };
 
   v16f acc[kFM][kFN];
@@ -236,87 +321,103 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
 #pragma unroll
     for (int j = 0; j < kFN; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
 
-  // A 32-row x 64-element operand of the 32x32x64 MFMA read from the staged
-  // 16-row x 128-element blocks: lane l takes row l % 32 (block 2f + bit 4 of
-  // l), K part 2h + l / 32 of the step -- in-block lane (l % 16) + 16 (2h + l / 32),
-  // so each 16 lanes read 256 contiguous bytes (conflict-free).
+  // Operands of one half of a step in registers: for half h (K elements
+  // [64h, 64h+64) of the step), the 32-row x 64-element MFMA operand of
+  // fragment i: lane l takes row l % 32 (block 2i + bit 4 of l) and K part
+  // 2h + l / 32, i.e. in-block lane (l % 16) + 16 (2h + l / 32); each 16 lanes
+  // read 256 contiguous bytes (conflict-free).
+  struct Half {
+    uint4 a[kFM], b[kFN];
+    uint32_t sa[kFM], sb[kFN];
+  };
+  // Per-lane LDS byte offsets of the reads within a stage; fragment and half
+  // add compile-time constants (the instruction's immediate offset).
   const int blk_sel = (lane >> 4) & 1;
   const int lib0 = (lane & 15) + 16 * (lane >> 5);
-  auto load_half = [&](const uint8_t* st, int h, uint4 (&a)[kFM], uint4 (&b)[kFN],
-                       uint32_t (&sa)[kFM], uint32_t (&sb)[kFN]) {
-    const int lib = lib0 + 32 * h;
+  const uint32_t a_lb = (wm * (kTM / 16) + blk_sel) * 1024 + lib0 * 16;
+  const uint32_t b_lb = L::kOffB + (wn * (kTN / 16) + blk_sel) * 1024 + lib0 * 16;
+  const uint32_t as_lb = kScaleDword ? L::kOffAs + (wm * kTM + (lane & 31)) * 4
+                                     : L::kOffAs + (wm * (kTM / 16) + blk_sel) * 256 + lib0 * 4;
+  const uint32_t bs_lb = L::kOffBs + (wn * (kTN / 16) + blk_sel) * 256 + lib0 * 4;
+  const uint32_t a_shift = 8 * (lane >> 5);   // row dword: part l / 32 to byte 0, 2 + l / 32 to byte 2
+  auto read = [&](const uint8_t* st, auto hc, Half& o) {
+    constexpr int h = decltype(hc)::value;
 #pragma unroll
     for (int i = 0; i < kFM; ++i) {
-      const int blk = wm * (kTM / 16) + 2 * i + blk_sel;
-      a[i] = *reinterpret_cast<const uint4*>(st + blk * 1024 + lib * 16);
-      sa[i] = *reinterpret_cast<const uint32_t*>(st + kOffAs + blk * 256 + lib * 4);
+      o.a[i] = *reinterpret_cast<const uint4*>(st + a_lb + (2 * i * 1024 + h * 512));
+      o.sa[i] = *reinterpret_cast<const uint32_t*>(
+          st + as_lb + (kScaleDword ? 32 * i * 4 : 2 * i * 256 + h * 128));
     }
 #pragma unroll
     for (int j = 0; j < kFN; ++j) {
-      const int blk = wn * (kTN / 16) + 2 * j + blk_sel;
-      b[j] = *reinterpret_cast<const uint4*>(st + kOffB + blk * 1024 + lib * 16);
-      sb[j] = *reinterpret_cast<const uint32_t*>(st + kOffBs + blk * 256 + lib * 4);
+      o.b[j] = *reinterpret_cast<const uint4*>(st + b_lb + (2 * j * 1024 + h * 512));
+      o.sb[j] = *reinterpret_cast<const uint32_t*>(st + bs_lb + (2 * j * 256 + h * 128));
     }
   };
-  auto mfma_half = [&](const uint4 (&a)[kFM], const uint4 (&b)[kFN], const uint32_t (&sa)[kFM],
-                       const uint32_t (&sb)[kFN]) {
+  // The MFMAs of half h of a step; kQ = step mod 4 picks the B scale byte.
+  auto mfma = [&](const Half& o, auto hc, auto qc) {
+    constexpr int h = decltype(hc)::value, kQ = decltype(qc)::value;
 #pragma unroll
-    for (int i = 0; i < kFM; ++i)
+    for (int i = 0; i < kFM; ++i) {
+      const uint32_t sa = kScaleDword ? (o.sa[i] >> a_shift) : o.sa[i];
 #pragma unroll
       for (int j = 0; j < kFN; ++j)
-        acc[i][j] = dev::mfma_fp4_32x32x64(a[i], b[j], sa[i], sb[j], acc[i][j]);
-  };
-  // With one wave per SIMD (4-wave workgroups) the register budget holds both
-  // K halves' operands, so all LDS reads of a step are issued before its
-  // MFMAs; with two waves per SIMD the halves go one after the other.
-  constexpr bool kBothHalves = kWaves <= 4;
-  auto compute = [&](const uint8_t* st) {
-    uint4 a0[kFM], b0[kFN];
-    uint32_t sa0[kFM], sb0[kFN];
-    load_half(st, 0, a0, b0, sa0, sb0);
-    if constexpr (kBothHalves) {
-      uint4 a1[kFM], b1[kFN];
-      uint32_t sa1[kFM], sb1[kFN];
-      load_half(st, 1, a1, b1, sa1, sb1);
-      mfma_half(a0, b0, sa0, sb0);
-      mfma_half(a1, b1, sa1, sb1);
-    } else {
-      mfma_half(a0, b0, sa0, sb0);
-      load_half(st, 1, a0, b0, sa0, sb0);
-      mfma_half(a0, b0, sa0, sb0);
+        acc[i][j] = dev::mfma_fp4_32x32x64_sel<kScaleDword ? 2 * h : (kPackedA ? kQ : 0), kQ>(
+            o.a[i], o.b[j], sa, o.sb[j], acc[i][j]);
     }
   };
 
-  // Prologue: steps 0 .. kNS-2 in flight.  Every wave issues the same
-  // sequence on every path: steps past the end reload the last step into a
-  // stage that is never read, and the wait, barrier and issue of a stage run
-  // even when its step is past the end (only its MFMAs are skipped).  Then
-  // exactly kNS - 2 later steps are in flight at every wait, one constant
-  // vmcnt serves every step, and the compiler sees that the stage about to be
-  // read has landed (a wait count chosen at run time, or a stage skipped as a
-  // whole, leaves it a path that makes it drain all loads first).
-  static_for<kNS - 1>([&](auto pc) {
+  // Pipeline, kNS stages of one K step each.  Prologue: steps 0 .. kNS-1 into
+  // every stage; wait for step 0; read its first half.  Iteration s:
+  //   MFMAs of half 0 of step s, while half 1 of step s is read from LDS;
+  //   wait until this wave's loads of step s+1 have landed and its LDS reads
+  //   are complete, one bare barrier (the same then holds for every wave, so
+  //   step s's stage is free), issue step s+kNS into it;
+  //   MFMAs of half 1 of step s, while half 0 of step s+1 is read.
+  // Every wave issues the same sequence on every path -- steps past the end
+  // reload the last step, and the wait, barrier, issue and reads of a step run
+  // even past the end (only its MFMAs are skipped) -- so one constant vmcnt
+  // serves every iteration and the compiler sees that the stage about to be
+  // read has landed (a wait count chosen at run time leaves it a path on which
+  // it drains every load first).  Scheduling barriers keep each wait and
+  // barrier between the MFMAs it separates.
+  static_for<kNS>([&](auto pc) {
     issue(min(static_cast<int>(decltype(pc)::value), steps - 1), stage(pc));
   });
-  // Main loop, unrolled by kNS so every stage is a known LDS object.
-  for (int s0 = 0; s0 < steps; s0 += kNS) {
-    static_for<kNS>([&](auto pc) {
-      constexpr int p = decltype(pc)::value;
-      const int s = s0 + p;
-      // This wave's loads of step s have landed; the bare barrier then says
-      // the same of every wave, and that every wave is done reading the stage
-      // the next issue overwrites.
-      wait_vmcnt<(kNS - 2) * kLoads>();
-      __builtin_amdgcn_s_barrier();
-      issue(min(s + kNS - 1, steps - 1), stage(IntC<(p + kNS - 1) % kNS>{}));
-      if (s < steps) compute(stage(pc));
-    });
-  }
+  wait_vmcnt<(kNS - 1) * kLoads>();
+  __builtin_amdgcn_s_barrier();
+  Half h0, h1;
+  read(st0, IntC<0>{}, h0);
+  auto body = [&](int s0, auto pc, auto gc) {
+    constexpr int p = decltype(pc)::value;
+    constexpr bool kGuard = decltype(gc)::value;
+    const int s = s0 + p;
+    const bool live = !kGuard || s < steps;
+    __builtin_amdgcn_sched_barrier(0);
+    if (live) mfma(h0, IntC<0>{}, IntC<p % 4>{});
+    read(stage(pc), IntC<1>{}, h1);
+    if constexpr (!kGuard) interleave<kMfmas / 2, 0, kReads / 2>();
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vmcnt<(kNS - 2) * kLoads>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    issue(min(s + kNS, steps - 1), stage(pc));
+    if (live) mfma(h1, IntC<1>{}, IntC<p % 4>{});
+    read(stage(IntC<p + 1>{}), IntC<0>{}, h0);
+    if constexpr (!kGuard) interleave<kMfmas / 2, kLoads, kReads / 2>();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // Whole groups of kU steps without guards (so the scheduler can interleave
+  // the LDS reads with the MFMAs), then one guarded group for the rest.
+  int s0 = 0;
+  for (; s0 + kU <= steps; s0 += kU)
+    static_for<kU>([&](auto pc) { body(s0, pc, IntC<0>{}); });
+  if (s0 < steps) static_for<kU>([&](auto pc) { body(s0, pc, IntC<1>{}); });
   wait_vmcnt<0>();   // no direct-to-LDS write outlives the workgroup
 
-  // Element e of a lane's fragment is C[8 (e / 4) + 4 (l / 32) + e % 4][l % 32]:
+  // Element q of a lane's fragment is C[8 (q / 4) + 4 (l / 32) + q % 4][l % 32]:
   // activation row, feature column (32 lanes store 128 contiguous bytes).
 #pragma unroll
   for (int i = 0; i < kFM; ++i)
@@ -324,44 +425,85 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
     for (int j = 0; j < kFN; ++j) {
       const int n = t0 * 16 + wn * kTN + j * 32 + (lane & 31);
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int m = row_begin + wm * kTM + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        if (m < row_end && n < N) Y[static_cast<int64_t>(m) * N + n] = acc[i][j][e];
+      for (int q = 0; q < 16; ++q) {
+        const int m = row_begin + wm * kTM + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
+        if (m < row_end && n < N) Y[static_cast<int64_t>(m) * N + n] = acc[i][j][q];
       }
     }
 }
 
-template <int kBM, int kBN, int kWM, int kWN, int kNS>
-hipError_t launch_shape(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off, int E,
-                        const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug, float* Y,
-                        hipStream_t stream) {
+template <int kBM, int kBN, int kWM, int kWN, int kNS, int kAMode>
+hipError_t launch_shape_scales(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off,
+                               int E, const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug,
+                               float* Y, hipStream_t stream) {
+  // The kernel addresses A and one expert's weight with 32-bit byte offsets.
+  const int64_t steps = (K_aug + kStepK - 1) / kStepK;
+  if (static_cast<int64_t>((M + 15) / 16) * steps * 1024 >= (int64_t{1} << 31) ||
+      static_cast<int64_t>(N / 16) * steps * 1024 >= (int64_t{1} << 31))
+    return hipErrorInvalidValue;
   const int n_ntiles = (N + kBN - 1) / kBN;
   // Grouped: an upper bound on the row tiles over all experts (extra ids exit).
   const int n_mtiles = off ? (M + kBM - 1) / kBM + E : (M + kBM - 1) / kBM;
   const int grid = n_mtiles * n_ntiles;
-  if (off)
-    gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, true><<<grid, kWM * kWN * 64, 0, stream>>>(
-        Aq, Asc, M, off, E, n_mtiles, Wp, Wps, N, K_aug, Y);
-  else
-    gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, false><<<grid, kWM * kWN * 64, 0, stream>>>(
-        Aq, Asc, M, nullptr, 1, n_mtiles, Wp, Wps, N, K_aug, Y);
+  if constexpr (kAMode == kAPacked) {
+    gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, false, kAMode>
+        <<<grid, kWM * kWN * 64, 0, stream>>>(Aq, Asc, M, nullptr, 1, n_mtiles, Wp, Wps, N, K_aug,
+                                              Y);
+  } else if (off) {
+    gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, true, kAMode>
+        <<<grid, kWM * kWN * 64, 0, stream>>>(Aq, Asc, M, off, E, n_mtiles, Wp, Wps, N, K_aug, Y);
+  } else {
+    gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, false, kAMode>
+        <<<grid, kWM * kWN * 64, 0, stream>>>(Aq, Asc, M, nullptr, 1, n_mtiles, Wp, Wps, N, K_aug,
+                                              Y);
+  }
   return hipGetLastError();
+}
+
+// Activation scale rows are dword-aligned when K_aug is a multiple of 128
+// (K_aug / 32 scale bytes per row) and Asc is; otherwise they are staged a
+// byte at a time.
+template <int kBM, int kBN, int kWM, int kWN, int kNSDword, int kNSByte>
+hipError_t launch_shape(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off, int E,
+                        const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug, float* Y,
+                        bool packed, hipStream_t stream) {
+  if (packed)
+    return launch_shape_scales<kBM, kBN, kWM, kWN, kNSDword, kAPacked>(Aq, Asc, M, nullptr, 1, Wp,
+                                                                       Wps, N, K_aug, Y, stream);
+  if (K_aug % 128 == 0 && (reinterpret_cast<uintptr_t>(Asc) & 3u) == 0)
+    return launch_shape_scales<kBM, kBN, kWM, kWN, kNSDword, kARowDword>(Aq, Asc, M, off, E, Wp,
+                                                                         Wps, N, K_aug, Y, stream);
+  return launch_shape_scales<kBM, kBN, kWM, kWN, kNSByte, kARowByte>(Aq, Asc, M, off, E, Wp, Wps,
+                                                                     N, K_aug, Y, stream);
+}
+
+hipError_t launch_any_shape(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off,
+                            int E, const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug,
+                            float* Y, int shape, bool packed, hipStream_t stream) {
+  switch (shape) {
+    case 0: return launch_shape<256, 256, 2, 2, 4, 3>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, stream);
+    case 1: return launch_shape<256, 128, 2, 2, 4, 4>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, stream);
+    default: return launch_shape<128, 128, 2, 2, 4, 4>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, stream);
+  }
 }
 
 }  // namespace
 
-int choose_tile_shape(int M_rows, int N, int num_cus) {
+int choose_tile_shape(int M_rows, int N, int num_cus, bool packed) {
   // Estimated cost ~ rounds of workgroups over the CUs x per-tile time; the
   // per-shape factors are measured throughputs per tile area relative to
-  // 256 x 256 (smaller tiles move more bytes per MFMA).
-  struct Shape { int id, bm, bn; double eff; };
-  const Shape shapes[] = {{0, 256, 256, 1.0}, {1, 256, 128, 0.6}, {2, 128, 128, 0.55}};
+  // 256 x 256 (smaller tiles move more bytes per MFMA; row-major activations
+  // cost the smaller tiles more).
+  struct Shape { int id, bm, bn; double eff_rows, eff_packed; };
+  const Shape shapes[] = {{0, 256, 256, 1.0, 1.0}, {1, 256, 128, 0.63, 0.83},
+                          {2, 128, 128, 0.5, 0.67}};
   int best = 2;
   double best_cost = 1e300;
   for (const Shape& s : shapes) {
     const int tiles = ((M_rows + s.bm - 1) / s.bm) * ((N + s.bn - 1) / s.bn);
     const int rounds = (tiles + num_cus - 1) / num_cus;
-    const double cost = rounds * static_cast<double>(s.bm) * s.bn / s.eff;
+    const double cost =
+        rounds * static_cast<double>(s.bm) * s.bn / (packed ? s.eff_packed : s.eff_rows);
     if (cost < best_cost) {
       best_cost = cost;
       best = s.id;
@@ -374,11 +516,13 @@ hipError_t launch_gemm_tile(const uint8_t* Aq, const uint8_t* Asc, int M,
                             const int32_t* group_offsets, int E, const uint8_t* Wp,
                             const uint8_t* Wps, int N, int K_aug, float* Y, int shape,
                             hipStream_t stream) {
-  switch (shape) {
-    case 0: return launch_shape<256, 256, 2, 4, 3>(Aq, Asc, M, group_offsets, E, Wp, Wps, N, K_aug, Y, stream);
-    case 1: return launch_shape<256, 128, 2, 2, 4>(Aq, Asc, M, group_offsets, E, Wp, Wps, N, K_aug, Y, stream);
-    default: return launch_shape<128, 128, 2, 2, 6>(Aq, Asc, M, group_offsets, E, Wp, Wps, N, K_aug, Y, stream);
-  }
+  return launch_any_shape(Aq, Asc, M, group_offsets, E, Wp, Wps, N, K_aug, Y, shape, false, stream);
+}
+
+hipError_t launch_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M,
+                                   const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug,
+                                   float* Y, int shape, hipStream_t stream) {
+  return launch_any_shape(Ap, Aps, M, nullptr, 1, Wp, Wps, N, K_aug, Y, shape, true, stream);
 }
 
 }  // namespace prq

@@ -88,6 +88,22 @@ __device__ __forceinline__ v16f mfma_fp4_32x32x64(const uint4& a, const uint4& b
                                                          static_cast<int>(sb));
 }
 
+// The same instruction with the scale bytes taken from byte kSelA of sa and
+// byte kSelB of sb (the instruction's scale byte selects), so one register
+// can carry the scales of several blocks.
+template <int kSelA, int kSelB>
+__device__ __forceinline__ v16f mfma_fp4_32x32x64_sel(const uint4& a, const uint4& b, uint32_t sa,
+                                                      uint32_t sb, v16f c) {
+  static_assert(kSelA >= 0 && kSelA < 4 && kSelB >= 0 && kSelB < 4, "byte select");
+  v8i av = {static_cast<int>(a.x), static_cast<int>(a.y), static_cast<int>(a.z),
+            static_cast<int>(a.w), 0, 0, 0, 0};
+  v8i bv = {static_cast<int>(b.x), static_cast<int>(b.y), static_cast<int>(b.z),
+            static_cast<int>(b.w), 0, 0, 0, 0};
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bv, c, 4, 4, kSelA,
+                                                         static_cast<int>(sa), kSelB,
+                                                         static_cast<int>(sb));
+}
+
 // Group g with off[g] <= row < off[g+1] for non-decreasing offsets
 // (empty groups are skipped): the largest g in [0, G) with off[g] <= row.
 __device__ __forceinline__ int find_group(const int32_t* __restrict__ off, int G, int row) {

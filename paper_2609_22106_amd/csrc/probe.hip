@@ -288,6 +288,16 @@ int prq_tune_gemm_tile(const uint8_t* Aq, const uint8_t* Asc, int M, const int32
              : -3;
 }
 
+// Tuning entry: the tile GEMM on a packed activation with an explicit tile shape.
+int prq_tune_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M, const uint8_t* Wp,
+                              const uint8_t* Wps, int N, int K_aug, float* Y, int shape,
+                              hipStream_t stream) {
+  if (shape < 0 || shape > 2 || N % 16 || K_aug % 32 || M <= 0) return -1;
+  return prq::launch_gemm_tile_packed(Ap, Aps, M, Wp, Wps, N, K_aug, Y, shape, stream) == hipSuccess
+             ? 0
+             : -3;
+}
+
 // g16: 1024 bytes, g1: 64 bytes, out: 8192 bytes (device).
 int prq_probe_lds_dma(const uint8_t* g16, const uint8_t* g1, uint8_t* out, hipStream_t stream) {
   lds_dma_probe<<<1, 64, 0, stream>>>(g16, g1, out);

@@ -44,6 +44,13 @@ hipError_t launch_act_quant_kernel(const uint16_t* X, int64_t ld_x, int M, int K
                                    const int32_t* group_offsets, int G, uint8_t* Aq, uint8_t* Asc,
                                    int num_cus, int kernel, hipStream_t stream);
 
+// The same with the output in the packed (weight) layout: Ap [ceil(M/16)][S][64][16],
+// Aps [ceil(M/16)][ceil(S/4)][64] uint32, rows past M and K parts past K_aug padded
+// (zero codes, scale byte 127).  Dense only.
+hipError_t launch_act_quant_packed(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail,
+                                   const float* inv_scale_pos, const int32_t* perm, uint8_t* Ap,
+                                   uint8_t* Aps, int num_cus, hipStream_t stream);
+
 // pack.hip: the packed weight layout the GEMM kernels read.
 size_t packed_code_bytes(int N, int K_aug, int E);
 size_t packed_scale_bytes(int N, int K_aug, int E);
@@ -52,12 +59,16 @@ hipError_t launch_pack_weight(const uint8_t* Wq, const uint8_t* Wsc, int N, int 
 
 // gemm_tile.hip / gemm_stream.hip (packed weights Wp/Wps).  group_offsets ==
 // nullptr means one group of M rows.
-// Tile shapes: 0 = 256x256 (8 waves), 1 = 256x128 (4 waves), 2 = 128x128 (4 waves).
-int choose_tile_shape(int M_rows, int N, int num_cus);
+// Tile shapes (4 waves each): 0 = 256x256, 1 = 256x128, 2 = 128x128.
+int choose_tile_shape(int M_rows, int N, int num_cus, bool packed);
 hipError_t launch_gemm_tile(const uint8_t* Aq, const uint8_t* Asc, int M,
                             const int32_t* group_offsets, int E, const uint8_t* Wp,
                             const uint8_t* Wps, int N, int K_aug, float* Y, int shape,
                             hipStream_t stream);
+// The tile GEMM with the activation in the packed layout (dense).
+hipError_t launch_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M,
+                                   const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug,
+                                   float* Y, int shape, hipStream_t stream);
 hipError_t launch_gemm_stream(const uint8_t* Aq, const uint8_t* Asc, int M,
                               const int32_t* group_offsets, int E, const uint8_t* Wp,
                               const uint8_t* Wps, int N, int K_aug, float* Y,

@@ -63,6 +63,11 @@ _gemm_ws_ex = _decl("prq_gemm_workspace_bytes_ex", _sz, [_i32, _i32, _i32, _i32,
 _gemm = _decl("prq_gemm", ctypes.c_int, [_p, _p, _i32, _p, _p, _i32, _i32, _p, _p, _sz, _p])
 _gemm_ex = _decl("prq_gemm_ex", ctypes.c_int,
                  [_p, _p, _i32, _p, _p, _i32, _i32, _p, _p, _sz, _i32, _i32, _p])
+_packed_act_bytes = _decl("prq_packed_act_bytes", ctypes.c_int,
+                          [_i32, _i32, ctypes.POINTER(_sz), ctypes.POINTER(_sz)])
+_quant_act_packed = _decl("prq_quant_act_packed", ctypes.c_int,
+                          [_p, _i64, _i32, _i32, _i32, _p, _p, _p, _p, _p])
+_gemm_packed = _decl("prq_gemm_packed", ctypes.c_int, [_p, _p, _i32, _p, _p, _i32, _i32, _p, _p])
 _ggemm_ws = _decl("prq_grouped_gemm_workspace_bytes", _sz, [_i32, _i32, _i32, _i32])
 _ggemm = _decl("prq_grouped_gemm", ctypes.c_int,
                [_p, _p, _p, _i32, _i32, _p, _p, _i32, _i32, _p, _p, _sz, _p])
@@ -327,6 +332,72 @@ def prq_gemm(Aq, Asc, W, Y=None, workspace=None, variant=GEMM_AUTO, splits=0, st
     st = _gemm_ex(_ptr(Aq), _ptr(Asc), M, _ptr(W.Wp), _ptr(W.Wps), N, K_aug, _ptr(Y),
                   _ptr(workspace), ws_bytes, variant, splits, _stream(stream))
     _check(st, "prq_gemm")
+    return Y
+
+
+class PackedAct:
+    """Device buffers of an activation in the packed layout (include/prq.h)."""
+
+    def __init__(self, Ap, Aps, M, K_aug):
+        self.Ap, self.Aps, self.M, self.K_aug = Ap, Aps, M, K_aug
+
+    def check_sizes(self):
+        cb, sb = prq_packed_act_bytes(self.M, self.K_aug)
+        _need(self.Ap, "A.Ap", torch.uint8, min_numel=cb)
+        _need(self.Aps, "A.Aps", torch.uint8, min_numel=sb)
+
+
+def prq_packed_act_bytes(M, K_aug):
+    cb, sb = _sz(0), _sz(0)
+    _check(_packed_act_bytes(M, K_aug, ctypes.byref(cb), ctypes.byref(sb)), "prq_packed_act_bytes")
+    return int(cb.value), int(sb.value)
+
+
+def prq_quant_act_packed(X, K, k_tail, inv_scale_pos=None, perm=None, out=None, stream=None):
+    """prq_quant_act (dense) into the packed activation layout -> PackedAct.
+    out: a PackedAct of the same M and K_aug to write into (else allocated)."""
+    if not isinstance(X, torch.Tensor) or X.dim() != 2 or X.dtype not in _BF16_LIKE:
+        raise ValueError("X must be a 2-D tensor of bf16 values (or their int16 bit patterns)")
+    M = X.shape[0]
+    K_aug = K + k_tail
+    if X.shape[1] < K or (M > 1 and X.stride(0) < K) or X.stride(1) != 1:
+        raise ValueError(f"X rows must hold K={K} contiguous values (shape {tuple(X.shape)}, "
+                         f"strides {X.stride()})")
+    if out is None:
+        cb, sb = prq_packed_act_bytes(M, K_aug)
+        out = PackedAct(torch.empty(cb, dtype=torch.uint8, device=X.device),
+                        torch.empty(sb, dtype=torch.uint8, device=X.device), M, K_aug)
+    if out.M != M or out.K_aug != K_aug:
+        raise ValueError(f"out holds {out.M} rows of K_aug {out.K_aug}, expected {M} x {K_aug}")
+    out.check_sizes()
+    if inv_scale_pos is not None:
+        _need(inv_scale_pos, "inv_scale_pos", torch.float32, min_numel=K)
+    if perm is not None:
+        _need(perm, "perm", torch.int32, min_numel=K)
+    _on_gpu(X=X, Ap=out.Ap, Aps=out.Aps, inv_scale_pos=inv_scale_pos, perm=perm)
+    ld = X.stride(0) if M > 1 else K
+    st = _quant_act_packed(_ptr(X), ld, M, K, k_tail, _ptr(inv_scale_pos), _ptr(perm),
+                           _ptr(out.Ap), _ptr(out.Aps), _stream(stream))
+    _check(st, "prq_quant_act_packed")
+    return out
+
+
+def prq_gemm_packed(A, W, Y=None, stream=None):
+    """Y [M, N] float32 = Eq. 3 over K_aug for a PackedAct A and a PackedWeight W (E = 1)."""
+    if W.E != 1:
+        raise ValueError("prq_gemm_packed takes a single weight (E = 1)")
+    if A.K_aug != W.K_aug:
+        raise ValueError(f"K_aug differs: activation {A.K_aug}, weight {W.K_aug}")
+    M, N = A.M, W.N
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float32, device=W.Wp.device)
+    _need(Y, "Y", torch.float32, (M, N))
+    A.check_sizes()
+    W.check_sizes()
+    _on_gpu(Ap=A.Ap, Aps=A.Aps, Y=Y, Wp=W.Wp, Wps=W.Wps)
+    st = _gemm_packed(_ptr(A.Ap), _ptr(A.Aps), M, _ptr(W.Wp), _ptr(W.Wps), N, W.K_aug, _ptr(Y),
+                      _stream(stream))
+    _check(st, "prq_gemm_packed")
     return Y
 
 

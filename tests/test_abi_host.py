@@ -156,6 +156,49 @@ def test_device_calls_validate_before_touching_the_gpu():
     assert prq._ggemm(None, None, fake, 4, 0, fake, fake, 32, 1088, None, None, 0, s) == prq.PRQ_OK
 
 
+def test_packed_activation_calls_validate_before_touching_the_gpu():
+    fake = ctypes.c_void_p(4096)   # 16-byte aligned, never dereferenced
+    odd = ctypes.c_void_p(4100)    # 4-byte aligned only
+    s = ctypes.c_void_p(0)
+    assert prq._quant_act_packed(fake, 1024, 4, 1000, 64, None, None, fake, fake, s) == prq.PRQ_EALIGN
+    assert prq._quant_act_packed(fake, 1024, 4, 1024, 2048, None, None, fake, fake, s) == prq.PRQ_EALIGN
+    assert prq._quant_act_packed(fake, 1024, 4, 1024, 64, None, None, fake, odd, s) == prq.PRQ_EALIGN
+    assert prq._quant_act_packed(fake, 1024, 4, 1024, 64, None, None, None, fake, s) == prq.PRQ_EINVAL
+    assert prq._quant_act_packed(fake, 1000, 4, 1024, 64, None, None, fake, fake, s) == prq.PRQ_EINVAL
+    assert prq._quant_act_packed(None, 1024, 0, 1024, 64, None, None, None, None, s) == prq.PRQ_OK
+    assert prq._gemm_packed(fake, fake, 4, fake, fake, 24, 1088, fake, s) == prq.PRQ_EALIGN   # N % 16
+    assert prq._gemm_packed(fake, odd, 4, fake, fake, 32, 1088, fake, s) == prq.PRQ_EALIGN    # Aps
+    assert prq._gemm_packed(fake, fake, 4, fake, odd, 32, 1088, fake, s) == prq.PRQ_EALIGN    # Wps
+    assert prq._gemm_packed(None, None, 0, fake, fake, 32, 1088, None, s) == prq.PRQ_OK
+
+
+def test_packed_activation_sizes():
+    """Row blocks of 16 rows, K steps of 128, scale groups of four steps."""
+    assert prq.prq_packed_act_bytes(1, 32) == (1024, 256)
+    assert prq.prq_packed_act_bytes(16, 128) == (1024, 256)
+    assert prq.prq_packed_act_bytes(17, 129 * 32) == (2 * 33 * 1024, 2 * 9 * 256)
+    assert prq.prq_packed_act_bytes(8192, 9984) == (512 * 78 * 1024, 512 * 20 * 256)
+    assert prq.prq_packed_act_bytes(0, 9984) == (0, 0)
+    with pytest.raises(prq.PRQError):
+        prq.prq_packed_act_bytes(4, 1000)
+
+
+def test_reference_packer_is_a_padded_permutation():
+    """The tests' layout reference moves every code and scale byte exactly
+    once and fills the rest with zero codes and scale byte 127."""
+    from tests.packing import pack_rows
+    rng = np.random.default_rng(3)
+    for R, K_aug in ((1, 32), (17, 96), (33, 1088), (16, 512)):
+        q = rng.integers(1, 256, (R, K_aug // 2), dtype=np.uint8)
+        sc = rng.integers(0, 127, (R, K_aug // 32), dtype=np.uint8)
+        P, Ps = pack_rows(q, sc)
+        cb, sb = prq.prq_packed_act_bytes(R, K_aug)
+        assert (P.size, Ps.size) == (cb, sb)
+        assert np.sort(P[P != 0]).tolist() == np.sort(q.ravel()).tolist()
+        assert np.sort(Ps[Ps != 127]).tolist() == np.sort(sc.ravel()).tolist()
+        assert np.count_nonzero(Ps == 127) == sb - sc.size
+
+
 def test_workspace_sizes():
     assert prq.prq_gemm_workspace_bytes(64, 2560, 9984, prq.GEMM_TILE) == 0
     assert prq.prq_gemm_workspace_bytes(64, 2560, 9984, prq.GEMM_STREAM, 1) == 0

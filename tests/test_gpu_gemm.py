@@ -10,6 +10,7 @@ torch = pytest.importorskip("torch")
 from oracle import prquant as pq                               # noqa: E402
 from paper_2609_22106_amd import inputs                        # noqa: E402
 from tests.gpu_util import assert_gemm_close, dev, host, say   # noqa: E402
+from tests.packing import pack_rows                            # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
@@ -288,25 +289,7 @@ def test_grouped_end_to_end_prepared_experts():
 # ------------------------------------------------------------- packing ---
 def _pack_reference(Wq, Wsc):
     """The packed layout written out from its definition in include/prq.h."""
-    E, N, Kh = Wq.shape
-    K_aug = 2 * Kh
-    S = -(-K_aug // 128)
-    Q = -(-S // 4)
-    nb = K_aug // 32
-    Wp = np.zeros((E, N // 16, S, 64, 16), np.uint8)
-    Wps = np.zeros((E, N // 16, Q, 64, 4), np.uint8)
-    for t in range(N // 16):
-        for l in range(64):
-            row = 16 * t + l % 16
-            for s in range(S):
-                k0 = (128 * s + 32 * (l // 16)) // 2
-                if k0 < Kh:
-                    Wp[:, t, s, l] = Wq[:, row, k0:k0 + 16]
-            for q in range(Q):
-                for j in range(4):
-                    b = 4 * (4 * q + j) + l // 16
-                    Wps[:, t, q, l, j] = Wsc[:, row, b] if b < nb else 127
-    return Wp.ravel(), Wps.ravel()
+    return pack_rows(Wq, Wsc)
 
 
 @pytest.mark.parametrize("E,N,K_aug", [(1, 16, 32), (1, 48, 1088), (3, 32, 832), (2, 64, 544)])

@@ -1,0 +1,122 @@
+"""The packed prefill pair: prq_quant_act_packed against the oracle's
+quantizer (Algorithm 1, step 11; online copy) laid out by the reference packer
+-- every code and scale byte, padding included -- and prq_gemm_packed (Eq. 3
+over K + k) against the oracle's float64 GEMM, max |dY| <= 1e-3 max |Y|, for
+every tile shape; then the two end to end on the down_proj shape."""
+import ctypes
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import prquant as pq                               # noqa: E402
+from paper_2609_22106_amd import inputs                        # noqa: E402
+from tests.gpu_util import assert_gemm_close, dev, host, say   # noqa: E402
+from tests.packing import pack_rows                            # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+def _prq():
+    from paper_2609_22106_amd import prq
+    return prq
+
+
+def _pos(inv, perm):
+    return inv if perm is None else np.asarray(inv)[np.asarray(perm)]
+
+
+QUANT = [(1, 1024, 64), (15, 1024, 64), (16, 1024, 0), (17, 96, 32), (300, 2560, 64),
+         (33, 9728, 256), (257, 1088, 0)]
+
+
+@pytest.mark.parametrize("M,K,k", QUANT)
+@pytest.mark.parametrize("scaled", [True, False])
+def test_quant_act_packed_bytes(M, K, k, scaled):
+    prq = _prq()
+    rng = np.random.default_rng(M * 13 + K + k + scaled)
+    X = inputs.f32_to_bf16_bits((rng.standard_normal((M, K)) *
+                                 rng.uniform(0.01, 30.0, K)).astype(np.float32))
+    inv = rng.uniform(0.25, 4.0, K).astype(np.float32) if scaled else None
+    perm = rng.permutation(K).astype(np.int32) if scaled else None
+    say("packed quant case:", M, K, k, scaled)
+    A = prq.prq_quant_act_packed(dev(X), K, k, None if inv is None else dev(_pos(inv, perm)),
+                                 None if perm is None else dev(perm))
+    torch.cuda.synchronize()
+    rq, rs = pq.quant_act(X, inv, perm, k)
+    ep, es = pack_rows(rq, rs)
+    np.testing.assert_array_equal(host(A.Aps), es, err_msg="packed scales")
+    np.testing.assert_array_equal(host(A.Ap), ep, err_msg="packed codes")
+
+
+def test_quant_act_packed_overwrites_stale_padding():
+    """Padding bytes are written, not left from a previous use of the buffers."""
+    prq = _prq()
+    rng = np.random.default_rng(5)
+    M, K, k = 21, 1088, 32
+    X = inputs.f32_to_bf16_bits(rng.standard_normal((M, K)).astype(np.float32))
+    cb, sb = prq.prq_packed_act_bytes(M, K + k)
+    out = prq.PackedAct(torch.full((cb,), 0xAB, dtype=torch.uint8, device="cuda"),
+                        torch.full((sb,), 0xCD, dtype=torch.uint8, device="cuda"), M, K + k)
+    prq.prq_quant_act_packed(dev(X), K, k, out=out)
+    torch.cuda.synchronize()
+    ep, es = pack_rows(*pq.quant_act(X, None, None, k))
+    np.testing.assert_array_equal(host(out.Aps), es)
+    np.testing.assert_array_equal(host(out.Ap), ep)
+
+
+def _tune_packed(shape, A, W, Y):
+    from paper_2609_22106_amd import build
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    P, I = ctypes.c_void_p, ctypes.c_int
+    lib.prq_tune_gemm_tile_packed.argtypes = [P, P, I, P, P, I, I, P, I, P]
+    lib.prq_tune_gemm_tile_packed.restype = I
+    return lib.prq_tune_gemm_tile_packed(A.Ap.data_ptr(), A.Aps.data_ptr(), A.M, W.Wp.data_ptr(),
+                                         W.Wps.data_ptr(), W.N, W.K_aug, Y.data_ptr(), shape,
+                                         torch.cuda.current_stream().cuda_stream)
+
+
+GEMM = [(300, 384, 1024), (513, 272, 1152), (40, 512, 9984), (257, 272, 1088), (130, 144, 4192),
+        (17, 48, 96), (64, 256, 256), (1, 16, 32)]
+
+
+@pytest.mark.parametrize("M,N,K_aug", GEMM)
+@pytest.mark.parametrize("shape", [None, 0, 1, 2])
+def test_gemm_packed(shape, M, N, K_aug):
+    prq = _prq()
+    rng = np.random.default_rng(M * 31 + N + K_aug)
+    Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+    Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
+    ap, aps = pack_rows(Aq, Asc)
+    A = prq.PackedAct(dev(ap), dev(aps), M, K_aug)
+    W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
+    say("packed gemm case:", shape, M, N, K_aug)
+    if shape is None:
+        Y = prq.prq_gemm_packed(A, W)
+    else:
+        Y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        assert _tune_packed(shape, A, W, Y) == 0
+    torch.cuda.synchronize()
+    assert_gemm_close(host(Y), pq.gemm(Aq, Asc, Wq, Wsc), f"packed shape {shape} {M}x{N}x{K_aug}")
+
+
+@pytest.mark.parametrize("M", [512, 2048])
+def test_packed_pair_down_proj(M):
+    """X -> prq_quant_act_packed -> prq_gemm_packed on the down_proj shape
+    (K = 9728, k = 256, N = 2560), against the oracle on 48 sampled rows."""
+    prq = _prq()
+    rng = np.random.default_rng(M)
+    K, k, N = 9728, 256, 2560
+    X = inputs.f32_to_bf16_bits((rng.standard_normal((M, K)) *
+                                 rng.uniform(0.01, 30.0, K)).astype(np.float32))
+    inv = rng.uniform(0.25, 4.0, K).astype(np.float32)
+    perm = rng.permutation(K).astype(np.int32)
+    Wq, Wsc = inputs.random_mxfp4(rng, N, K + k)
+    W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
+    say("packed pair case:", M)
+    A = prq.prq_quant_act_packed(dev(X), K, k, dev(_pos(inv, perm)), dev(perm))
+    Y = host(prq.prq_gemm_packed(A, W))
+    rows = np.sort(rng.choice(M, 48, replace=False))
+    rq, rs = pq.quant_act(X[rows], inv, perm, k)
+    assert_gemm_close(Y[rows], pq.gemm(rq, rs, Wq, Wsc), f"packed pair M={M}")
