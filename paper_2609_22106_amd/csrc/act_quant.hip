@@ -114,11 +114,11 @@ __device__ __forceinline__ void quantize_store(const float (&z)[8], int u, int t
   amax = dev::quad_max(amax);
   const uint32_t code = dev::e8m0_code(amax);
   const float mul = dev::e8m0_reciprocal(code);
-  uint32_t w = 0;
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-    w |= (__builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, z[2 * j] * mul, z[2 * j + 1] * mul, 1.0f, 0) &
-          0xFFu) << (8 * j);
+  // four converts, each writing its pair into one byte of the word
+  uint32_t w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, z[0] * mul, z[1] * mul, 1.0f, 0);
+  w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, z[2] * mul, z[3] * mul, 1.0f, 1);
+  w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, z[4] * mul, z[5] * mul, 1.0f, 2);
+  w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, z[6] * mul, z[7] * mul, 1.0f, 3);
   out.word(u, w);
   if ((u & 3) == 0) out.scale(u >> 2, code);
   if (u >= tail_unit0) {  // online copy of the quantized tail and its scales
@@ -323,6 +323,157 @@ __global__ __launch_bounds__(kLdsThreads) void act_quant_lds_kernel(
   }
 }
 
+// Many rows, rows copied by direct global->LDS loads.  A workgroup takes a
+// contiguous range of rows and runs them through kNS LDS stages (one row each).
+// Two copy waves issue the row copies, kNS - 2 rows in flight beyond the one
+// being quantized, with one constant wait per row; eight compute waves hold
+// their units' source channels and inverse scales in registers and quantize the
+// staged row.  Stores count in the same memory counter as loads, so the waves
+// that store the output are not the ones that wait for the copies.  Per row i:
+// the copy waves wait for their copies of row i, every wave passes one bare
+// barrier (the compute waves having finished reading row i-1, whose stage the
+// copy waves then refill with row i+kNS-1), the compute waves quantize row i.
+// The copies are issued as inline assembly: the compiler then sees no
+// direct-to-LDS write that the compute waves' stage reads could alias (it would
+// make them wait for all their outstanding stores); their ordering is the copy
+// waves' explicit wait and the barrier.
+#define PRQ_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
+
+constexpr int kCopyWaves = 2;
+constexpr int kComputeThreads = 512;
+constexpr int kDmaThreads = kComputeThreads + kCopyWaves * 64;
+
+// s_waitcnt: vmcnt(n) with lgkmcnt(0) (n = 63: LDS only).
+template <int n>
+__device__ __forceinline__ void wait_vmcnt_lgkm0() {
+  static_assert(n >= 0 && n < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((n & 0xF) | ((n >> 4) << 14) | (0x7 << 4));
+}
+
+// One direct global->LDS copy of 16 bytes per lane: lane l's 16 bytes at src
+// land at LDS byte lds + 16 l (lds: wave-uniform LDS address, through M0).
+__device__ __forceinline__ void lds_copy16(const void* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(lds)
+               : "memory", "m0");
+}
+
+template <bool kGrouped, bool kPacked, int kStage, int kNS, int kUnits>
+__global__ __launch_bounds__(kDmaThreads) void act_quant_dma_kernel(
+    const uint16_t* __restrict__ X, int64_t ld_x, int M, int K, int k_tail,
+    const float* __restrict__ inv, const int32_t* __restrict__ perm,
+    const int32_t* __restrict__ offsets, int G, int rows_per_wg, uint8_t* __restrict__ Aq,
+    uint8_t* __restrict__ Asc) {
+  static_assert(kNS >= 3 && kNS <= 8, "stages");
+  constexpr int kCpw = kStage / 1024 / kCopyWaves;   // copies per copy wave per row
+  static_assert(kCpw * kCopyWaves * 1024 == kStage, "stage of whole copy rounds");
+  static_assert((kNS - 2) * kCpw < 64, "vmcnt");
+  __shared__ __align__(16) uint8_t stg[kNS * kStage];
+  const int r0 = blockIdx.x * rows_per_wg;
+  const int r1 = min(M, r0 + rows_per_wg);
+  if (r0 >= r1) return;                            // uniform
+  const int n = r1 - r0;
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
+  const bool copier = wave >= kComputeThreads / 64;
+  const int cw = wave - kComputeThreads / 64;      // copy wave index (copiers)
+  const int row_bytes_x = 2 * K;
+  const int chunks = (row_bytes_x + 1023) >> 10;   // <= kStage / 1024 (host check)
+  const int k_aug = K + k_tail;
+  const int64_t row_bytes = k_aug >> 1;
+  const int nb = k_aug >> 5;
+  const int tail_unit0 = (K - k_tail) >> 3;
+  const int steps = (k_aug + 127) >> 7;
+  const int sgroups = (steps + 3) >> 2;
+  const int units = K >> 3;
+  const uint32_t stg_lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(PRQ_LPTR(stg)));
+
+  // Row i of the range into its stage (copy waves; i clamped into the range,
+  // lanes past the row read its start into the stage's pad).
+  auto copy_row = [&](int i) {
+    const uint8_t* src = reinterpret_cast<const uint8_t*>(X + static_cast<int64_t>(r0 + min(i, n - 1)) * ld_x);
+    const uint32_t st = stg_lds + static_cast<uint32_t>(i % kNS) * kStage;
+#pragma unroll
+    for (int j = 0; j < kCpw; ++j) {
+      const int c = min(cw + j * kCopyWaves, chunks - 1);
+      const int off = c * 1024 + lane * 16;
+      lds_copy16(src + (off < row_bytes_x ? off : 0), __builtin_amdgcn_readfirstlane(st + c * 1024));
+    }
+  };
+
+  PackedUnit un[kUnits];
+  int cur_g = -1;
+  // (Re)load the units' permutation entries and inverse scales, then wait for
+  // them right here: later uses then see nothing outstanding.
+  auto load_units = [&](int g) {
+#pragma unroll
+    for (int j = 0; j < kUnits; ++j) {
+      const int u = min(tid + j * kComputeThreads, units - 1);
+      load_packed_unit(perm, inv, g, K, u, &un[j]);
+    }
+    __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));   // vmcnt(0)
+    cur_g = g;
+  };
+  if (!copier) load_units(kGrouped ? dev::find_group(offsets, G, r0) : 0);
+
+  if (copier)
+    for (int i = 0; i < kNS - 1; ++i) copy_row(i);
+  for (int i = 0; i < n; ++i) {
+    if (copier) {
+      wait_vmcnt_lgkm0<(kNS - 2) * kCpw>();         // row i has landed
+      __builtin_amdgcn_s_barrier();
+      copy_row(i + kNS - 1);                        // into the stage of row i-1
+      continue;
+    }
+    wait_vmcnt_lgkm0<63>();                         // this wave's LDS reads of row i-1
+    __builtin_amdgcn_s_barrier();
+    const int r = r0 + i;
+    if (kGrouped) {
+      const int g = dev::find_group(offsets, G, r);
+      if (g != cur_g) load_units(g);
+    }
+    const uint16_t* row = reinterpret_cast<const uint16_t*>(stg + (i % kNS) * kStage);
+    const RowSink rsink{Aq + static_cast<int64_t>(r) * row_bytes, Asc + static_cast<int64_t>(r) * nb};
+    const PackedSink psink(Aq, Asc, r, steps, sgroups);
+    if constexpr (kPacked) pad_row_tail(psink, tid, units, nb, steps, sgroups);
+    // Units below the last always exist (the host picks kUnits = ceil(units /
+    // kComputeThreads)): no guard, so their LDS gathers can all be in flight
+    // together; the last unit is guarded (quad-uniform: units % 4 == 0).
+#pragma unroll
+    for (int j = 0; j < kUnits; ++j) {
+      const int u = tid + j * kComputeThreads;
+      if (j + 1 < kUnits || u < units) {
+        float z[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t sp = un[j].src2[e];
+          z[2 * e] = __uint_as_float(static_cast<uint32_t>(row[sp & 0xFFFFu]) << 16) * un[j].d[2 * e];
+          z[2 * e + 1] = __uint_as_float(static_cast<uint32_t>(row[sp >> 16]) << 16) * un[j].d[2 * e + 1];
+        }
+        if constexpr (kPacked)
+          quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, psink);
+        else
+          quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, rsink);
+      }
+    }
+  }
+  if (copier) __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));   // no copy outlives the workgroup
+
+  // Packed layout: the workgroup with the last row also fills the rows of the
+  // last 16-row block past M (zero codes, scale byte 127).
+  if constexpr (kPacked) {
+    if (r1 == M && !copier) {
+      for (int r = M; r < ((M + 15) & ~15); ++r) {
+        const PackedSink psink(Aq, Asc, r, steps, sgroups);
+        for (int v = tid; v < steps * 16; v += kComputeThreads) psink.word(v, 0u);
+        for (int b = tid; b < sgroups * 16; b += kComputeThreads) psink.scale(b, 127u);
+      }
+    }
+  }
+}
+
 template <bool kGrouped, int kUnits, bool kPacked = false>
 void launch_lds(dim3 grid, size_t lds, hipStream_t stream, const uint16_t* X, int64_t ld_x,
                 int M, int K, int k_tail, const float* inv, const int32_t* perm,
@@ -338,6 +489,31 @@ int lds_rows_per_wg(int M, int units, int num_cus) {
   const int target = std::max(1, num_cus * 2);
   int rows_per_wg = std::max(1, (M + target - 1) / target);
   return (rows_per_wg + rpp - 1) / rpp * rpp;
+}
+
+// Stage classes of the copy kernel by row length (2K bytes): stage bytes, stages,
+// units per compute thread (K/8 units over 512 threads).  At most 128 KiB of LDS.
+static_assert(kComputeThreads == 512, "stage classes assume 512 compute threads");
+template <bool kGrouped, bool kPacked>
+hipError_t launch_dma(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail, const float* inv,
+                      const int32_t* perm, const int32_t* offsets, int G, uint8_t* Aq, uint8_t* Asc,
+                      int num_cus, hipStream_t stream) {
+  const int rb = 2 * K;
+  const int per_cu = rb <= 8192 ? 2 : 1;           // workgroups a CU holds (LDS)
+  const int target = std::max(1, num_cus * per_cu);
+  const int rows_per_wg = std::max(1, (M + target - 1) / target);
+  const dim3 grid((M + rows_per_wg - 1) / rows_per_wg);
+#define PRQ_DMA(STAGE, NS, U)                                                                     \
+  act_quant_dma_kernel<kGrouped, kPacked, STAGE, NS, U><<<grid, kDmaThreads, 0, stream>>>(       \
+      X, ld_x, M, K, k_tail, inv, perm, offsets, G, rows_per_wg, Aq, Asc)
+  // kUnits = ceil(K / 8 / 512) exactly: every unit but the last exists.
+  if (rb <= 4096) PRQ_DMA(4096, 8, 1);
+  else if (rb <= 8192) PRQ_DMA(8192, 8, 1);
+  else if (rb <= 16384) PRQ_DMA(16384, 7, 2);
+  else if (rb <= 24576) PRQ_DMA(24576, 5, 3);
+  else PRQ_DMA(32768, 4, 4);
+#undef PRQ_DMA
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -367,6 +543,16 @@ hipError_t launch_act_quant_kernel(const uint16_t* X, int64_t ld_x, int M, int K
       act_quant_rows_kernel<false><<<grid, kRowsThreads, 0, stream>>>(
           X, ld_x, M, K, k_tail, inv_scale_pos, perm, nullptr, 1, rows_per_wg, Aq, Asc);
     return hipGetLastError();
+  }
+  const int32_t* goff = grouped ? group_offsets : nullptr;
+  // Long rows (K >= 2048): rows copied into LDS stages; shorter rows: several
+  // rows per pass of the register-staged kernel (measured faster at K = 768).
+  if (kernel == 3 || (kernel == 0 && K >= 2048)) {
+    if (grouped)
+      return launch_dma<true, false>(X, ld_x, M, K, k_tail, inv_scale_pos, perm, goff, G, Aq, Asc,
+                                     num_cus, stream);
+    return launch_dma<false, false>(X, ld_x, M, K, k_tail, inv_scale_pos, perm, nullptr, 1, Aq, Asc,
+                                    num_cus, stream);
   }
   // At most 2 * 2048 * 16 bytes = 64 KiB of LDS: within the default limit.
   const size_t lds = lds_kernel_bytes(K);
@@ -398,6 +584,17 @@ hipError_t launch_act_quant_kernel(const uint16_t* X, int64_t ld_x, int M, int K
 hipError_t launch_act_quant_packed(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail,
                                    const float* inv_scale_pos, const int32_t* perm, uint8_t* Ap,
                                    uint8_t* Aps, int num_cus, hipStream_t stream) {
+  return launch_act_quant_packed_kernel(X, ld_x, M, K, k_tail, inv_scale_pos, perm, Ap, Aps,
+                                        num_cus, 0, stream);
+}
+
+hipError_t launch_act_quant_packed_kernel(const uint16_t* X, int64_t ld_x, int M, int K,
+                                          int k_tail, const float* inv_scale_pos,
+                                          const int32_t* perm, uint8_t* Ap, uint8_t* Aps,
+                                          int num_cus, int kernel, hipStream_t stream) {
+  if (kernel == 3 || (kernel == 0 && K >= 2048))
+    return launch_dma<false, true>(X, ld_x, M, K, k_tail, inv_scale_pos, perm, nullptr, 1, Ap, Aps,
+                                   num_cus, stream);
   const int units = K >> 3;
   const size_t lds = lds_kernel_bytes(K);
   const int per_thread = (units + kLdsThreads - 1) / kLdsThreads;

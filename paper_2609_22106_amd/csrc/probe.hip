@@ -54,6 +54,18 @@ __global__ void cvt_pairs(const float* x, const float* y, const float* s, int n,
   if (i < n) out[i] = static_cast<uint8_t>(__builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, x[i], y[i], s[i], 0) & 0xFFu);
 }
 
+// The FP32 -> FP4 pair conversion with each destination byte select: lane l
+// converts (x[l], y[l]) at scale 1 into byte `sel` of old = 0x89ABCDEF for
+// sel = 0..3; out[4 l + sel] is the whole result word.
+__global__ __launch_bounds__(64) void cvt_sel_probe(const float* x, const float* y, uint32_t* out) {
+  const int l = threadIdx.x;
+  const uint32_t old = 0x89ABCDEFu;
+  out[4 * l + 0] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, x[l], y[l], 1.0f, 0);
+  out[4 * l + 1] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, x[l], y[l], 1.0f, 1);
+  out[4 * l + 2] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, x[l], y[l], 1.0f, 2);
+  out[4 * l + 3] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, x[l], y[l], 1.0f, 3);
+}
+
 __global__ void empty_kernel() {}
 
 // MFMA issue rate: every wave runs `iters` rounds of 8 independent
@@ -137,6 +149,12 @@ int prq_probe_mfma16(const void* a, const void* b, const uint32_t* sa, const uin
 // result: device uint32[1 + 2*8], zero-filled by the caller.
 int prq_probe_cvt_sweep(uint32_t* result, hipStream_t stream) {
   cvt_sweep<<<65536, 256, 0, stream>>>(result);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+// x, y: 64 floats each, out: 256 uint32 (device).
+int prq_probe_cvt_sel(const float* x, const float* y, uint32_t* out, hipStream_t stream) {
+  cvt_sel_probe<<<1, 64, 0, stream>>>(x, y, out);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
@@ -238,13 +256,27 @@ int prq_probe_mfma_rate(int blocks, int iters, float* out, hipStream_t stream) {
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
-// Activation quantization with a forced kernel (1 few-rows, 2 many-rows).
+// Activation quantization with a forced kernel (1 few-rows, 2 many-rows with
+// register-staged rows, 3 many-rows with rows copied into LDS stages).
 int prq_tune_act_quant(const void* X, int64_t ld_x, int M, int K, int k_tail, const float* inv,
                        const int32_t* perm, uint8_t* Aq, uint8_t* Asc, int kernel,
                        hipStream_t stream) {
   if (M <= 0 || K <= 0 || K % 32 || k_tail % 32 || k_tail > K || K > 16384 || ld_x < K) return -1;
   return prq::launch_act_quant_kernel(static_cast<const uint16_t*>(X), ld_x, M, K, k_tail, inv, perm,
                                       nullptr, 1, Aq, Asc, 256, kernel, stream) == hipSuccess
+             ? 0
+             : -3;
+}
+
+// The same into the packed activation layout (2 register-staged, 3 LDS stages).
+int prq_tune_act_quant_packed(const void* X, int64_t ld_x, int M, int K, int k_tail,
+                              const float* inv, const int32_t* perm, uint8_t* Ap, uint8_t* Aps,
+                              int kernel, hipStream_t stream) {
+  if (M <= 0 || K <= 0 || K % 32 || k_tail % 32 || k_tail > K || K > 16384 || ld_x < K ||
+      (kernel != 2 && kernel != 3))
+    return -1;
+  return prq::launch_act_quant_packed_kernel(static_cast<const uint16_t*>(X), ld_x, M, K, k_tail,
+                                             inv, perm, Ap, Aps, 256, kernel, stream) == hipSuccess
              ? 0
              : -3;
 }

@@ -38,7 +38,8 @@ hipError_t launch_act_quant(const uint16_t* X, int64_t ld_x, int M, int K, int k
                             const float* inv_scale, const int32_t* perm,
                             const int32_t* group_offsets, int G, uint8_t* Aq, uint8_t* Asc,
                             int num_cus, hipStream_t stream);
-// kernel: 0 = by row count, 1 = the few-rows kernel, 2 = the many-rows kernel.
+// kernel: 0 = by row count, 1 = the few-rows kernel, 2 = the many-rows kernel with
+// register-staged rows, 3 = the many-rows kernel with rows copied into LDS stages.
 hipError_t launch_act_quant_kernel(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail,
                                    const float* inv_scale, const int32_t* perm,
                                    const int32_t* group_offsets, int G, uint8_t* Aq, uint8_t* Asc,
@@ -50,6 +51,11 @@ hipError_t launch_act_quant_kernel(const uint16_t* X, int64_t ld_x, int M, int K
 hipError_t launch_act_quant_packed(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail,
                                    const float* inv_scale_pos, const int32_t* perm, uint8_t* Ap,
                                    uint8_t* Aps, int num_cus, hipStream_t stream);
+// kernel: 0 = automatic, 2 = register-staged rows, 3 = rows copied into LDS stages.
+hipError_t launch_act_quant_packed_kernel(const uint16_t* X, int64_t ld_x, int M, int K,
+                                          int k_tail, const float* inv_scale_pos,
+                                          const int32_t* perm, uint8_t* Ap, uint8_t* Aps,
+                                          int num_cus, int kernel, hipStream_t stream);
 
 // pack.hip: the packed weight layout the GEMM kernels read.
 size_t packed_code_bytes(int N, int K_aug, int E);

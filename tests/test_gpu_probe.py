@@ -157,3 +157,31 @@ def test_direct_global_to_lds_load_layout():
     slots = o[4096:4096 + 256].reshape(64, 4)
     np.testing.assert_array_equal(slots[:, 0], g1)
     assert not slots[:, 1:].any() and not o[4096 + 256:].any()
+
+
+def test_fp4_convert_destination_byte_select():
+    """Byte `sel` of the result holds the pair's codes (x low nibble, y high),
+    the other three bytes of the old value are kept: the quantizers build a
+    word of 8 codes with four converts and no masking."""
+    lib = _probe_lib()
+    lib.prq_probe_cvt_sel.argtypes = [ctypes.c_void_p] * 4
+    rng = np.random.default_rng(4)
+    x = rng.choice(E2M1, 64).astype(np.float32)
+    y = rng.choice(E2M1, 64).astype(np.float32)
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    out = torch.zeros(256, dtype=torch.int32, device="cuda")
+    assert lib.prq_probe_cvt_sel(xd.data_ptr(), yd.data_ptr(), out.data_ptr(),
+                                 torch.cuda.current_stream().cuda_stream) == 0
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().view(np.uint32).reshape(64, 4)
+    code = {float(v): i for i, v in enumerate(E2M1[:8])}
+
+    def c(v):
+        return code[abs(float(v))] | (8 if np.signbit(v) else 0)
+    old = 0x89ABCDEF
+    for l in range(64):
+        pair = c(x[l]) | (c(y[l]) << 4)
+        for sel in range(4):
+            want = (old & ~(0xFF << (8 * sel))) | (pair << (8 * sel))
+            assert int(got[l, sel]) == want, (l, sel, hex(int(got[l, sel])), hex(want))
+
