@@ -215,8 +215,8 @@ int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t*
                                                    workspace, stream));
     }
   }
-  return launch_status(prq::launch_gemm_tile(Aq, Asc, M, nullptr, 1, Wp, Wps, N, K_aug, Y,
-                                             prq::choose_tile_shape(M, N, dev.num_cus, false), stream));
+  return launch_status(prq::launch_gemm_tile_planned(Aq, Asc, M, Wp, Wps, N, K_aug, Y, false,
+                                                     dev.num_cus, stream));
 }
 
 int prq_gemm(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t* Wp,
@@ -265,9 +265,8 @@ int prq_gemm_packed(const uint8_t* Ap, const uint8_t* Aps, int32_t M, const uint
   DeviceInfo dev;
   st = current_device(&dev);
   if (st != PRQ_OK) return st;
-  return launch_status(prq::launch_gemm_tile_packed(Ap, Aps, M, Wp, Wps, N, K_aug, Y,
-                                                    prq::choose_tile_shape(M, N, dev.num_cus, true),
-                                                    stream));
+  return launch_status(prq::launch_gemm_tile_planned(Ap, Aps, M, Wp, Wps, N, K_aug, Y, true,
+                                                     dev.num_cus, stream));
 }
 
 size_t prq_grouped_gemm_workspace_bytes(int32_t M_total, int32_t E, int32_t N, int32_t K_aug) {

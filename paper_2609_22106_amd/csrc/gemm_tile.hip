@@ -158,12 +158,12 @@ struct TileStage {
   static constexpr int kBytes = kOffBs + kBBlk * 256;
 };
 
-constexpr int lcm4(int n) { return n % 4 == 0 ? n : (n % 2 == 0 ? 2 * n : 4 * n); }
 
 template <int kBM, int kBN, int kWM, int kWN, int kNS, bool kGrouped, int kAMode>
 __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
     const uint8_t* __restrict__ Aq, const uint8_t* __restrict__ Asc, int M,
-    const int32_t* __restrict__ off, int E, int n_mtiles, const uint8_t* __restrict__ Wp,
+    const int32_t* __restrict__ off, int E, int n_mtiles, int tile_base, int region_tiles,
+    const uint8_t* __restrict__ Wp,
     const uint8_t* __restrict__ Wps, int N, int K_aug, float* __restrict__ Y) {
   using L = TileStage<kBM, kBN, kAMode>;
   constexpr bool kScaleDword = kAMode == kARowDword;
@@ -189,7 +189,7 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   constexpr int kLoads = kAPer + kBPer + kAsPer + kBsPer;   // direct-to-LDS loads per wave per step
   static_assert(kNS >= 2 && kNS <= 4, "stages");
   static_assert(kNS * L::kBytes + (kGrouped ? kThreads * 4 + 16 : 0) <= 160 * 1024, "LDS");
-  constexpr int kU = lcm4(kNS);   // main-loop unroll: stage index and step mod 4 both known
+  constexpr int kU = kNS;         // main-loop unroll: the stage index is known
   constexpr int kMfmas = 2 * kFM * kFN;                                  // per step
   constexpr int kReads = 4 * (kFM + kFN);                                // LDS reads per step
   // One LDS object per stage: the compiler then knows which stage an in-flight
@@ -208,7 +208,7 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   };
 
   const int ntiles = N >> 4;
-  const int n_ntiles = (N + kBN - 1) / kBN;
+  const int n_ntiles = (region_tiles + kBBlk - 1) / kBBlk;   // column tiles of the region
   const int total = n_mtiles * n_ntiles;
   const int logical = xcd_remap(blockIdx.x, total);
   const int mt = logical / n_ntiles, nt = logical % n_ntiles;
@@ -220,7 +220,8 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
     row_begin = mt * kBM;
     row_end = min(M, row_begin + kBM);
   }
-  const int t0 = nt * kBBlk;                         // first 16-feature tile
+  const int t0 = tile_base + nt * kBBlk;             // first 16-feature tile
+  const int n_end = min(N, (tile_base + region_tiles) * 16);   // the region's columns
   const int64_t row_bytes = K_aug >> 1;
   const int nb = K_aug >> 5;
   const int steps = (K_aug + kStepK - 1) / kStepK;
@@ -356,16 +357,22 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
       o.sb[j] = *reinterpret_cast<const uint32_t*>(st + bs_lb + (2 * j * 256 + h * 128));
     }
   };
-  // The MFMAs of half h of a step; kQ = step mod 4 picks the B scale byte.
-  auto mfma = [&](const Half& o, auto hc, auto qc) {
-    constexpr int h = decltype(hc)::value, kQ = decltype(qc)::value;
+  // The MFMAs of half h of step s.  Packed scale dwords hold four K steps:
+  // byte s mod 4 is shifted down to byte 0 (one shift per fragment and step;
+  // a compile-time byte select would force a 4-step unroll).
+  auto mfma = [&](const Half& o, auto hc, int s) {
+    constexpr int h = decltype(hc)::value;
+    const uint32_t qshift = 8u * static_cast<uint32_t>(s & 3);
+    uint32_t sb[kFN];
+#pragma unroll
+    for (int j = 0; j < kFN; ++j) sb[j] = o.sb[j] >> qshift;
 #pragma unroll
     for (int i = 0; i < kFM; ++i) {
-      const uint32_t sa = kScaleDword ? (o.sa[i] >> a_shift) : o.sa[i];
+      const uint32_t sa = kScaleDword ? (o.sa[i] >> a_shift) : (kPackedA ? (o.sa[i] >> qshift) : o.sa[i]);
 #pragma unroll
       for (int j = 0; j < kFN; ++j)
-        acc[i][j] = dev::mfma_fp4_32x32x64_sel<kScaleDword ? 2 * h : (kPackedA ? kQ : 0), kQ>(
-            o.a[i], o.b[j], sa, o.sb[j], acc[i][j]);
+        acc[i][j] = dev::mfma_fp4_32x32x64_sel<kScaleDword ? 2 * h : 0, 0>(o.a[i], o.b[j], sa,
+                                                                          sb[j], acc[i][j]);
     }
   };
 
@@ -396,7 +403,7 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
     const int s = s0 + p;
     const bool live = !kGuard || s < steps;
     __builtin_amdgcn_sched_barrier(0);
-    if (live) mfma(h0, IntC<0>{}, IntC<p % 4>{});
+    if (live) mfma(h0, IntC<0>{}, s);
     read(stage(pc), IntC<1>{}, h1);
     if constexpr (!kGuard) interleave<kMfmas / 2, 0, kReads / 2>();
     __builtin_amdgcn_sched_barrier(0);
@@ -404,7 +411,7 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     issue(min(s + kNS, steps - 1), stage(pc));
-    if (live) mfma(h1, IntC<1>{}, IntC<p % 4>{});
+    if (live) mfma(h1, IntC<1>{}, s);
     read(stage(IntC<p + 1>{}), IntC<0>{}, h0);
     if constexpr (!kGuard) interleave<kMfmas / 2, kLoads, kReads / 2>();
     __builtin_amdgcn_sched_barrier(0);
@@ -427,7 +434,7 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const int m = row_begin + wm * kTM + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
-        if (m < row_end && n < N) Y[static_cast<int64_t>(m) * N + n] = acc[i][j][q];
+        if (m < row_end && n < n_end) Y[static_cast<int64_t>(m) * N + n] = acc[i][j][q];
       }
     }
 }
@@ -435,27 +442,26 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
 template <int kBM, int kBN, int kWM, int kWN, int kNS, int kAMode>
 hipError_t launch_shape_scales(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off,
                                int E, const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug,
-                               float* Y, hipStream_t stream) {
+                               float* Y, int tile_base, int region_tiles, hipStream_t stream) {
   // The kernel addresses A and one expert's weight with 32-bit byte offsets.
   const int64_t steps = (K_aug + kStepK - 1) / kStepK;
   if (static_cast<int64_t>((M + 15) / 16) * steps * 1024 >= (int64_t{1} << 31) ||
       static_cast<int64_t>(N / 16) * steps * 1024 >= (int64_t{1} << 31))
     return hipErrorInvalidValue;
-  const int n_ntiles = (N + kBN - 1) / kBN;
+  if (region_tiles <= 0) return hipSuccess;
+  const int n_ntiles = (region_tiles + kBN / 16 - 1) / (kBN / 16);
   // Grouped: an upper bound on the row tiles over all experts (extra ids exit).
   const int n_mtiles = off ? (M + kBM - 1) / kBM + E : (M + kBM - 1) / kBM;
   const int grid = n_mtiles * n_ntiles;
   if constexpr (kAMode == kAPacked) {
-    gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, false, kAMode>
-        <<<grid, kWM * kWN * 64, 0, stream>>>(Aq, Asc, M, nullptr, 1, n_mtiles, Wp, Wps, N, K_aug,
-                                              Y);
+    gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, false, kAMode><<<grid, kWM * kWN * 64, 0, stream>>>(
+        Aq, Asc, M, nullptr, 1, n_mtiles, tile_base, region_tiles, Wp, Wps, N, K_aug, Y);
   } else if (off) {
-    gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, true, kAMode>
-        <<<grid, kWM * kWN * 64, 0, stream>>>(Aq, Asc, M, off, E, n_mtiles, Wp, Wps, N, K_aug, Y);
+    gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, true, kAMode><<<grid, kWM * kWN * 64, 0, stream>>>(
+        Aq, Asc, M, off, E, n_mtiles, tile_base, region_tiles, Wp, Wps, N, K_aug, Y);
   } else {
-    gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, false, kAMode>
-        <<<grid, kWM * kWN * 64, 0, stream>>>(Aq, Asc, M, nullptr, 1, n_mtiles, Wp, Wps, N, K_aug,
-                                              Y);
+    gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, false, kAMode><<<grid, kWM * kWN * 64, 0, stream>>>(
+        Aq, Asc, M, nullptr, 1, n_mtiles, tile_base, region_tiles, Wp, Wps, N, K_aug, Y);
   }
   return hipGetLastError();
 }
@@ -466,46 +472,111 @@ hipError_t launch_shape_scales(const uint8_t* Aq, const uint8_t* Asc, int M, con
 template <int kBM, int kBN, int kWM, int kWN, int kNSDword, int kNSByte>
 hipError_t launch_shape(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off, int E,
                         const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug, float* Y,
-                        bool packed, hipStream_t stream) {
+                        bool packed, int tile_base, int region_tiles, hipStream_t stream) {
   if (packed)
-    return launch_shape_scales<kBM, kBN, kWM, kWN, kNSDword, kAPacked>(Aq, Asc, M, nullptr, 1, Wp,
-                                                                       Wps, N, K_aug, Y, stream);
+    return launch_shape_scales<kBM, kBN, kWM, kWN, kNSDword, kAPacked>(
+        Aq, Asc, M, nullptr, 1, Wp, Wps, N, K_aug, Y, tile_base, region_tiles, stream);
   if (K_aug % 128 == 0 && (reinterpret_cast<uintptr_t>(Asc) & 3u) == 0)
-    return launch_shape_scales<kBM, kBN, kWM, kWN, kNSDword, kARowDword>(Aq, Asc, M, off, E, Wp,
-                                                                         Wps, N, K_aug, Y, stream);
-  return launch_shape_scales<kBM, kBN, kWM, kWN, kNSByte, kARowByte>(Aq, Asc, M, off, E, Wp, Wps,
-                                                                     N, K_aug, Y, stream);
+    return launch_shape_scales<kBM, kBN, kWM, kWN, kNSDword, kARowDword>(
+        Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, tile_base, region_tiles, stream);
+  return launch_shape_scales<kBM, kBN, kWM, kWN, kNSByte, kARowByte>(
+      Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, tile_base, region_tiles, stream);
 }
 
-hipError_t launch_any_shape(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off,
-                            int E, const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug,
-                            float* Y, int shape, bool packed, hipStream_t stream) {
+// Columns [16 tile_base, 16 (tile_base + region_tiles)) of Y with one tile shape.
+hipError_t launch_region(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off, int E,
+                         const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug, float* Y,
+                         int shape, bool packed, int tile_base, int region_tiles,
+                         hipStream_t stream) {
   switch (shape) {
-    case 0: return launch_shape<256, 256, 2, 2, 4, 3>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, stream);
-    case 1: return launch_shape<256, 128, 2, 2, 4, 4>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, stream);
-    default: return launch_shape<128, 128, 2, 2, 4, 4>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, stream);
+    case 0: return launch_shape<256, 256, 2, 2, 4, 3>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, tile_base, region_tiles, stream);
+    case 1: return launch_shape<256, 128, 2, 2, 4, 4>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, tile_base, region_tiles, stream);
+    default: return launch_shape<128, 128, 2, 2, 4, 4>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, tile_base, region_tiles, stream);
   }
+}
+
+struct Shape {
+  int id, bm, bn;
+  double eff_rows, eff_packed;   // measured throughput per tile area relative to 256 x 256
+};
+constexpr Shape kShapes[] = {{0, 256, 256, 1.0, 1.0}, {1, 256, 128, 0.63, 0.83},
+                             {2, 128, 128, 0.5, 0.67}};
+
+// Plan of a dense tile GEMM: one shape over all N columns, or a main region of
+// whole column tiles in one shape and the remaining columns in another, so
+// that each launch fills the CUs in whole rounds (M = 8192, N = 2560: 256
+// tiles of 256 x 256 over 2048 columns, then 256 tiles of 128 x 128).  Cost =
+// workgroup rounds x tile area / measured throughput factor, plus a fixed cost
+// for a second launch.
+struct TilePlan {
+  int shape[2] = {2, 2};
+  int tiles[2] = {0, 0};   // 16-column tiles of each region
+  int parts = 1;
+};
+
+TilePlan plan_tile_gemm(int M, int N, int K_aug, int num_cus, bool packed) {
+  const int cus = std::max(num_cus, 1);
+  const int ntiles = N / 16;
+  auto cost = [&](const Shape& s, int cols16) {
+    if (cols16 <= 0) return 0.0;
+    const long tiles = static_cast<long>((M + s.bm - 1) / s.bm) * ((cols16 * 16 + s.bn - 1) / s.bn);
+    const long rounds = (tiles + cus - 1) / cus;
+    return rounds * static_cast<double>(s.bm) * s.bn / (packed ? s.eff_packed : s.eff_rows);
+  };
+  // A second launch costs ~3 us; a 256 x 256 tile at K + k = 9984 ~70 us.
+  const double launch_cost = 65536.0 * (3.0 / 70.0) * (9984.0 / std::max(K_aug, 128));
+  TilePlan best;
+  double best_cost = 1e300;
+  for (const Shape& s : kShapes) {
+    const double c = cost(s, ntiles);
+    if (c < best_cost) {
+      best_cost = c;
+      best = TilePlan{};
+      best.shape[0] = s.id;
+      best.tiles[0] = ntiles;
+    }
+  }
+  for (const Shape& a : kShapes)
+    for (int main16 = a.bn / 16; main16 < ntiles; main16 += a.bn / 16)
+      for (const Shape& b : kShapes) {
+        const double c = cost(a, main16) + cost(b, ntiles - main16) + launch_cost;
+        if (c < best_cost) {
+          best_cost = c;
+          best.shape[0] = a.id;
+          best.shape[1] = b.id;
+          best.tiles[0] = main16;
+          best.tiles[1] = ntiles - main16;
+          best.parts = 2;
+        }
+      }
+  return best;
+}
+
+hipError_t launch_plan(const uint8_t* Aq, const uint8_t* Asc, int M, const uint8_t* Wp,
+                       const uint8_t* Wps, int N, int K_aug, float* Y, bool packed,
+                       const TilePlan& plan, hipStream_t stream) {
+  int base = 0;
+  for (int p = 0; p < plan.parts; ++p) {
+    const hipError_t e = launch_region(Aq, Asc, M, nullptr, 1, Wp, Wps, N, K_aug, Y,
+                                       plan.shape[p], packed, base, plan.tiles[p], stream);
+    if (e != hipSuccess) return e;
+    base += plan.tiles[p];
+  }
+  return hipSuccess;
 }
 
 }  // namespace
 
 int choose_tile_shape(int M_rows, int N, int num_cus, bool packed) {
-  // Estimated cost ~ rounds of workgroups over the CUs x per-tile time; the
-  // per-shape factors are measured throughputs per tile area relative to
-  // 256 x 256 (smaller tiles move more bytes per MFMA; row-major activations
-  // cost the smaller tiles more).
-  struct Shape { int id, bm, bn; double eff_rows, eff_packed; };
-  const Shape shapes[] = {{0, 256, 256, 1.0, 1.0}, {1, 256, 128, 0.63, 0.83},
-                          {2, 128, 128, 0.5, 0.67}};
+  // One shape over all columns (grouped calls and the tuning entry).
   int best = 2;
   double best_cost = 1e300;
-  for (const Shape& s : shapes) {
-    const int tiles = ((M_rows + s.bm - 1) / s.bm) * ((N + s.bn - 1) / s.bn);
-    const int rounds = (tiles + num_cus - 1) / num_cus;
-    const double cost =
-        rounds * static_cast<double>(s.bm) * s.bn / (packed ? s.eff_packed : s.eff_rows);
-    if (cost < best_cost) {
-      best_cost = cost;
+  for (const Shape& s : kShapes) {
+    const long tiles = static_cast<long>((M_rows + s.bm - 1) / s.bm) * ((N + s.bn - 1) / s.bn);
+    const long rounds = (tiles + num_cus - 1) / std::max(num_cus, 1);
+    const double c = rounds * static_cast<double>(s.bm) * s.bn / (packed ? s.eff_packed : s.eff_rows);
+    if (c < best_cost) {
+      best_cost = c;
       best = s.id;
     }
   }
@@ -516,13 +587,22 @@ hipError_t launch_gemm_tile(const uint8_t* Aq, const uint8_t* Asc, int M,
                             const int32_t* group_offsets, int E, const uint8_t* Wp,
                             const uint8_t* Wps, int N, int K_aug, float* Y, int shape,
                             hipStream_t stream) {
-  return launch_any_shape(Aq, Asc, M, group_offsets, E, Wp, Wps, N, K_aug, Y, shape, false, stream);
+  return launch_region(Aq, Asc, M, group_offsets, E, Wp, Wps, N, K_aug, Y, shape, false, 0, N / 16,
+                       stream);
 }
 
 hipError_t launch_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M,
                                    const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug,
                                    float* Y, int shape, hipStream_t stream) {
-  return launch_any_shape(Ap, Aps, M, nullptr, 1, Wp, Wps, N, K_aug, Y, shape, true, stream);
+  return launch_region(Ap, Aps, M, nullptr, 1, Wp, Wps, N, K_aug, Y, shape, true, 0, N / 16,
+                       stream);
+}
+
+hipError_t launch_gemm_tile_planned(const uint8_t* Aq, const uint8_t* Asc, int M,
+                                    const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug,
+                                    float* Y, bool packed, int num_cus, hipStream_t stream) {
+  return launch_plan(Aq, Asc, M, Wp, Wps, N, K_aug, Y, packed,
+                     plan_tile_gemm(M, N, K_aug, num_cus, packed), stream);
 }
 
 }  // namespace prq

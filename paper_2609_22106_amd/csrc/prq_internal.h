@@ -71,6 +71,12 @@ hipError_t launch_gemm_tile(const uint8_t* Aq, const uint8_t* Asc, int M,
                             const int32_t* group_offsets, int E, const uint8_t* Wp,
                             const uint8_t* Wps, int N, int K_aug, float* Y, int shape,
                             hipStream_t stream);
+// Dense tile GEMM over all columns with the planned shapes (one launch, or a
+// main column region and the rest in another shape, each filling the CUs in
+// whole rounds).
+hipError_t launch_gemm_tile_planned(const uint8_t* Aq, const uint8_t* Asc, int M,
+                                    const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug,
+                                    float* Y, bool packed, int num_cus, hipStream_t stream);
 // The tile GEMM with the activation in the packed layout (dense).
 hipError_t launch_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M,
                                    const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug,

@@ -101,7 +101,7 @@ def test_gemm_packed(shape, M, N, K_aug):
     assert_gemm_close(host(Y), pq.gemm(Aq, Asc, Wq, Wsc), f"packed shape {shape} {M}x{N}x{K_aug}")
 
 
-@pytest.mark.parametrize("M", [512, 2048])
+@pytest.mark.parametrize("M", [512, 2048, 8192])
 def test_packed_pair_down_proj(M):
     """X -> prq_quant_act_packed -> prq_gemm_packed on the down_proj shape
     (K = 9728, k = 256, N = 2560), against the oracle on 48 sampled rows."""
@@ -120,3 +120,26 @@ def test_packed_pair_down_proj(M):
     rows = np.sort(rng.choice(M, 48, replace=False))
     rq, rs = pq.quant_act(X[rows], inv, perm, k)
     assert_gemm_close(Y[rows], pq.gemm(rq, rs, Wq, Wsc), f"packed pair M={M}")
+
+
+@pytest.mark.parametrize("packed", [True, False])
+def test_planned_column_regions(packed):
+    """A GEMM whose columns the planner splits into two regions of different
+    tile shapes (4096 x 9728 over K + k = 2624: 256 x 256 tiles over the first
+    7680 columns, 256 x 128 over the rest), on 40 sampled rows, every column."""
+    prq = _prq()
+    rng = np.random.default_rng(21 + packed)
+    M, N, K_aug = 4096, 9728, 2624
+    Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+    Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
+    W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
+    say("planned regions case: packed =", packed)
+    if packed:
+        ap, aps = pack_rows(Aq, Asc)
+        Y = prq.prq_gemm_packed(prq.PackedAct(dev(ap), dev(aps), M, K_aug), W)
+    else:
+        Y = prq.prq_gemm(dev(Aq), dev(Asc), W, variant=prq.GEMM_TILE)
+    Y = host(Y)
+    rows = np.unique(np.concatenate([rng.choice(M, 38, replace=False), [0, M - 1]]))
+    assert_gemm_close(Y[rows], pq.gemm(Aq[rows], Asc[rows], Wq, Wsc), f"regions packed={packed}")
+
