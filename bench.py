@@ -33,6 +33,7 @@ import hashlib
 import json
 import math
 import os
+import re
 import sys
 import time
 
@@ -448,13 +449,13 @@ def gemm_source_hash():
 
 
 def traffic_record(workload):
-    """HBM bytes per GEMM launch from committed counter runs, or None when the
+    """HBM bytes per GEMM call from committed counter runs, or None when the
     GEMM sources changed since they were taken."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    return rec.get("bytes_per_launch") if rec.get("gemm_src_sha256_16") == gemm_source_hash() else None
+    return rec.get("bytes_per_call") if rec.get("gemm_src_sha256_16") == gemm_source_hash() else None
 
 
 def _counter_rows(run_dir, counter):
@@ -476,11 +477,29 @@ def _counter_rows(run_dir, counter):
     return list(per.values())
 
 
+# GEMM calls per step of each workload (one per op; a call may be several
+# dispatches, e.g. the two column regions of a planned tile GEMM).
+GEMM_OPS_PER_STEP = {"decode": 4, "prefill": 3, "experts": 1, "experts_prefill": 1, "layers": 7}
+
+
+def _steps_run(command):
+    """Steps a counter run executed: --warmup + --steps + the one step that
+    measures the host enqueue cost (bench.py defaults when absent)."""
+    def opt(name, default):
+        m = re.search(rf"--{name}\s+(\d+)", command)
+        return int(m.group(1)) if m else default
+    return opt("warmup", 10) + opt("steps", 50) + 1
+
+
 def traffic_from_counters(workload, fetch_dir, write_dir, command):
     """Write profiles/traffic_<workload>.json from a FETCH_SIZE run and a
     WRITE_SIZE run of `bench.py --copy-calibration` (KiB per dispatch), each
-    scaled by what the same counter reads for the calibration kernel."""
+    scaled by what the same counter reads for the calibration kernel.  The
+    record is HBM bytes per GEMM call (all of a call's dispatches), the unit of
+    the roofline's algorithmic bytes."""
     out = {"workload": workload, "command": command, "calibration_bytes": CALIB_BYTES}
+    calls = _steps_run(command) * GEMM_OPS_PER_STEP[workload]
+    out["gemm_calls"] = calls
     total = 0.0
     for counter, run_dir in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         rows = _counter_rows(run_dir, counter)
@@ -492,12 +511,12 @@ def traffic_from_counters(workload, fetch_dir, write_dir, command):
         if not calib or not launches:
             raise SystemExit(f"{counter}: calibration or GEMM dispatches missing in {run_dir}")
         scale = CALIB_BYTES / (sorted(calib)[len(calib) // 2] * 1024.0)
-        per_launch = sum(v for _, v in gemm) * 1024.0 * scale / len(launches)
+        per_call = sum(v for _, v in gemm) * 1024.0 * scale / calls
         out[counter] = {"calibration_kib_median": sorted(calib)[len(calib) // 2], "scale": scale,
                         "gemm_dispatches": len(launches), "helper_dispatches": len(gemm) - len(launches),
-                        "bytes_per_launch": per_launch}
-        total += per_launch
-    out["bytes_per_launch"] = round(total, 1)
+                        "bytes_per_call": per_call}
+        total += per_call
+    out["bytes_per_call"] = round(total, 1)
     out["gemm_src_sha256_16"] = gemm_source_hash()
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     with open(path, "w") as f:
