@@ -9,11 +9,15 @@ prq_prepare runs once before timing.  Weights are rotated through enough
 copies (>= 1 GiB) that every step streams them from HBM rather than from the
 256 MB Infinity Cache.
 
-Timed region: `--steps` whole steps launched eagerly but queued behind a GPU
-spin-sleep long enough for the host to enqueue all of them, with HIP events on
-the launch stream around every kernel; the GPU then runs the steps back to
-back, as it does when a serving loop replays them from a graph (the same steps
-replayed from one captured HIP graph are timed too: ``graph_ms_per_step``).
+Timed region: exactly `--steps` whole steps captured into one HIP graph (each
+step binding the next rotated weight copy) and replayed once, bracketed by
+torch.cuda.synchronize() on both sides and HIP events on the stream -- how a
+serving loop launches a step, and free of per-kernel instrumentation.  The
+per-kernel durations (detail, roofline) come from a separate pass of the same
+steps launched eagerly, queued behind a GPU spin-sleep, with fence-free HIP
+events around every kernel; its step time is reported as
+``eager_ms_per_step`` (events add ~2-4 us per kernel).  --no-graph times the
+eager pass instead.
 
 Prints ONE JSON line on stdout (everything else goes to stderr):
   value = algorithmic bytes of one step / step time (GB/s), plus per-M
@@ -294,8 +298,9 @@ def run_steps(torch, ops, steps, warmup, stream):
 
 
 def graph_step_time(torch, ops, steps):
-    """The same steps captured once into a HIP graph and replayed (how a
-    serving loop launches them): seconds per step."""
+    """Exactly `steps` steps captured into one HIP graph and replayed once
+    (after one untimed replay), bracketed by synchronize: (GPU seconds per
+    step from events around the replay, host wall seconds of the replay)."""
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
@@ -313,15 +318,16 @@ def graph_step_time(torch, ops, steps):
             step_once(ops)
     g.replay()
     torch.cuda.synchronize()
-    reps = 2
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
     a.record()
-    for _ in range(reps):
-        g.replay()
+    g.replay()
     b.record()
     torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
     del g
-    return a.elapsed_time(b) * 1e-3 / (reps * per_graph)
+    return a.elapsed_time(b) * 1e-3 / per_graph, wall
 
 
 def copy_context(torch, prq, layers, M_list, reps=50):
@@ -569,11 +575,15 @@ def main(argv=None):
     # untimed warmup, then the timed region: whole steps, with HIP events on
     # the launch stream around every kernel for the per-kernel durations
     t_gpu, queue_info = run_steps(torch, ops, args.steps, args.warmup, stream)
-    t_graph = graph_step_time(torch, ops, args.steps) if not args.no_graph else None
-    ms_per_step = t_gpu / args.steps * 1e3
+    t_eager_step = t_gpu / args.steps
+    if args.no_graph:
+        t_step, t_wall = t_eager_step, None
+    else:
+        t_step, t_wall = graph_step_time(torch, ops, args.steps)
+    ms_per_step = t_step * 1e3
     step_bytes = sum(op.gemm_bytes + op.act_bytes for op in ops)
     step_flops = sum(op.flops for op in ops)
-    value = step_bytes / (t_gpu / args.steps) / 1e9
+    value = step_bytes / t_step / 1e9
 
     detail = {}
     g_bytes = g_time = 0.0
@@ -639,11 +649,17 @@ def main(argv=None):
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "mxfp4", "data": "synthetic", "config": config,
-        "tflops": round(step_flops / (t_gpu / args.steps) / 1e12, 3),
+        "tflops": round(step_flops / t_step / 1e12, 3),
         "roofline": roofline, "cpu_baseline": cpu, "detail": detail,
-        "timing": dict(queue_info, method="eager launches queued behind a GPU spin-sleep; HIP "
-                       "events (hipEventDisableSystemFence) on the launch stream around every kernel"),
-        "graph_ms_per_step": None if t_graph is None else round(t_graph * 1e3, 5),
+        "timing": {
+            "method": ("eager: the steps launched directly" if args.no_graph else
+                       f"{args.steps} steps in one HIP graph, replayed once between "
+                       "torch.cuda.synchronize() calls, HIP events around the replay"),
+            "replay_wall_s": None if t_wall is None else round(t_wall, 6),
+            "eager_ms_per_step": round(t_eager_step * 1e3, 5),
+            "eager_method": "eager launches queued behind a GPU spin-sleep; HIP events "
+                            "(hipEventDisableSystemFence) on the launch stream around every kernel",
+            **queue_info},
     }
     print(json.dumps(line), flush=True)
     return 0
