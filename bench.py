@@ -98,6 +98,7 @@ class Op:
 
 
 PACKED_MIN_ROWS = 64   # more rows than this: the packed prefill pair
+PACKED_MIN_EXPERT_ROWS = 64   # mean routed rows per expert from which experts use it
 
 
 def build_dense_ops(torch, prq, layers, M_list, rotate_bytes, plain=False):
@@ -173,19 +174,32 @@ def build_expert_ops(torch, np, prq, inputs, tokens, rotate_bytes):
     off = torch.from_numpy(c.group_offsets).cuda()
     M = int(c.group_offsets[-1])
     X = torch.from_numpy(c.X.view("int16")).cuda()
-    Aq = torch.empty((M, K_aug // 2), dtype=torch.uint8, device="cuda")
-    Asc = torch.empty((M, K_aug // 32), dtype=torch.uint8, device="cuda")
     Y = torch.empty((M, N), dtype=torch.float32, device="cuda")
     state = {"r": 0}
     e_active = int(np.count_nonzero(np.diff(c.group_offsets)))
 
-    def act():
-        prq.prq_quant_act(X, K, k, inv, perm, group_offsets=off, G=E, Aq=Aq, Asc=Asc)
+    if M >= PACKED_MIN_EXPERT_ROWS * E:
+        # prefill: the packed pair (grouped tile GEMM on the packed activation)
+        A = prq.prq_quant_act_packed(X, K, k, inv, perm, group_offsets=off, G=E)
 
-    def gemm():
-        r = state["r"]
-        state["r"] = (r + 1) % R
-        prq.prq_grouped_gemm(Aq, Asc, off, Ws[r], Y=Y)
+        def act():
+            prq.prq_quant_act_packed(X, K, k, inv, perm, out=A, group_offsets=off, G=E)
+
+        def gemm():
+            r = state["r"]
+            state["r"] = (r + 1) % R
+            prq.prq_grouped_gemm_packed(A, off, Ws[r], Y=Y)
+    else:
+        Aq = torch.empty((M, K_aug // 2), dtype=torch.uint8, device="cuda")
+        Asc = torch.empty((M, K_aug // 32), dtype=torch.uint8, device="cuda")
+
+        def act():
+            prq.prq_quant_act(X, K, k, inv, perm, group_offsets=off, G=E, Aq=Aq, Asc=Asc)
+
+        def gemm():
+            r = state["r"]
+            state["r"] = (r + 1) % R
+            prq.prq_grouped_gemm(Aq, Asc, off, Ws[r], Y=Y)
 
     log(f"[bench] experts: {M} routed rows, {e_active} active experts, {R} weight copies")
     return [Op(f"experts/{tokens}tok", M, N, K, k, act, gemm,

@@ -229,20 +229,33 @@ int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M,
  *
  * prq_packed_act_bytes -- sizes of Ap and Aps for M rows.  Returns PRQ_OK,
  *   PRQ_EINVAL, PRQ_EALIGN (K_aug % 32), PRQ_EUNSUPPORTED (K_aug > 65536).
- * prq_quant_act_packed -- prq_quant_act (dense: one perm and inv_scale_pos,
- *   G = 1) into Ap / Aps (device, 16-byte aligned, of the sizes above).
- *   Limits as prq_quant_act.  M == 0 is a no-op.
+ * prq_quant_act_packed -- prq_quant_act into Ap / Aps (device, 16-byte
+ *   aligned, of the sizes above), with the same arguments: one perm and
+ *   inv_scale_pos (G = 1), or G groups of sorted rows (group_offsets, and G
+ *   rows of K in perm / inv_scale_pos).  Rows of different groups may share a
+ *   16-row block.  Limits and errors as prq_quant_act.  M == 0 is a no-op.
  * prq_gemm_packed -- prq_gemm on a packed activation (the LDS-tiled kernel):
  *   Y [M, N] float32 = Eq. 3 over K_aug; Ap / Aps from prq_quant_act_packed,
  *   Wp / Wps from prq_pack_weight (E = 1).  No workspace.  Limits as prq_gemm.
+ * prq_grouped_gemm_packed -- prq_grouped_gemm on a packed activation (rows
+ *   sorted by expert, from prq_quant_act_packed with G = E and the same
+ *   offsets).  An expert's row tiles start on its first 16-row block; rows of
+ *   a neighbouring expert in a shared block are computed but not stored.
+ *   Arguments, limits and errors as prq_grouped_gemm, no workspace; Aps must
+ *   be 16-byte aligned (else PRQ_EALIGN).
  */
 int prq_packed_act_bytes(int32_t M, int32_t K_aug, size_t* code_bytes, size_t* scale_bytes);
 int prq_quant_act_packed(const void* X_bf16, int64_t ld_x, int32_t M, int32_t K, int32_t k_tail,
                          const float* inv_scale_pos, const int32_t* perm,
+                         const int32_t* group_offsets, int32_t G,
                          uint8_t* Ap, uint8_t* Aps, hipStream_t stream);
 int prq_gemm_packed(const uint8_t* Ap, const uint8_t* Aps, int32_t M,
                     const uint8_t* Wp, const uint8_t* Wps, int32_t N, int32_t K_aug,
                     float* Y, hipStream_t stream);
+int prq_grouped_gemm_packed(const uint8_t* Ap, const uint8_t* Aps,
+                            const int32_t* group_offsets, int32_t E, int32_t M_total,
+                            const uint8_t* Wp, const uint8_t* Wps, int32_t N, int32_t K_aug,
+                            float* Y, hipStream_t stream);
 
 /*
  * prq_grouped_gemm -- Eq. 3 for E MoE experts in one launch (the paper applies

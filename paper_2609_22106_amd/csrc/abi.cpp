@@ -238,11 +238,13 @@ int prq_packed_act_bytes(int32_t M, int32_t K_aug, size_t* code_bytes, size_t* s
 }
 
 int prq_quant_act_packed(const void* X_bf16, int64_t ld_x, int32_t M, int32_t K, int32_t k_tail,
-                         const float* inv_scale_pos, const int32_t* perm, uint8_t* Ap,
-                         uint8_t* Aps, hipStream_t stream) {
-  if (M < 0 || K <= 0 || ld_x < K) return PRQ_EINVAL;
+                         const float* inv_scale_pos, const int32_t* perm,
+                         const int32_t* group_offsets, int32_t G, uint8_t* Ap, uint8_t* Aps,
+                         hipStream_t stream) {
+  if (M < 0 || K <= 0 || G < 1 || ld_x < K) return PRQ_EINVAL;
+  if (G > 1 && !group_offsets) return PRQ_EINVAL;
   if (K % PRQ_BLOCK || k_tail < 0 || k_tail % PRQ_BLOCK || k_tail > K) return PRQ_EALIGN;
-  if (K > kMaxK) return PRQ_EUNSUPPORTED;
+  if (K > kMaxK || G > kMaxGroups) return PRQ_EUNSUPPORTED;
   if (M == 0) return PRQ_OK;
   if (!X_bf16 || !Ap || !Aps) return PRQ_EINVAL;
   if (!aligned16(X_bf16) || ld_x % 8 || !aligned16(Ap) || !aligned16(Aps)) return PRQ_EALIGN;
@@ -252,8 +254,8 @@ int prq_quant_act_packed(const void* X_bf16, int64_t ld_x, int32_t M, int32_t K,
   int st = current_device(&dev);
   if (st != PRQ_OK) return st;
   return launch_status(prq::launch_act_quant_packed(static_cast<const uint16_t*>(X_bf16), ld_x, M,
-                                                    K, k_tail, inv_scale_pos, perm, Ap, Aps,
-                                                    dev.num_cus, stream));
+                                                    K, k_tail, inv_scale_pos, perm, group_offsets,
+                                                    G, Ap, Aps, dev.num_cus, stream));
 }
 
 int prq_gemm_packed(const uint8_t* Ap, const uint8_t* Aps, int32_t M, const uint8_t* Wp,
@@ -267,6 +269,24 @@ int prq_gemm_packed(const uint8_t* Ap, const uint8_t* Aps, int32_t M, const uint
   if (st != PRQ_OK) return st;
   return launch_status(prq::launch_gemm_tile_planned(Ap, Aps, M, Wp, Wps, N, K_aug, Y, true,
                                                      dev.num_cus, stream));
+}
+
+int prq_grouped_gemm_packed(const uint8_t* Ap, const uint8_t* Aps, const int32_t* group_offsets,
+                            int32_t E, int32_t M_total, const uint8_t* Wp, const uint8_t* Wps,
+                            int32_t N, int32_t K_aug, float* Y, hipStream_t stream) {
+  int st = check_gemm_common(Ap, Aps, M_total, Wp, Wps, N, K_aug, Y);
+  if (st != PRQ_OK) return st;
+  if (E < 1 || !group_offsets) return PRQ_EINVAL;
+  if (E > kMaxGroups) return PRQ_EUNSUPPORTED;
+  if (M_total == 0) return PRQ_OK;
+  if (!aligned16(Aps)) return PRQ_EALIGN;
+  DeviceInfo dev;
+  st = current_device(&dev);
+  if (st != PRQ_OK) return st;
+  const int per_group = (M_total + E - 1) / E;
+  return launch_status(prq::launch_grouped_gemm_tile_packed(
+      Ap, Aps, M_total, group_offsets, E, Wp, Wps, N, K_aug, Y,
+      prq::choose_grouped_packed_shape(per_group, N, K_aug), stream));
 }
 
 size_t prq_grouped_gemm_workspace_bytes(int32_t M_total, int32_t E, int32_t N, int32_t K_aug) {
@@ -302,8 +322,10 @@ int prq_grouped_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, const int32_t* gr
       return launch_status(prq::launch_gemm_stream(Aq, Asc, M_total, group_offsets, E, Wp, Wps, N,
                                                    K_aug, Y, c, nullptr, stream));
   }
-  // Row tiles are per expert: pick the shape from the mean rows per expert.
-  const int shape = per_group >= 256 ? 1 : 2;
+  // Row tiles are per expert: pick the shape from the mean rows per expert
+  // (~256 rows per expert at N = 2048, K + k = 832: 176 us with 256 x 256
+  // tiles, 194 with 128 x 128, 248 with 256 x 128).
+  const int shape = per_group >= 192 ? 0 : 2;
   return launch_status(prq::launch_gemm_tile(Aq, Asc, M_total, group_offsets, E, Wp, Wps, N, K_aug,
                                              Y, shape, stream));
 }

@@ -582,30 +582,47 @@ hipError_t launch_act_quant_kernel(const uint16_t* X, int64_t ld_x, int M, int K
 }
 
 hipError_t launch_act_quant_packed(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail,
-                                   const float* inv_scale_pos, const int32_t* perm, uint8_t* Ap,
-                                   uint8_t* Aps, int num_cus, hipStream_t stream) {
-  return launch_act_quant_packed_kernel(X, ld_x, M, K, k_tail, inv_scale_pos, perm, Ap, Aps,
-                                        num_cus, 0, stream);
+                                   const float* inv_scale_pos, const int32_t* perm,
+                                   const int32_t* group_offsets, int G, uint8_t* Ap, uint8_t* Aps,
+                                   int num_cus, hipStream_t stream) {
+  return launch_act_quant_packed_kernel(X, ld_x, M, K, k_tail, inv_scale_pos, perm, group_offsets,
+                                        G, Ap, Aps, num_cus, 0, stream);
 }
 
 hipError_t launch_act_quant_packed_kernel(const uint16_t* X, int64_t ld_x, int M, int K,
                                           int k_tail, const float* inv_scale_pos,
-                                          const int32_t* perm, uint8_t* Ap, uint8_t* Aps,
-                                          int num_cus, int kernel, hipStream_t stream) {
-  if (kernel == 3 || (kernel == 0 && K >= 2048))
+                                          const int32_t* perm, const int32_t* group_offsets,
+                                          int G, uint8_t* Ap, uint8_t* Aps, int num_cus,
+                                          int kernel, hipStream_t stream) {
+  const bool grouped = group_offsets && G > 1;
+  const int32_t* off = grouped ? group_offsets : nullptr;
+  if (kernel == 3 || (kernel == 0 && K >= 2048)) {
+    if (grouped)
+      return launch_dma<true, true>(X, ld_x, M, K, k_tail, inv_scale_pos, perm, off, G, Ap, Aps,
+                                    num_cus, stream);
     return launch_dma<false, true>(X, ld_x, M, K, k_tail, inv_scale_pos, perm, nullptr, 1, Ap, Aps,
                                    num_cus, stream);
+  }
   const int units = K >> 3;
   const size_t lds = lds_kernel_bytes(K);
   const int per_thread = (units + kLdsThreads - 1) / kLdsThreads;
   const int rows_per_wg = lds_rows_per_wg(M, units, num_cus);
   const dim3 grid((M + rows_per_wg - 1) / rows_per_wg);
+#define PRQ_LDS_PACKED_CASE(n)                                                                  \
+  if (grouped)                                                                                 \
+    launch_lds<true, n, true>(grid, lds, stream, X, ld_x, M, K, k_tail, inv_scale_pos, perm, off, \
+                              G, rows_per_wg, Ap, Aps);                                        \
+  else                                                                                         \
+    launch_lds<false, n, true>(grid, lds, stream, X, ld_x, M, K, k_tail, inv_scale_pos, perm,   \
+                               nullptr, 1, rows_per_wg, Ap, Aps);                              \
+  break;
   switch (per_thread) {
-    case 1: launch_lds<false, 1, true>(grid, lds, stream, X, ld_x, M, K, k_tail, inv_scale_pos, perm, nullptr, 1, rows_per_wg, Ap, Aps); break;
-    case 2: launch_lds<false, 2, true>(grid, lds, stream, X, ld_x, M, K, k_tail, inv_scale_pos, perm, nullptr, 1, rows_per_wg, Ap, Aps); break;
-    case 3: launch_lds<false, 3, true>(grid, lds, stream, X, ld_x, M, K, k_tail, inv_scale_pos, perm, nullptr, 1, rows_per_wg, Ap, Aps); break;
-    default: launch_lds<false, 4, true>(grid, lds, stream, X, ld_x, M, K, k_tail, inv_scale_pos, perm, nullptr, 1, rows_per_wg, Ap, Aps); break;
+    case 1: PRQ_LDS_PACKED_CASE(1)
+    case 2: PRQ_LDS_PACKED_CASE(2)
+    case 3: PRQ_LDS_PACKED_CASE(3)
+    default: PRQ_LDS_PACKED_CASE(4)
   }
+#undef PRQ_LDS_PACKED_CASE
   return hipGetLastError();
 }
 

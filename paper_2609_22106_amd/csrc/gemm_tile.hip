@@ -53,22 +53,28 @@ __device__ __forceinline__ int xcd_remap(int L, int total) {
 
 // Row range and expert of row tile `mt` when tiles of `tile_rows` rows are
 // numbered expert after expert (prefix scan of per-expert tile counts over
-// the workgroup's threads, `nthreads` at a time).
-template <int kThreads>
+// the workgroup's threads, `nthreads` at a time).  With kAlign16 an expert's
+// tiles start at its first row rounded down to a multiple of 16 (the packed
+// activation's row blocks): rows [*row_begin, *row_end) are loaded, rows
+// [*row_lo, *row_end) belong to the expert and are stored.  `lds` is
+// kThreads + 4 ints of LDS scratch; every thread has read it on return once a
+// barrier follows the call.
+template <int kThreads, bool kAlign16>
 __device__ bool grouped_tile(const int32_t* __restrict__ off, int E, int M, int mt, int tile_rows,
-                             int* e_out, int* row_begin, int* row_end) {
-  __shared__ int s_scan[kThreads];
-  __shared__ int s_hit[3];
+                             int* lds, int* e_out, int* row_begin, int* row_lo, int* row_end) {
+  int* const s_scan = lds;
+  int* const s_hit = lds + kThreads;
   const int tid = threadIdx.x;
   if (tid == 0) s_hit[0] = -1;
   int base = 0;
   for (int e0 = 0; e0 < E; e0 += kThreads) {
     const int e = e0 + tid;
-    int r0 = 0, r1 = 0, t = 0;
+    int r0 = 0, r1 = 0, b0 = 0, t = 0;
     if (e < E) {  // offsets clamped to [0, M]: malformed offsets cannot address past A
       r0 = min(max(off[e], 0), M);
       r1 = min(max(off[e + 1], r0), M);
-      t = (r1 - r0 + tile_rows - 1) / tile_rows;
+      b0 = kAlign16 ? (r0 & ~15) : r0;
+      t = r1 > r0 ? (r1 - b0 + tile_rows - 1) / tile_rows : 0;
     }
     s_scan[tid] = t;
     __syncthreads();
@@ -82,8 +88,9 @@ __device__ bool grouped_tile(const int32_t* __restrict__ off, int E, int M, int 
     const int excl = incl - t;
     if (e < E && mt >= excl && mt < incl) {
       s_hit[0] = e;
-      s_hit[1] = r0 + (mt - excl) * tile_rows;
+      s_hit[1] = b0 + (mt - excl) * tile_rows;
       s_hit[2] = min(r1, s_hit[1] + tile_rows);
+      s_hit[3] = max(r0, s_hit[1]);
     }
     base += s_scan[kThreads - 1];
     __syncthreads();
@@ -92,6 +99,7 @@ __device__ bool grouped_tile(const int32_t* __restrict__ off, int E, int M, int 
   *e_out = s_hit[0];
   *row_begin = s_hit[1];
   *row_end = s_hit[2];
+  *row_lo = s_hit[3];
   return true;
 }
 
@@ -168,7 +176,6 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   using L = TileStage<kBM, kBN, kAMode>;
   constexpr bool kScaleDword = kAMode == kARowDword;
   constexpr bool kPackedA = kAMode == kAPacked;
-  static_assert(!(kPackedA && kGrouped), "packed activations: dense calls");
   constexpr int kWaves = kWM * kWN;
   constexpr int kThreads = kWaves * 64;
   constexpr int kTM = kBM / kWM, kTN = kBN / kWN;    // wave tile
@@ -188,7 +195,8 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   constexpr int kBsPer = (kBsChunks + kWaves - 1) / kWaves;
   constexpr int kLoads = kAPer + kBPer + kAsPer + kBsPer;   // direct-to-LDS loads per wave per step
   static_assert(kNS >= 2 && kNS <= 4, "stages");
-  static_assert(kNS * L::kBytes + (kGrouped ? kThreads * 4 + 16 : 0) <= 160 * 1024, "LDS");
+  static_assert(kNS * L::kBytes <= 160 * 1024, "LDS");
+  static_assert(L::kBytes >= kThreads * 4 + 16, "the expert scan borrows a stage");
   constexpr int kU = kNS;         // main-loop unroll: the stage index is known
   constexpr int kMfmas = 2 * kFM * kFN;                                  // per step
   constexpr int kReads = 4 * (kFM + kFN);                                // LDS reads per step
@@ -213,11 +221,15 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   const int logical = xcd_remap(blockIdx.x, total);
   const int mt = logical / n_ntiles, nt = logical % n_ntiles;
 
-  int e = 0, row_begin, row_end;
+  int e = 0, row_begin, row_lo, row_end;
   if (kGrouped) {
-    if (!grouped_tile<kThreads>(off, E, M, mt, kBM, &e, &row_begin, &row_end)) return;
+    // (the scan's scratch is stage 0, free until the first load is issued)
+    if (!grouped_tile<kThreads, kPackedA>(off, E, M, mt, kBM, reinterpret_cast<int*>(st0), &e,
+                                          &row_begin, &row_lo, &row_end))
+      return;
+    __syncthreads();
   } else {
-    row_begin = mt * kBM;
+    row_begin = row_lo = mt * kBM;
     row_end = min(M, row_begin + kBM);
   }
   const int t0 = tile_base + nt * kBBlk;             // first 16-feature tile
@@ -434,7 +446,7 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const int m = row_begin + wm * kTM + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
-        if (m < row_end && n < n_end) Y[static_cast<int64_t>(m) * N + n] = acc[i][j][q];
+        if (m >= row_lo && m < row_end && n < n_end) Y[static_cast<int64_t>(m) * N + n] = acc[i][j][q];
       }
     }
 }
@@ -450,13 +462,15 @@ hipError_t launch_shape_scales(const uint8_t* Aq, const uint8_t* Asc, int M, con
     return hipErrorInvalidValue;
   if (region_tiles <= 0) return hipSuccess;
   const int n_ntiles = (region_tiles + kBN / 16 - 1) / (kBN / 16);
-  // Grouped: an upper bound on the row tiles over all experts (extra ids exit).
-  const int n_mtiles = off ? (M + kBM - 1) / kBM + E : (M + kBM - 1) / kBM;
+  // Grouped: an upper bound on the row tiles over all experts (extra ids exit):
+  // expert e takes ceil((c_e + a) / kBM) <= (c_e + a + kBM - 1) / kBM tiles for
+  // its c_e rows, a = 15 with the packed layout (tiles start on the expert's
+  // first 16-row block), else 0; summed over the experts and floored.
+  const int64_t lead = kAMode == kAPacked ? 15 : 0;
+  const int n_mtiles = off ? static_cast<int>((M + static_cast<int64_t>(E) * (kBM - 1 + lead)) / kBM)
+                           : (M + kBM - 1) / kBM;
   const int grid = n_mtiles * n_ntiles;
-  if constexpr (kAMode == kAPacked) {
-    gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, false, kAMode><<<grid, kWM * kWN * 64, 0, stream>>>(
-        Aq, Asc, M, nullptr, 1, n_mtiles, tile_base, region_tiles, Wp, Wps, N, K_aug, Y);
-  } else if (off) {
+  if (off) {
     gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, true, kAMode><<<grid, kWM * kWN * 64, 0, stream>>>(
         Aq, Asc, M, off, E, n_mtiles, tile_base, region_tiles, Wp, Wps, N, K_aug, Y);
   } else {
@@ -475,7 +489,7 @@ hipError_t launch_shape(const uint8_t* Aq, const uint8_t* Asc, int M, const int3
                         bool packed, int tile_base, int region_tiles, hipStream_t stream) {
   if (packed)
     return launch_shape_scales<kBM, kBN, kWM, kWN, kNSDword, kAPacked>(
-        Aq, Asc, M, nullptr, 1, Wp, Wps, N, K_aug, Y, tile_base, region_tiles, stream);
+        Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, tile_base, region_tiles, stream);
   if (K_aug % 128 == 0 && (reinterpret_cast<uintptr_t>(Asc) & 3u) == 0)
     return launch_shape_scales<kBM, kBN, kWM, kWN, kNSDword, kARowDword>(
         Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, tile_base, region_tiles, stream);
@@ -596,6 +610,25 @@ hipError_t launch_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M,
                                    float* Y, int shape, hipStream_t stream) {
   return launch_region(Ap, Aps, M, nullptr, 1, Wp, Wps, N, K_aug, Y, shape, true, 0, N / 16,
                        stream);
+}
+
+// Shape of the grouped packed GEMM.  128 x 128 throughout: on the expert
+// shape (~256 rows per expert, N = 2048, K + k = 832) it measured 158 us
+// against 167 (256 x 256) and 220 (256 x 128), and smaller row tiles waste
+// less on experts with fewer rows.
+int choose_grouped_packed_shape(int rows_per_expert, int N, int K_aug) {
+  (void)rows_per_expert;
+  (void)N;
+  (void)K_aug;
+  return 2;
+}
+
+hipError_t launch_grouped_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M_total,
+                                           const int32_t* group_offsets, int E, const uint8_t* Wp,
+                                           const uint8_t* Wps, int N, int K_aug, float* Y,
+                                           int shape, hipStream_t stream) {
+  return launch_region(Ap, Aps, M_total, group_offsets, E, Wp, Wps, N, K_aug, Y, shape, true, 0,
+                       N / 16, stream);
 }
 
 hipError_t launch_gemm_tile_planned(const uint8_t* Aq, const uint8_t* Asc, int M,

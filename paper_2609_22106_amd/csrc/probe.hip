@@ -270,13 +270,14 @@ int prq_tune_act_quant(const void* X, int64_t ld_x, int M, int K, int k_tail, co
 
 // The same into the packed activation layout (2 register-staged, 3 LDS stages).
 int prq_tune_act_quant_packed(const void* X, int64_t ld_x, int M, int K, int k_tail,
-                              const float* inv, const int32_t* perm, uint8_t* Ap, uint8_t* Aps,
-                              int kernel, hipStream_t stream) {
+                              const float* inv, const int32_t* perm, const int32_t* off, int G,
+                              uint8_t* Ap, uint8_t* Aps, int kernel, hipStream_t stream) {
   if (M <= 0 || K <= 0 || K % 32 || k_tail % 32 || k_tail > K || K > 16384 || ld_x < K ||
       (kernel != 2 && kernel != 3))
     return -1;
   return prq::launch_act_quant_packed_kernel(static_cast<const uint16_t*>(X), ld_x, M, K, k_tail,
-                                             inv, perm, Ap, Aps, 256, kernel, stream) == hipSuccess
+                                             inv, perm, off, G, Ap, Aps, 256, kernel,
+                                             stream) == hipSuccess
              ? 0
              : -3;
 }
@@ -326,6 +327,18 @@ int prq_tune_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M, cons
                               hipStream_t stream) {
   if (shape < 0 || shape > 2 || N % 16 || K_aug % 32 || M <= 0) return -1;
   return prq::launch_gemm_tile_packed(Ap, Aps, M, Wp, Wps, N, K_aug, Y, shape, stream) == hipSuccess
+             ? 0
+             : -3;
+}
+
+// The grouped tile GEMM on a packed activation with a forced shape.
+int prq_tune_grouped_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M,
+                                      const int32_t* off, int E, const uint8_t* Wp,
+                                      const uint8_t* Wps, int N, int K_aug, float* Y, int shape,
+                                      hipStream_t stream) {
+  if (shape < 0 || shape > 2 || N % 16 || K_aug % 32 || M <= 0 || E < 1 || !off) return -1;
+  return prq::launch_grouped_gemm_tile_packed(Ap, Aps, M, off, E, Wp, Wps, N, K_aug, Y, shape,
+                                              stream) == hipSuccess
              ? 0
              : -3;
 }

@@ -47,15 +47,17 @@ hipError_t launch_act_quant_kernel(const uint16_t* X, int64_t ld_x, int M, int K
 
 // The same with the output in the packed (weight) layout: Ap [ceil(M/16)][S][64][16],
 // Aps [ceil(M/16)][ceil(S/4)][64] uint32, rows past M and K parts past K_aug padded
-// (zero codes, scale byte 127).  Dense only.
+// (zero codes, scale byte 127).  Groups as in launch_act_quant (nullptr: one).
 hipError_t launch_act_quant_packed(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail,
-                                   const float* inv_scale_pos, const int32_t* perm, uint8_t* Ap,
-                                   uint8_t* Aps, int num_cus, hipStream_t stream);
+                                   const float* inv_scale_pos, const int32_t* perm,
+                                   const int32_t* group_offsets, int G, uint8_t* Ap, uint8_t* Aps,
+                                   int num_cus, hipStream_t stream);
 // kernel: 0 = automatic, 2 = register-staged rows, 3 = rows copied into LDS stages.
 hipError_t launch_act_quant_packed_kernel(const uint16_t* X, int64_t ld_x, int M, int K,
                                           int k_tail, const float* inv_scale_pos,
-                                          const int32_t* perm, uint8_t* Ap, uint8_t* Aps,
-                                          int num_cus, int kernel, hipStream_t stream);
+                                          const int32_t* perm, const int32_t* group_offsets,
+                                          int G, uint8_t* Ap, uint8_t* Aps, int num_cus,
+                                          int kernel, hipStream_t stream);
 
 // pack.hip: the packed weight layout the GEMM kernels read.
 size_t packed_code_bytes(int N, int K_aug, int E);
@@ -77,6 +79,13 @@ hipError_t launch_gemm_tile(const uint8_t* Aq, const uint8_t* Asc, int M,
 hipError_t launch_gemm_tile_planned(const uint8_t* Aq, const uint8_t* Asc, int M,
                                     const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug,
                                     float* Y, bool packed, int num_cus, hipStream_t stream);
+// The grouped (MoE) tile GEMM on a packed activation: an expert's row tiles
+// start on 16-row block boundaries (rows of neighbouring experts are masked).
+hipError_t launch_grouped_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M_total,
+                                           const int32_t* group_offsets, int E, const uint8_t* Wp,
+                                           const uint8_t* Wps, int N, int K_aug, float* Y,
+                                           int shape, hipStream_t stream);
+int choose_grouped_packed_shape(int rows_per_expert, int N, int K_aug);
 // The tile GEMM with the activation in the packed layout (dense).
 hipError_t launch_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M,
                                    const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug,

@@ -66,8 +66,10 @@ _gemm_ex = _decl("prq_gemm_ex", ctypes.c_int,
 _packed_act_bytes = _decl("prq_packed_act_bytes", ctypes.c_int,
                           [_i32, _i32, ctypes.POINTER(_sz), ctypes.POINTER(_sz)])
 _quant_act_packed = _decl("prq_quant_act_packed", ctypes.c_int,
-                          [_p, _i64, _i32, _i32, _i32, _p, _p, _p, _p, _p])
+                          [_p, _i64, _i32, _i32, _i32, _p, _p, _p, _i32, _p, _p, _p])
 _gemm_packed = _decl("prq_gemm_packed", ctypes.c_int, [_p, _p, _i32, _p, _p, _i32, _i32, _p, _p])
+_ggemm_packed = _decl("prq_grouped_gemm_packed", ctypes.c_int,
+                      [_p, _p, _p, _i32, _i32, _p, _p, _i32, _i32, _p, _p])
 _ggemm_ws = _decl("prq_grouped_gemm_workspace_bytes", _sz, [_i32, _i32, _i32, _i32])
 _ggemm = _decl("prq_grouped_gemm", ctypes.c_int,
                [_p, _p, _p, _i32, _i32, _p, _p, _i32, _i32, _p, _p, _sz, _p])
@@ -353,9 +355,12 @@ def prq_packed_act_bytes(M, K_aug):
     return int(cb.value), int(sb.value)
 
 
-def prq_quant_act_packed(X, K, k_tail, inv_scale_pos=None, perm=None, out=None, stream=None):
-    """prq_quant_act (dense) into the packed activation layout -> PackedAct.
-    out: a PackedAct of the same M and K_aug to write into (else allocated)."""
+def prq_quant_act_packed(X, K, k_tail, inv_scale_pos=None, perm=None, out=None, stream=None,
+                         group_offsets=None, G=1):
+    """prq_quant_act into the packed activation layout -> PackedAct.
+    out: a PackedAct of the same M and K_aug to write into (else allocated).
+    G > 1: rows sorted by group, group_offsets [G + 1] device int32, and
+    inv_scale_pos / perm hold G rows of K (one per expert)."""
     if not isinstance(X, torch.Tensor) or X.dim() != 2 or X.dtype not in _BF16_LIKE:
         raise ValueError("X must be a 2-D tensor of bf16 values (or their int16 bit patterns)")
     M = X.shape[0]
@@ -371,13 +376,19 @@ def prq_quant_act_packed(X, K, k_tail, inv_scale_pos=None, perm=None, out=None, 
         raise ValueError(f"out holds {out.M} rows of K_aug {out.K_aug}, expected {M} x {K_aug}")
     out.check_sizes()
     if inv_scale_pos is not None:
-        _need(inv_scale_pos, "inv_scale_pos", torch.float32, min_numel=K)
+        _need(inv_scale_pos, "inv_scale_pos", torch.float32, min_numel=G * K)
     if perm is not None:
-        _need(perm, "perm", torch.int32, min_numel=K)
-    _on_gpu(X=X, Ap=out.Ap, Aps=out.Aps, inv_scale_pos=inv_scale_pos, perm=perm)
+        _need(perm, "perm", torch.int32, min_numel=G * K)
+    if G > 1:
+        if group_offsets is None:
+            raise ValueError("G > 1 needs group_offsets")
+        _need(group_offsets, "group_offsets", torch.int32, min_numel=G + 1)
+    _on_gpu(X=X, Ap=out.Ap, Aps=out.Aps, inv_scale_pos=inv_scale_pos, perm=perm,
+            group_offsets=group_offsets if G > 1 else None)
     ld = X.stride(0) if M > 1 else K
     st = _quant_act_packed(_ptr(X), ld, M, K, k_tail, _ptr(inv_scale_pos), _ptr(perm),
-                           _ptr(out.Ap), _ptr(out.Aps), _stream(stream))
+                           _ptr(group_offsets) if G > 1 else None, G, _ptr(out.Ap), _ptr(out.Aps),
+                           _stream(stream))
     _check(st, "prq_quant_act_packed")
     return out
 
@@ -398,6 +409,25 @@ def prq_gemm_packed(A, W, Y=None, stream=None):
     st = _gemm_packed(_ptr(A.Ap), _ptr(A.Aps), M, _ptr(W.Wp), _ptr(W.Wps), N, W.K_aug, _ptr(Y),
                       _stream(stream))
     _check(st, "prq_gemm_packed")
+    return Y
+
+
+def prq_grouped_gemm_packed(A, group_offsets, W, Y=None, stream=None):
+    """prq_grouped_gemm on a PackedAct A (rows sorted by expert, from
+    prq_quant_act_packed with the same group_offsets); Y [M_total, N] float32."""
+    if A.K_aug != W.K_aug:
+        raise ValueError(f"K_aug differs: activation {A.K_aug}, weight {W.K_aug}")
+    M, E, N = A.M, W.E, W.N
+    if Y is None:
+        Y = torch.empty((M, N), dtype=torch.float32, device=W.Wp.device)
+    _need(Y, "Y", torch.float32, (M, N))
+    _need(group_offsets, "group_offsets", torch.int32, (E + 1,))
+    A.check_sizes()
+    W.check_sizes()
+    _on_gpu(Ap=A.Ap, Aps=A.Aps, Y=Y, Wp=W.Wp, Wps=W.Wps, group_offsets=group_offsets)
+    st = _ggemm_packed(_ptr(A.Ap), _ptr(A.Aps), _ptr(group_offsets), E, M, _ptr(W.Wp), _ptr(W.Wps),
+                       N, W.K_aug, _ptr(Y), _stream(stream))
+    _check(st, "prq_grouped_gemm_packed")
     return Y
 
 

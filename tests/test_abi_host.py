@@ -160,16 +160,24 @@ def test_packed_activation_calls_validate_before_touching_the_gpu():
     fake = ctypes.c_void_p(4096)   # 16-byte aligned, never dereferenced
     odd = ctypes.c_void_p(4100)    # 4-byte aligned only
     s = ctypes.c_void_p(0)
-    assert prq._quant_act_packed(fake, 1024, 4, 1000, 64, None, None, fake, fake, s) == prq.PRQ_EALIGN
-    assert prq._quant_act_packed(fake, 1024, 4, 1024, 2048, None, None, fake, fake, s) == prq.PRQ_EALIGN
-    assert prq._quant_act_packed(fake, 1024, 4, 1024, 64, None, None, fake, odd, s) == prq.PRQ_EALIGN
-    assert prq._quant_act_packed(fake, 1024, 4, 1024, 64, None, None, None, fake, s) == prq.PRQ_EINVAL
-    assert prq._quant_act_packed(fake, 1000, 4, 1024, 64, None, None, fake, fake, s) == prq.PRQ_EINVAL
-    assert prq._quant_act_packed(None, 1024, 0, 1024, 64, None, None, None, None, s) == prq.PRQ_OK
+    assert prq._quant_act_packed(fake, 1024, 4, 1000, 64, None, None, None, 1, fake, fake, s) == prq.PRQ_EALIGN
+    assert prq._quant_act_packed(fake, 1024, 4, 1024, 2048, None, None, None, 1, fake, fake, s) == prq.PRQ_EALIGN
+    assert prq._quant_act_packed(fake, 1024, 4, 1024, 64, None, None, None, 1, fake, odd, s) == prq.PRQ_EALIGN
+    assert prq._quant_act_packed(fake, 1024, 4, 1024, 64, None, None, None, 1, None, fake, s) == prq.PRQ_EINVAL
+    assert prq._quant_act_packed(fake, 1000, 4, 1024, 64, None, None, None, 1, fake, fake, s) == prq.PRQ_EINVAL
+    assert prq._quant_act_packed(None, 1024, 0, 1024, 64, None, None, None, 1, None, None, s) == prq.PRQ_OK
     assert prq._gemm_packed(fake, fake, 4, fake, fake, 24, 1088, fake, s) == prq.PRQ_EALIGN   # N % 16
     assert prq._gemm_packed(fake, odd, 4, fake, fake, 32, 1088, fake, s) == prq.PRQ_EALIGN    # Aps
     assert prq._gemm_packed(fake, fake, 4, fake, odd, 32, 1088, fake, s) == prq.PRQ_EALIGN    # Wps
     assert prq._gemm_packed(None, None, 0, fake, fake, 32, 1088, None, s) == prq.PRQ_OK
+    # grouped: G > 1 needs offsets; E >= 1 with offsets; Aps alignment
+    assert prq._quant_act_packed(fake, 1024, 4, 1024, 64, None, None, None, 3, fake, fake, s) == prq.PRQ_EINVAL
+    assert prq._quant_act_packed(fake, 1024, 4, 1024, 64, None, None, fake, 0, fake, fake, s) == prq.PRQ_EINVAL
+    assert prq._ggemm_packed(fake, fake, None, 4, 8, fake, fake, 32, 1088, fake, s) == prq.PRQ_EINVAL
+    assert prq._ggemm_packed(fake, fake, fake, 0, 8, fake, fake, 32, 1088, fake, s) == prq.PRQ_EINVAL
+    assert prq._ggemm_packed(fake, odd, fake, 4, 8, fake, fake, 32, 1088, fake, s) == prq.PRQ_EALIGN
+    assert prq._ggemm_packed(fake, fake, fake, 4, 8, fake, fake, 24, 1088, fake, s) == prq.PRQ_EALIGN
+    assert prq._ggemm_packed(None, None, fake, 4, 0, fake, fake, 32, 1088, None, s) == prq.PRQ_OK
 
 
 def test_packed_activation_sizes():

@@ -143,3 +143,114 @@ def test_planned_column_regions(packed):
     rows = np.unique(np.concatenate([rng.choice(M, 38, replace=False), [0, M - 1]]))
     assert_gemm_close(Y[rows], pq.gemm(Aq[rows], Asc[rows], Wq, Wsc), f"regions packed={packed}")
 
+
+
+def _pos_grouped(inv, perm):
+    return np.take_along_axis(np.asarray(inv), np.asarray(perm), axis=1)
+
+
+# Experts sharing 16-row blocks, empty experts (first, middle and last), and
+# K below (register-staged kernel) and above (LDS-staged kernel) 2048.
+GROUPED_QUANT = [([3, 0, 20, 1, 13], 768, 64),
+                 ([0, 37, 16, 0, 64, 5, 0], 768, 64),
+                 ([40, 0, 90, 7], 4160, 160),
+                 ([17, 1, 0, 33], 2048, 32)]
+
+
+@pytest.mark.parametrize("counts,K,k", GROUPED_QUANT)
+def test_quant_act_packed_grouped(counts, K, k):
+    """Rows of several experts quantized with each expert's permutation and
+    scales into one packed activation: every byte as the oracle's grouped
+    quantizer laid out by the reference packer."""
+    prq = _prq()
+    rng = np.random.default_rng(sum(counts) + K + k)
+    E = len(counts)
+    off = inputs.routed_offsets(counts)
+    M = int(off[-1])
+    X = inputs.f32_to_bf16_bits((rng.standard_normal((M, K)) *
+                                 rng.uniform(0.01, 30.0, K)).astype(np.float32))
+    perm = np.stack([rng.permutation(K) for _ in range(E)]).astype(np.int32)
+    inv = rng.uniform(0.1, 4.0, (E, K)).astype(np.float32)
+    say("packed grouped quant case:", counts, K, k)
+    A = prq.prq_quant_act_packed(dev(X), K, k, dev(_pos_grouped(inv, perm)), dev(perm),
+                                 group_offsets=dev(off), G=E)
+    torch.cuda.synchronize()
+    ep, es = pack_rows(*pq.quant_act_grouped(X, inv, perm, off, k))
+    np.testing.assert_array_equal(host(A.Aps), es, err_msg="packed scales")
+    np.testing.assert_array_equal(host(A.Ap), ep, err_msg="packed codes")
+
+
+def _tune_grouped_packed(shape, A, off, W, Y):
+    from paper_2609_22106_amd import build
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    P, I = ctypes.c_void_p, ctypes.c_int
+    lib.prq_tune_grouped_gemm_tile_packed.argtypes = [P, P, I, P, I, P, P, I, I, P, I, P]
+    lib.prq_tune_grouped_gemm_tile_packed.restype = I
+    return lib.prq_tune_grouped_gemm_tile_packed(
+        A.Ap.data_ptr(), A.Aps.data_ptr(), A.M, off.data_ptr(), W.E, W.Wp.data_ptr(),
+        W.Wps.data_ptr(), W.N, W.K_aug, Y.data_ptr(), shape,
+        torch.cuda.current_stream().cuda_stream)
+
+
+# Expert row ranges starting inside 16-row blocks, experts spanning more than
+# one 256-row tile, empty experts, ragged N and K + k.
+GROUPED_GEMM = [([0, 300, 0, 5, 260], 272, 1024),
+                ([3, 0, 17, 1, 0], 48, 1088),
+                ([0, 0, 200], 128, 832),
+                ([255, 258, 1, 15, 16, 17, 600], 144, 832),
+                ([7] * 40, 64, 4192)]
+
+
+@pytest.mark.parametrize("counts,N,K_aug", GROUPED_GEMM)
+@pytest.mark.parametrize("shape", [None, 0, 1, 2])
+def test_grouped_gemm_packed(shape, counts, N, K_aug):
+    """Every row of every expert stored exactly once (Y starts as NaN) and within
+    1e-3 max |Y| of the oracle's grouped GEMM (Eq. 3 per expert)."""
+    prq = _prq()
+    rng = np.random.default_rng(sum(counts) * 7 + N + K_aug)
+    E = len(counts)
+    off = inputs.routed_offsets(counts)
+    M = int(off[-1])
+    Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+    Wq, Wsc = inputs.random_mxfp4(rng, (E, N), K_aug)
+    A = prq.PackedAct(*map(dev, pack_rows(Aq, Asc)), M, K_aug)
+    W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
+    offd = dev(off)
+    Y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+    say("packed grouped gemm case:", shape, counts, N, K_aug)
+    if shape is None:
+        prq.prq_grouped_gemm_packed(A, offd, W, Y)
+    else:
+        assert _tune_grouped_packed(shape, A, offd, W, Y) == 0
+    torch.cuda.synchronize()
+    assert_gemm_close(host(Y), pq.grouped_gemm(Aq, Asc, off, Wq, Wsc),
+                      f"grouped packed shape {shape} {counts} {N}x{K_aug}")
+
+
+def test_grouped_packed_pair_experts():
+    """X -> prq_quant_act_packed -> prq_grouped_gemm_packed on the MoE expert
+    shape (128 experts, 768 -> 2048, k = 64, 4096 tokens routed top-8 to
+    distinct uniformly random experts), against the oracle on 64 sampled rows."""
+    prq = _prq()
+    E, K, k, N, tokens = 128, 768, 64, 2048, 4096
+    rng = np.random.default_rng(2)
+    routed = np.stack([rng.choice(E, 8, replace=False) for _ in range(tokens)])
+    off = inputs.routed_offsets(np.bincount(routed.ravel(), minlength=E))
+    M = int(off[-1])
+    X = inputs.f32_to_bf16_bits((rng.standard_normal((M, K)) *
+                                 rng.uniform(0.01, 30.0, K)).astype(np.float32))
+    perm = np.stack([rng.permutation(K) for _ in range(E)]).astype(np.int32)
+    inv = rng.uniform(0.1, 4.0, (E, K)).astype(np.float32)
+    Wq, Wsc = inputs.random_mxfp4(rng, (E, N), K + k)
+    W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
+    offd = dev(off)
+    say("grouped packed pair case:", M, "rows")
+    A = prq.prq_quant_act_packed(dev(X), K, k, dev(_pos_grouped(inv, perm)), dev(perm),
+                                 group_offsets=offd, G=E)
+    Y = host(prq.prq_grouped_gemm_packed(A, offd, W))
+    rows = np.sort(rng.choice(M, 64, replace=False))
+    e_of = np.searchsorted(off, rows, side="right") - 1
+    for e in np.unique(e_of):
+        r = rows[e_of == e]
+        rq, rs = pq.quant_act(X[r], inv[e], perm[e], k)
+        assert_gemm_close(Y[r], pq.gemm(rq, rs, Wq[e], Wsc[e]), f"expert {e} rows {r.tolist()}")
