@@ -128,14 +128,16 @@ def build_dense_ops(torch, prq, layers, M_list, rotate_bytes, plain=False):
                 # prefill: the packed pair (activation written in the layout the
                 # tile GEMM copies in whole kilobytes)
                 A = prq.prq_quant_act_packed(Xm, K, k, inv, perm)
+                ws_n = prq.prq_gemm_packed_workspace_bytes(M, N, K_aug)   # split along K
+                ws = torch.empty(ws_n, dtype=torch.uint8, device="cuda") if ws_n else None
 
                 def act(Xm=Xm, A=A, K=K, k=k, inv=inv, perm=perm):
                     prq.prq_quant_act_packed(Xm, K, k, inv, perm, out=A)
 
-                def gemm(A=A, Y=Y, state=state, R=R, Ws=Ws):
+                def gemm(A=A, Y=Y, ws=ws, state=state, R=R, Ws=Ws):
                     r = state["r"]
                     state["r"] = (r + 1) % R
-                    prq.prq_gemm_packed(A, Ws[r], Y=Y)
+                    prq.prq_gemm_packed(A, Ws[r], Y=Y, workspace=ws)
             else:
                 Aq = torch.empty((M, K_aug // 2), dtype=torch.uint8, device="cuda")
                 Asc = torch.empty((M, K_aug // 32), dtype=torch.uint8, device="cuda")

@@ -196,9 +196,11 @@ int prq_pack_weight(const uint8_t* Wq, const uint8_t* Wsc, int32_t E, int32_t N,
  *   accumulator [M][N] plus one arrival counter per output tile, which every
  *   call leaves zero-filled again (atomic mode, up to 32 rows), or partial
  *   sums [splits][M][N] that are rewritten before being read and added in a
- *   fixed order (deterministic mode, more rows).  It must be zero-filled once
- *   before its first use.  Calls that share one workspace must be ordered
- *   (same stream).
+ *   fixed order (deterministic mode, more rows; the LDS-tiled kernel's split
+ *   along K keeps splits - 1 of them and needs workspace and Y 16-byte
+ *   aligned).  It must be zero-filled once before its first use.  Calls that
+ *   share one workspace must be ordered (same stream).  Without the workspace
+ *   the LDS-tiled kernel runs unsplit (same result up to float rounding).
  * Limits: N % 16 == 0, K_aug <= 65536.  M == 0 is a no-op.
  */
 size_t prq_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K_aug);
@@ -236,7 +238,13 @@ int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M,
  *   16-row block.  Limits and errors as prq_quant_act.  M == 0 is a no-op.
  * prq_gemm_packed -- prq_gemm on a packed activation (the LDS-tiled kernel):
  *   Y [M, N] float32 = Eq. 3 over K_aug; Ap / Aps from prq_quant_act_packed,
- *   Wp / Wps from prq_pack_weight (E = 1).  No workspace.  Limits as prq_gemm.
+ *   Wp / Wps from prq_pack_weight (E = 1).  workspace: at least
+ *   prq_gemm_packed_workspace_bytes(M, N, K_aug) bytes, 16-byte aligned, for
+ *   the split along K that the planner picks when few output tiles would
+ *   leave CUs idle (splits - 1 partial sums [M][N], rewritten before being
+ *   read, added to Y in a fixed order by a second kernel; no zero-fill
+ *   needed); with less (or NULL) the call runs unsplit.  Calls sharing a
+ *   workspace must be ordered.  Limits as prq_gemm.
  * prq_grouped_gemm_packed -- prq_grouped_gemm on a packed activation (rows
  *   sorted by expert, from prq_quant_act_packed with G = E and the same
  *   offsets).  An expert's row tiles start on its first 16-row block; rows of
@@ -249,9 +257,10 @@ int prq_quant_act_packed(const void* X_bf16, int64_t ld_x, int32_t M, int32_t K,
                          const float* inv_scale_pos, const int32_t* perm,
                          const int32_t* group_offsets, int32_t G,
                          uint8_t* Ap, uint8_t* Aps, hipStream_t stream);
+size_t prq_gemm_packed_workspace_bytes(int32_t M, int32_t N, int32_t K_aug);
 int prq_gemm_packed(const uint8_t* Ap, const uint8_t* Aps, int32_t M,
                     const uint8_t* Wp, const uint8_t* Wps, int32_t N, int32_t K_aug,
-                    float* Y, hipStream_t stream);
+                    float* Y, void* workspace, size_t workspace_bytes, hipStream_t stream);
 int prq_grouped_gemm_packed(const uint8_t* Ap, const uint8_t* Aps,
                             const int32_t* group_offsets, int32_t E, int32_t M_total,
                             const uint8_t* Wp, const uint8_t* Wps, int32_t N, int32_t K_aug,

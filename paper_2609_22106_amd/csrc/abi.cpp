@@ -174,6 +174,7 @@ size_t prq_gemm_workspace_bytes_ex(int32_t M, int32_t N, int32_t K_aug, int32_t 
                                    int32_t splits) {
   if (M <= 0 || N <= 0 || K_aug <= 0 || N % 16 || K_aug % PRQ_BLOCK || splits < 0) return 0;
   if (variant == PRQ_GEMM_AUTO) variant = prq::choose_variant(M, N, K_aug);
+  if (variant == PRQ_GEMM_TILE) return prq::tile_workspace_bytes(M, N, K_aug, false, device_cus());
   if (variant != PRQ_GEMM_STREAM) return 0;
   if (splits <= 1 && prq::choose_decode_config(M, N, K_aug, 0, 0, 0, device_cus()).ok) return 0;
   const prq::StreamConfig c = dense_stream_config(M, N, K_aug, splits, device_cus());
@@ -216,7 +217,8 @@ int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t*
     }
   }
   return launch_status(prq::launch_gemm_tile_planned(Aq, Asc, M, Wp, Wps, N, K_aug, Y, false,
-                                                     dev.num_cus, stream));
+                                                     dev.num_cus, workspace, workspace_bytes,
+                                                     stream));
 }
 
 int prq_gemm(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t* Wp,
@@ -258,8 +260,14 @@ int prq_quant_act_packed(const void* X_bf16, int64_t ld_x, int32_t M, int32_t K,
                                                     G, Ap, Aps, dev.num_cus, stream));
 }
 
+size_t prq_gemm_packed_workspace_bytes(int32_t M, int32_t N, int32_t K_aug) {
+  if (M <= 0 || N <= 0 || K_aug <= 0 || N % 16 || K_aug % PRQ_BLOCK || K_aug > kMaxKAug) return 0;
+  return prq::tile_workspace_bytes(M, N, K_aug, true, device_cus());
+}
+
 int prq_gemm_packed(const uint8_t* Ap, const uint8_t* Aps, int32_t M, const uint8_t* Wp,
-                    const uint8_t* Wps, int32_t N, int32_t K_aug, float* Y, hipStream_t stream) {
+                    const uint8_t* Wps, int32_t N, int32_t K_aug, float* Y, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream) {
   int st = check_gemm_common(Ap, Aps, M, Wp, Wps, N, K_aug, Y);
   if (st != PRQ_OK) return st;
   if (M == 0) return PRQ_OK;
@@ -268,7 +276,8 @@ int prq_gemm_packed(const uint8_t* Ap, const uint8_t* Aps, int32_t M, const uint
   st = current_device(&dev);
   if (st != PRQ_OK) return st;
   return launch_status(prq::launch_gemm_tile_planned(Ap, Aps, M, Wp, Wps, N, K_aug, Y, true,
-                                                     dev.num_cus, stream));
+                                                     dev.num_cus, workspace, workspace_bytes,
+                                                     stream));
 }
 
 int prq_grouped_gemm_packed(const uint8_t* Ap, const uint8_t* Aps, const int32_t* group_offsets,

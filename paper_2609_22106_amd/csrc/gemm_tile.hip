@@ -172,7 +172,8 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
     const uint8_t* __restrict__ Aq, const uint8_t* __restrict__ Asc, int M,
     const int32_t* __restrict__ off, int E, int n_mtiles, int tile_base, int region_tiles,
     const uint8_t* __restrict__ Wp,
-    const uint8_t* __restrict__ Wps, int N, int K_aug, float* __restrict__ Y) {
+    const uint8_t* __restrict__ Wps, int N, int K_aug, float* __restrict__ Y, int splits,
+    int split_steps, float* __restrict__ ws) {
   using L = TileStage<kBM, kBN, kAMode>;
   constexpr bool kScaleDword = kAMode == kARowDword;
   constexpr bool kPackedA = kAMode == kAPacked;
@@ -217,9 +218,14 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
 
   const int ntiles = N >> 4;
   const int n_ntiles = (region_tiles + kBBlk - 1) / kBBlk;   // column tiles of the region
-  const int total = n_mtiles * n_ntiles;
-  const int logical = xcd_remap(blockIdx.x, total);
-  const int mt = logical / n_ntiles, nt = logical % n_ntiles;
+  // Split-K: workgroup id = split * tiles + tile; split p takes K steps
+  // [p * split_steps, (p + 1) * split_steps) (the host makes every range
+  // non-empty) and writes its partial sum to Y (p = 0) or ws[p - 1].
+  const int n_tiles = n_mtiles * n_ntiles;
+  const int logical = xcd_remap(blockIdx.x, n_tiles * splits);
+  const int split = logical / n_tiles;
+  const int tl = logical - split * n_tiles;
+  const int mt = tl / n_ntiles, nt = tl % n_ntiles;
 
   int e = 0, row_begin, row_lo, row_end;
   if (kGrouped) {
@@ -238,6 +244,8 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   const int nb = K_aug >> 5;
   const int steps = (K_aug + kStepK - 1) / kStepK;
   const int sgroups = (steps + 3) >> 2;
+  const int s_lo = split * split_steps;
+  const int s_hi = min(steps, s_lo + split_steps);
   const int nblk = (M + 15) >> 4;                    // packed activation row blocks
   const uint8_t* We = Wp + static_cast<int64_t>(e) * ntiles * steps * 1024;
   const uint8_t* Wse = Wps + static_cast<int64_t>(e) * ntiles * sgroups * 256;
@@ -403,7 +411,7 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   // it drains every load first).  Scheduling barriers keep each wait and
   // barrier between the MFMAs it separates.
   static_for<kNS>([&](auto pc) {
-    issue(min(static_cast<int>(decltype(pc)::value), steps - 1), stage(pc));
+    issue(min(s_lo + static_cast<int>(decltype(pc)::value), s_hi - 1), stage(pc));
   });
   wait_vmcnt<(kNS - 1) * kLoads>();
   __builtin_amdgcn_s_barrier();
@@ -413,7 +421,7 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
     constexpr int p = decltype(pc)::value;
     constexpr bool kGuard = decltype(gc)::value;
     const int s = s0 + p;
-    const bool live = !kGuard || s < steps;
+    const bool live = !kGuard || s < s_hi;
     __builtin_amdgcn_sched_barrier(0);
     if (live) mfma(h0, IntC<0>{}, s);
     read(stage(pc), IntC<1>{}, h1);
@@ -422,7 +430,7 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
     wait_vmcnt<(kNS - 2) * kLoads>();
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    issue(min(s + kNS, steps - 1), stage(pc));
+    issue(min(s + kNS, s_hi - 1), stage(pc));
     if (live) mfma(h1, IntC<1>{}, s);
     read(stage(IntC<p + 1>{}), IntC<0>{}, h0);
     if constexpr (!kGuard) interleave<kMfmas / 2, kLoads, kReads / 2>();
@@ -430,14 +438,15 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   };
   // Whole groups of kU steps without guards (so the scheduler can interleave
   // the LDS reads with the MFMAs), then one guarded group for the rest.
-  int s0 = 0;
-  for (; s0 + kU <= steps; s0 += kU)
+  int s0 = s_lo;
+  for (; s0 + kU <= s_hi; s0 += kU)
     static_for<kU>([&](auto pc) { body(s0, pc, IntC<0>{}); });
-  if (s0 < steps) static_for<kU>([&](auto pc) { body(s0, pc, IntC<1>{}); });
+  if (s0 < s_hi) static_for<kU>([&](auto pc) { body(s0, pc, IntC<1>{}); });
   wait_vmcnt<0>();   // no direct-to-LDS write outlives the workgroup
 
   // Element q of a lane's fragment is C[8 (q / 4) + 4 (l / 32) + q % 4][l % 32]:
   // activation row, feature column (32 lanes store 128 contiguous bytes).
+  float* const dst = split == 0 ? Y : ws + static_cast<int64_t>(split - 1) * M * N;
 #pragma unroll
   for (int i = 0; i < kFM; ++i)
 #pragma unroll
@@ -446,15 +455,34 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const int m = row_begin + wm * kTM + i * 32 + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
-        if (m >= row_lo && m < row_end && n < n_end) Y[static_cast<int64_t>(m) * N + n] = acc[i][j][q];
+        if (m >= row_lo && m < row_end && n < n_end) dst[static_cast<int64_t>(m) * N + n] = acc[i][j][q];
       }
     }
+}
+
+// Split-K sum: Y[i] = ((Y[i] + P_0[i]) + P_1[i]) + ... over `parts` partial
+// arrays of n4 float4 each, in that fixed order.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(float4* __restrict__ Y,
+                                                          const float4* __restrict__ P,
+                                                          int64_t n4, int parts) {
+  for (int64_t i = blockIdx.x * 256 + threadIdx.x; i < n4; i += static_cast<int64_t>(gridDim.x) * 256) {
+    float4 v = Y[i];
+    for (int p = 0; p < parts; ++p) {
+      const float4 w = P[p * n4 + i];
+      v.x += w.x;
+      v.y += w.y;
+      v.z += w.z;
+      v.w += w.w;
+    }
+    Y[i] = v;
+  }
 }
 
 template <int kBM, int kBN, int kWM, int kWN, int kNS, int kAMode>
 hipError_t launch_shape_scales(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off,
                                int E, const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug,
-                               float* Y, int tile_base, int region_tiles, hipStream_t stream) {
+                               float* Y, int tile_base, int region_tiles, int splits, float* ws,
+                               hipStream_t stream) {
   // The kernel addresses A and one expert's weight with 32-bit byte offsets.
   const int64_t steps = (K_aug + kStepK - 1) / kStepK;
   if (static_cast<int64_t>((M + 15) / 16) * steps * 1024 >= (int64_t{1} << 31) ||
@@ -469,14 +497,33 @@ hipError_t launch_shape_scales(const uint8_t* Aq, const uint8_t* Asc, int M, con
   const int64_t lead = kAMode == kAPacked ? 15 : 0;
   const int n_mtiles = off ? static_cast<int>((M + static_cast<int64_t>(E) * (kBM - 1 + lead)) / kBM)
                            : (M + kBM - 1) / kBM;
-  const int grid = n_mtiles * n_ntiles;
+  // Split-K (dense, whole-width calls only): every split a non-empty K range.
+  int split_steps = static_cast<int>(steps);
+  if (splits > 1) {
+    if (off || !ws || tile_base != 0 || region_tiles != N / 16) return hipErrorInvalidValue;
+    split_steps = static_cast<int>((steps + splits - 1) / splits);
+    splits = static_cast<int>((steps + split_steps - 1) / split_steps);
+  } else {
+    splits = 1;
+  }
+  const int grid = n_mtiles * n_ntiles * splits;
   if (off) {
     gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, true, kAMode><<<grid, kWM * kWN * 64, 0, stream>>>(
-        Aq, Asc, M, off, E, n_mtiles, tile_base, region_tiles, Wp, Wps, N, K_aug, Y);
+        Aq, Asc, M, off, E, n_mtiles, tile_base, region_tiles, Wp, Wps, N, K_aug, Y, 1,
+        split_steps, nullptr);
   } else {
     gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, false, kAMode><<<grid, kWM * kWN * 64, 0, stream>>>(
-        Aq, Asc, M, nullptr, 1, n_mtiles, tile_base, region_tiles, Wp, Wps, N, K_aug, Y);
+        Aq, Asc, M, nullptr, 1, n_mtiles, tile_base, region_tiles, Wp, Wps, N, K_aug, Y, splits,
+        split_steps, ws);
   }
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess || splits == 1) return err;
+  // Y += ws[0] + ws[1] + ... in that order (deterministic).
+  const int64_t n4 = static_cast<int64_t>(M) * N / 4;
+  const int blocks = static_cast<int>(std::min<int64_t>((n4 + 255) / 256, 2048));
+  splitk_reduce_kernel<<<blocks, 256, 0, stream>>>(reinterpret_cast<float4*>(Y),
+                                                    reinterpret_cast<const float4*>(ws), n4,
+                                                    splits - 1);
   return hipGetLastError();
 }
 
@@ -486,26 +533,29 @@ hipError_t launch_shape_scales(const uint8_t* Aq, const uint8_t* Asc, int M, con
 template <int kBM, int kBN, int kWM, int kWN, int kNSDword, int kNSByte>
 hipError_t launch_shape(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off, int E,
                         const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug, float* Y,
-                        bool packed, int tile_base, int region_tiles, hipStream_t stream) {
+                        bool packed, int tile_base, int region_tiles, int splits, float* ws,
+                        hipStream_t stream) {
   if (packed)
     return launch_shape_scales<kBM, kBN, kWM, kWN, kNSDword, kAPacked>(
-        Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, tile_base, region_tiles, stream);
+        Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, tile_base, region_tiles, splits, ws, stream);
   if (K_aug % 128 == 0 && (reinterpret_cast<uintptr_t>(Asc) & 3u) == 0)
     return launch_shape_scales<kBM, kBN, kWM, kWN, kNSDword, kARowDword>(
-        Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, tile_base, region_tiles, stream);
+        Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, tile_base, region_tiles, splits, ws, stream);
   return launch_shape_scales<kBM, kBN, kWM, kWN, kNSByte, kARowByte>(
-      Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, tile_base, region_tiles, stream);
+      Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, tile_base, region_tiles, splits, ws, stream);
 }
 
-// Columns [16 tile_base, 16 (tile_base + region_tiles)) of Y with one tile shape.
+// Columns [16 tile_base, 16 (tile_base + region_tiles)) of Y with one tile shape
+// (split along K into `splits` ranges when > 1: whole-width dense calls, ws of
+// (splits - 1) * M * N floats).
 hipError_t launch_region(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off, int E,
                          const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug, float* Y,
                          int shape, bool packed, int tile_base, int region_tiles,
-                         hipStream_t stream) {
+                         hipStream_t stream, int splits = 1, float* ws = nullptr) {
   switch (shape) {
-    case 0: return launch_shape<256, 256, 2, 2, 4, 3>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, tile_base, region_tiles, stream);
-    case 1: return launch_shape<256, 128, 2, 2, 4, 4>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, tile_base, region_tiles, stream);
-    default: return launch_shape<128, 128, 2, 2, 4, 4>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, tile_base, region_tiles, stream);
+    case 0: return launch_shape<256, 256, 2, 2, 4, 3>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, tile_base, region_tiles, splits, ws, stream);
+    case 1: return launch_shape<256, 128, 2, 2, 4, 4>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, tile_base, region_tiles, splits, ws, stream);
+    default: return launch_shape<128, 128, 2, 2, 4, 4>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, tile_base, region_tiles, splits, ws, stream);
   }
 }
 
@@ -516,46 +566,64 @@ struct Shape {
 constexpr Shape kShapes[] = {{0, 256, 256, 1.0, 1.0}, {1, 256, 128, 0.63, 0.83},
                              {2, 128, 128, 0.5, 0.67}};
 
-// Plan of a dense tile GEMM: one shape over all N columns, or a main region of
-// whole column tiles in one shape and the remaining columns in another, so
-// that each launch fills the CUs in whole rounds (M = 8192, N = 2560: 256
-// tiles of 256 x 256 over 2048 columns, then 256 tiles of 128 x 128).  Cost =
-// workgroup rounds x tile area / measured throughput factor, plus a fixed cost
-// for a second launch.
+// Plan of a dense tile GEMM: one shape over all N columns (optionally split
+// along K), or a main region of whole column tiles in one shape and the
+// remaining columns in another, so that each launch fills the CUs in whole
+// rounds (M = 8192, N = 2560: 256 tiles of 256 x 256 over 2048 columns, then
+// 256 tiles of 128 x 128).  Modelled time: workgroup rounds x (K steps per
+// workgroup + a fixed pipeline fill and store cost) x the shape's measured
+// time per step, plus a fixed cost for a second launch, or for split-K the
+// reduction (a launch plus the partial sums written, read and added).
 struct TilePlan {
   int shape[2] = {2, 2};
   int tiles[2] = {0, 0};   // 16-column tiles of each region
   int parts = 1;
+  int splits = 1;          // K ranges (single region only)
 };
 
-TilePlan plan_tile_gemm(int M, int N, int K_aug, int num_cus, bool packed) {
+constexpr double kStepUs256 = 0.9;      // one K step of a 256 x 256 tile in a full round
+constexpr double kFillSteps = 3.0;      // pipeline fill, drain and Y store, in steps
+constexpr double kLaunchUs = 3.0;       // a second launch
+constexpr double kReduceBytesPerUs = 5.0e6;
+
+TilePlan plan_tile_gemm(int M, int N, int K_aug, int num_cus, bool packed, bool allow_split) {
   const int cus = std::max(num_cus, 1);
   const int ntiles = N / 16;
-  auto cost = [&](const Shape& s, int cols16) {
+  const int steps = (K_aug + kStepK - 1) / kStepK;
+  auto cost = [&](const Shape& s, int cols16, int splits) {
     if (cols16 <= 0) return 0.0;
     const long tiles = static_cast<long>((M + s.bm - 1) / s.bm) * ((cols16 * 16 + s.bn - 1) / s.bn);
-    const long rounds = (tiles + cus - 1) / cus;
-    return rounds * static_cast<double>(s.bm) * s.bn / (packed ? s.eff_packed : s.eff_rows);
+    const int per = (steps + splits - 1) / splits;
+    const long rounds = (tiles * ((steps + per - 1) / per) + cus - 1) / cus;
+    const double step_us =
+        kStepUs256 * s.bm * s.bn / 65536.0 / (packed ? s.eff_packed : s.eff_rows);
+    double c = rounds * (per + kFillSteps) * step_us;
+    if (splits > 1)   // partials written, then Y and the partials read and Y written
+      c += kLaunchUs + 2.0 * ((steps + per - 1) / per) * 4.0 * M * N / kReduceBytesPerUs;
+    return c;
   };
-  // A second launch costs ~3 us; a 256 x 256 tile at K + k = 9984 ~70 us.
-  const double launch_cost = 65536.0 * (3.0 / 70.0) * (9984.0 / std::max(K_aug, 128));
   TilePlan best;
   double best_cost = 1e300;
-  for (const Shape& s : kShapes) {
-    const double c = cost(s, ntiles);
-    if (c < best_cost) {
-      best_cost = c;
-      best = TilePlan{};
-      best.shape[0] = s.id;
-      best.tiles[0] = ntiles;
+  static const int kSplits[] = {1, 2, 3, 4, 6, 8};
+  for (const Shape& s : kShapes)
+    for (int sp : kSplits) {
+      if (sp > 1 && (!allow_split || sp > steps)) break;
+      const double c = cost(s, ntiles, sp);
+      if (c < best_cost) {
+        best_cost = c;
+        best = TilePlan{};
+        best.shape[0] = s.id;
+        best.tiles[0] = ntiles;
+        best.splits = sp;
+      }
     }
-  }
   for (const Shape& a : kShapes)
     for (int main16 = a.bn / 16; main16 < ntiles; main16 += a.bn / 16)
       for (const Shape& b : kShapes) {
-        const double c = cost(a, main16) + cost(b, ntiles - main16) + launch_cost;
+        const double c = cost(a, main16, 1) + cost(b, ntiles - main16, 1) + kLaunchUs;
         if (c < best_cost) {
           best_cost = c;
+          best = TilePlan{};
           best.shape[0] = a.id;
           best.shape[1] = b.id;
           best.tiles[0] = main16;
@@ -563,16 +631,21 @@ TilePlan plan_tile_gemm(int M, int N, int K_aug, int num_cus, bool packed) {
           best.parts = 2;
         }
       }
+  if (best.splits > 1) {   // the launcher's normalisation: every range non-empty
+    const int per = (steps + best.splits - 1) / best.splits;
+    best.splits = (steps + per - 1) / per;
+  }
   return best;
 }
 
 hipError_t launch_plan(const uint8_t* Aq, const uint8_t* Asc, int M, const uint8_t* Wp,
                        const uint8_t* Wps, int N, int K_aug, float* Y, bool packed,
-                       const TilePlan& plan, hipStream_t stream) {
+                       const TilePlan& plan, float* ws, hipStream_t stream) {
   int base = 0;
   for (int p = 0; p < plan.parts; ++p) {
     const hipError_t e = launch_region(Aq, Asc, M, nullptr, 1, Wp, Wps, N, K_aug, Y,
-                                       plan.shape[p], packed, base, plan.tiles[p], stream);
+                                       plan.shape[p], packed, base, plan.tiles[p], stream,
+                                       plan.splits, ws);
     if (e != hipSuccess) return e;
     base += plan.tiles[p];
   }
@@ -631,11 +704,31 @@ hipError_t launch_grouped_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps
                        N / 16, stream);
 }
 
+size_t tile_workspace_bytes(int M, int N, int K_aug, bool packed, int num_cus) {
+  const TilePlan plan = plan_tile_gemm(M, N, K_aug, num_cus, packed, true);
+  return plan.splits > 1 ? static_cast<size_t>(plan.splits - 1) * M * N * sizeof(float) : 0;
+}
+
 hipError_t launch_gemm_tile_planned(const uint8_t* Aq, const uint8_t* Asc, int M,
                                     const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug,
-                                    float* Y, bool packed, int num_cus, hipStream_t stream) {
+                                    float* Y, bool packed, int num_cus, void* workspace,
+                                    size_t workspace_bytes, hipStream_t stream) {
+  // Split-K only with room for its partial sums and 16-byte aligned Y and
+  // workspace (the reduction moves float4s); otherwise the best plan without.
+  const bool aligned = (reinterpret_cast<uintptr_t>(Y) & 15u) == 0 &&
+                       (reinterpret_cast<uintptr_t>(workspace) & 15u) == 0;
+  const size_t need = tile_workspace_bytes(M, N, K_aug, packed, num_cus);
+  const bool split = workspace && aligned && need > 0 && workspace_bytes >= need;
   return launch_plan(Aq, Asc, M, Wp, Wps, N, K_aug, Y, packed,
-                     plan_tile_gemm(M, N, K_aug, num_cus, packed), stream);
+                     plan_tile_gemm(M, N, K_aug, num_cus, packed, split),
+                     static_cast<float*>(workspace), stream);
+}
+
+hipError_t launch_gemm_tile_split(const uint8_t* Aq, const uint8_t* Asc, int M, const uint8_t* Wp,
+                                  const uint8_t* Wps, int N, int K_aug, float* Y, bool packed,
+                                  int shape, int splits, float* ws, hipStream_t stream) {
+  return launch_region(Aq, Asc, M, nullptr, 1, Wp, Wps, N, K_aug, Y, shape, packed, 0, N / 16,
+                       stream, splits, ws);
 }
 
 }  // namespace prq

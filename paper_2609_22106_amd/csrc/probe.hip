@@ -331,6 +331,23 @@ int prq_tune_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M, cons
              : -3;
 }
 
+// The dense tile GEMM with a forced shape and split count along K (packed or
+// row-major activation); ws: (splits - 1) * M * N floats (ws_bytes checked),
+// 16-byte aligned.
+int prq_tune_gemm_tile_split(const uint8_t* A, const uint8_t* As, int M, const uint8_t* Wp,
+                             const uint8_t* Wps, int N, int K_aug, float* Y, int shape,
+                             int splits, int packed, float* ws, size_t ws_bytes,
+                             hipStream_t stream) {
+  if (shape < 0 || shape > 2 || N % 16 || K_aug % 32 || M <= 0 || splits < 1) return -1;
+  if (splits > 1 &&
+      (!ws || static_cast<size_t>(splits - 1) * M * N * sizeof(float) > ws_bytes))
+    return -2;   // the partial sums would not fit
+  return prq::launch_gemm_tile_split(A, As, M, Wp, Wps, N, K_aug, Y, packed != 0, shape, splits,
+                                     ws, stream) == hipSuccess
+             ? 0
+             : -3;
+}
+
 // The grouped tile GEMM on a packed activation with a forced shape.
 int prq_tune_grouped_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M,
                                       const int32_t* off, int E, const uint8_t* Wp,

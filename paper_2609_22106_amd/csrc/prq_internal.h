@@ -75,10 +75,18 @@ hipError_t launch_gemm_tile(const uint8_t* Aq, const uint8_t* Asc, int M,
                             hipStream_t stream);
 // Dense tile GEMM over all columns with the planned shapes (one launch, or a
 // main column region and the rest in another shape, each filling the CUs in
-// whole rounds).
+// whole rounds, or one shape split along K with a deterministic reduction when
+// the workspace holds tile_workspace_bytes).
+size_t tile_workspace_bytes(int M, int N, int K_aug, bool packed, int num_cus);
 hipError_t launch_gemm_tile_planned(const uint8_t* Aq, const uint8_t* Asc, int M,
                                     const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug,
-                                    float* Y, bool packed, int num_cus, hipStream_t stream);
+                                    float* Y, bool packed, int num_cus, void* workspace,
+                                    size_t workspace_bytes, hipStream_t stream);
+// One shape, `splits` K ranges (ws: (splits - 1) * M * N floats, 16-byte
+// aligned like Y); the tuning entry.
+hipError_t launch_gemm_tile_split(const uint8_t* Aq, const uint8_t* Asc, int M, const uint8_t* Wp,
+                                  const uint8_t* Wps, int N, int K_aug, float* Y, bool packed,
+                                  int shape, int splits, float* ws, hipStream_t stream);
 // The grouped (MoE) tile GEMM on a packed activation: an expert's row tiles
 // start on 16-row block boundaries (rows of neighbouring experts are masked).
 hipError_t launch_grouped_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M_total,

@@ -67,7 +67,9 @@ _packed_act_bytes = _decl("prq_packed_act_bytes", ctypes.c_int,
                           [_i32, _i32, ctypes.POINTER(_sz), ctypes.POINTER(_sz)])
 _quant_act_packed = _decl("prq_quant_act_packed", ctypes.c_int,
                           [_p, _i64, _i32, _i32, _i32, _p, _p, _p, _i32, _p, _p, _p])
-_gemm_packed = _decl("prq_gemm_packed", ctypes.c_int, [_p, _p, _i32, _p, _p, _i32, _i32, _p, _p])
+_gemm_packed_ws = _decl("prq_gemm_packed_workspace_bytes", _sz, [_i32, _i32, _i32])
+_gemm_packed = _decl("prq_gemm_packed", ctypes.c_int,
+                     [_p, _p, _i32, _p, _p, _i32, _i32, _p, _p, _sz, _p])
 _ggemm_packed = _decl("prq_grouped_gemm_packed", ctypes.c_int,
                       [_p, _p, _p, _i32, _i32, _p, _p, _i32, _i32, _p, _p])
 _ggemm_ws = _decl("prq_grouped_gemm_workspace_bytes", _sz, [_i32, _i32, _i32, _i32])
@@ -393,8 +395,14 @@ def prq_quant_act_packed(X, K, k_tail, inv_scale_pos=None, perm=None, out=None, 
     return out
 
 
-def prq_gemm_packed(A, W, Y=None, stream=None):
-    """Y [M, N] float32 = Eq. 3 over K_aug for a PackedAct A and a PackedWeight W (E = 1)."""
+def prq_gemm_packed_workspace_bytes(M, N, K_aug):
+    return int(_gemm_packed_ws(M, N, K_aug))
+
+
+def prq_gemm_packed(A, W, Y=None, workspace=None, stream=None):
+    """Y [M, N] float32 = Eq. 3 over K_aug for a PackedAct A and a PackedWeight W (E = 1).
+    workspace: uint8 device tensor of prq_gemm_packed_workspace_bytes (split along
+    K when the planner wants it; without it the call runs unsplit)."""
     if W.E != 1:
         raise ValueError("prq_gemm_packed takes a single weight (E = 1)")
     if A.K_aug != W.K_aug:
@@ -406,8 +414,12 @@ def prq_gemm_packed(A, W, Y=None, stream=None):
     A.check_sizes()
     W.check_sizes()
     _on_gpu(Ap=A.Ap, Aps=A.Aps, Y=Y, Wp=W.Wp, Wps=W.Wps)
+    if workspace is not None:
+        _need(workspace, "workspace", torch.uint8)
+        _on_gpu(workspace=workspace)
+    ws_bytes = workspace.numel() if workspace is not None else 0
     st = _gemm_packed(_ptr(A.Ap), _ptr(A.Aps), M, _ptr(W.Wp), _ptr(W.Wps), N, W.K_aug, _ptr(Y),
-                      _stream(stream))
+                      _ptr(workspace), ws_bytes, _stream(stream))
     _check(st, "prq_gemm_packed")
     return Y
 

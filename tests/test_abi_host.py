@@ -166,10 +166,10 @@ def test_packed_activation_calls_validate_before_touching_the_gpu():
     assert prq._quant_act_packed(fake, 1024, 4, 1024, 64, None, None, None, 1, None, fake, s) == prq.PRQ_EINVAL
     assert prq._quant_act_packed(fake, 1000, 4, 1024, 64, None, None, None, 1, fake, fake, s) == prq.PRQ_EINVAL
     assert prq._quant_act_packed(None, 1024, 0, 1024, 64, None, None, None, 1, None, None, s) == prq.PRQ_OK
-    assert prq._gemm_packed(fake, fake, 4, fake, fake, 24, 1088, fake, s) == prq.PRQ_EALIGN   # N % 16
-    assert prq._gemm_packed(fake, odd, 4, fake, fake, 32, 1088, fake, s) == prq.PRQ_EALIGN    # Aps
-    assert prq._gemm_packed(fake, fake, 4, fake, odd, 32, 1088, fake, s) == prq.PRQ_EALIGN    # Wps
-    assert prq._gemm_packed(None, None, 0, fake, fake, 32, 1088, None, s) == prq.PRQ_OK
+    assert prq._gemm_packed(fake, fake, 4, fake, fake, 24, 1088, fake, None, 0, s) == prq.PRQ_EALIGN   # N % 16
+    assert prq._gemm_packed(fake, odd, 4, fake, fake, 32, 1088, fake, None, 0, s) == prq.PRQ_EALIGN    # Aps
+    assert prq._gemm_packed(fake, fake, 4, fake, odd, 32, 1088, fake, None, 0, s) == prq.PRQ_EALIGN    # Wps
+    assert prq._gemm_packed(None, None, 0, fake, fake, 32, 1088, None, None, 0, s) == prq.PRQ_OK
     # grouped: G > 1 needs offsets; E >= 1 with offsets; Aps alignment
     assert prq._quant_act_packed(fake, 1024, 4, 1024, 64, None, None, None, 3, fake, fake, s) == prq.PRQ_EINVAL
     assert prq._quant_act_packed(fake, 1024, 4, 1024, 64, None, None, fake, 0, fake, fake, s) == prq.PRQ_EINVAL
@@ -208,7 +208,15 @@ def test_reference_packer_is_a_padded_permutation():
 
 
 def test_workspace_sizes():
-    assert prq.prq_gemm_workspace_bytes(64, 2560, 9984, prq.GEMM_TILE) == 0
+    # the LDS-tiled kernel splits along K when its tiles would leave CUs idle:
+    # splits - 1 partial sums of M x N floats; a full round of tiles is unsplit
+    ws = prq.prq_gemm_workspace_bytes(64, 2560, 9984, prq.GEMM_TILE)
+    assert ws > 0 and ws % (64 * 2560 * 4) == 0
+    assert prq.prq_gemm_workspace_bytes(8192, 2560, 9984, prq.GEMM_TILE) == 0
+    ws = prq.prq_gemm_packed_workspace_bytes(512, 2560, 9984)
+    assert ws > 0 and ws % (512 * 2560 * 4) == 0
+    assert prq.prq_gemm_packed_workspace_bytes(8192, 2560, 9984) == 0
+    assert prq.prq_gemm_packed_workspace_bytes(512, 2560, 9980) == 0     # invalid K_aug
     assert prq.prq_gemm_workspace_bytes(64, 2560, 9984, prq.GEMM_STREAM, 1) == 0
     ws = prq.prq_gemm_workspace_bytes(64, 2560, 9984, prq.GEMM_STREAM, 4)
     assert ws >= 64 * 2560 * 4 + (2560 // 16) * 4     # float accumulator + arrival counters

@@ -104,7 +104,8 @@ def test_gemm_packed(shape, M, N, K_aug):
 @pytest.mark.parametrize("M", [512, 2048, 8192])
 def test_packed_pair_down_proj(M):
     """X -> prq_quant_act_packed -> prq_gemm_packed on the down_proj shape
-    (K = 9728, k = 256, N = 2560), against the oracle on 48 sampled rows."""
+    (K = 9728, k = 256, N = 2560), against the oracle on 48 sampled rows; with
+    the planner's workspace (split along K where it picks it) and without."""
     prq = _prq()
     rng = np.random.default_rng(M)
     K, k, N = 9728, 256, 2560
@@ -116,10 +117,15 @@ def test_packed_pair_down_proj(M):
     W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
     say("packed pair case:", M)
     A = prq.prq_quant_act_packed(dev(X), K, k, dev(_pos(inv, perm)), dev(perm))
-    Y = host(prq.prq_gemm_packed(A, W))
+    ws_n = prq.prq_gemm_packed_workspace_bytes(M, N, K + k)
+    ws = torch.empty(ws_n, dtype=torch.uint8, device="cuda") if ws_n else None
+    Y = host(prq.prq_gemm_packed(A, W, workspace=ws))
+    Y0 = host(prq.prq_gemm_packed(A, W))
     rows = np.sort(rng.choice(M, 48, replace=False))
     rq, rs = pq.quant_act(X[rows], inv, perm, k)
-    assert_gemm_close(Y[rows], pq.gemm(rq, rs, Wq, Wsc), f"packed pair M={M}")
+    Yo = pq.gemm(rq, rs, Wq, Wsc)
+    assert_gemm_close(Y[rows], Yo, f"packed pair M={M} workspace {ws_n}")
+    assert_gemm_close(Y0[rows], Yo, f"packed pair M={M} without workspace")
 
 
 @pytest.mark.parametrize("packed", [True, False])

@@ -83,3 +83,53 @@ def test_tile_shape_grouped(shape, counts, N, K_aug):
     Y = _run(shape, Aq, Asc, Wq, Wsc, off=off, E=E)
     assert_gemm_close(Y, pq.grouped_gemm(Aq, Asc, off, Wq, Wsc),
                       f"grouped shape {shape} {counts} {N}x{K_aug}")
+
+
+def _split_lib():
+    from paper_2609_22106_amd import build, prq  # noqa: F401
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    P, I = ctypes.c_void_p, ctypes.c_int
+    lib.prq_tune_gemm_tile_split.argtypes = [P, P, I, P, P, I, I, P, I, I, I, P, ctypes.c_size_t,
+                                             P]
+    lib.prq_tune_gemm_tile_split.restype = I
+    return lib
+
+
+# (M, N, K_aug, splits): split ranges of unequal length, more splits than
+# whole 4-step groups, a last range of one step, ragged rows and features.
+SPLIT = [(300, 272, 1024, 3),      # 8 steps -> 3 + 3 + 2
+         (513, 144, 9984, 8),      # 78 steps -> 10 x 7 + 8
+         (40, 512, 4192, 4),       # 33 steps -> 9 + 9 + 9 + 6 (byte scales when row-major)
+         (129, 64, 1152, 9),       # 9 steps -> one step each
+         (64, 256, 640, 2)]        # 5 steps -> 3 + 2
+
+
+@pytest.mark.parametrize("M,N,K_aug,splits", SPLIT)
+@pytest.mark.parametrize("packed", [True, False])
+@pytest.mark.parametrize("shape", SHAPE_IDS)
+def test_tile_split_k(shape, packed, M, N, K_aug, splits):
+    """The tile GEMM split along K (partial sums in the workspace, added to Y in
+    a fixed order by the reduction): within the tolerance of the oracle, and
+    bit-identical over two calls (deterministic)."""
+    from paper_2609_22106_amd import prq
+    from tests.packing import pack_rows
+    rng = np.random.default_rng(M * 3 + N + K_aug + splits)
+    Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+    Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
+    W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
+    A, As = (map(dev, pack_rows(Aq, Asc)) if packed else (dev(Aq), dev(Asc)))
+    ws = torch.full((max(splits - 1, 1) * M * N,), float("nan"), dtype=torch.float32, device="cuda")
+    outs = []
+    for _ in range(2):
+        Y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        say("tile split case:", shape, packed, M, N, K_aug, splits)
+        rc = _split_lib().prq_tune_gemm_tile_split(
+            A.data_ptr(), As.data_ptr(), M, W.Wp.data_ptr(), W.Wps.data_ptr(), N, K_aug,
+            Y.data_ptr(), shape, splits, int(packed), ws.data_ptr(), ws.numel() * 4,
+            torch.cuda.current_stream().cuda_stream)
+        assert rc == 0, rc
+        torch.cuda.synchronize()
+        outs.append(host(Y))
+    np.testing.assert_array_equal(outs[0], outs[1])
+    assert_gemm_close(outs[0], pq.gemm(Aq, Asc, Wq, Wsc),
+                      f"split shape {shape} packed {packed} {M}x{N}x{K_aug} / {splits}")
