@@ -528,7 +528,7 @@ def traffic_from_counters(workload, fetch_dir, write_dir, command):
         calib = [v for n, v in rows if "neg_kernel" in n]
         gemm = [(n, v) for n, v in rows if "prq" in n and any(
             t in n for t in ("gemm_decode_kernel", "gemm_stream_kernel", "gemm_tile_kernel",
-                             "reduce_partials_kernel", "zero_kernel"))]
+                             "reduce_partials_kernel", "zero_kernel", "splitk_reduce_kernel"))]
         launches = [v for n, v in gemm if "gemm_" in n]
         if not calib or not launches:
             raise SystemExit(f"{counter}: calibration or GEMM dispatches missing in {run_dir}")

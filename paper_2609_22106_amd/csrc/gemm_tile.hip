@@ -221,8 +221,14 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   // Split-K: workgroup id = split * tiles + tile; split p takes K steps
   // [p * split_steps, (p + 1) * split_steps) (the host makes every range
   // non-empty) and writes its partial sum to Y (p = 0) or ws[p - 1].
+  // Grouped launches keep the hardware's round-robin order: their grid is an
+  // upper bound, and contiguous per-XCD bands would hand the surplus ids (all
+  // at the end) to the last XCDs, idling them (146 against 170 us on the
+  // expert prefill shape).  An expert's weight column tile still stays on one
+  // XCD (id mod 8 fixes the column tile when the column tiles are a multiple
+  // of 8).
   const int n_tiles = n_mtiles * n_ntiles;
-  const int logical = xcd_remap(blockIdx.x, n_tiles * splits);
+  const int logical = kGrouped ? static_cast<int>(blockIdx.x) : xcd_remap(blockIdx.x, n_tiles * splits);
   const int split = logical / n_tiles;
   const int tl = logical - split * n_tiles;
   const int mt = tl / n_ntiles, nt = tl % n_ntiles;
