@@ -295,7 +295,7 @@ int prq_grouped_gemm_packed(const uint8_t* Ap, const uint8_t* Aps, const int32_t
   const int per_group = (M_total + E - 1) / E;
   return launch_status(prq::launch_grouped_gemm_tile_packed(
       Ap, Aps, M_total, group_offsets, E, Wp, Wps, N, K_aug, Y,
-      prq::choose_grouped_packed_shape(per_group, N, K_aug), stream));
+      prq::choose_grouped_packed_shape(per_group, N, K_aug, E), dev.num_cus, stream));
 }
 
 size_t prq_grouped_gemm_workspace_bytes(int32_t M_total, int32_t E, int32_t N, int32_t K_aug) {

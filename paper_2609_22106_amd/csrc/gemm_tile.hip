@@ -466,6 +466,284 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
     }
 }
 
+// Grouped (MoE) tile GEMM on a packed activation, persistent and pipelined
+// across tiles.  XCD x (workgroup ids are dealt to the XCDs in turn) owns
+// experts x, x + 8, x + 16, ... and its workgroups stride over that list's
+// tiles (expert-major, row tiles then column tiles), so each expert's weight
+// and rows are fetched into one L2.  Lane j of every wave holds expert x + 8 j
+// (up to 512 experts) and the inclusive prefix of the list's row-tile counts
+// (a wave scan: no LDS, no barrier); a tile's expert is the number of lanes
+// whose prefix ends at or before it.
+//
+// A tile takes P = ceil(steps / kNS) * kNS pipeline slots (slots past the K
+// steps compute nothing), so every tile starts on stage 0; slot s issues slot
+// s + kNS, which from slot P - kNS on is the first steps of the workgroup's
+// next tile.  The next tile's loads are therefore in flight while the current
+// tile finishes and stores, and its first half step is already in registers
+// when its MFMAs start.  The same per-step wait, barrier and load sequence as
+// gemm_tile_kernel; the first slots of a tile also wait for the previous
+// tile's Y stores (they share the memory counter), which is conservative.
+template <int kBM, int kBN, int kWM, int kWN, int kNS>
+__global__ __launch_bounds__(kWM * kWN * 64) void gemm_grouped_persist_kernel(
+    const uint8_t* __restrict__ Ap, const uint8_t* __restrict__ Aps, int M,
+    const int32_t* __restrict__ off, int E, const uint8_t* __restrict__ Wp,
+    const uint8_t* __restrict__ Wps, int N, int K_aug, float* __restrict__ Y) {
+  using L = TileStage<kBM, kBN, kAPacked>;
+  constexpr int kWaves = kWM * kWN;
+  constexpr int kTM = kBM / kWM, kTN = kBN / kWN;
+  constexpr int kFM = kTM / 32, kFN = kTN / 32;
+  static_assert(kTM % 32 == 0 && kTN % 32 == 0, "wave tile of whole 32x32 fragments");
+  constexpr int kABlk = L::kABlk, kBBlk = L::kBBlk;
+  static_assert(kABlk % kWaves == 0 && kBBlk % kWaves == 0, "code blocks split evenly over waves");
+  static_assert(kABlk % 4 == 0 && kBBlk % 4 == 0, "scales move four block entries per instruction");
+  constexpr int kAPer = kABlk / kWaves, kBPer = kBBlk / kWaves;
+  constexpr int kAsChunks = kABlk / 4, kBsChunks = kBBlk / 4;
+  constexpr int kAsPer = (kAsChunks + kWaves - 1) / kWaves;
+  constexpr int kBsPer = (kBsChunks + kWaves - 1) / kWaves;
+  constexpr int kLoads = kAPer + kBPer + kAsPer + kBsPer;
+  static_assert(kNS >= 2 && kNS <= 4, "stages");
+  static_assert(kNS * L::kBytes <= 160 * 1024, "LDS");
+  constexpr int kU = kNS;
+  constexpr int kMfmas = 2 * kFM * kFN;
+  constexpr int kReads = 4 * (kFM + kFN);
+  __shared__ __align__(16) uint8_t st0[L::kBytes];
+  __shared__ __align__(16) uint8_t st1[L::kBytes];
+  __shared__ __align__(16) uint8_t st2[kNS > 2 ? L::kBytes : 16];
+  __shared__ __align__(16) uint8_t st3[kNS > 3 ? L::kBytes : 16];
+  auto stage = [&](auto pc) -> uint8_t* {
+    constexpr int p = decltype(pc)::value % kNS;
+    if constexpr (p == 0) return st0;
+    else if constexpr (p == 1) return st1;
+    else if constexpr (p == 2) return st2;
+    else return st3;
+  };
+
+  const int ntiles = N >> 4;
+  const int n_ntiles = (ntiles + kBBlk - 1) / kBBlk;
+  const int steps = (K_aug + kStepK - 1) / kStepK;
+  const int sgroups = (steps + 3) >> 2;
+  const int nblk = (M + 15) >> 4;
+  const int slots = (steps + kNS - 1) / kNS * kNS;   // P: pipeline slots per tile
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / kWN, wn = wave % kWN;
+
+  // This XCD's experts, one per lane.
+  const int xcd = static_cast<int>(blockIdx.x) % kXcds;
+  int px_r0 = 0, px_r1 = 0, px_b0 = 0, px_t = 0;
+  {
+    const int ex = xcd + kXcds * lane;
+    if (ex < E) {   // offsets clamped to [0, M]: malformed offsets cannot address past A
+      px_r0 = min(max(off[ex], 0), M);
+      px_r1 = min(max(off[ex + 1], px_r0), M);
+      px_b0 = px_r0 & ~15;
+      px_t = px_r1 > px_r0 ? (px_r1 - px_b0 + kBM - 1) / kBM : 0;
+    }
+  }
+  int px_incl = px_t;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int u = __shfl_up(px_incl, d, 64);
+    if (lane >= d) px_incl += u;
+  }
+  const int n_tiles = __builtin_amdgcn_readlane(px_incl, 63) * n_ntiles;
+  const int q_step = static_cast<int>(gridDim.x) / kXcds;
+  int q = static_cast<int>(blockIdx.x) / kXcds;
+  if (q >= n_tiles) return;
+
+  struct Tile {
+    int row_begin, row_lo, row_end, t0;
+    const uint8_t* W;    // the expert's packed weight codes
+    const uint8_t* Ws;   // and scales
+  };
+  // Tile q of this XCD's list (q < n_tiles).
+  auto tile_at = [&](int tq) {
+    const int mtl = tq / n_ntiles;
+    const int j = __popcll(__ballot(px_incl <= mtl));
+    const int e = xcd + kXcds * j;
+    const int first = __builtin_amdgcn_readlane(px_incl, j) - __builtin_amdgcn_readlane(px_t, j);
+    Tile t;
+    t.row_begin = __builtin_amdgcn_readlane(px_b0, j) + (mtl - first) * kBM;
+    t.row_end = min(__builtin_amdgcn_readlane(px_r1, j), t.row_begin + kBM);
+    t.row_lo = max(__builtin_amdgcn_readlane(px_r0, j), t.row_begin);
+    t.t0 = (tq - mtl * n_ntiles) * kBBlk;
+    t.W = Wp + static_cast<int64_t>(e) * ntiles * steps * 1024;
+    t.Ws = Wps + static_cast<int64_t>(e) * ntiles * sgroups * 256;
+    return t;
+  };
+  // Per-lane byte offsets of a tile's loads (rows and feature tiles clamped
+  // into the operands; 32-bit offsets checked on the host).
+  struct Offs {
+    uint32_t a[kAPer], as[kAsPer], b[kBPer], bs[kBsPer];
+  };
+  auto offsets = [&](const Tile& t) {
+    Offs o;
+#pragma unroll
+    for (int i = 0; i < kAPer; ++i) {
+      const int rb = min((t.row_begin >> 4) + wave + i * kWaves, nblk - 1);
+      o.a[i] = static_cast<uint32_t>(rb) * steps * 1024 + lane * 16;
+    }
+#pragma unroll
+    for (int i = 0; i < kAsPer; ++i) {
+      const int c = (wave + i * kWaves) % kAsChunks;
+      const int rb = min((t.row_begin >> 4) + c * 4 + (lane >> 4), nblk - 1);
+      o.as[i] = static_cast<uint32_t>(rb) * sgroups * 256 + (lane & 15) * 16;
+    }
+#pragma unroll
+    for (int i = 0; i < kBPer; ++i) {
+      const int ft = min(t.t0 + wave + i * kWaves, ntiles - 1);
+      o.b[i] = static_cast<uint32_t>(ft) * steps * 1024 + lane * 16;
+    }
+#pragma unroll
+    for (int i = 0; i < kBsPer; ++i) {
+      const int c = (wave + i * kWaves) % kBsChunks;
+      const int ft = min(t.t0 + c * 4 + (lane >> 4), ntiles - 1);
+      o.bs[i] = static_cast<uint32_t>(ft) * sgroups * 256 + (lane & 15) * 16;
+    }
+    return o;
+  };
+
+  Tile cur = tile_at(q);
+  bool has_next = q + q_step < n_tiles;
+  Tile nxt = has_next ? tile_at(q + q_step) : cur;
+  Offs oc = offsets(cur), on = offsets(nxt);
+
+  // Slot `slot` of the current tile into stage `st`: slots past the tile are
+  // the next tile's first slots (or, after the last tile, reload its last step).
+  // The operand selection is branch-free: every wave issues the same loads.
+  auto issue = [&](int slot, uint8_t* st) {
+    const bool use_next = has_next && slot >= slots;
+    const int s = use_next ? min(slot - slots, steps - 1) : min(slot, steps - 1);
+    const uint8_t* W = use_next ? nxt.W : cur.W;
+    const uint8_t* Ws = use_next ? nxt.Ws : cur.Ws;
+#pragma unroll
+    for (int i = 0; i < kAPer; ++i)
+      __builtin_amdgcn_global_load_lds(PRQ_GPTR(Ap + ((use_next ? on.a[i] : oc.a[i]) + s * 1024u)),
+                                       PRQ_LPTR(st + (wave + i * kWaves) * 1024), 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < kBPer; ++i)
+      __builtin_amdgcn_global_load_lds(PRQ_GPTR(W + ((use_next ? on.b[i] : oc.b[i]) + s * 1024u)),
+                                       PRQ_LPTR(st + L::kOffB + (wave + i * kWaves) * 1024), 16,
+                                       0, 0);
+#pragma unroll
+    for (int i = 0; i < kAsPer; ++i) {
+      const int c = (wave + i * kWaves) % kAsChunks;
+      __builtin_amdgcn_global_load_lds(
+          PRQ_GPTR(Aps + ((use_next ? on.as[i] : oc.as[i]) + (s >> 2) * 256u)),
+          PRQ_LPTR(st + L::kOffAs + c * 1024), 16, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < kBsPer; ++i) {
+      const int c = (wave + i * kWaves) % kBsChunks;
+      __builtin_amdgcn_global_load_lds(
+          PRQ_GPTR(Ws + ((use_next ? on.bs[i] : oc.bs[i]) + (s >> 2) * 256u)),
+          PRQ_LPTR(st + L::kOffBs + c * 1024), 16, 0, 0);
+    }
+  };
+
+  // Operand registers and LDS reads as in gemm_tile_kernel (packed layout).
+  struct Half {
+    uint4 a[kFM], b[kFN];
+    uint32_t sa[kFM], sb[kFN];
+  };
+  const int blk_sel = (lane >> 4) & 1;
+  const int lib0 = (lane & 15) + 16 * (lane >> 5);
+  const uint32_t a_lb = (wm * (kTM / 16) + blk_sel) * 1024 + lib0 * 16;
+  const uint32_t b_lb = L::kOffB + (wn * (kTN / 16) + blk_sel) * 1024 + lib0 * 16;
+  const uint32_t as_lb = L::kOffAs + (wm * (kTM / 16) + blk_sel) * 256 + lib0 * 4;
+  const uint32_t bs_lb = L::kOffBs + (wn * (kTN / 16) + blk_sel) * 256 + lib0 * 4;
+  auto read = [&](const uint8_t* st, auto hc, Half& o) {
+    constexpr int h = decltype(hc)::value;
+#pragma unroll
+    for (int i = 0; i < kFM; ++i) {
+      o.a[i] = *reinterpret_cast<const uint4*>(st + a_lb + (2 * i * 1024 + h * 512));
+      o.sa[i] = *reinterpret_cast<const uint32_t*>(st + as_lb + (2 * i * 256 + h * 128));
+    }
+#pragma unroll
+    for (int j = 0; j < kFN; ++j) {
+      o.b[j] = *reinterpret_cast<const uint4*>(st + b_lb + (2 * j * 1024 + h * 512));
+      o.sb[j] = *reinterpret_cast<const uint32_t*>(st + bs_lb + (2 * j * 256 + h * 128));
+    }
+  };
+  v16f acc[kFM][kFN];
+  auto mfma = [&](const Half& o, int s) {
+    const uint32_t qshift = 8u * static_cast<uint32_t>(s & 3);
+#pragma unroll
+    for (int i = 0; i < kFM; ++i) {
+      const uint32_t sa = o.sa[i] >> qshift;
+#pragma unroll
+      for (int j = 0; j < kFN; ++j)
+        acc[i][j] = dev::mfma_fp4_32x32x64_sel<0, 0>(o.a[i], o.b[j], sa, o.sb[j] >> qshift,
+                                                     acc[i][j]);
+    }
+  };
+
+  // Prologue of the first tile: slots 0 .. kNS-1, all landed, half 0 of slot 0 read.
+  static_for<kNS>([&](auto pc) { issue(static_cast<int>(decltype(pc)::value), stage(pc)); });
+  wait_vmcnt<0>();
+  __builtin_amdgcn_s_barrier();
+  Half h0, h1;
+  read(st0, IntC<0>{}, h0);
+  auto body = [&](int s0, auto pc, auto gc) {
+    constexpr int p = decltype(pc)::value;
+    constexpr bool kGuard = decltype(gc)::value;
+    const int s = s0 + p;
+    const bool live = !kGuard || s < steps;
+    __builtin_amdgcn_sched_barrier(0);
+    if (live) mfma(h0, s);
+    read(stage(pc), IntC<1>{}, h1);
+    if constexpr (!kGuard) interleave<kMfmas / 2, 0, kReads / 2>();
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vmcnt<(kNS - 2) * kLoads>();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    issue(s + kNS, stage(pc));
+    if (live) mfma(h1, s);
+    read(stage(IntC<p + 1>{}), IntC<0>{}, h0);
+    if constexpr (!kGuard) interleave<kMfmas / 2, kLoads, kReads / 2>();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  for (;;) {
+#pragma unroll
+    for (int i = 0; i < kFM; ++i)
+#pragma unroll
+      for (int j = 0; j < kFN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+    int s0 = 0;
+    for (; s0 + kU <= steps; s0 += kU)
+      static_for<kU>([&](auto pc) { body(s0, pc, IntC<0>{}); });
+    if (s0 < steps) static_for<kU>([&](auto pc) { body(s0, pc, IntC<1>{}); });
+
+    // Y rows [row_lo, row_end) of the tile (element e of a lane's fragment is
+    // C[8 (e / 4) + 4 (l / 32) + e % 4][l % 32]).
+#pragma unroll
+    for (int i = 0; i < kFM; ++i)
+#pragma unroll
+      for (int j = 0; j < kFN; ++j) {
+        const int n = cur.t0 * 16 + wn * kTN + j * 32 + (lane & 31);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int m = cur.row_begin + wm * kTM + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+          if (m >= cur.row_lo && m < cur.row_end && n < N)
+            Y[static_cast<int64_t>(m) * N + n] = acc[i][j][e];
+        }
+      }
+    if (!has_next) break;
+    q += q_step;
+    cur = nxt;
+    oc = on;
+    has_next = q + q_step < n_tiles;
+    if (has_next) {
+      nxt = tile_at(q + q_step);
+      on = offsets(nxt);
+    }
+  }
+  wait_vmcnt<0>();   // no direct-to-LDS write outlives the workgroup
+}
+
 // Split-K sum: Y[i] = ((Y[i] + P_0[i]) + P_1[i]) + ... over `parts` partial
 // arrays of n4 float4 each, in that fixed order.
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(float4* __restrict__ Y,
@@ -691,21 +969,49 @@ hipError_t launch_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M,
                        stream);
 }
 
+// The persistent grouped kernel (128 x 128 tiles) over num_cus CUs: as many
+// workgroups as fit on them at once, a multiple of the XCD count.
+hipError_t launch_grouped_persist(const uint8_t* Ap, const uint8_t* Aps, int M,
+                                  const int32_t* off, int E, const uint8_t* Wp,
+                                  const uint8_t* Wps, int N, int K_aug, float* Y, int num_cus,
+                                  hipStream_t stream) {
+  const int64_t steps = (K_aug + kStepK - 1) / kStepK;
+  if (!off || E < 1 || E > 64 * kXcds || num_cus < 1 ||
+      static_cast<int64_t>((M + 15) / 16) * steps * 1024 >= (int64_t{1} << 31) ||
+      static_cast<int64_t>(N / 16) * steps * 1024 >= (int64_t{1} << 31))
+    return hipErrorInvalidValue;
+  constexpr int kThreads = 256;
+  auto kernel = gemm_grouped_persist_kernel<128, 128, 2, 2, 4>;
+  static int per_cu = 0;   // the kernel's occupancy (same on every device of this build)
+  if (per_cu == 0) {
+    int n = 0;
+    const hipError_t err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, kThreads, 0);
+    if (err != hipSuccess) return err;
+    per_cu = std::max(n, 1);
+  }
+  const int grid = std::max(kXcds, num_cus * per_cu / kXcds * kXcds);
+  kernel<<<grid, kThreads, 0, stream>>>(Ap, Aps, M, off, E, Wp, Wps, N, K_aug, Y);
+  return hipGetLastError();
+}
+
 // Shape of the grouped packed GEMM.  128 x 128 throughout: on the expert
 // shape (~256 rows per expert, N = 2048, K + k = 832) it measured 158 us
 // against 167 (256 x 256) and 220 (256 x 128), and smaller row tiles waste
 // less on experts with fewer rows.
-int choose_grouped_packed_shape(int rows_per_expert, int N, int K_aug) {
+int choose_grouped_packed_shape(int rows_per_expert, int N, int K_aug, int E) {
   (void)rows_per_expert;
   (void)N;
   (void)K_aug;
-  return 2;
+  return E <= 64 * kXcds ? kShapePersist : 2;
 }
 
 hipError_t launch_grouped_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M_total,
                                            const int32_t* group_offsets, int E, const uint8_t* Wp,
                                            const uint8_t* Wps, int N, int K_aug, float* Y,
-                                           int shape, hipStream_t stream) {
+                                           int shape, int num_cus, hipStream_t stream) {
+  if (shape == kShapePersist)
+    return launch_grouped_persist(Ap, Aps, M_total, group_offsets, E, Wp, Wps, N, K_aug, Y,
+                                  num_cus, stream);
   return launch_region(Ap, Aps, M_total, group_offsets, E, Wp, Wps, N, K_aug, Y, shape, true, 0,
                        N / 16, stream);
 }

@@ -348,14 +348,17 @@ int prq_tune_gemm_tile_split(const uint8_t* A, const uint8_t* As, int M, const u
              : -3;
 }
 
-// The grouped tile GEMM on a packed activation with a forced shape.
+// The grouped tile GEMM on a packed activation with a forced shape (0-2: a
+// workgroup per tile; 3: the persistent kernel over num_cus CUs).
 int prq_tune_grouped_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M,
                                       const int32_t* off, int E, const uint8_t* Wp,
                                       const uint8_t* Wps, int N, int K_aug, float* Y, int shape,
-                                      hipStream_t stream) {
-  if (shape < 0 || shape > 2 || N % 16 || K_aug % 32 || M <= 0 || E < 1 || !off) return -1;
+                                      int num_cus, hipStream_t stream) {
+  if (shape < 0 || shape > prq::kShapePersist || N % 16 || K_aug % 32 || M <= 0 || E < 1 ||
+      !off || num_cus < 0 || (shape == prq::kShapePersist && (num_cus < 1 || E > 512)))
+    return -1;
   return prq::launch_grouped_gemm_tile_packed(Ap, Aps, M, off, E, Wp, Wps, N, K_aug, Y, shape,
-                                              stream) == hipSuccess
+                                              num_cus, stream) == hipSuccess
              ? 0
              : -3;
 }

@@ -89,11 +89,15 @@ hipError_t launch_gemm_tile_split(const uint8_t* Aq, const uint8_t* Asc, int M, 
                                   int shape, int splits, float* ws, hipStream_t stream);
 // The grouped (MoE) tile GEMM on a packed activation: an expert's row tiles
 // start on 16-row block boundaries (rows of neighbouring experts are masked).
+// shape 0-2: a workgroup per tile; kShapePersist: the persistent kernel
+// (128 x 128 tiles, each XCD working through its own experts, pipelined across
+// tiles; up to 512 experts) over num_cus CUs.
+constexpr int kShapePersist = 3;
 hipError_t launch_grouped_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M_total,
                                            const int32_t* group_offsets, int E, const uint8_t* Wp,
                                            const uint8_t* Wps, int N, int K_aug, float* Y,
-                                           int shape, hipStream_t stream);
-int choose_grouped_packed_shape(int rows_per_expert, int N, int K_aug);
+                                           int shape, int num_cus, hipStream_t stream);
+int choose_grouped_packed_shape(int rows_per_expert, int N, int K_aug, int E);
 // The tile GEMM with the activation in the packed layout (dense).
 hipError_t launch_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M,
                                    const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug,

@@ -186,15 +186,15 @@ def test_quant_act_packed_grouped(counts, K, k):
     np.testing.assert_array_equal(host(A.Ap), ep, err_msg="packed codes")
 
 
-def _tune_grouped_packed(shape, A, off, W, Y):
+def _tune_grouped_packed(shape, A, off, W, Y, num_cus):
     from paper_2609_22106_amd import build
     lib = ctypes.CDLL(build.PROBE_LIB)
     P, I = ctypes.c_void_p, ctypes.c_int
-    lib.prq_tune_grouped_gemm_tile_packed.argtypes = [P, P, I, P, I, P, P, I, I, P, I, P]
+    lib.prq_tune_grouped_gemm_tile_packed.argtypes = [P, P, I, P, I, P, P, I, I, P, I, I, P]
     lib.prq_tune_grouped_gemm_tile_packed.restype = I
     return lib.prq_tune_grouped_gemm_tile_packed(
         A.Ap.data_ptr(), A.Aps.data_ptr(), A.M, off.data_ptr(), W.E, W.Wp.data_ptr(),
-        W.Wps.data_ptr(), W.N, W.K_aug, Y.data_ptr(), shape,
+        W.Wps.data_ptr(), W.N, W.K_aug, Y.data_ptr(), shape, num_cus,
         torch.cuda.current_stream().cuda_stream)
 
 
@@ -204,14 +204,20 @@ GROUPED_GEMM = [([0, 300, 0, 5, 260], 272, 1024),
                 ([3, 0, 17, 1, 0], 48, 1088),
                 ([0, 0, 200], 128, 832),
                 ([255, 258, 1, 15, 16, 17, 600], 144, 832),
-                ([7] * 40, 64, 4192)]
+                ([7] * 40, 64, 4192),
+                ([0, 3, 1, 0, 2] * 60, 32, 256)]      # 300 experts (38 per XCD), mostly one tile
 
 
 @pytest.mark.parametrize("counts,N,K_aug", GROUPED_GEMM)
-@pytest.mark.parametrize("shape", [None, 0, 1, 2])
-def test_grouped_gemm_packed(shape, counts, N, K_aug):
+@pytest.mark.parametrize("shape,cus", [(None, None), (0, 0), (1, 0), (2, 0), (3, 256), (3, 8),
+                                       (3, 1)])
+def test_grouped_gemm_packed(shape, cus, counts, N, K_aug):
     """Every row of every expert stored exactly once (Y starts as NaN) and within
-    1e-3 max |Y| of the oracle's grouped GEMM (Eq. 3 per expert)."""
+    1e-3 max |Y| of the oracle's grouped GEMM (Eq. 3 per expert): a workgroup per
+    tile (shapes 0-2), or the persistent kernel (shape 3) in which each XCD's
+    workgroups stride over its own experts' tiles with the next tile's loads in
+    flight -- on all CUs, and on 8 or 1 CU(s) so that every workgroup runs many
+    tiles back to back."""
     prq = _prq()
     rng = np.random.default_rng(sum(counts) * 7 + N + K_aug)
     E = len(counts)
@@ -223,14 +229,14 @@ def test_grouped_gemm_packed(shape, counts, N, K_aug):
     W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
     offd = dev(off)
     Y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
-    say("packed grouped gemm case:", shape, counts, N, K_aug)
+    say("packed grouped gemm case:", shape, cus, counts, N, K_aug)
     if shape is None:
         prq.prq_grouped_gemm_packed(A, offd, W, Y)
     else:
-        assert _tune_grouped_packed(shape, A, offd, W, Y) == 0
+        assert _tune_grouped_packed(shape, A, offd, W, Y, cus) == 0
     torch.cuda.synchronize()
     assert_gemm_close(host(Y), pq.grouped_gemm(Aq, Asc, off, Wq, Wsc),
-                      f"grouped packed shape {shape} {counts} {N}x{K_aug}")
+                      f"grouped packed shape {shape} cus {cus} {counts} {N}x{K_aug}")
 
 
 def test_grouped_packed_pair_experts():
