@@ -266,6 +266,7 @@ __global__ __launch_bounds__(kLdsThreads) void act_quant_lds_kernel(
   const int u0 = tid - ro * units;                // its first unit
   PackedUnit un[kUnits];
   int cur_g = -1;
+  dev::GroupCursor gc;   // this thread's rows only increase
   int pass = 0;
   for (int rb = r0; rb < r1; rb += rpp, ++pass) {
     uint4* const sb = (pass & 1) ? buf1 : buf0;
@@ -278,7 +279,7 @@ __global__ __launch_bounds__(kLdsThreads) void act_quant_lds_kernel(
 
     const int r = rb + ro;
     if (ro < rpp && r < r1) {                     // quad-uniform: units is a multiple of 4
-      const int g = kGrouped ? dev::find_group(offsets, G, r) : 0;
+      const int g = kGrouped ? gc.at(offsets, G, r) : 0;
       if (g != cur_g) {
 #pragma unroll
         for (int j = 0; j < kUnits; ++j) {
@@ -416,7 +417,8 @@ __global__ __launch_bounds__(kDmaThreads) void act_quant_dma_kernel(
     __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));   // vmcnt(0)
     cur_g = g;
   };
-  if (!copier) load_units(kGrouped ? dev::find_group(offsets, G, r0) : 0);
+  dev::GroupCursor gc;
+  if (!copier) load_units(kGrouped ? gc.at(offsets, G, r0) : 0);
 
   if (copier)
     for (int i = 0; i < kNS - 1; ++i) copy_row(i);
@@ -430,8 +432,8 @@ __global__ __launch_bounds__(kDmaThreads) void act_quant_dma_kernel(
     wait_vmcnt_lgkm0<63>();                         // this wave's LDS reads of row i-1
     __builtin_amdgcn_s_barrier();
     const int r = r0 + i;
-    if (kGrouped) {
-      const int g = dev::find_group(offsets, G, r);
+    if (kGrouped) {   // a load only when the row leaves its group
+      const int g = gc.at(offsets, G, r);
       if (g != cur_g) load_units(g);
     }
     const uint16_t* row = reinterpret_cast<const uint16_t*>(stg + (i % kNS) * kStage);

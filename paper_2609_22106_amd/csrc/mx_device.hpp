@@ -118,5 +118,21 @@ __device__ __forceinline__ int find_group(const int32_t* __restrict__ off, int G
   return lo;
 }
 
+// Group of rows visited in increasing order: a binary search for the first
+// row, then a step forward past the groups' ends as rows cross them (a load
+// only when a row leaves its group).  Same result as find_group for
+// non-decreasing offsets; g stays in [0, G) whatever the offsets hold.
+struct GroupCursor {
+  int g = -1, g_end = 0;
+  __device__ __forceinline__ int at(const int32_t* __restrict__ off, int G, int row) {
+    if (g < 0 || row >= g_end) {
+      if (g < 0) g = find_group(off, G, row);
+      while (g + 1 < G && off[g + 1] <= row) ++g;
+      g_end = g + 1 < G ? off[g + 1] : 0x7fffffff;
+    }
+    return g;
+  }
+};
+
 }  // namespace dev
 }  // namespace prq
