@@ -194,7 +194,12 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   constexpr int kBsChunks = kBBlk / 4;
   constexpr int kAsPer = (kAsChunks + kWaves - 1) / kWaves;
   constexpr int kBsPer = (kBsChunks + kWaves - 1) / kWaves;
-  constexpr int kLoads = kAPer + kBPer + kAsPer + kBsPer;   // direct-to-LDS loads per wave per step
+  // Packed activations: the A and B scale chunks (a kilobyte each) are one list
+  // dealt to the waves in turn, so no wave reloads a chunk another wave loads.
+  constexpr int kScChunks = kAsChunks + kBsChunks;
+  constexpr int kScPer = (kScChunks + kWaves - 1) / kWaves;
+  // direct-to-LDS loads per wave per step
+  constexpr int kLoads = kAPer + kBPer + (kPackedA ? kScPer : kAsPer + kBsPer);
   static_assert(kNS >= 2 && kNS <= 4, "stages");
   static_assert(kNS * L::kBytes <= 160 * 1024, "LDS");
   static_assert(L::kBytes >= kThreads * 4 + 16, "the expert scan borrows a stage");
@@ -265,7 +270,7 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   // Per-lane byte offsets of this wave's loads from uniform bases (fixed over
   // the K loop; rows and tiles clamped into the operands; the host checks that
   // the operands fit 32-bit offsets).
-  uint32_t a_off[kAPer], as_off[kAsPer], b_off[kBPer], bs_off[kBsPer];
+  uint32_t a_off[kAPer], as_off[kAsPer], b_off[kBPer], bs_off[kBsPer], sc_off[kScPer];
 #pragma unroll
   for (int i = 0; i < kAPer; ++i) {
     if constexpr (kPackedA) {
@@ -279,14 +284,16 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
 #pragma unroll
   for (int i = 0; i < kAsPer; ++i) {
     const int c = (wave + i * kWaves) % kAsChunks;
-    if constexpr (kPackedA) {
-      const int rb = min((row_begin >> 4) + c * 4 + (lane >> 4), nblk - 1);
-      as_off[i] = static_cast<uint32_t>(rb) * sgroups * 256 + (lane & 15) * 16;
-    } else {
-      const int m = kScaleDword ? min(row_begin + c * 64 + lane, row_end - 1)
-                                : min(row_begin + c * 16 + lr, row_end - 1);
-      as_off[i] = static_cast<uint32_t>(m) * nb + (kScaleDword ? 0 : lk);
-    }
+    const int m = kScaleDword ? min(row_begin + c * 64 + lane, row_end - 1)
+                              : min(row_begin + c * 16 + lr, row_end - 1);
+    as_off[i] = static_cast<uint32_t>(m) * nb + (kScaleDword ? 0 : lk);
+  }
+#pragma unroll
+  for (int i = 0; i < kScPer; ++i) {   // packed: A chunks first, then B chunks
+    const int c = (wave + i * kWaves) % kScChunks;
+    const int blk = c < kAsChunks ? min((row_begin >> 4) + c * 4 + (lane >> 4), nblk - 1)
+                                  : min(t0 + (c - kAsChunks) * 4 + (lane >> 4), ntiles - 1);
+    sc_off[i] = static_cast<uint32_t>(blk) * sgroups * 256 + (lane & 15) * 16;
   }
 #pragma unroll
   for (int i = 0; i < kBPer; ++i) {
@@ -320,25 +327,33 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
       __builtin_amdgcn_global_load_lds(PRQ_GPTR(We + (b_off[i] + s * 1024u)),
                                        PRQ_LPTR(st + L::kOffB + (wave + i * kWaves) * 1024), 16,
                                        0, 0);
+    if constexpr (kPackedA) {
 #pragma unroll
-    for (int i = 0; i < kAsPer; ++i) {
-      const int c = (wave + i * kWaves) % kAsChunks;
-      if constexpr (kPackedA)      // four blocks' entries of the step's group
-        __builtin_amdgcn_global_load_lds(PRQ_GPTR(Asc + (as_off[i] + (s >> 2) * 256u)),
-                                         PRQ_LPTR(st + L::kOffAs + c * 1024), 16, 0, 0);
-      else if constexpr (kScaleDword)   // K_aug % 128 == 0: the row's 4 bytes of step s, aligned
-        __builtin_amdgcn_global_load_lds(PRQ_GPTR(Asc + (as_off[i] + s * 4)),
-                                         PRQ_LPTR(st + L::kOffAs + c * 256), 4, 0, 0);
-      else
-        __builtin_amdgcn_global_load_lds(
-            PRQ_GPTR(Asc + (kok ? as_off[i] + s * 4 : as_off[i] - lk)),
-            PRQ_LPTR(st + L::kOffAs + c * 256), 1, 0, 0);
-    }
+      for (int i = 0; i < kScPer; ++i) {   // four blocks' entries of the step's group
+        const int c = (wave + i * kWaves) % kScChunks;   // uniform: the source is a select
+        const uint8_t* src = c < kAsChunks ? Asc : Wse;
+        const int dst = c < kAsChunks ? L::kOffAs + c * 1024 : L::kOffBs + (c - kAsChunks) * 1024;
+        __builtin_amdgcn_global_load_lds(PRQ_GPTR(src + (sc_off[i] + (s >> 2) * 256u)),
+                                         PRQ_LPTR(st + dst), 16, 0, 0);
+      }
+    } else {
 #pragma unroll
-    for (int i = 0; i < kBsPer; ++i) {
-      const int c = (wave + i * kWaves) % kBsChunks;
-      __builtin_amdgcn_global_load_lds(PRQ_GPTR(Wse + (bs_off[i] + (s >> 2) * 256u)),
-                                       PRQ_LPTR(st + L::kOffBs + c * 1024), 16, 0, 0);
+      for (int i = 0; i < kAsPer; ++i) {
+        const int c = (wave + i * kWaves) % kAsChunks;
+        if constexpr (kScaleDword)   // K_aug % 128 == 0: the row's 4 bytes of step s, aligned
+          __builtin_amdgcn_global_load_lds(PRQ_GPTR(Asc + (as_off[i] + s * 4)),
+                                           PRQ_LPTR(st + L::kOffAs + c * 256), 4, 0, 0);
+        else
+          __builtin_amdgcn_global_load_lds(
+              PRQ_GPTR(Asc + (kok ? as_off[i] + s * 4 : as_off[i] - lk)),
+              PRQ_LPTR(st + L::kOffAs + c * 256), 1, 0, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < kBsPer; ++i) {
+        const int c = (wave + i * kWaves) % kBsChunks;
+        __builtin_amdgcn_global_load_lds(PRQ_GPTR(Wse + (bs_off[i] + (s >> 2) * 256u)),
+                                         PRQ_LPTR(st + L::kOffBs + c * 1024), 16, 0, 0);
+      }
     }
   };
 
@@ -498,9 +513,9 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_grouped_persist_kernel(
   static_assert(kABlk % 4 == 0 && kBBlk % 4 == 0, "scales move four block entries per instruction");
   constexpr int kAPer = kABlk / kWaves, kBPer = kBBlk / kWaves;
   constexpr int kAsChunks = kABlk / 4, kBsChunks = kBBlk / 4;
-  constexpr int kAsPer = (kAsChunks + kWaves - 1) / kWaves;
-  constexpr int kBsPer = (kBsChunks + kWaves - 1) / kWaves;
-  constexpr int kLoads = kAPer + kBPer + kAsPer + kBsPer;
+  constexpr int kScChunks = kAsChunks + kBsChunks;   // one list dealt to the waves
+  constexpr int kScPer = (kScChunks + kWaves - 1) / kWaves;
+  constexpr int kLoads = kAPer + kBPer + kScPer;
   static_assert(kNS >= 2 && kNS <= 4, "stages");
   static_assert(kNS * L::kBytes <= 160 * 1024, "LDS");
   constexpr int kU = kNS;
@@ -575,7 +590,7 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_grouped_persist_kernel(
   // Per-lane byte offsets of a tile's loads (rows and feature tiles clamped
   // into the operands; 32-bit offsets checked on the host).
   struct Offs {
-    uint32_t a[kAPer], as[kAsPer], b[kBPer], bs[kBsPer];
+    uint32_t a[kAPer], b[kBPer], sc[kScPer];
   };
   auto offsets = [&](const Tile& t) {
     Offs o;
@@ -585,21 +600,16 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_grouped_persist_kernel(
       o.a[i] = static_cast<uint32_t>(rb) * steps * 1024 + lane * 16;
     }
 #pragma unroll
-    for (int i = 0; i < kAsPer; ++i) {
-      const int c = (wave + i * kWaves) % kAsChunks;
-      const int rb = min((t.row_begin >> 4) + c * 4 + (lane >> 4), nblk - 1);
-      o.as[i] = static_cast<uint32_t>(rb) * sgroups * 256 + (lane & 15) * 16;
-    }
-#pragma unroll
     for (int i = 0; i < kBPer; ++i) {
       const int ft = min(t.t0 + wave + i * kWaves, ntiles - 1);
       o.b[i] = static_cast<uint32_t>(ft) * steps * 1024 + lane * 16;
     }
 #pragma unroll
-    for (int i = 0; i < kBsPer; ++i) {
-      const int c = (wave + i * kWaves) % kBsChunks;
-      const int ft = min(t.t0 + c * 4 + (lane >> 4), ntiles - 1);
-      o.bs[i] = static_cast<uint32_t>(ft) * sgroups * 256 + (lane & 15) * 16;
+    for (int i = 0; i < kScPer; ++i) {   // A scale chunks first, then B
+      const int c = (wave + i * kWaves) % kScChunks;
+      const int blk = c < kAsChunks ? min((t.row_begin >> 4) + c * 4 + (lane >> 4), nblk - 1)
+                                    : min(t.t0 + (c - kAsChunks) * 4 + (lane >> 4), ntiles - 1);
+      o.sc[i] = static_cast<uint32_t>(blk) * sgroups * 256 + (lane & 15) * 16;
     }
     return o;
   };
@@ -627,18 +637,13 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_grouped_persist_kernel(
                                        PRQ_LPTR(st + L::kOffB + (wave + i * kWaves) * 1024), 16,
                                        0, 0);
 #pragma unroll
-    for (int i = 0; i < kAsPer; ++i) {
-      const int c = (wave + i * kWaves) % kAsChunks;
+    for (int i = 0; i < kScPer; ++i) {
+      const int c = (wave + i * kWaves) % kScChunks;   // uniform: the source is a select
+      const uint8_t* src = c < kAsChunks ? Aps : Ws;
+      const int dst = c < kAsChunks ? L::kOffAs + c * 1024 : L::kOffBs + (c - kAsChunks) * 1024;
       __builtin_amdgcn_global_load_lds(
-          PRQ_GPTR(Aps + ((use_next ? on.as[i] : oc.as[i]) + (s >> 2) * 256u)),
-          PRQ_LPTR(st + L::kOffAs + c * 1024), 16, 0, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < kBsPer; ++i) {
-      const int c = (wave + i * kWaves) % kBsChunks;
-      __builtin_amdgcn_global_load_lds(
-          PRQ_GPTR(Ws + ((use_next ? on.bs[i] : oc.bs[i]) + (s >> 2) * 256u)),
-          PRQ_LPTR(st + L::kOffBs + c * 1024), 16, 0, 0);
+          PRQ_GPTR(src + ((use_next ? on.sc[i] : oc.sc[i]) + (s >> 2) * 256u)),
+          PRQ_LPTR(st + dst), 16, 0, 0);
     }
   };
 
@@ -845,10 +850,25 @@ hipError_t launch_region(const uint8_t* Aq, const uint8_t* Asc, int M, const int
 
 struct Shape {
   int id, bm, bn;
-  double eff_rows, eff_packed;   // measured throughput per tile area relative to 256 x 256
+  double eff_rows;      // measured throughput per tile area relative to 256 x 256 (row-major A)
+  // Packed A, by the most tiles any CU runs (1, 2, 3 or more), relative to one
+  // 256 x 256 tile per CU; fitted to the down_proj sweep (M = 1024 .. 8192, N =
+  // 2560, K + k = 9984, weights rotated): 128 x 128 workgroups fit two to a CU
+  // and hide each other's latency, so two per CU run far better than one.
+  double eff_packed[3];
 };
-constexpr Shape kShapes[] = {{0, 256, 256, 1.0, 1.0}, {1, 256, 128, 0.63, 0.83},
-                             {2, 128, 128, 0.5, 0.67}};
+constexpr Shape kShapes[] = {{0, 256, 256, 1.0, {1.0, 0.92, 0.92}},
+                             {1, 256, 128, 0.63, {0.73, 0.87, 0.80}},
+                             {2, 128, 128, 0.5, {0.58, 0.81, 0.68}}};
+
+// Cost of `tiles` tiles of shape s on `cus` CUs in tile-area units (one
+// 256 x 256 tile alone on its CU = 65536): the busiest CU's tiles over the
+// shape's efficiency at that load.
+double shape_cost(const Shape& s, bool packed, long tiles, int cus) {
+  const long per_cu = (tiles + cus - 1) / cus;
+  const double eff = packed ? s.eff_packed[std::min<long>(per_cu, 3) - 1] : s.eff_rows;
+  return per_cu * static_cast<double>(s.bm) * s.bn / eff;
+}
 
 // Plan of a dense tile GEMM: one shape over all N columns (optionally split
 // along K), or a main region of whole column tiles in one shape and the
@@ -878,10 +898,10 @@ TilePlan plan_tile_gemm(int M, int N, int K_aug, int num_cus, bool packed, bool 
     if (cols16 <= 0) return 0.0;
     const long tiles = static_cast<long>((M + s.bm - 1) / s.bm) * ((cols16 * 16 + s.bn - 1) / s.bn);
     const int per = (steps + splits - 1) / splits;
-    const long rounds = (tiles * ((steps + per - 1) / per) + cus - 1) / cus;
-    const double step_us =
-        kStepUs256 * s.bm * s.bn / 65536.0 / (packed ? s.eff_packed : s.eff_rows);
-    double c = rounds * (per + kFillSteps) * step_us;
+    const long wgs = tiles * ((steps + per - 1) / per);
+    // per-step time of the busiest CU: kStepUs256 per 256 x 256 tile alone
+    const double step_us = kStepUs256 * shape_cost(s, packed, wgs, cus) / 65536.0;
+    double c = (per + kFillSteps) * step_us;
     if (splits > 1)   // partials written, then Y and the partials read and Y written
       c += kLaunchUs + 2.0 * ((steps + per - 1) / per) * 4.0 * M * N / kReduceBytesPerUs;
     return c;
@@ -944,8 +964,7 @@ int choose_tile_shape(int M_rows, int N, int num_cus, bool packed) {
   double best_cost = 1e300;
   for (const Shape& s : kShapes) {
     const long tiles = static_cast<long>((M_rows + s.bm - 1) / s.bm) * ((N + s.bn - 1) / s.bn);
-    const long rounds = (tiles + num_cus - 1) / std::max(num_cus, 1);
-    const double c = rounds * static_cast<double>(s.bm) * s.bn / (packed ? s.eff_packed : s.eff_rows);
+    const double c = shape_cost(s, packed, tiles, std::max(num_cus, 1));
     if (c < best_cost) {
       best_cost = c;
       best = s.id;
