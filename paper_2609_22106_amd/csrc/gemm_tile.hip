@@ -842,7 +842,7 @@ hipError_t launch_region(const uint8_t* Aq, const uint8_t* Asc, int M, const int
                          int shape, bool packed, int tile_base, int region_tiles,
                          hipStream_t stream, int splits = 1, float* ws = nullptr) {
   switch (shape) {
-    case 0: return launch_shape<256, 256, 2, 2, 4, 3>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, tile_base, region_tiles, splits, ws, stream);
+    case 0: return launch_shape<256, 256, 2, 4, 4, 3>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, tile_base, region_tiles, splits, ws, stream);
     case 1: return launch_shape<256, 128, 2, 2, 4, 4>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, tile_base, region_tiles, splits, ws, stream);
     default: return launch_shape<128, 128, 2, 2, 4, 4>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, tile_base, region_tiles, splits, ws, stream);
   }

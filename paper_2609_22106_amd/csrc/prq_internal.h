@@ -67,7 +67,7 @@ hipError_t launch_pack_weight(const uint8_t* Wq, const uint8_t* Wsc, int N, int 
 
 // gemm_tile.hip / gemm_stream.hip (packed weights Wp/Wps).  group_offsets ==
 // nullptr means one group of M rows.
-// Tile shapes (4 waves each): 0 = 256x256, 1 = 256x128, 2 = 128x128.
+// Tile shapes: 0 = 256x256 (8 waves, two per SIMD), 1 = 256x128, 2 = 128x128 (4 waves).
 int choose_tile_shape(int M_rows, int N, int num_cus, bool packed);
 hipError_t launch_gemm_tile(const uint8_t* Aq, const uint8_t* Asc, int M,
                             const int32_t* group_offsets, int E, const uint8_t* Wp,
