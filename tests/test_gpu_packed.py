@@ -239,6 +239,28 @@ def test_grouped_gemm_packed(shape, cus, counts, N, K_aug):
                       f"grouped packed shape {shape} cus {cus} {counts} {N}x{K_aug}")
 
 
+@pytest.mark.parametrize("counts", [[300], [0, 1, 0, 2] * 150, [33] * 513])
+def test_grouped_gemm_packed_expert_counts(counts):
+    """prq_grouped_gemm_packed's own choice at the ends of the expert range: one
+    expert (persistent, all its tiles on one XCD), 600 experts and 513 experts
+    (above the persistent kernel's 512: one workgroup per tile), against the
+    oracle's grouped GEMM; every row stored (Y starts as NaN)."""
+    prq = _prq()
+    rng = np.random.default_rng(len(counts))
+    E, N, K_aug = len(counts), 48, 320
+    off = inputs.routed_offsets(counts)
+    M = int(off[-1])
+    Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+    Wq, Wsc = inputs.random_mxfp4(rng, (E, N), K_aug)
+    A = prq.PackedAct(*map(dev, pack_rows(Aq, Asc)), M, K_aug)
+    W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
+    Y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+    say("packed grouped expert-count case:", E, "experts,", M, "rows")
+    prq.prq_grouped_gemm_packed(A, dev(off), W, Y)
+    torch.cuda.synchronize()
+    assert_gemm_close(host(Y), pq.grouped_gemm(Aq, Asc, off, Wq, Wsc), f"{E} experts")
+
+
 def test_grouped_packed_pair_experts():
     """X -> prq_quant_act_packed -> prq_grouped_gemm_packed on the MoE expert
     shape (128 experts, 768 -> 2048, k = 64, 4096 tokens routed top-8 to
