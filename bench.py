@@ -554,7 +554,7 @@ def main(argv=None):
         return traffic_from_counters(args.workload, *args.traffic_from, args.traffic_command)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU "
-              "sharding of this path is described in DESIGN.md and not built.", file=sys.stderr)
+              "sharding of this path is not built.", file=sys.stderr)
         return 2
     import numpy as np
     import torch

@@ -1001,7 +1001,7 @@ hipError_t launch_grouped_persist(const uint8_t* Ap, const uint8_t* Aps, int M,
     return hipErrorInvalidValue;
   constexpr int kThreads = 256;
   auto kernel = gemm_grouped_persist_kernel<128, 128, 2, 2, 4>;
-  static int per_cu = 0;   // the kernel's occupancy (same on every device of this build)
+  static int per_cu = 0;   // the kernel's occupancy (gfx950 only: the same on every device)
   if (per_cu == 0) {
     int n = 0;
     const hipError_t err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, kThreads, 0);

@@ -14,8 +14,8 @@ def pytest_configure(config):
 
 
 def pytest_collection_modifyitems(config, items):
-    # GPU tests run in one process on the GPU machine; on a machine without a GPU
-    # they are skipped rather than failing on device allocation.
+    # GPU tests run in one process on a machine with the GPU; on one without a
+    # GPU they are skipped rather than failing on device allocation.
     try:
         import torch
         have_gpu = torch.cuda.is_available()
