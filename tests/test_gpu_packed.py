@@ -288,3 +288,28 @@ def test_grouped_packed_pair_experts():
         r = rows[e_of == e]
         rq, rs = pq.quant_act(X[r], inv[e], perm[e], k)
         assert_gemm_close(Y[r], pq.gemm(rq, rs, Wq[e], Wsc[e]), f"expert {e} rows {r.tolist()}")
+
+
+@pytest.mark.parametrize("name,N,K", inputs.LAYER_SET)
+def test_packed_pair_layer_shapes(name, N, K):
+    """The seven linears of a Qwen3-4B-shaped decoder layer at M = 4096 (k = K/40
+    rounded down to a multiple of 32), through the packed pair as the benchmark
+    launches it (the planner's tile shapes, column regions and workspace),
+    against the oracle on 32 sampled rows and every column."""
+    prq = _prq()
+    rng = np.random.default_rng(N + K)
+    M, k = 4096, inputs.tail_width(K)
+    X = inputs.f32_to_bf16_bits((rng.standard_normal((M, K)) *
+                                 rng.uniform(0.01, 30.0, K)).astype(np.float32))
+    inv = rng.uniform(0.25, 4.0, K).astype(np.float32)
+    perm = rng.permutation(K).astype(np.int32)
+    Wq, Wsc = inputs.random_mxfp4(rng, N, K + k)
+    W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
+    say("layer shape case:", name, M, N, K, k)
+    A = prq.prq_quant_act_packed(dev(X), K, k, dev(_pos(inv, perm)), dev(perm))
+    ws_n = prq.prq_gemm_packed_workspace_bytes(M, N, K + k)
+    ws = torch.empty(ws_n, dtype=torch.uint8, device="cuda") if ws_n else None
+    Y = host(prq.prq_gemm_packed(A, W, workspace=ws))
+    rows = np.unique(np.concatenate([rng.choice(M, 30, replace=False), [0, M - 1]]))
+    rq, rs = pq.quant_act(X[rows], inv, perm, k)
+    assert_gemm_close(Y[rows], pq.gemm(rq, rs, Wq, Wsc), f"{name} {M}x{N}x{K}+{k}")
