@@ -183,9 +183,12 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   constexpr int kFM = kTM / 32, kFN = kTN / 32;      // 32x32 fragments per wave
   static_assert(kTM % 32 == 0 && kTN % 32 == 0, "wave tile of whole 32x32 fragments");
   constexpr int kABlk = L::kABlk, kBBlk = L::kBBlk;
-  static_assert(kABlk % kWaves == 0 && kBBlk % kWaves == 0, "code blocks split evenly over waves");
+  static_assert(kABlk % kWaves == 0, "A code blocks split evenly over waves");
   static_assert(kBBlk % 4 == 0, "B scales move four tile entries per instruction");
-  constexpr int kAPer = kABlk / kWaves, kBPer = kBBlk / kWaves;
+  // B blocks are dealt to the waves in turn; when they do not divide evenly
+  // (256 x 320: 20 blocks, 8 waves) the last block is loaded again into its own
+  // place (the same bytes), so that every wave issues the same loads.
+  constexpr int kAPer = kABlk / kWaves, kBPer = (kBBlk + kWaves - 1) / kWaves;
   // Scale instructions per step: A as 64 row dwords, one per 16-row block
   // (bytes), or four block entries of 256 bytes (packed); B as four tile
   // entries.  When there are fewer than waves, several waves load the same
@@ -297,7 +300,7 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   }
 #pragma unroll
   for (int i = 0; i < kBPer; ++i) {
-    const int t = min(t0 + wave + i * kWaves, ntiles - 1);
+    const int t = min(t0 + min(wave + i * kWaves, kBBlk - 1), ntiles - 1);
     b_off[i] = static_cast<uint32_t>(t) * steps * 1024 + lane * 16;
   }
 #pragma unroll
@@ -325,7 +328,7 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
 #pragma unroll
     for (int i = 0; i < kBPer; ++i)
       __builtin_amdgcn_global_load_lds(PRQ_GPTR(We + (b_off[i] + s * 1024u)),
-                                       PRQ_LPTR(st + L::kOffB + (wave + i * kWaves) * 1024), 16,
+                                       PRQ_LPTR(st + L::kOffB + min(wave + i * kWaves, kBBlk - 1) * 1024), 16,
                                        0, 0);
     if constexpr (kPackedA) {
 #pragma unroll
@@ -844,6 +847,7 @@ hipError_t launch_region(const uint8_t* Aq, const uint8_t* Asc, int M, const int
   switch (shape) {
     case 0: return launch_shape<256, 256, 2, 4, 4, 3>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, tile_base, region_tiles, splits, ws, stream);
     case 1: return launch_shape<256, 128, 2, 2, 4, 4>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, tile_base, region_tiles, splits, ws, stream);
+    case 3: return launch_shape<256, 320, 4, 2, 3, 3>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, tile_base, region_tiles, splits, ws, stream);
     default: return launch_shape<128, 128, 2, 2, 4, 4>(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, packed, tile_base, region_tiles, splits, ws, stream);
   }
 }
@@ -857,9 +861,15 @@ struct Shape {
   // and hide each other's latency, so two per CU run far better than one.
   double eff_packed[3];
 };
+// 256 x 320 (8 waves, 64 x 160 each, 3 stages): where it fills the CUs evenly
+// it beats every other plan -- 8192 x 2560 x 9984 in one round of 256 tiles,
+// 106 against 120 us for 256 x 256 over 2048 columns and 128 x 128 over the
+// rest; 4096 x 9728 x 2624, 80 against 93 us -- and loses elsewhere (half-empty
+// rounds); its factors are set to pick it exactly there.
 constexpr Shape kShapes[] = {{0, 256, 256, 1.0, {1.0, 0.92, 0.92}},
                              {1, 256, 128, 0.63, {0.73, 0.87, 0.80}},
-                             {2, 128, 128, 0.5, {0.58, 0.81, 0.68}}};
+                             {2, 128, 128, 0.5, {0.58, 0.81, 0.68}},
+                             {3, 256, 320, 0.5, {0.9, 0.9, 0.85}}};
 
 // Cost of `tiles` tiles of shape s on `cus` CUs in tile-area units (one
 // 256 x 256 tile alone on its CU = 65536): the busiest CU's tiles over the

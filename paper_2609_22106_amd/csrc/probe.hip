@@ -315,7 +315,7 @@ int prq_probe_stream_read(const uint8_t* Wp, int tiles, int steps, int splits, i
 int prq_tune_gemm_tile(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off, int E,
                        const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug, float* Y, int shape,
                        hipStream_t stream) {
-  if (shape < 0 || shape > 2 || N % 16 || K_aug % 32 || M <= 0) return -1;
+  if (shape < 0 || shape > 3 || N % 16 || K_aug % 32 || M <= 0) return -1;
   return prq::launch_gemm_tile(Aq, Asc, M, off, E, Wp, Wps, N, K_aug, Y, shape, stream) == hipSuccess
              ? 0
              : -3;
@@ -325,7 +325,7 @@ int prq_tune_gemm_tile(const uint8_t* Aq, const uint8_t* Asc, int M, const int32
 int prq_tune_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M, const uint8_t* Wp,
                               const uint8_t* Wps, int N, int K_aug, float* Y, int shape,
                               hipStream_t stream) {
-  if (shape < 0 || shape > 2 || N % 16 || K_aug % 32 || M <= 0) return -1;
+  if (shape < 0 || shape > 3 || N % 16 || K_aug % 32 || M <= 0) return -1;
   return prq::launch_gemm_tile_packed(Ap, Aps, M, Wp, Wps, N, K_aug, Y, shape, stream) == hipSuccess
              ? 0
              : -3;
@@ -338,7 +338,7 @@ int prq_tune_gemm_tile_split(const uint8_t* A, const uint8_t* As, int M, const u
                              const uint8_t* Wps, int N, int K_aug, float* Y, int shape,
                              int splits, int packed, float* ws, size_t ws_bytes,
                              hipStream_t stream) {
-  if (shape < 0 || shape > 2 || N % 16 || K_aug % 32 || M <= 0 || splits < 1) return -1;
+  if (shape < 0 || shape > 3 || N % 16 || K_aug % 32 || M <= 0 || splits < 1) return -1;
   if (splits > 1 &&
       (!ws || static_cast<size_t>(splits - 1) * M * N * sizeof(float) > ws_bytes))
     return -2;   // the partial sums would not fit
@@ -348,8 +348,8 @@ int prq_tune_gemm_tile_split(const uint8_t* A, const uint8_t* As, int M, const u
              : -3;
 }
 
-// The grouped tile GEMM on a packed activation with a forced shape (0-2: a
-// workgroup per tile; 3: the persistent kernel over num_cus CUs).
+// The grouped tile GEMM on a packed activation with a forced shape (0-3: a
+// workgroup per tile; 4: the persistent kernel over num_cus CUs).
 int prq_tune_grouped_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M,
                                       const int32_t* off, int E, const uint8_t* Wp,
                                       const uint8_t* Wps, int N, int K_aug, float* Y, int shape,

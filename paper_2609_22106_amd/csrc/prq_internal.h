@@ -67,7 +67,8 @@ hipError_t launch_pack_weight(const uint8_t* Wq, const uint8_t* Wsc, int N, int 
 
 // gemm_tile.hip / gemm_stream.hip (packed weights Wp/Wps).  group_offsets ==
 // nullptr means one group of M rows.
-// Tile shapes: 0 = 256x256 (8 waves, two per SIMD), 1 = 256x128, 2 = 128x128 (4 waves).
+// Tile shapes: 0 = 256x256 (8 waves, two per SIMD), 1 = 256x128, 2 = 128x128 (4 waves),
+// 3 = 256x320 (8 waves).
 int choose_tile_shape(int M_rows, int N, int num_cus, bool packed);
 hipError_t launch_gemm_tile(const uint8_t* Aq, const uint8_t* Asc, int M,
                             const int32_t* group_offsets, int E, const uint8_t* Wp,
@@ -89,10 +90,10 @@ hipError_t launch_gemm_tile_split(const uint8_t* Aq, const uint8_t* Asc, int M, 
                                   int shape, int splits, float* ws, hipStream_t stream);
 // The grouped (MoE) tile GEMM on a packed activation: an expert's row tiles
 // start on 16-row block boundaries (rows of neighbouring experts are masked).
-// shape 0-2: a workgroup per tile; kShapePersist: the persistent kernel
+// shape 0-3: a workgroup per tile; kShapePersist: the persistent kernel
 // (128 x 128 tiles, each XCD working through its own experts, pipelined across
 // tiles; up to 512 experts) over num_cus CUs.
-constexpr int kShapePersist = 3;
+constexpr int kShapePersist = 4;
 hipError_t launch_grouped_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int M_total,
                                            const int32_t* group_offsets, int E, const uint8_t* Wp,
                                            const uint8_t* Wps, int N, int K_aug, float* Y,

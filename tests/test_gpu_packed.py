@@ -82,7 +82,7 @@ GEMM = [(300, 384, 1024), (513, 272, 1152), (40, 512, 9984), (257, 272, 1088), (
 
 
 @pytest.mark.parametrize("M,N,K_aug", GEMM)
-@pytest.mark.parametrize("shape", [None, 0, 1, 2])
+@pytest.mark.parametrize("shape", [None, 0, 1, 2, 3])
 def test_gemm_packed(shape, M, N, K_aug):
     prq = _prq()
     rng = np.random.default_rng(M * 31 + N + K_aug)
@@ -209,12 +209,12 @@ GROUPED_GEMM = [([0, 300, 0, 5, 260], 272, 1024),
 
 
 @pytest.mark.parametrize("counts,N,K_aug", GROUPED_GEMM)
-@pytest.mark.parametrize("shape,cus", [(None, None), (0, 0), (1, 0), (2, 0), (3, 256), (3, 8),
-                                       (3, 1)])
+@pytest.mark.parametrize("shape,cus", [(None, None), (0, 0), (1, 0), (2, 0), (3, 0), (4, 256),
+                                       (4, 8), (4, 1)])
 def test_grouped_gemm_packed(shape, cus, counts, N, K_aug):
     """Every row of every expert stored exactly once (Y starts as NaN) and within
     1e-3 max |Y| of the oracle's grouped GEMM (Eq. 3 per expert): a workgroup per
-    tile (shapes 0-2), or the persistent kernel (shape 3) in which each XCD's
+    tile (shapes 0-3), or the persistent kernel (shape 4) in which each XCD's
     workgroups stride over its own experts' tiles with the next tile's loads in
     flight -- on all CUs, and on 8 or 1 CU(s) so that every workgroup runs many
     tiles back to back."""

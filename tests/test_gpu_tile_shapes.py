@@ -18,7 +18,7 @@ from tests.gpu_util import assert_gemm_close, dev, host, say   # noqa: E402
 
 pytestmark = pytest.mark.gpu
 
-SHAPE_IDS = (0, 1, 2)   # 256x256, 256x128, 128x128
+SHAPE_IDS = (0, 1, 2, 3)   # 256x256, 256x128, 128x128, 256x320
 
 
 def _lib():
