@@ -98,6 +98,25 @@ struct PackedSink {
   }
 };
 
+// One row of an 8-row window of the packed layout staged in LDS: the window's
+// codes as [S][4 K parts][8 rows][16 bytes] and then its scales as
+// [ceil(S/4)][4 K parts][8 rows][4 bytes] -- the packed layout with the row
+// block cut to the window's 8 rows, so that every (step, K part) of the window
+// is 128 contiguous bytes in LDS and in global memory (its 32-byte scale runs
+// likewise).
+struct LdsPackedSink {
+  uint8_t* code;    // window codes + j 16 (j = the row's place in the window)
+  uint8_t* sc;      // window scales + j 4
+  __device__ void word(int v, uint32_t w) const {
+    const int b = v >> 2;
+    *reinterpret_cast<uint32_t*>(code + (b >> 2) * 512 + (b & 3) * 128 + (v & 3) * 4) = w;
+  }
+  __device__ void scale(int b, uint32_t c) const {
+    const int s = b >> 2;
+    sc[(s >> 2) * 128 + (b & 3) * 32 + (s & 3)] = static_cast<uint8_t>(c);
+  }
+};
+
 // Quantize 8 values of a quarter block (the quad holds the whole block) and
 // write the word, the scale and, for tail blocks, their copies.  t = z * 2^-e
 // is exact (a power-of-two product whose magnitude stays below 8, or a
@@ -131,7 +150,8 @@ __device__ __forceinline__ void quantize_store(const float (&z)[8], int u, int t
 // the last K step, scale byte 127 up to the end of the last group of four
 // steps (fewer than 16 blocks; the row's thread with unit u0 writes blocks
 // nb + u0, nb + u0 + units, ...).
-__device__ __forceinline__ void pad_row_tail(const PackedSink& out, int u0, int units, int nb,
+template <class Sink>
+__device__ __forceinline__ void pad_row_tail(const Sink& out, int u0, int units, int nb,
                                              int steps, int sgroups) {
   for (int t = u0; t < 16; t += units) {
     const int b = nb + t;
@@ -338,6 +358,12 @@ __global__ __launch_bounds__(kLdsThreads) void act_quant_lds_kernel(
 // direct-to-LDS write that the compute waves' stage reads could alias (it would
 // make them wait for all their outstanding stores); their ordering is the copy
 // waves' explicit wait and the barrier.
+// Packed output with kOut > 0: a row's 16-byte code pieces lie 256 bytes apart
+// in the packed layout, so written straight away each 128-byte line takes eight
+// partial writes.  The compute waves instead quantize into an LDS window of 8
+// rows (LdsPackedSink) and, once a row opens the next window (after the row
+// barrier, so every wave's writes are in), copy the window out in whole lines
+// and pass a second barrier (every wave in step) before they refill it.
 #define PRQ_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
 
 constexpr int kCopyWaves = 2;
@@ -360,7 +386,7 @@ __device__ __forceinline__ void lds_copy16(const void* src, uint32_t lds) {
                : "memory", "m0");
 }
 
-template <bool kGrouped, bool kPacked, int kStage, int kNS, int kUnits>
+template <bool kGrouped, bool kPacked, int kStage, int kNS, int kUnits, int kOut>
 __global__ __launch_bounds__(kDmaThreads) void act_quant_dma_kernel(
     const uint16_t* __restrict__ X, int64_t ld_x, int M, int K, int k_tail,
     const float* __restrict__ inv, const int32_t* __restrict__ perm,
@@ -370,7 +396,9 @@ __global__ __launch_bounds__(kDmaThreads) void act_quant_dma_kernel(
   constexpr int kCpw = kStage / 1024 / kCopyWaves;   // copies per copy wave per row
   static_assert(kCpw * kCopyWaves * 1024 == kStage, "stage of whole copy rounds");
   static_assert((kNS - 2) * kCpw < 64, "vmcnt");
+  constexpr bool kWindow = kPacked && kOut > 0;   // host check: 512 S + 128 ceil(S/4) <= kOut
   __shared__ __align__(16) uint8_t stg[kNS * kStage];
+  __shared__ __align__(16) uint8_t win[kWindow ? kOut : 16];
   const int r0 = blockIdx.x * rows_per_wg;
   const int r1 = min(M, r0 + rows_per_wg);
   if (r0 >= r1) return;                            // uniform
@@ -420,18 +448,42 @@ __global__ __launch_bounds__(kDmaThreads) void act_quant_dma_kernel(
   dev::GroupCursor gc;
   if (!copier) load_units(kGrouped ? gc.at(offsets, G, r0) : 0);
 
+  // Rows [lo, hi) of the window of rows [w0, w0 + 8) from LDS to the packed
+  // layout (compute waves): 16-byte code pieces, consecutive threads on
+  // consecutive pieces of one 128-byte line; 4-byte scale pieces likewise.
+  uint8_t* const win_sc = win + steps * 512;
+  auto flush = [&](int w0, int lo, int hi) {
+    const int j = tid & 7;                          // the thread's row in the window, fixed
+    if (j < lo - w0 || j >= hi - w0) return;
+    uint8_t* const gcode = Aq + static_cast<int64_t>(w0 >> 4) * steps * 1024 + (w0 & 8) * 16;
+    for (int c = tid; c < steps * 32; c += kComputeThreads)
+      *reinterpret_cast<uint4*>(gcode + (c >> 3) * 256 + j * 16) =
+          *reinterpret_cast<const uint4*>(win + c * 16);
+    uint8_t* const gsc = Asc + static_cast<int64_t>(w0 >> 4) * sgroups * 256 + (w0 & 8) * 4;
+    for (int e = tid; e < sgroups * 32; e += kComputeThreads)
+      *reinterpret_cast<uint32_t*>(gsc + (e >> 3) * 64 + j * 4) =
+          *reinterpret_cast<const uint32_t*>(win_sc + e * 4);
+  };
+
   if (copier)
     for (int i = 0; i < kNS - 1; ++i) copy_row(i);
   for (int i = 0; i < n; ++i) {
+    const int r = r0 + i;
+    const bool window_out = kWindow && i > 0 && (r & 7) == 0;   // uniform
     if (copier) {
       wait_vmcnt_lgkm0<(kNS - 2) * kCpw>();         // row i has landed
       __builtin_amdgcn_s_barrier();
       copy_row(i + kNS - 1);                        // into the stage of row i-1
+      if (window_out) __builtin_amdgcn_s_barrier();
       continue;
     }
-    wait_vmcnt_lgkm0<63>();                         // this wave's LDS reads of row i-1
+    wait_vmcnt_lgkm0<63>();                         // this wave's LDS reads of row i-1 (and writes)
     __builtin_amdgcn_s_barrier();
-    const int r = r0 + i;
+    if (window_out) {                               // the window of rows r-8..r-1 is complete
+      flush(r - 8, max(r0, r - 8), r);
+      wait_vmcnt_lgkm0<63>();
+      __builtin_amdgcn_s_barrier();
+    }
     if (kGrouped) {   // a load only when the row leaves its group
       const int g = gc.at(offsets, G, r);
       if (g != cur_g) load_units(g);
@@ -439,7 +491,9 @@ __global__ __launch_bounds__(kDmaThreads) void act_quant_dma_kernel(
     const uint16_t* row = reinterpret_cast<const uint16_t*>(stg + (i % kNS) * kStage);
     const RowSink rsink{Aq + static_cast<int64_t>(r) * row_bytes, Asc + static_cast<int64_t>(r) * nb};
     const PackedSink psink(Aq, Asc, r, steps, sgroups);
-    if constexpr (kPacked) pad_row_tail(psink, tid, units, nb, steps, sgroups);
+    const LdsPackedSink wsink{win + (r & 7) * 16, win_sc + (r & 7) * 4};
+    if constexpr (kWindow) pad_row_tail(wsink, tid, units, nb, steps, sgroups);
+    else if constexpr (kPacked) pad_row_tail(psink, tid, units, nb, steps, sgroups);
     // Units below the last always exist (the host picks kUnits = ceil(units /
     // kComputeThreads)): no guard, so their LDS gathers can all be in flight
     // together; the last unit is guarded (quad-uniform: units % 4 == 0).
@@ -454,7 +508,9 @@ __global__ __launch_bounds__(kDmaThreads) void act_quant_dma_kernel(
           z[2 * e] = __uint_as_float(static_cast<uint32_t>(row[sp & 0xFFFFu]) << 16) * un[j].d[2 * e];
           z[2 * e + 1] = __uint_as_float(static_cast<uint32_t>(row[sp >> 16]) << 16) * un[j].d[2 * e + 1];
         }
-        if constexpr (kPacked)
+        if constexpr (kWindow)
+          quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, wsink);
+        else if constexpr (kPacked)
           quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, psink);
         else
           quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, rsink);
@@ -462,6 +518,12 @@ __global__ __launch_bounds__(kDmaThreads) void act_quant_dma_kernel(
     }
   }
   if (copier) __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));   // no copy outlives the workgroup
+  if constexpr (kWindow) {   // the last (possibly partial) window: every wave passes the barrier
+    if (!copier) wait_vmcnt_lgkm0<63>();
+    __builtin_amdgcn_s_barrier();
+    const int w0 = (r1 - 1) & ~7;
+    if (!copier) flush(w0, max(r0, w0), r1);
+  }
 
   // Packed layout: the workgroup with the last row also fills the rows of the
   // last 16-row block past M (zero codes, scale byte 127).
@@ -494,20 +556,49 @@ int lds_rows_per_wg(int M, int units, int num_cus) {
 }
 
 // Stage classes of the copy kernel by row length (2K bytes): stage bytes, stages,
-// units per compute thread (K/8 units over 512 threads).  At most 128 KiB of LDS.
+// units per compute thread (K/8 units over 512 threads), LDS bytes of the packed
+// output window (each workgroup's LDS within 160 KiB / workgroups per CU; the
+// window holds K + k up to 2K in the first three classes, up to 15360 in the
+// fourth, never in the last).  window: 0 = where it pays, 1 = where it fits,
+// 2 = never (packed output stored directly).  It pays on long rows with many
+// rows per workgroup: a row block's lines then stay partial in L2 too long
+// (cold, M = 8192 x 9728: 56.5 -> 42.5 us, M = 4096: 29.5 -> 23.7); with short
+// rows they complete in L2 anyway and the window's last flush is pure latency
+// (M = 4096 x 2560: 8.5 -> 12.3 us; M = 512 x 9728, two rows each: 6.8 -> 8.1).
 static_assert(kComputeThreads == 512, "stage classes assume 512 compute threads");
+constexpr int kWindowBytes[5] = {17408, 34816, 69632, 65536, 0};
+constexpr int cls_of(int stage) {
+  return stage <= 4096 ? 0 : stage <= 8192 ? 1 : stage <= 16384 ? 2 : stage <= 24576 ? 3 : 4;
+}
+
+int packed_window_bytes(int K_aug) {
+  const int steps = (K_aug + 127) / 128;
+  return steps * 512 + (steps + 3) / 4 * 128;
+}
+
 template <bool kGrouped, bool kPacked>
 hipError_t launch_dma(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail, const float* inv,
                       const int32_t* perm, const int32_t* offsets, int G, uint8_t* Aq, uint8_t* Asc,
-                      int num_cus, hipStream_t stream) {
+                      int num_cus, hipStream_t stream, int window = 0) {
   const int rb = 2 * K;
   const int per_cu = rb <= 8192 ? 2 : 1;           // workgroups a CU holds (LDS)
   const int target = std::max(1, num_cus * per_cu);
   const int rows_per_wg = std::max(1, (M + target - 1) / target);
   const dim3 grid((M + rows_per_wg - 1) / rows_per_wg);
-#define PRQ_DMA(STAGE, NS, U)                                                                     \
-  act_quant_dma_kernel<kGrouped, kPacked, STAGE, NS, U><<<grid, kDmaThreads, 0, stream>>>(       \
+  const int cls = rb <= 4096 ? 0 : rb <= 8192 ? 1 : rb <= 16384 ? 2 : rb <= 24576 ? 3 : 4;
+  const bool pays = K > 8192 && rows_per_wg >= 16;
+  const bool win = kPacked && window != 2 && (window == 1 || pays) &&
+                   packed_window_bytes(K + k_tail) <= kWindowBytes[cls];
+#define PRQ_DMA_OUT(STAGE, NS, U, OUT)                                                            \
+  act_quant_dma_kernel<kGrouped, kPacked, STAGE, NS, U, OUT><<<grid, kDmaThreads, 0, stream>>>(  \
       X, ld_x, M, K, k_tail, inv, perm, offsets, G, rows_per_wg, Aq, Asc)
+#define PRQ_DMA(STAGE, NS, U)                                                                     \
+  do {                                                                                            \
+    if (kPacked && win)                                                                           \
+      PRQ_DMA_OUT(STAGE, NS, U, (kPacked ? kWindowBytes[cls_of(STAGE)] : 0));                     \
+    else                                                                                          \
+      PRQ_DMA_OUT(STAGE, NS, U, 0);                                                               \
+  } while (0)
   // kUnits = ceil(K / 8 / 512) exactly: every unit but the last exists.
   // Four stages in every class: with all of a
   // workgroup's rows requested at once (up to 8 stages) the copies of the
@@ -518,8 +609,9 @@ hipError_t launch_dma(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail,
   else if (rb <= 8192) PRQ_DMA(8192, 4, 1);
   else if (rb <= 16384) PRQ_DMA(16384, 4, 2);
   else if (rb <= 24576) PRQ_DMA(24576, 4, 3);
-  else PRQ_DMA(32768, 4, 4);
+  else PRQ_DMA_OUT(32768, 4, 4, 0);
 #undef PRQ_DMA
+#undef PRQ_DMA_OUT
   return hipGetLastError();
 }
 
@@ -603,12 +695,13 @@ hipError_t launch_act_quant_packed_kernel(const uint16_t* X, int64_t ld_x, int M
                                           int kernel, hipStream_t stream) {
   const bool grouped = group_offsets && G > 1;
   const int32_t* off = grouped ? group_offsets : nullptr;
-  if (kernel == 3 || (kernel == 0 && K >= 2048)) {
+  if (kernel == 3 || kernel == 4 || (kernel == 0 && K >= 2048)) {
+    const int window = kernel == 3 ? 1 : kernel == 4 ? 2 : 0;
     if (grouped)
       return launch_dma<true, true>(X, ld_x, M, K, k_tail, inv_scale_pos, perm, off, G, Ap, Aps,
-                                    num_cus, stream);
+                                    num_cus, stream, window);
     return launch_dma<false, true>(X, ld_x, M, K, k_tail, inv_scale_pos, perm, nullptr, 1, Ap, Aps,
-                                   num_cus, stream);
+                                   num_cus, stream, window);
   }
   const int units = K >> 3;
   const size_t lds = lds_kernel_bytes(K);

@@ -52,7 +52,9 @@ hipError_t launch_act_quant_packed(const uint16_t* X, int64_t ld_x, int M, int K
                                    const float* inv_scale_pos, const int32_t* perm,
                                    const int32_t* group_offsets, int G, uint8_t* Ap, uint8_t* Aps,
                                    int num_cus, hipStream_t stream);
-// kernel: 0 = automatic, 2 = register-staged rows, 3 = rows copied into LDS stages.
+// kernel: 0 = automatic, 2 = register-staged rows, 3 = rows copied into LDS stages
+// with the output through an 8-row LDS window wherever it fits (automatic: only
+// where it pays), 4 = as 3 with the output stored directly.
 hipError_t launch_act_quant_packed_kernel(const uint16_t* X, int64_t ld_x, int M, int K,
                                           int k_tail, const float* inv_scale_pos,
                                           const int32_t* perm, const int32_t* group_offsets,

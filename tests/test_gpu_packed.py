@@ -66,6 +66,66 @@ def test_quant_act_packed_overwrites_stale_padding():
     np.testing.assert_array_equal(host(out.Ap), ep)
 
 
+def _tune_quant_packed(X, K, k, inv_pos, perm, off, G, kernel, num_cus):
+    """The packed quantizer through the tuning entry (kernel 3: output through
+    the 8-row LDS window where it fits; 4: stored directly), its row ranges
+    sized for num_cus CUs, into buffers pre-filled with other bytes."""
+    from paper_2609_22106_amd import build
+    prq = _prq()
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    P, I = ctypes.c_void_p, ctypes.c_int
+    lib.prq_tune_act_quant_packed.argtypes = [P, ctypes.c_int64, I, I, I, P, P, P, I, P, P, I, I,
+                                              P]
+    lib.prq_tune_act_quant_packed.restype = I
+    M = X.shape[0]
+    cb, sb = prq.prq_packed_act_bytes(M, K + k)
+    Ap = torch.full((cb,), 0xAB, dtype=torch.uint8, device="cuda")
+    Aps = torch.full((sb,), 0xCD, dtype=torch.uint8, device="cuda")
+    Xd = dev(X)
+    args = [dev(a) if a is not None else None for a in (inv_pos, perm, off)]
+    rc = lib.prq_tune_act_quant_packed(
+        Xd.data_ptr(), K, M, K, k, *[a.data_ptr() if a is not None else None for a in args], G,
+        Ap.data_ptr(), Aps.data_ptr(), kernel, num_cus, torch.cuda.current_stream().cuda_stream)
+    assert rc == 0, rc
+    torch.cuda.synchronize()
+    return host(Ap), host(Aps)
+
+
+# (M, K, k, num_cus): row ranges of several rows that start and end inside
+# 8-row windows (a CU count that makes them so), ragged M, K + k not a whole
+# number of 128-element steps, the largest K + k each stage class takes through
+# the window (2K in the first three classes, 17408 and 65280 window bytes) and
+# sizes past it (stored directly), the largest class (always direct).
+WINDOW_QUANT = [(1000, 2560, 64, 13),     # 39 rows per workgroup, 8192-byte stages
+                (517, 9728, 256, 7),      # 74 rows, the down_proj row, 24576-byte stages
+                (300, 4096, 1024, 5),     # 30 rows
+                (260, 8192, 2048, 3),     # 87 rows, 16384-byte stages
+                (77, 2048, 2048, 2),      # 4096-byte stages, window exactly full
+                (40, 12288, 3072, 2),     # 24576-byte stages, K + k = 15360 (65280 bytes)
+                (40, 12288, 4096, 2),     # K + k = 16384: past the window, stored directly
+                (24, 16384, 512, 2),      # 32768-byte stages: stored directly
+                (100, 2080, 32, 3)]       # K + k = 2112 = 16.5 steps
+
+
+@pytest.mark.parametrize("M,K,k,cus", WINDOW_QUANT)
+@pytest.mark.parametrize("kernel", [3, 4])
+def test_quant_act_packed_windows(kernel, M, K, k, cus):
+    """The LDS-staged packed quantizer with multi-row workgroup ranges, its
+    output through the 8-row LDS window (kernel 3) or stored directly (4):
+    every code and scale byte, padding included, as the oracle's quantizer laid
+    out by the reference packer."""
+    rng = np.random.default_rng(M * 7 + K + k + kernel)
+    X = inputs.f32_to_bf16_bits((rng.standard_normal((M, K)) *
+                                 rng.uniform(0.01, 30.0, K)).astype(np.float32))
+    inv = rng.uniform(0.25, 4.0, K).astype(np.float32)
+    perm = rng.permutation(K).astype(np.int32)
+    say("packed window quant case:", kernel, M, K, k, cus)
+    ap, aps = _tune_quant_packed(X, K, k, _pos(inv, perm), perm, None, 1, kernel, cus)
+    ep, es = pack_rows(*pq.quant_act(X, inv, perm, k))
+    np.testing.assert_array_equal(aps, es, err_msg="packed scales")
+    np.testing.assert_array_equal(ap, ep, err_msg="packed codes")
+
+
 def _tune_packed(shape, A, W, Y):
     from paper_2609_22106_amd import build
     lib = ctypes.CDLL(build.PROBE_LIB)
@@ -184,6 +244,33 @@ def test_quant_act_packed_grouped(counts, K, k):
     ep, es = pack_rows(*pq.quant_act_grouped(X, inv, perm, off, k))
     np.testing.assert_array_equal(host(A.Aps), es, err_msg="packed scales")
     np.testing.assert_array_equal(host(A.Ap), ep, err_msg="packed codes")
+
+
+# Experts changing inside 8-row windows and inside a workgroup's range.
+GROUPED_WINDOW_QUANT = [([40, 0, 90, 7, 300], 4160, 160, 3),
+                        ([17, 1, 0, 33, 250, 2], 2048, 32, 5),
+                        ([5, 60, 0, 129], 9728, 256, 2)]
+
+
+@pytest.mark.parametrize("counts,K,k,cus", GROUPED_WINDOW_QUANT)
+@pytest.mark.parametrize("kernel", [3, 4])
+def test_quant_act_packed_grouped_windows(kernel, counts, K, k, cus):
+    """Grouped rows through the LDS-staged packed quantizer with multi-row
+    workgroup ranges (window or direct output): every byte as the oracle's
+    grouped quantizer laid out by the reference packer."""
+    rng = np.random.default_rng(sum(counts) * 3 + K + k + kernel)
+    E = len(counts)
+    off = inputs.routed_offsets(counts)
+    M = int(off[-1])
+    X = inputs.f32_to_bf16_bits((rng.standard_normal((M, K)) *
+                                 rng.uniform(0.01, 30.0, K)).astype(np.float32))
+    perm = np.stack([rng.permutation(K) for _ in range(E)]).astype(np.int32)
+    inv = rng.uniform(0.1, 4.0, (E, K)).astype(np.float32)
+    say("packed grouped window quant case:", kernel, counts, K, k, cus)
+    ap, aps = _tune_quant_packed(X, K, k, _pos_grouped(inv, perm), perm, off, E, kernel, cus)
+    ep, es = pack_rows(*pq.quant_act_grouped(X, inv, perm, off, k))
+    np.testing.assert_array_equal(aps, es, err_msg="packed scales")
+    np.testing.assert_array_equal(ap, ep, err_msg="packed codes")
 
 
 def _tune_grouped_packed(shape, A, off, W, Y, num_cus):
