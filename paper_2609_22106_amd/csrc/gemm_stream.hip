@@ -3,12 +3,13 @@
 // few activation rows meet each weight row and the kernel is bound by
 // reading W_aug once from HBM.
 //
-//   * A workgroup owns kT tiles of 16 output features and one split of the
-//     K steps (128 elements each); its kWaves waves are kT tiles x
-//     (kWaves / kT) K chunks of kU contiguous steps.  The weight, in the
-//     packed layout of pack.hip, is the MFMA A operand: each wave reads kU
-//     contiguous kilobytes and issues all of them before anything else, so a
-//     launch has all of W_aug in flight.
+//   * A workgroup owns kT x kTW tiles of 16 output features and one split of
+//     the K steps (128 elements each); its kWaves waves are kT tile groups x
+//     (kWaves / kT) K chunks of kU contiguous steps, a wave computing the kTW
+//     tiles of its group over its chunk.  The weight, in the packed layout of
+//     pack.hip, is the MFMA A operand: each wave reads kTW x kU kilobytes and
+//     issues all of them before anything else, so a launch has all of W_aug
+//     in flight.  An activation operand a wave loads feeds its kTW tiles.
 //   * The activation rows of the pass (16 * kG rows) over the split's K range
 //     are staged once per workgroup into LDS (rows padded so that the 16-byte
 //     lane reads of one MFMA operand fall in distinct banks) and shared by all
@@ -67,15 +68,15 @@ __global__ __launch_bounds__(256) void zero_kernel(float* __restrict__ Y, int64_
 // 16-byte bank groups.
 __host__ __device__ inline int act_row_stride(int nst) { return ((nst + 3) & ~3) * kStepBytes + 16; }
 
-inline size_t stream_lds_bytes(int waves, int groups, int nst, bool stage_lds) {
+inline size_t stream_lds_bytes(int waves, int groups, int nst, bool stage_lds, int wave_tiles) {
   const size_t stage = stage_lds
       ? static_cast<size_t>(16 * groups) * (act_row_stride(nst) + ((nst + 3) & ~3) * 4)
       : 0;
-  const size_t red = static_cast<size_t>(waves) * groups * 64 * 4 * sizeof(float);
+  const size_t red = static_cast<size_t>(waves) * wave_tiles * groups * 64 * 4 * sizeof(float);
   return std::max(stage, red);
 }
 
-template <bool kGrouped, int kWaves, int kU, int kG, int kT>
+template <bool kGrouped, int kWaves, int kU, int kG, int kT, int kTW>
 __global__ __launch_bounds__(kWaves * 64) void gemm_stream_kernel(
     const uint8_t* __restrict__ Aq, const uint8_t* __restrict__ Asc, int M,
     const int32_t* __restrict__ off, const uint8_t* __restrict__ Wp,
@@ -103,8 +104,7 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_stream_kernel(
   const int lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 15, lk = lane >> 4;
   const int t_in = wave % kT, chunk = wave / kT;
-  const int tile = blockIdx.x * kT + t_in;
-  const bool tile_ok = tile < ntiles;
+  const int tile0 = (blockIdx.x * kT + t_in) * kTW;  // the wave's first tile
   const int s_begin = steps * split / splits;        // steps * splits < 2^31
   const int s_end = steps * (split + 1) / splits;
   const int nst = s_end - s_begin;
@@ -115,34 +115,47 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_stream_kernel(
   //    loads are unconditional; nothing reads their results until every load
   //    of the kernel is in flight (a use would make the wave wait for all of
   //    them, the memory counter being in order).
-  const int64_t et = static_cast<int64_t>(e) * ntiles + (tile_ok ? tile : 0);
-  const uint8_t* Wt = Wp + (et * steps + s_begin) * 1024 + lane * 16;
-  const uint32_t* Wst = reinterpret_cast<const uint32_t*>(Wps) + et * sgroups * 64 + lane;
-  uint4 w[kU];
-  uint32_t wsraw[kU];
+  uint4 w[kTW][kU];
+  uint32_t wsraw[kTW][kU];
+  bool tile_ok[kTW];
 #pragma unroll
-  for (int j = 0; j < kU; ++j) {
-    const int st = min(st0 + j, nst - 1);
-    w[j] = *reinterpret_cast<const uint4*>(Wt + static_cast<int64_t>(st) * 1024);
+  for (int tw = 0; tw < kTW; ++tw) {
+    tile_ok[tw] = tile0 + tw < ntiles;
+    const int64_t et = static_cast<int64_t>(e) * ntiles + (tile_ok[tw] ? tile0 + tw : 0);
+    const uint8_t* Wt = Wp + (et * steps + s_begin) * 1024 + lane * 16;
+#pragma unroll
+    for (int j = 0; j < kU; ++j) {
+      const int st = min(st0 + j, nst - 1);
+      w[tw][j] = *reinterpret_cast<const uint4*>(Wt + static_cast<int64_t>(st) * 1024);
+    }
   }
 #pragma unroll
-  for (int j = 0; j < kU; ++j) wsraw[j] = Wst[((s_begin + min(st0 + j, nst - 1)) >> 2) * 64];
+  for (int tw = 0; tw < kTW; ++tw) {
+    const int64_t et = static_cast<int64_t>(e) * ntiles + (tile_ok[tw] ? tile0 + tw : 0);
+    const uint32_t* Wst = reinterpret_cast<const uint32_t*>(Wps) + et * sgroups * 64 + lane;
+#pragma unroll
+    for (int j = 0; j < kU; ++j) wsraw[tw][j] = Wst[((s_begin + min(st0 + j, nst - 1)) >> 2) * 64];
+  }
 
   const int stride = act_row_stride(nst);
   const int sstride = ((nst + 3) & ~3) * 4;          // scale bytes per staged row
   uint8_t* sA = smem;
   uint8_t* sAs = smem + 16 * kG * stride;
   float* s_red = reinterpret_cast<float*>(smem);     // reused after the MFMAs
-  const int cols = min(16 * kT, N - static_cast<int>(blockIdx.x) * 16 * kT);
-  bool kok[kU];
+  const int cols = min(16 * kT * kTW, N - static_cast<int>(blockIdx.x) * 16 * kT * kTW);
+  bool kok[kTW][kU];
 #pragma unroll
-  for (int j = 0; j < kU; ++j) kok[j] = tile_ok && st0 + j < nst;
+  for (int tw = 0; tw < kTW; ++tw)
+#pragma unroll
+    for (int j = 0; j < kU; ++j) kok[tw][j] = tile_ok[tw] && st0 + j < nst;
 
   for (int pass_row = row_begin; pass_row < row_end; pass_row += 16 * kG) {
     const int rows = min(16 * kG, row_end - pass_row);
-    v4f acc[kG];
+    v4f acc[kTW][kG];
 #pragma unroll
-    for (int g = 0; g < kG; ++g) acc[g] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int tw = 0; tw < kTW; ++tw)
+#pragma unroll
+      for (int g = 0; g < kG; ++g) acc[tw][g] = v4f{0.f, 0.f, 0.f, 0.f};
     if (stage) {
       // 2. Stage the pass's activation rows over [s_begin, s_end) in LDS
       //    (zero codes and a neutral scale past K_aug).  Four items per
@@ -179,17 +192,21 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_stream_kernel(
 #pragma unroll
       for (int j = 0; j < kU; ++j) {
         const int s = s_begin + st0 + j;
-        const uint4 wj = kok[j] ? w[j] : make_uint4(0, 0, 0, 0);
-        const uint32_t sw = kok[j] ? (wsraw[j] >> (8 * (s & 3))) & 0xFFu : kNeutralScale;
         const int st = min(st0 + j, nst - 1);
 #pragma unroll
         for (int g = 0; g < kG; ++g) {
           const int r = min(g * 16 + lr, rows - 1);
-          const bool ok = kok[j] && g * 16 + lr < rows;
+          const bool rok = g * 16 + lr < rows;
           const uint4 a = *reinterpret_cast<const uint4*>(sA + r * stride + st * kStepBytes + lk * 16);
           const uint32_t sa = sAs[r * sstride + st * 4 + lk];
-          acc[g] = dev::mfma_fp4_16x16x128(wj, ok ? a : make_uint4(0, 0, 0, 0), sw,
-                                           ok ? sa : kNeutralScale, acc[g]);
+#pragma unroll
+          for (int tw = 0; tw < kTW; ++tw) {
+            const uint4 wj = kok[tw][j] ? w[tw][j] : make_uint4(0, 0, 0, 0);
+            const uint32_t sw = kok[tw][j] ? (wsraw[tw][j] >> (8 * (s & 3))) & 0xFFu : kNeutralScale;
+            const bool ok = kok[tw][j] && rok;
+            acc[tw][g] = dev::mfma_fp4_16x16x128(wj, ok ? a : make_uint4(0, 0, 0, 0), sw,
+                                                 ok ? sa : kNeutralScale, acc[tw][g]);
+          }
         }
       }
     } else {
@@ -211,35 +228,49 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_stream_kernel(
 #pragma unroll
       for (int j = 0; j < kU; ++j) {
         const int s = s_begin + st0 + j;
-        const bool kin = kok[j] && s * kStepK + lk * 32 < K_aug;
-        const uint4 wj = kok[j] ? w[j] : make_uint4(0, 0, 0, 0);
-        const uint32_t sw = kok[j] ? (wsraw[j] >> (8 * (s & 3))) & 0xFFu : kNeutralScale;
 #pragma unroll
-        for (int g = 0; g < kG; ++g) {
-          const bool ok = kin && g * 16 + lr < rows;
-          acc[g] = dev::mfma_fp4_16x16x128(wj, ok ? a[j][g] : make_uint4(0, 0, 0, 0), sw,
-                                           ok ? static_cast<uint32_t>(sa[j][g]) : kNeutralScale, acc[g]);
+        for (int tw = 0; tw < kTW; ++tw) {
+          const bool kin = kok[tw][j] && s * kStepK + lk * 32 < K_aug;
+          const uint4 wj = kok[tw][j] ? w[tw][j] : make_uint4(0, 0, 0, 0);
+          const uint32_t sw = kok[tw][j] ? (wsraw[tw][j] >> (8 * (s & 3))) & 0xFFu : kNeutralScale;
+#pragma unroll
+          for (int g = 0; g < kG; ++g) {
+            const bool ok = kin && g * 16 + lr < rows;
+            acc[tw][g] = dev::mfma_fp4_16x16x128(wj, ok ? a[j][g] : make_uint4(0, 0, 0, 0), sw,
+                                                 ok ? static_cast<uint32_t>(sa[j][g]) : kNeutralScale,
+                                                 acc[tw][g]);
+          }
         }
       }
     }
     __syncthreads();   // the staging buffer becomes the reduction buffer
 
-    // 3. Reduce the K chunks of each tile.  acc[g][q] of this lane is
-    //    Y[pass_row + 16 g + lr][16 tile + 4 lk + q]; wave = chunk * kT + t_in.
+    // 3. Reduce the K chunks of each tile.  acc[tw][g][q] of this lane is
+    //    Y[pass_row + 16 g + lr][16 (tile0 + tw) + 4 lk + q]; wave = chunk * kT + t_in.
 #pragma unroll
-    for (int g = 0; g < kG; ++g)
+    for (int tw = 0; tw < kTW; ++tw)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) s_red[((wave * kG + g) * 64 + lane) * 4 + q] = acc[g][q];
+      for (int g = 0; g < kG; ++g)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          s_red[(((wave * kTW + tw) * kG + g) * 64 + lane) * 4 + q] = acc[tw][g][q];
     __syncthreads();
-    for (int idx = tid; idx < kT * kG * 256; idx += kWaves * 64) {
-      const int t = idx / (kG * 256), r = idx % (kG * 256);
-      const int g = r >> 8, l = (r >> 2) & 63, q = r & 3;
-      const int m = pass_row + g * 16 + (l & 15);
-      const int out_tile = blockIdx.x * kT + t;
+    // Thread idx: tile t * kTW + tw of the workgroup, row group g, lane l, q;
+    // consecutive threads cover a row's 16 features and then the next tile,
+    // so a row of the workgroup's columns is written in one contiguous run.
+    for (int idx = tid; idx < kT * kTW * kG * 256; idx += kWaves * 64) {
+      const int g = idx / (kT * kTW * 256), r = idx % (kT * kTW * 256);
+      const int lr16 = r / (kT * kTW * 16), c16 = r % (kT * kTW * 16);
+      const int tt = c16 >> 4, f = c16 & 15;             // workgroup tile, feature in tile
+      const int t = tt / kTW, tw = tt % kTW;
+      const int l = (f >> 2) * 16 + lr16, q = f & 3;     // the lane and element holding it
+      const int m = pass_row + g * 16 + lr16;
+      const int out_tile = (blockIdx.x * kT + t) * kTW + tw;
       if (m < row_end && out_tile < ntiles) {
         float v = 0.0f;
 #pragma unroll
-        for (int c = 0; c < kChunks; ++c) v += s_red[(((c * kT + t) * kG + g) * 64 + l) * 4 + q];
+        for (int c = 0; c < kChunks; ++c)
+          v += s_red[((((c * kT + t) * kTW + tw) * kG + g) * 64 + l) * 4 + q];
         const int64_t o = static_cast<int64_t>(m) * N + out_tile * 16 + 4 * (l >> 4) + q;
         if (splits == 1)
           Y[o] = v;
@@ -266,7 +297,7 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_stream_kernel(
   const int count = (row_end - row_begin) * cols;
   for (int idx = tid; idx < count; idx += kWaves * 64) {
     const int64_t o = static_cast<int64_t>(row_begin + idx / cols) * N +
-                      static_cast<int64_t>(blockIdx.x) * 16 * kT + idx % cols;
+                      static_cast<int64_t>(blockIdx.x) * 16 * kT * kTW + idx % cols;
     Y[o] = atomicExch(&acc_ws[o], 0.0f);
   }
   if (tid == 0) atomicExch(ctr, 0u);
@@ -278,24 +309,30 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_stream_kernel(
       const uint8_t *Wp, const uint8_t *Wps, int N, int K_aug, float *Y, int splits,        \
       int flags, float *acc, uint32_t *ctr, hipStream_t stream
 
-template <bool kGrouped, int kWaves, int kU, int kG, int kT>
+template <bool kGrouped, int kWaves, int kU, int kG, int kT, int kTW>
 hipError_t launch_cfg(PRQ_STREAM_PARAMS) {
   static std::once_flag attr_once;   // dynamic LDS above the 64 KiB default
   std::call_once(attr_once, [] {
     (void)hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&gemm_stream_kernel<kGrouped, kWaves, kU, kG, kT>),
+        reinterpret_cast<const void*>(&gemm_stream_kernel<kGrouped, kWaves, kU, kG, kT, kTW>),
         hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kMaxStreamLds));
     (void)hipGetLastError();
   });
-  gemm_stream_kernel<kGrouped, kWaves, kU, kG, kT><<<grid, kWaves * 64, lds, stream>>>(
+  gemm_stream_kernel<kGrouped, kWaves, kU, kG, kT, kTW><<<grid, kWaves * 64, lds, stream>>>(
       Aq, Asc, M, off, Wp, Wps, N, K_aug, Y, splits, flags, acc, ctr);
   return hipGetLastError();
 }
 
+// T: 1 = one tile per workgroup, 4 = four tiles per workgroup (one per wave
+// group), 5 = four tiles per wave (one wave group; at most 8 waves of at most
+// 4 steps and one row group, so that the 16 weight kilobytes of a wave fit
+// its registers -- stream_config_covers admits no other).
 template <bool kGrouped, int kWaves, int kU, int kG>
 hipError_t launch_t(int T, PRQ_STREAM_PARAMS) {
-  if (!kGrouped && T == 4) return launch_cfg<kGrouped, kWaves, kU, kG, 4>(PRQ_STREAM_ARGS);
-  return launch_cfg<kGrouped, kWaves, kU, kG, 1>(PRQ_STREAM_ARGS);
+  if constexpr (kWaves <= 8 && kU <= 4 && kG == 1)
+    if (T == 5) return launch_cfg<kGrouped, kWaves, kU, kG, 1, 4>(PRQ_STREAM_ARGS);
+  if (T == 4) return launch_cfg<kGrouped, kWaves, kU, kG, 4, 1>(PRQ_STREAM_ARGS);
+  return launch_cfg<kGrouped, kWaves, kU, kG, 1, 1>(PRQ_STREAM_ARGS);
 }
 
 template <bool kGrouped, int kWaves, int kU>
@@ -339,6 +376,12 @@ StreamConfig choose_stream_config(int M_per_group, int N, int K_aug, int grouped
     c.stage_lds = false;
     c.waves = steps <= 32 ? 4 : 16;
     c.unroll = round_unroll((steps + c.waves - 1) / c.waves);
+    // Four tiles per wave where the registers allow: an activation operand a
+    // wave loads (one kilobyte per lane group for the expert's few rows) then
+    // feeds four weight kilobytes instead of one, and a row's Y values of the
+    // workgroup are 256 contiguous bytes (128 experts x 2048 x 832, 512 routed
+    // rows: 29.3 -> 24.6 us; eight tiles per wave, half the workgroups: 30.8).
+    if (c.waves <= 8 && c.unroll <= 4 && c.groups == 1) c.wave_tiles = 4;
   } else {
     // Decode shapes (measured on the 9728 -> 2560 down_proj): up to 32 rows,
     // 8-wave workgroups, 3 K splits, activation operands loaded per wave,
@@ -381,11 +424,14 @@ bool stream_config_covers(const StreamConfig& c, int K_aug) {
                       c.unroll == 6 || c.unroll == 8) &&
                      (c.groups == 1 || c.groups == 2 || c.groups == 4) && c.splits >= 1 &&
                      c.splits <= steps;
-  const bool tiles_ok = c.tiles == 1 || (c.tiles == 4 && c.waves >= 4);
+  const bool tiles_ok = (c.tiles == 1 || (c.tiles == 4 && c.waves >= 4)) &&
+                        (c.wave_tiles == 1 ||
+                         (c.wave_tiles == 4 && c.tiles == 1 && c.waves <= 8 && c.unroll <= 4 &&
+                          c.groups == 1));
   if (!shape || !tiles_ok || c.reduce < 0 || c.reduce > 2) return false;
   const int nst_max = (steps + c.splits - 1) / c.splits;
   return static_cast<int64_t>(c.waves / c.tiles) * c.unroll >= nst_max &&
-         stream_lds_bytes(c.waves, c.groups, nst_max, c.stage_lds) <= kMaxStreamLds;
+         stream_lds_bytes(c.waves, c.groups, nst_max, c.stage_lds, c.wave_tiles) <= kMaxStreamLds;
 }
 
 int choose_variant(int M_per_group, int N, int K_aug) {
@@ -419,18 +465,20 @@ hipError_t launch_gemm_stream(const uint8_t* Aq, const uint8_t* Asc, int M,
   }
   const int flags = (cfg.stage_lds ? 0 : kDirectA) | (cfg.reduce << 1);
   const int steps = (K_aug + kStepK - 1) / kStepK;
-  const size_t lds = stream_lds_bytes(cfg.waves, cfg.groups, (steps + cfg.splits - 1) / cfg.splits, cfg.stage_lds);
-  const int T = group_offsets ? 1 : cfg.tiles;
-  const dim3 grid((N / 16 + T - 1) / T, cfg.splits, group_offsets ? E : 1);
+  const size_t lds = stream_lds_bytes(cfg.waves, cfg.groups, (steps + cfg.splits - 1) / cfg.splits,
+                                      cfg.stage_lds, cfg.wave_tiles);
+  const int per_wg = cfg.tiles * cfg.wave_tiles;     // 16-feature tiles per workgroup
+  const int T = cfg.wave_tiles == 4 ? 5 : cfg.tiles;
+  const dim3 grid((N / 16 + per_wg - 1) / per_wg, cfg.splits, group_offsets ? E : 1);
   const int U = cfg.unroll, G = cfg.groups;
   const int32_t* off = group_offsets;
   const int splits = cfg.splits;
   hipError_t err;
   if (group_offsets) {
     switch (cfg.waves) {
-      case 4: err = launch_u<true, 4>(U, G, 1, PRQ_STREAM_ARGS); break;
-      case 8: err = launch_u<true, 8>(U, G, 1, PRQ_STREAM_ARGS); break;
-      default: err = launch_u<true, 16>(U, G, 1, PRQ_STREAM_ARGS); break;
+      case 4: err = launch_u<true, 4>(U, G, T, PRQ_STREAM_ARGS); break;
+      case 8: err = launch_u<true, 8>(U, G, T, PRQ_STREAM_ARGS); break;
+      default: err = launch_u<true, 16>(U, G, T, PRQ_STREAM_ARGS); break;
     }
   } else {
     switch (cfg.waves) {

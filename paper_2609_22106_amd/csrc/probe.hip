@@ -171,9 +171,11 @@ int prq_probe_cvt_pairs(const float* x, const float* y, const float* s, int n, u
 int prq_tune_gemm_stream(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off, int E,
                          const uint8_t* Wq, const uint8_t* Wsc, int N, int K_aug, float* Y,
                          int splits, int waves, int unroll, int groups, int tiles,
-                         int stage_lds, int reduce, void* workspace, hipStream_t stream) {
+                         int stage_lds, int reduce, int wave_tiles, void* workspace,
+                         hipStream_t stream) {
   prq::StreamConfig c;
   c.tiles = tiles;
+  c.wave_tiles = wave_tiles;
   c.stage_lds = stage_lds != 0;
   c.reduce = reduce;
   c.splits = splits;

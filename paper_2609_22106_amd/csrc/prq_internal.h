@@ -17,7 +17,8 @@ struct StreamConfig {
   int waves = 16;   // waves per workgroup (4, 8 or 16)
   int unroll = 8;   // K steps per wave (1, 2, 3, 4, 6 or 8)
   int groups = 1;   // 16-row activation column groups per pass (1, 2 or 4)
-  int tiles = 1;    // 16-feature tiles per workgroup (1 or 4; dense only)
+  int tiles = 1;    // 16-feature tile groups per workgroup (1 or 4)
+  int wave_tiles = 1;  // 16-feature tiles per wave (1, or 4 with one tile group)
   bool stage_lds = true;  // activation staged in LDS per workgroup (else per-wave loads)
   int reduce = 0;   // split-K: 0 atomic accumulator + last arriver, 1 partial sums +
                     // reduce kernel (deterministic), 2 atomics into Y zeroed first

@@ -140,6 +140,71 @@ def test_split_k_workspace_reuse_and_two_splits_are_deterministic():
             np.testing.assert_array_equal(ys[0].view(np.uint32), ys[2].view(np.uint32))
 
 
+def _tune_stream(Aq, Asc, Wq, Wsc, splits, waves, unroll, stage, reduce, wave_tiles, off=None,
+                 E=1):
+    """The weight-streaming kernel with an explicit configuration (one row
+    group per pass, one tile group per workgroup)."""
+    import ctypes
+    from paper_2609_22106_amd import build
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    P, I = ctypes.c_void_p, ctypes.c_int
+    lib.prq_tune_gemm_stream.argtypes = [P, P, I, P, I, P, P, I, I, P] + [I] * 8 + [P, P]
+    W = _packed(Wq, Wsc)
+    A, S = dev(Aq), dev(Asc)
+    M = Aq.shape[0]
+    Y = torch.full((M, W.N), float("nan"), dtype=torch.float32, device="cuda")
+    ws = torch.zeros(splits * M * W.N * 4 + 4 * 65536, dtype=torch.uint8, device="cuda")
+    o = dev(off) if off is not None else None
+    st = lib.prq_tune_gemm_stream(A.data_ptr(), S.data_ptr(), M, None if o is None else o.data_ptr(),
+                                  E, W.Wp.data_ptr(), W.Wps.data_ptr(), W.N, W.K_aug, Y.data_ptr(),
+                                  splits, waves, unroll, 1, 1, stage, reduce, wave_tiles,
+                                  ws.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    return st, host(Y)
+
+
+# (splits, waves, unroll, stage, reduce) over 9 K steps (K + k = 1088): one
+# split, and three splits under each reduction (atomic accumulator with a last
+# arriver, partial sums added by a second kernel, atomics into Y zeroed first).
+WAVE_TILE_CFGS = [(1, 4, 3, 0, 0), (1, 8, 2, 1, 0), (3, 4, 1, 0, 0), (3, 4, 1, 1, 1),
+                  (3, 8, 1, 0, 2)]
+
+
+@pytest.mark.parametrize("splits,waves,unroll,stage,reduce", WAVE_TILE_CFGS)
+def test_stream_four_tiles_per_wave(splits, waves, unroll, stage, reduce):
+    """Four 16-feature tiles per wave sharing its activation operands: dense
+    with N = 272 (17 tiles, the last group of four cut by N) and rows in two
+    passes, and grouped with empty experts and an expert past 16 rows, each
+    against the oracle's float64 GEMM."""
+    rng = np.random.default_rng(splits * 10 + waves + stage + reduce)
+    M, N, K_aug = 21, 272, 1088
+    Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+    Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
+    say("gemm case: stream four tiles per wave", splits, waves, unroll, stage, reduce)
+    st, Y = _tune_stream(Aq, Asc, Wq, Wsc, splits, waves, unroll, stage, reduce, 4)
+    assert st == 0
+    assert_gemm_close(Y, pq.gemm(Aq, Asc, Wq, Wsc), f"dense wave tiles {splits} {waves} {unroll}")
+    if splits == 1:
+        counts = [3, 0, 17, 1, 0]
+        off, Aq, Asc, Wq, Wsc = _grouped_case(counts, 48, K_aug, 11)
+        st, Y = _tune_stream(Aq, Asc, Wq, Wsc, 1, waves, unroll, stage, 0, 4, off=off,
+                             E=len(counts))
+        assert st == 0
+        assert_gemm_close(Y, pq.grouped_gemm(Aq, Asc, off, Wq, Wsc), "grouped wave tiles")
+
+
+def test_stream_four_tiles_per_wave_rejected_past_registers():
+    """Configurations whose weight registers would not fit (more than four
+    steps per wave, or more than one row group) are refused, nothing launched."""
+    rng = np.random.default_rng(2)
+    Aq, Asc = inputs.random_mxfp4(rng, 4, 1088)
+    Wq, Wsc = inputs.random_mxfp4(rng, 64, 1088)
+    st, _ = _tune_stream(Aq, Asc, Wq, Wsc, 1, 4, 6, 0, 0, 4)
+    assert st == -1
+    st, _ = _tune_stream(Aq, Asc, Wq, Wsc, 1, 16, 1, 0, 0, 4)
+    assert st == -1
+
+
 def test_decode_kernel_grouped_mode():
     """The decode kernel's grouped mode (one tile per workgroup, the expert's
     16-row groups looped in one workgroup), empty experts included."""
