@@ -161,6 +161,37 @@ def test_gemm_packed(shape, M, N, K_aug):
     assert_gemm_close(host(Y), pq.gemm(Aq, Asc, Wq, Wsc), f"packed shape {shape} {M}x{N}x{K_aug}")
 
 
+@pytest.mark.parametrize("M,K,k", [(8192, 9728, 256), (4100, 9728, 224)])
+def test_quant_act_packed_full_size_sampled_blocks(M, K, k):
+    """The packed quantizer as the prefill benchmark launches it (the public
+    entry on all CUs: 16 or more rows per workgroup of long rows, so the rows
+    go through the 8-row LDS window), every code and scale byte of sampled
+    16-row blocks -- the first, the last (ragged M: padded rows), blocks at
+    workgroup range boundaries and random ones -- against the oracle's
+    quantizer laid out by the reference packer."""
+    prq = _prq()
+    rng = np.random.default_rng(M + k)
+    X = inputs.f32_to_bf16_bits((rng.standard_normal((M, K)) *
+                                 rng.uniform(0.01, 30.0, K)).astype(np.float32))
+    inv = rng.uniform(0.25, 4.0, K).astype(np.float32)
+    perm = rng.permutation(K).astype(np.int32)
+    say("packed quant full size case:", M, K, k)
+    A = prq.prq_quant_act_packed(dev(X), K, k, dev(_pos(inv, perm)), dev(perm))
+    torch.cuda.synchronize()
+    ap, aps = host(A.Ap), host(A.Aps)
+    nblk = -(-M // 16)
+    steps = -(-(K + k) // 128)
+    sgroups = -(-steps // 4)
+    blocks = {0, nblk - 1, 1, nblk // 2, nblk // 2 - 1} | set(rng.choice(nblk, 6).tolist())
+    for b in sorted(blocks):
+        rows = np.arange(16 * b, min(16 * b + 16, M))
+        ep, es = pack_rows(*pq.quant_act(X[rows], inv, perm, k))
+        np.testing.assert_array_equal(ap[b * steps * 1024:(b + 1) * steps * 1024], ep,
+                                      err_msg=f"codes of row block {b}")
+        np.testing.assert_array_equal(aps[b * sgroups * 256:(b + 1) * sgroups * 256], es,
+                                      err_msg=f"scales of row block {b}")
+
+
 @pytest.mark.parametrize("M", [512, 2048, 8192])
 def test_packed_pair_down_proj(M):
     """X -> prq_quant_act_packed -> prq_gemm_packed on the down_proj shape
