@@ -277,6 +277,50 @@ def test_quant_act_packed_grouped(counts, K, k):
     np.testing.assert_array_equal(host(A.Ap), ep, err_msg="packed codes")
 
 
+# (M, K, k, num_cus) through the register-staged kernel: several rows per pass
+# (each thread one unit of two rows, half a pass apart), a pass of exactly two
+# rows (256 <= K/8 < 512), tiny rows, ragged ranges of many passes.
+SHORT_QUANT = [(300, 768, 64, 7), (97, 2400, 96, 3), (1000, 64, 32, 5), (333, 96, 0, 2),
+               (41, 4064, 32, 2)]
+
+
+@pytest.mark.parametrize("M,K,k,cus", SHORT_QUANT)
+def test_quant_act_packed_register_staged(M, K, k, cus):
+    """The register-staged packed quantizer (forced) with multi-pass workgroup
+    ranges: every code and scale byte, padding included, as the oracle's
+    quantizer laid out by the reference packer."""
+    rng = np.random.default_rng(M * 5 + K + k)
+    X = inputs.f32_to_bf16_bits((rng.standard_normal((M, K)) *
+                                 rng.uniform(0.01, 30.0, K)).astype(np.float32))
+    inv = rng.uniform(0.25, 4.0, K).astype(np.float32)
+    perm = rng.permutation(K).astype(np.int32)
+    say("packed register-staged quant case:", M, K, k, cus)
+    ap, aps = _tune_quant_packed(X, K, k, _pos(inv, perm), perm, None, 1, 2, cus)
+    ep, es = pack_rows(*pq.quant_act(X, inv, perm, k))
+    np.testing.assert_array_equal(aps, es, err_msg="packed scales")
+    np.testing.assert_array_equal(ap, ep, err_msg="packed codes")
+
+
+@pytest.mark.parametrize("counts,K,k,cus", [([5, 60, 0, 129, 1, 0, 33], 768, 64, 2),
+                                            ([0, 3, 250, 7], 2400, 96, 3)])
+def test_quant_act_packed_register_staged_grouped(counts, K, k, cus):
+    """Grouped rows through the register-staged packed quantizer: a thread's
+    two rows of a pass may belong to different experts."""
+    rng = np.random.default_rng(sum(counts) + K)
+    E = len(counts)
+    off = inputs.routed_offsets(counts)
+    M = int(off[-1])
+    X = inputs.f32_to_bf16_bits((rng.standard_normal((M, K)) *
+                                 rng.uniform(0.01, 30.0, K)).astype(np.float32))
+    perm = np.stack([rng.permutation(K) for _ in range(E)]).astype(np.int32)
+    inv = rng.uniform(0.1, 4.0, (E, K)).astype(np.float32)
+    say("packed register-staged grouped quant case:", counts, K, k, cus)
+    ap, aps = _tune_quant_packed(X, K, k, _pos_grouped(inv, perm), perm, off, E, 2, cus)
+    ep, es = pack_rows(*pq.quant_act_grouped(X, inv, perm, off, k))
+    np.testing.assert_array_equal(aps, es, err_msg="packed scales")
+    np.testing.assert_array_equal(ap, ep, err_msg="packed codes")
+
+
 # Experts changing inside 8-row windows and inside a workgroup's range.
 GROUPED_WINDOW_QUANT = [([40, 0, 90, 7, 300], 4160, 160, 3),
                         ([17, 1, 0, 33, 250, 2], 2048, 32, 5),
