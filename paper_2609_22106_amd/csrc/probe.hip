@@ -66,27 +66,6 @@ __global__ __launch_bounds__(64) void cvt_sel_probe(const float* x, const float*
   out[4 * l + 3] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(old, x[l], y[l], 1.0f, 3);
 }
 
-__global__ void empty_kernel() {}
-
-// MFMA issue rate: every wave runs `iters` rounds of 8 independent
-// block-scaled FP4 MFMAs on register operands (no memory traffic in the loop).
-__global__ __launch_bounds__(256) void mfma_rate_probe(int iters, float* out) {
-  const uint32_t l = threadIdx.x;
-  const uint4 a = make_uint4(0x22222222u ^ l, 0x12121212u, 0x21212121u, 0x11111111u);
-  const uint4 b = make_uint4(0x11111111u, 0x22222222u ^ l, 0x12121212u, 0x21212121u);
-  prq::dev::v4f acc[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) acc[i] = prq::dev::v4f{0.f, 0.f, 0.f, 0.f};
-  for (int it = 0; it < iters; ++it) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] = prq::dev::mfma_fp4_16x16x128(a, b, 120u + i, 121u, acc[i]);
-  }
-  float sum = 0.f;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) sum += acc[i][0] + acc[i][1] + acc[i][2] + acc[i][3];
-  out[blockIdx.x * blockDim.x + threadIdx.x] = sum;
-}
-
 // Direct global->LDS loads (one wave): 16 bytes per lane from g16 into LDS at
 // byte 0, one byte per lane from g1 into LDS at byte 4096; the 8 KiB LDS image
 // (zeroed first) is copied out so the host can see where each lane's data went.
@@ -103,36 +82,6 @@ __global__ __launch_bounds__(64) void lds_dma_probe(const uint8_t* g16, const ui
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   for (int i = l; i < 8192 / 16; i += 64) reinterpret_cast<uint4*>(out)[i] = reinterpret_cast<uint4*>(s)[i];
-}
-
-// Reads the packed weight with the stream GEMM's grid mapping (tile per
-// blockIdx.x, split per blockIdx.y, kU contiguous kilobytes per wave) and
-// writes one dword per workgroup: the memory side of that kernel alone.
-template <int kU>
-__global__ __launch_bounds__(1024) void stream_read_probe(const uint8_t* __restrict__ Wp, int steps,
-                                                          int splits, uint32_t* __restrict__ out) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int tile = blockIdx.x, split = blockIdx.y;
-  const int s_begin = steps * split / splits, s_end = steps * (split + 1) / splits;
-  const int s0 = s_begin + wave * kU;
-  const uint8_t* base = Wp + static_cast<int64_t>(tile) * steps * 1024 + lane * 16;
-  uint4 v[kU];
-#pragma unroll
-  for (int j = 0; j < kU; ++j)
-    v[j] = (s0 + j < s_end) ? *reinterpret_cast<const uint4*>(base + static_cast<int64_t>(s0 + j) * 1024)
-                            : make_uint4(0, 0, 0, 0);
-  uint32_t x = 0;
-#pragma unroll
-  for (int j = 0; j < kU; ++j) x ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
-  __shared__ uint32_t s_x[16];
-  for (int o = 32; o > 0; o >>= 1) x ^= __shfl_xor(x, o);
-  if (lane == 0) s_x[wave] = x;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t t = 0;
-    for (int w = 0; w < static_cast<int>(blockDim.x >> 6); ++w) t ^= s_x[w];
-    out[blockIdx.y * gridDim.x + blockIdx.x] = t;
-  }
 }
 
 }  // namespace
@@ -166,7 +115,6 @@ int prq_probe_cvt_pairs(const float* x, const float* y, const float* s, int n, u
 }
 
 // Tuning entry: the weight-streaming GEMM with an explicit configuration.
-// A bounded empty kernel for the launch-floor measurement follows.
 // Returns -1 when the configuration does not cover K_aug (nothing launched).
 int prq_tune_gemm_stream(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off, int E,
                          const uint8_t* Wq, const uint8_t* Wsc, int N, int K_aug, float* Y,
@@ -193,29 +141,6 @@ int prq_tune_gemm_stream(const uint8_t* Aq, const uint8_t* Asc, int M, const int
 
 typedef float v16f_t __attribute__((ext_vector_type(16)));
 
-// The same for the 32x32x64 block-scaled FP4 MFMA (4 independent chains).
-__global__ __launch_bounds__(256) void mfma32_rate_probe(int iters, float* out) {
-  const int l = static_cast<int>(threadIdx.x);
-  const prq::dev::v8i a = {0x22222222 ^ l, 0x12121212, 0x21212121, 0x11111111, 0, 0, 0, 0};
-  const prq::dev::v8i b = {0x11111111, 0x22222222 ^ l, 0x12121212, 0x21212121, 0, 0, 0, 0};
-  v16f_t acc[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 16; ++j) acc[i][j] = 0.f;
-  for (int it = 0; it < iters; ++it) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      acc[i] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, acc[i], 4, 4, 0, 120 + i, 0, 121);
-  }
-  float sum = 0.f;
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 16; ++j) sum += acc[i][j];
-  out[blockIdx.x * blockDim.x + threadIdx.x] = sum;
-}
-
 // One 32x32x64 block-scaled FP4 MFMA on lane-supplied operands: a, b are
 // [64 lanes][16 bytes], sa, sb one E8M0 byte per lane; out [64 lanes][16].
 __global__ __launch_bounds__(64) void mfma32_probe(const uint4* a, const uint4* b,
@@ -241,20 +166,6 @@ int prq_probe_mfma32(const void* a, const void* b, const void* sa, const void* s
   mfma32_probe<<<1, 64, 0, stream>>>(static_cast<const uint4*>(a), static_cast<const uint4*>(b),
                                      static_cast<const uint32_t*>(sa),
                                      static_cast<const uint32_t*>(sb), out);
-  return hipGetLastError() == hipSuccess ? 0 : -3;
-}
-
-// 4 waves per block, 4 * iters 32x32x64 MFMAs per wave.
-int prq_probe_mfma32_rate(int blocks, int iters, float* out, hipStream_t stream) {
-  if (blocks <= 0 || iters <= 0) return -1;
-  mfma32_rate_probe<<<blocks, 256, 0, stream>>>(iters, out);
-  return hipGetLastError() == hipSuccess ? 0 : -3;
-}
-
-// out: float[blocks * 256]; 4 waves per block, 8 * iters MFMAs per wave.
-int prq_probe_mfma_rate(int blocks, int iters, float* out, hipStream_t stream) {
-  if (blocks <= 0 || iters <= 0) return -1;
-  mfma_rate_probe<<<blocks, 256, 0, stream>>>(iters, out);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
@@ -299,21 +210,6 @@ int prq_tune_gemm_decode(const uint8_t* Aq, const uint8_t* Asc, int M, const int
   return prq::launch_gemm_decode(Aq, Asc, M, off, E, Wq, Wsc, N, K_aug, Y, c, stream) == hipSuccess
              ? 0
              : -3;
-}
-
-// out: uint32[tiles * splits]; Wp: tiles * steps kilobytes; waves * unroll * splits >= steps.
-int prq_probe_stream_read(const uint8_t* Wp, int tiles, int steps, int splits, int waves,
-                          int unroll, uint32_t* out, hipStream_t stream) {
-  if (waves < 1 || waves > 16 || static_cast<int64_t>(waves) * unroll * splits < steps) return -1;
-  const dim3 grid(tiles, splits);
-  switch (unroll) {
-    case 1: stream_read_probe<1><<<grid, waves * 64, 0, stream>>>(Wp, steps, splits, out); break;
-    case 2: stream_read_probe<2><<<grid, waves * 64, 0, stream>>>(Wp, steps, splits, out); break;
-    case 4: stream_read_probe<4><<<grid, waves * 64, 0, stream>>>(Wp, steps, splits, out); break;
-    case 8: stream_read_probe<8><<<grid, waves * 64, 0, stream>>>(Wp, steps, splits, out); break;
-    default: return -1;
-  }
-  return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
 // Tuning entry: the tile GEMM with an explicit tile shape (0, 1 or 2).
@@ -371,11 +267,6 @@ int prq_tune_grouped_gemm_tile_packed(const uint8_t* Ap, const uint8_t* Aps, int
 // g16: 1024 bytes, g1: 64 bytes, out: 8192 bytes (device).
 int prq_probe_lds_dma(const uint8_t* g16, const uint8_t* g1, uint8_t* out, hipStream_t stream) {
   lds_dma_probe<<<1, 64, 0, stream>>>(g16, g1, out);
-  return hipGetLastError() == hipSuccess ? 0 : -3;
-}
-
-int prq_probe_empty(int blocks, int threads, hipStream_t stream) {
-  empty_kernel<<<blocks, threads, 0, stream>>>();
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

@@ -38,3 +38,18 @@ def assert_gemm_close(Y_gpu, Y_ref, what=""):
     err = np.max(np.abs(Y_gpu - Y_ref)) if Y_ref.size else 0.0
     assert err <= GEMM_RTOL_OF_MAX * scale, f"{what}: max|dY| = {err:.3e}, max|Y| = {scale:.3e}"
     return err / scale if scale else 0.0
+
+
+def nan_output(M, N):
+    """A float32 [M, N] device output filled with NaN, so that an element the
+    kernel never writes fails the finiteness check."""
+    return torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+
+
+def rows_per_block(M, rng, block=16):
+    """One random row of every `block`-row block of [0, M) plus the first and
+    the last row: every row tile of every tile shape (whose heights are
+    multiples of 16) holds at least one checked row."""
+    starts = np.arange(0, M, block)
+    picks = starts + rng.integers(0, block, starts.size)
+    return np.unique(np.concatenate([np.minimum(picks, M - 1), [0, M - 1]]))

@@ -9,7 +9,8 @@ torch = pytest.importorskip("torch")
 
 from oracle import prquant as pq                               # noqa: E402
 from paper_2609_22106_amd import inputs                        # noqa: E402
-from tests.gpu_util import assert_gemm_close, dev, host, say   # noqa: E402
+from tests.gpu_util import (assert_gemm_close, dev, host, nan_output, rows_per_block,  # noqa: E402
+                            say)
 from tests.packing import pack_rows                            # noqa: E402
 
 pytestmark = pytest.mark.gpu
@@ -263,16 +264,20 @@ def test_down_proj_decode_end_to_end(c1_art, M):
 
 @pytest.mark.parametrize("M", [512, 2048, 8192])
 def test_down_proj_prefill_sampled_rows(c1_art, M):
+    """The oracle's down_proj export, GPU act-quant + prq_gemm (row-major
+    activation, auto kernel): every element written (Y starts as NaN), one
+    oracle row in every 16-row block and every column within the GEMM bar."""
     prq = _prq()
     _, art = c1_art
     c = inputs.down_proj_prefill()
     X = c.X[:M]
     say("gemm case: down_proj prefill M =", M)
     Aq, Asc = prq.prq_quant_act(dev(X), 9728, 256, dev(art["inv_scale"][art["perm"]]), dev(art["perm"]))
-    Y = host(prq.prq_gemm(Aq, Asc, _packed(art["Wq"], art["Wsc"])))
-    torch.cuda.synchronize()
-    rows = np.unique(np.concatenate([np.random.default_rng(M).choice(M, 48, replace=False),
-                                     [0, M - 1]]))
+    Yd = nan_output(M, 2560)
+    prq.prq_gemm(Aq, Asc, _packed(art["Wq"], art["Wsc"]), Y=Yd)
+    Y = host(Yd)
+    assert np.all(np.isfinite(Y)), "an output element was not written"
+    rows = rows_per_block(M, np.random.default_rng(M))
     rq, rs = pq.quant_act(X[rows], art["inv_scale"], art["perm"], 256)
     assert_gemm_close(Y[rows], pq.gemm(rq, rs, art["Wq"], art["Wsc"]), f"prefill M={M}")
 
@@ -310,8 +315,9 @@ def test_grouped_random(counts, N, K_aug, variant):
 
 @pytest.mark.parametrize("tokens", [64, 4096])
 def test_grouped_expert_shapes(tokens):
-    """128 experts of 2048 x 832 (768 + 64), rows routed top-8; all rows checked
-    at 512 routed rows, four experts' rows at 32768 routed rows."""
+    """128 experts of 2048 x 832 (768 + 64), rows routed top-8 (512 and 32768
+    routed rows): every element of Y (which starts as NaN) against the oracle's
+    grouped GEMM."""
     prq = _prq()
     rng = np.random.default_rng(tokens)
     E, N, K_aug = 128, 2048, 832
@@ -320,13 +326,9 @@ def test_grouped_expert_shapes(tokens):
     Aq, Asc = inputs.random_mxfp4(rng, int(off[-1]), K_aug)
     Wq, Wsc = inputs.random_mxfp4(rng, (E, N), K_aug)
     say("grouped case: experts", tokens, "tokens")
-    Y = _gpu_grouped(off, Aq, Asc, Wq, Wsc, prq.GEMM_AUTO)
-    if tokens <= 64:
-        assert_gemm_close(Y, pq.grouped_gemm(Aq, Asc, off, Wq, Wsc), "experts decode")
-    else:
-        for e in (0, 17, 64, 127):
-            r0, r1 = int(off[e]), int(off[e + 1])
-            assert_gemm_close(Y[r0:r1], pq.gemm(Aq[r0:r1], Asc[r0:r1], Wq[e], Wsc[e]), f"expert {e}")
+    Yd = nan_output(int(off[-1]), N)
+    prq.prq_grouped_gemm(dev(Aq), dev(Asc), dev(off), _packed(Wq, Wsc), Y=Yd)
+    assert_gemm_close(host(Yd), pq.grouped_gemm(Aq, Asc, off, Wq, Wsc), f"experts {tokens} tokens")
 
 
 def test_grouped_end_to_end_prepared_experts():

@@ -12,7 +12,8 @@ torch = pytest.importorskip("torch")
 
 from oracle import prquant as pq                               # noqa: E402
 from paper_2609_22106_amd import inputs                        # noqa: E402
-from tests.gpu_util import assert_gemm_close, dev, host, say   # noqa: E402
+from tests.gpu_util import (assert_gemm_close, dev, host, nan_output, rows_per_block,  # noqa: E402
+                            say)
 from tests.packing import pack_rows                            # noqa: E402
 
 pytestmark = pytest.mark.gpu
@@ -195,8 +196,10 @@ def test_quant_act_packed_full_size_sampled_blocks(M, K, k):
 @pytest.mark.parametrize("M", [512, 2048, 8192])
 def test_packed_pair_down_proj(M):
     """X -> prq_quant_act_packed -> prq_gemm_packed on the down_proj shape
-    (K = 9728, k = 256, N = 2560), against the oracle on 48 sampled rows; with
-    the planner's workspace (split along K where it picks it) and without."""
+    (K = 9728, k = 256, N = 2560), with the planner's workspace (split along K
+    where it picks it) and without: every element of both outputs written (Y
+    starts as NaN), and one oracle row in every 16-row block (so every row tile
+    of every tile shape) within the GEMM bar."""
     prq = _prq()
     rng = np.random.default_rng(M)
     K, k, N = 9728, 256, 2560
@@ -210,13 +213,40 @@ def test_packed_pair_down_proj(M):
     A = prq.prq_quant_act_packed(dev(X), K, k, dev(_pos(inv, perm)), dev(perm))
     ws_n = prq.prq_gemm_packed_workspace_bytes(M, N, K + k)
     ws = torch.empty(ws_n, dtype=torch.uint8, device="cuda") if ws_n else None
-    Y = host(prq.prq_gemm_packed(A, W, workspace=ws))
-    Y0 = host(prq.prq_gemm_packed(A, W))
-    rows = np.sort(rng.choice(M, 48, replace=False))
+    Yd, Yd0 = nan_output(M, N), nan_output(M, N)     # both live: no reuse of one block
+    prq.prq_gemm_packed(A, W, Y=Yd, workspace=ws)
+    prq.prq_gemm_packed(A, W, Y=Yd0)
+    Y, Y0 = host(Yd), host(Yd0)
+    assert np.all(np.isfinite(Y)) and np.all(np.isfinite(Y0)), "an output element was not written"
+    rows = rows_per_block(M, rng)
     rq, rs = pq.quant_act(X[rows], inv, perm, k)
     Yo = pq.gemm(rq, rs, Wq, Wsc)
     assert_gemm_close(Y[rows], Yo, f"packed pair M={M} workspace {ws_n}")
     assert_gemm_close(Y0[rows], Yo, f"packed pair M={M} without workspace")
+
+
+@pytest.mark.parametrize("entry", ["packed", "rowmajor"])
+def test_full_prefill_gemm_every_element(entry):
+    """The largest down_proj prefill GEMM (8192 x 2560 over K + k = 9984) with
+    random MXFP4 operands, every element of Y (which starts as NaN) against the
+    oracle's float64 product: the packed pair's GEMM with its planner's
+    workspace, and the row-major prq_gemm."""
+    prq = _prq()
+    rng = np.random.default_rng(8192)
+    M, N, K_aug = 8192, 2560, 9984
+    Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+    Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
+    W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
+    Yd = nan_output(M, N)
+    say("full prefill gemm case:", entry)
+    if entry == "packed":
+        ap, aps = pack_rows(Aq, Asc)
+        ws_n = prq.prq_gemm_packed_workspace_bytes(M, N, K_aug)
+        ws = torch.empty(ws_n, dtype=torch.uint8, device="cuda") if ws_n else None
+        prq.prq_gemm_packed(prq.PackedAct(dev(ap), dev(aps), M, K_aug), W, Y=Yd, workspace=ws)
+    else:
+        prq.prq_gemm(dev(Aq), dev(Asc), W, Y=Yd)
+    assert_gemm_close(host(Yd), pq.gemm(Aq, Asc, Wq, Wsc), f"full prefill {entry}")
 
 
 @pytest.mark.parametrize("packed", [True, False])
@@ -426,7 +456,9 @@ def test_grouped_gemm_packed_expert_counts(counts):
 def test_grouped_packed_pair_experts():
     """X -> prq_quant_act_packed -> prq_grouped_gemm_packed on the MoE expert
     shape (128 experts, 768 -> 2048, k = 64, 4096 tokens routed top-8 to
-    distinct uniformly random experts), against the oracle on 64 sampled rows."""
+    distinct uniformly random experts): every element written (Y starts as
+    NaN), and the first and last row of every expert plus one row of every
+    16-row block against the oracle."""
     prq = _prq()
     E, K, k, N, tokens = 128, 768, 64, 2048, 4096
     rng = np.random.default_rng(2)
@@ -443,9 +475,14 @@ def test_grouped_packed_pair_experts():
     say("grouped packed pair case:", M, "rows")
     A = prq.prq_quant_act_packed(dev(X), K, k, dev(_pos_grouped(inv, perm)), dev(perm),
                                  group_offsets=offd, G=E)
-    Y = host(prq.prq_grouped_gemm_packed(A, offd, W))
-    rows = np.sort(rng.choice(M, 64, replace=False))
+    Yd = nan_output(M, N)
+    prq.prq_grouped_gemm_packed(A, offd, W, Y=Yd)
+    Y = host(Yd)
+    assert np.all(np.isfinite(Y)), "an output element was not written"
+    ends = np.concatenate([off[:-1][np.diff(off) > 0], off[1:][np.diff(off) > 0] - 1])
+    rows = np.unique(np.concatenate([rows_per_block(M, rng), ends]))
     e_of = np.searchsorted(off, rows, side="right") - 1
+    assert set(np.unique(e_of)) == set(np.flatnonzero(np.diff(off) > 0))
     for e in np.unique(e_of):
         r = rows[e_of == e]
         rq, rs = pq.quant_act(X[r], inv[e], perm[e], k)
@@ -457,7 +494,8 @@ def test_packed_pair_layer_shapes(name, N, K):
     """The seven linears of a Qwen3-4B-shaped decoder layer at M = 4096 (k = K/40
     rounded down to a multiple of 32), through the packed pair as the benchmark
     launches it (the planner's tile shapes, column regions and workspace),
-    against the oracle on 32 sampled rows and every column."""
+    every element written (Y starts as NaN), one oracle row in every 16-row
+    block and every column."""
     prq = _prq()
     rng = np.random.default_rng(N + K)
     M, k = 4096, inputs.tail_width(K)
@@ -471,7 +509,10 @@ def test_packed_pair_layer_shapes(name, N, K):
     A = prq.prq_quant_act_packed(dev(X), K, k, dev(_pos(inv, perm)), dev(perm))
     ws_n = prq.prq_gemm_packed_workspace_bytes(M, N, K + k)
     ws = torch.empty(ws_n, dtype=torch.uint8, device="cuda") if ws_n else None
-    Y = host(prq.prq_gemm_packed(A, W, workspace=ws))
-    rows = np.unique(np.concatenate([rng.choice(M, 30, replace=False), [0, M - 1]]))
+    Yd = nan_output(M, N)
+    prq.prq_gemm_packed(A, W, Y=Yd, workspace=ws)
+    Y = host(Yd)
+    assert np.all(np.isfinite(Y)), "an output element was not written"
+    rows = rows_per_block(M, rng)
     rq, rs = pq.quant_act(X[rows], inv, perm, k)
     assert_gemm_close(Y[rows], pq.gemm(rq, rs, Wq, Wsc), f"{name} {M}x{N}x{K}+{k}")

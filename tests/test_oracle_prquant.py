@@ -444,3 +444,89 @@ def test_prepare_rejects_misaligned():
         pq.prepare(c.W, c.Xcal, 1.5, 64)
     with pytest.raises(ValueError):
         pq.prepare(c.W[:, :100], c.Xcal[:, :100], 0.5, 32)
+
+
+# ---------------------------------------- normalized error, ablation table ---
+def test_nrmse_hand_values():
+    """||Y_hat - Y||_F / ||Y||_F (reading of the paper's normalized
+    reconstruction error, Sec. 4.3) on hand-computed cases: the norm of the
+    difference over the norm of the REFERENCE (not of the estimate), not
+    squared, taken over every element of the matrix."""
+    assert pq.nrmse([[3.0, 5.0]], [[3.0, 4.0]]) == 0.2          # 1 / 5
+    assert pq.nrmse([[1.0, 2.0], [2.0, 7.0]], [[1.0, 2.0], [2.0, 4.0]]) == 0.6   # 3 / 5
+    assert pq.nrmse([[0.0, 0.0]], [[3.0, 4.0]]) == 1.0          # the zero estimate
+    assert pq.nrmse([[6.0, 8.0]], [[3.0, 4.0]]) == 1.0          # twice the reference
+    assert pq.nrmse([[3.0, 4.0]], [[3.0, 4.0]]) == 0.0
+    # a column vector and its transpose give the same Frobenius ratio
+    assert pq.nrmse([[0.0], [1.0]], [[0.0], [2.0]]) == 0.5
+
+
+def _eq3_direct(X_bf16, W_bf16, s, k, searched=False):
+    """Eq. 3 assembled here from the MXFP4 primitives for given scales s:
+    W~ = (W s)[:, P] with P the tail permutation of the k columns of largest
+    MXFP4 error of W s (ties to the smaller index), R = W~_tail - deq Q(W~)_tail,
+    A = Q([Z~, Z~_tail]) with Z~ = (X / s)[:, P], Y = deq(A) deq([Q(W~) | Q(R)])^T.
+    `searched` quantizes W~ and R with the E8M0 block-scale search."""
+    Xf = pq.bf16_bits_to_f32(X_bf16)
+    Wf = pq.bf16_bits_to_f32(W_bf16)
+    s = np.asarray(s, np.float32)
+    inv = (np.float32(1.0) / s).astype(np.float32)
+    K = Wf.shape[1]
+    W_s = (Wf * s[None, :]).astype(np.float32)
+    deq0 = mx.qdq(W_s)
+    err = np.array([sum((float(W_s[n, j]) - float(deq0[n, j])) ** 2 for n in range(W_s.shape[0]))
+                    for j in range(K)])
+    order = sorted(range(K), key=lambda j: (-err[j], j))
+    sel = sorted(order[:k])
+    P = np.array([j for j in range(K) if j not in set(sel)] + sel, np.int64)
+    Wt = W_s[:, P]
+    quant = mx.mx_quantize_searched if searched else mx.mx_quantize
+    cw, sw = quant(Wt)
+    R = (Wt[:, K - k:].astype(np.float64) - mx.mx_dequantize(cw, sw)[:, K - k:]).astype(np.float32)
+    cr, sr = quant(R) if k else (np.zeros((Wt.shape[0], 0), np.uint8),
+                                 np.zeros((Wt.shape[0], 0), np.uint8))
+    Zt = (Xf * inv[None, :]).astype(np.float32)[:, P]
+    ca, sa = mx.mx_quantize(np.ascontiguousarray(np.concatenate([Zt, Zt[:, K - k:]], axis=1)))
+    Wd = np.concatenate([mx.mx_dequantize(cw, sw), mx.mx_dequantize(cr, sr)], axis=1)
+    return mx.mx_dequantize(ca, sa) @ Wd.T
+
+
+def test_ablation_variants_match_their_definitions():
+    """Each entry of the ablation grid (Sec. Ablation Studies) is the variant
+    its name defines, assembled directly from the MXFP4 primitives:
+      plain MXFP4: Q(X) Q(W)^T (no scaling, no tail);
+      w/o Res:     Q(X / s) Q(W s)^T with the SmoothQuant scales (k = 0);
+      w/o AWQ:     Eq. 3 with s = 1 and the k-column tail;
+      PRQuant:     Eq. 3 with the SmoothQuant scales and the tail;
+      E8M0-W:      PRQuant with the weight block scales searched;
+    and the device grid's variant table is the oracle's."""
+    from paper_2609_22106_amd import ablation
+    assert ablation.VARIANTS == pq.ABLATION_VARIANTS
+    rng = np.random.default_rng(31)
+    N, K, k, alpha = 24, 128, 32, 0.5
+    W = 0.02 * rng.standard_normal((N, K))
+    W[:, rng.choice(K, 5, replace=False)] *= 15
+    Wb = _bf16(W)
+    out = rng.choice(K, 4, replace=False)
+    Xc = rng.standard_normal((16, K))
+    Xc[:, out] *= 30
+    X = rng.standard_normal((6, K))
+    X[:, out] *= 30
+    Xcb, Xb = _bf16(Xc), _bf16(X)
+    g = pq.ablation_grid(Xb, Wb, Xcb, alpha, k)
+    ref = pq.bf16_bits_to_f32(Xb).astype(np.float64) @ pq.bf16_bits_to_f32(Wb).astype(np.float64).T
+    s, _ = pq.channel_scales(Wb, Xcb, alpha, "smooth")
+    plain = mx.qdq(pq.bf16_bits_to_f32(Xb)) @ mx.qdq(pq.bf16_bits_to_f32(Wb)).T
+    want = {
+        "plain MXFP4": plain,
+        "w/o Res": _eq3_direct(Xb, Wb, s, 0),
+        "w/o AWQ": _eq3_direct(Xb, Wb, np.ones(K, np.float32), k),
+        "PRQuant": _eq3_direct(Xb, Wb, s, k),
+        "E8M0-W": _eq3_direct(Xb, Wb, s, k, searched=True),
+    }
+    for name, y in want.items():
+        e = float(np.linalg.norm(y - ref) / np.linalg.norm(ref))
+        assert g[name] == pytest.approx(e, rel=1e-12, abs=0), name
+    # the five values are distinct, so no two names can trade places unnoticed
+    vals = [g[n] for n in want]
+    assert len(set(vals)) == len(vals), g
