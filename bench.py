@@ -447,7 +447,7 @@ def cpu_baseline(np, layers, M_list, budget_s=12.0):
 
 
 CALIB_BYTES = 512 * 2 ** 20
-GEMM_SOURCES = ("gemm_decode.hip", "gemm_stream.hip", "gemm_tile.hip", "mx_device.hpp",
+GEMM_SOURCES = ("gemm_decode.hip", "gemm_stream.hip", "gemm_streamk.hip", "gemm_tile.hip", "mx_device.hpp",
                 "prq_internal.h", "abi.cpp")
 
 

@@ -67,8 +67,16 @@ enum {
 enum {
   PRQ_GEMM_AUTO = 0,   /* chosen from the shape                               */
   PRQ_GEMM_TILE = 1,   /* LDS-tiled block-scaled MFMA kernel (prefill shapes) */
-  PRQ_GEMM_STREAM = 2  /* weight-streaming decode kernels: whole-K workgroups
+  PRQ_GEMM_STREAM = 2, /* weight-streaming decode kernels: whole-K workgroups
                           (splits 0 or 1), split-K for a forced split count > 1 */
+  PRQ_GEMM_STREAM_K = 3 /* stream-K decode kernel (up to 64 rows; AUTO's choice up
+                          to 8): equal contiguous ranges of the weight's
+                          (16-feature tile, 128-element K step) units, one
+                          workgroup per tile where the tiles fill at least half
+                          of the CUs, else one per CU; a tile shared by several
+                          workgroups is finished by the last to arrive, which
+                          adds the partial tiles in a fixed order (bitwise
+                          reproducible) and needs the workspace. */
 };
 
 /* Human-readable text of a status code (static storage). */
@@ -192,15 +200,24 @@ int prq_pack_weight(const uint8_t* Wq, const uint8_t* Wsc, int32_t E, int32_t N,
  *   Wp, Wps: the weight in the packed layout above (E = 1), from
  *            prq_pack_weight of prq_prepare's Wq / Wsc
  *   workspace: device buffer of at least prq_gemm_workspace_bytes(M, N, K_aug)
- *   bytes (may be NULL when that is 0) for split-K: either a float
- *   accumulator [M][N] plus one arrival counter per output tile, which every
- *   call leaves zero-filled again (atomic mode, up to 32 rows), or partial
- *   sums [splits][M][N] that are rewritten before being read and added in a
- *   fixed order (deterministic mode, more rows; the LDS-tiled kernel's split
- *   along K keeps splits - 1 of them and needs workspace and Y 16-byte
- *   aligned).  It must be zero-filled once before its first use.  Calls that
- *   share one workspace must be ordered (same stream).  Without the workspace
- *   the LDS-tiled kernel runs unsplit (same result up to float rounding).
+ *   bytes (may be NULL when that is 0), 16-byte aligned.  Every GEMM
+ *   workspace (this call, prq_gemm_ex, prq_gemm_packed) starts with a 16 KiB
+ *   state head: the stream-K kernel's uint32 arrival counters, one per
+ *   16-feature tile, which must be zero before the buffer's first use
+ *   (zero-fill it once) and which every call leaves zero; no kernel writes
+ *   anything else there.  The scratch of the kernel that runs follows it and
+ *   is rewritten before it is read: the stream-K kernel's partial tiles
+ *   [workgroups][2][M][16] floats (only where its plan shares tiles between
+ *   workgroups; none for the 9728 -> 2560 down_proj); for a forced split count of the
+ *   split-K kernel partial sums [splits][M][N] added in a fixed order; for the
+ *   LDS-tiled kernel's split along K, splits - 1 partial sums [M][N] (Y
+ *   16-byte aligned).  One buffer may therefore serve calls of any shape in
+ *   turn, as long as it is large enough for each; calls that share it must be
+ *   ordered (same stream).  AUTO runs the stream-K kernel up to 8 rows, the
+ *   whole-K decode kernel up to 64, the LDS-tiled kernel above; a call whose
+ *   plan would use more workspace than it is given (or NULL) runs without it
+ *   (the whole-K decode kernel instead of a stream-K plan that shares tiles,
+ *   the LDS-tiled kernel unsplit; same result up to float rounding).
  * Limits: N % 16 == 0, K_aug <= 65536.  M == 0 is a no-op.
  */
 size_t prq_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K_aug);
@@ -239,11 +256,12 @@ int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M,
  * prq_gemm_packed -- prq_gemm on a packed activation (the LDS-tiled kernel):
  *   Y [M, N] float32 = Eq. 3 over K_aug; Ap / Aps from prq_quant_act_packed,
  *   Wp / Wps from prq_pack_weight (E = 1).  workspace: at least
- *   prq_gemm_packed_workspace_bytes(M, N, K_aug) bytes, 16-byte aligned, for
- *   the split along K that the planner picks when few output tiles would
- *   leave CUs idle (splits - 1 partial sums [M][N], rewritten before being
- *   read, added to Y in a fixed order by a second kernel; no zero-fill
- *   needed); with less (or NULL) the call runs unsplit.  Calls sharing a
+ *   prq_gemm_packed_workspace_bytes(M, N, K_aug) bytes, 16-byte aligned, in
+ *   prq_gemm's layout (the 16 KiB state head, which this call never writes,
+ *   then the scratch), for the split along K that the planner picks when few
+ *   output tiles would leave CUs idle (splits - 1 partial sums [M][N],
+ *   rewritten before being read, added to Y in a fixed order by a second
+ *   kernel); with less (or NULL) the call runs unsplit.  Calls sharing a
  *   workspace must be ordered.  Limits as prq_gemm.
  * prq_grouped_gemm_packed -- prq_grouped_gemm on a packed activation (rows
  *   sorted by expert, from prq_quant_act_packed with G = E and the same

@@ -34,6 +34,7 @@ HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-ffp-contract=off", "-Wall",
               "-D__HIP_PLATFORM_AMD__", f"-I{ROCM}/include"]
 
 DEVICE_SOURCES = ["act_quant.hip", "pack.hip", "gemm_tile.hip", "gemm_stream.hip", "gemm_decode.hip",
+                  "gemm_streamk.hip",
                   "evaluate.hip"]
 HOST_SOURCES = ["prepare.cpp", "abi.cpp"]
 PROBE_SOURCES = ["probe.hip"]

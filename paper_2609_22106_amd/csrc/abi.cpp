@@ -138,6 +138,9 @@ namespace {
 // split count (the wave count and unroll are then re-derived for coverage).
 prq::StreamConfig dense_stream_config(int M, int N, int K_aug, int splits_req, int num_cus) {
   prq::StreamConfig c = prq::choose_stream_config(M, N, K_aug, 0, num_cus);
+  // split-K through the ABI always adds partial sums in a fixed order (the
+  // workspace's scratch then never has to start at zero)
+  c.reduce = 1;
   if (splits_req > 0 && splits_req != c.splits) {
     const int steps = (K_aug + 127) / 128;
     c.splits = splits_req;
@@ -161,9 +164,45 @@ prq::StreamConfig dense_stream_config(int M, int N, int K_aug, int splits_req, i
   return c;
 }
 
+// Workspace layout shared by every GEMM call: the state head (stream-K arrival
+// counters, zero between calls), then the scratch of the kernel that runs.
+size_t with_head(size_t scratch) { return scratch ? prq::kWorkspaceStateBytes + scratch : 0; }
+
+void* scratch_of(void* workspace, size_t workspace_bytes) {
+  return workspace && workspace_bytes > prq::kWorkspaceStateBytes
+             ? static_cast<char*>(workspace) + prq::kWorkspaceStateBytes
+             : nullptr;
+}
+
+size_t scratch_bytes(const void* workspace, size_t workspace_bytes) {
+  return workspace && workspace_bytes > prq::kWorkspaceStateBytes
+             ? workspace_bytes - prq::kWorkspaceStateBytes
+             : 0;
+}
+
 int device_cus() {
   DeviceInfo dev;
   return current_device(&dev) == PRQ_OK ? dev.num_cus : 256;
+}
+
+// Rows up to which AUTO runs the stream-K kernel.  Measured on the 9728 ->
+// 2560 down_proj (one workgroup per tile, weights rotated, back-to-back
+// launches): M = 1 5.3 vs 6.1 us for the whole-K decode kernel, M = 8 6.3 vs
+// 7.0, M = 16 8.0 vs 7.8; from two 16-row groups on, each workgroup reading
+// the activation of all K steps costs more than the whole-K kernel's staging.
+constexpr int kStreamKMaxRows = 8;
+
+// The variant an AUTO call runs when given `workspace_bytes` of workspace:
+// the stream-K kernel for up to kStreamKMaxRows rows wherever it applies (and
+// its workspace, if its plan shares tiles, is there), else the shape's default
+// (whole-K decode kernel up to 64 rows, LDS-tiled kernel above).
+int auto_variant(int M, int N, int K_aug, size_t workspace_bytes, int num_cus) {
+  const int v = prq::choose_variant(M, N, K_aug);
+  if (v == PRQ_GEMM_STREAM && M <= kStreamKMaxRows &&
+      prq::choose_streamk_config(M, N, K_aug, num_cus).ok &&
+      workspace_bytes >= prq::streamk_workspace_bytes(M, N, K_aug, num_cus))
+    return PRQ_GEMM_STREAM_K;
+  return v;
 }
 
 }  // namespace
@@ -173,12 +212,14 @@ extern "C" {
 size_t prq_gemm_workspace_bytes_ex(int32_t M, int32_t N, int32_t K_aug, int32_t variant,
                                    int32_t splits) {
   if (M <= 0 || N <= 0 || K_aug <= 0 || N % 16 || K_aug % PRQ_BLOCK || splits < 0) return 0;
-  if (variant == PRQ_GEMM_AUTO) variant = prq::choose_variant(M, N, K_aug);
-  if (variant == PRQ_GEMM_TILE) return prq::tile_workspace_bytes(M, N, K_aug, false, device_cus());
+  if (variant == PRQ_GEMM_AUTO) variant = auto_variant(M, N, K_aug, SIZE_MAX, device_cus());
+  if (variant == PRQ_GEMM_STREAM_K) return prq::streamk_workspace_bytes(M, N, K_aug, device_cus());
+  if (variant == PRQ_GEMM_TILE)
+    return with_head(prq::tile_workspace_bytes(M, N, K_aug, false, device_cus()));
   if (variant != PRQ_GEMM_STREAM) return 0;
   if (splits <= 1 && prq::choose_decode_config(M, N, K_aug, 0, 0, 0, device_cus()).ok) return 0;
   const prq::StreamConfig c = dense_stream_config(M, N, K_aug, splits, device_cus());
-  return c.ok ? prq::stream_workspace_bytes(M, 1, N, c.splits, c.reduce) : 0;
+  return c.ok ? with_head(prq::stream_workspace_bytes(M, 1, N, c.splits, c.reduce)) : 0;
 }
 
 size_t prq_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K_aug) {
@@ -190,12 +231,22 @@ int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t*
                 size_t workspace_bytes, int32_t variant, int32_t splits, hipStream_t stream) {
   int st = check_gemm_common(Aq, Asc, M, Wp, Wps, N, K_aug, Y);
   if (st != PRQ_OK) return st;
-  if (variant < PRQ_GEMM_AUTO || variant > PRQ_GEMM_STREAM || splits < 0) return PRQ_EINVAL;
+  if (variant < PRQ_GEMM_AUTO || variant > PRQ_GEMM_STREAM_K || splits < 0) return PRQ_EINVAL;
   if (M == 0) return PRQ_OK;
   DeviceInfo dev;
   st = current_device(&dev);
   if (st != PRQ_OK) return st;
-  if (variant == PRQ_GEMM_AUTO) variant = prq::choose_variant(M, N, K_aug);
+  if (variant == PRQ_GEMM_AUTO)
+    variant = auto_variant(M, N, K_aug, workspace ? workspace_bytes : 0, dev.num_cus);
+  if (variant == PRQ_GEMM_STREAM_K) {
+    const prq::StreamKConfig c = prq::choose_streamk_config(M, N, K_aug, dev.num_cus);
+    if (!c.ok) return PRQ_EUNSUPPORTED;
+    const size_t need = prq::streamk_workspace_bytes(M, N, K_aug, dev.num_cus);
+    if (need && (!workspace || workspace_bytes < need || !aligned16(workspace)))
+      return PRQ_EWORKSPACE;
+    return launch_status(prq::launch_gemm_streamk(Aq, Asc, M, Wp, Wps, N, K_aug, Y, c, workspace,
+                                                  stream));
+  }
   if (variant == PRQ_GEMM_STREAM && splits <= 1) {
     // no split-K: the decode kernel, unless K_aug exceeds what it stages
     const prq::DecodeConfig d = prq::choose_decode_config(M, N, K_aug, 0, 0, 0, dev.num_cus);
@@ -209,16 +260,16 @@ int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t*
       if (splits > 0) return PRQ_EINVAL;   // the forced split count cannot cover K_aug
       variant = PRQ_GEMM_TILE;
     } else {
-      const size_t need = prq::stream_workspace_bytes(M, 1, N, c.splits, c.reduce);
+      const size_t need = with_head(prq::stream_workspace_bytes(M, 1, N, c.splits, c.reduce));
       if (need && (!workspace || workspace_bytes < need || !aligned16(workspace)))
         return PRQ_EWORKSPACE;
       return launch_status(prq::launch_gemm_stream(Aq, Asc, M, nullptr, 1, Wp, Wps, N, K_aug, Y, c,
-                                                   workspace, stream));
+                                                   scratch_of(workspace, workspace_bytes), stream));
     }
   }
-  return launch_status(prq::launch_gemm_tile_planned(Aq, Asc, M, Wp, Wps, N, K_aug, Y, false,
-                                                     dev.num_cus, workspace, workspace_bytes,
-                                                     stream));
+  return launch_status(prq::launch_gemm_tile_planned(
+      Aq, Asc, M, Wp, Wps, N, K_aug, Y, false, dev.num_cus, scratch_of(workspace, workspace_bytes),
+      scratch_bytes(workspace, workspace_bytes), stream));
 }
 
 int prq_gemm(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t* Wp,
@@ -262,7 +313,7 @@ int prq_quant_act_packed(const void* X_bf16, int64_t ld_x, int32_t M, int32_t K,
 
 size_t prq_gemm_packed_workspace_bytes(int32_t M, int32_t N, int32_t K_aug) {
   if (M <= 0 || N <= 0 || K_aug <= 0 || N % 16 || K_aug % PRQ_BLOCK || K_aug > kMaxKAug) return 0;
-  return prq::tile_workspace_bytes(M, N, K_aug, true, device_cus());
+  return with_head(prq::tile_workspace_bytes(M, N, K_aug, true, device_cus()));
 }
 
 int prq_gemm_packed(const uint8_t* Ap, const uint8_t* Aps, int32_t M, const uint8_t* Wp,
@@ -275,9 +326,9 @@ int prq_gemm_packed(const uint8_t* Ap, const uint8_t* Aps, int32_t M, const uint
   DeviceInfo dev;
   st = current_device(&dev);
   if (st != PRQ_OK) return st;
-  return launch_status(prq::launch_gemm_tile_planned(Ap, Aps, M, Wp, Wps, N, K_aug, Y, true,
-                                                     dev.num_cus, workspace, workspace_bytes,
-                                                     stream));
+  return launch_status(prq::launch_gemm_tile_planned(
+      Ap, Aps, M, Wp, Wps, N, K_aug, Y, true, dev.num_cus, scratch_of(workspace, workspace_bytes),
+      scratch_bytes(workspace, workspace_bytes), stream));
 }
 
 int prq_grouped_gemm_packed(const uint8_t* Ap, const uint8_t* Aps, const int32_t* group_offsets,

@@ -212,6 +212,34 @@ int prq_tune_gemm_decode(const uint8_t* Aq, const uint8_t* Asc, int M, const int
              : -3;
 }
 
+// Tuning entry: the stream-K decode GEMM planned for `num_cus` CUs with
+// `workgroups` workgroups (0: the planner's choice; the workspace sized for
+// that plan).  Returns -1 when the kernel does not apply (nothing launched).
+int prq_tune_gemm_streamk(const uint8_t* Aq, const uint8_t* Asc, int M, const uint8_t* Wp,
+                          const uint8_t* Wps, int N, int K_aug, float* Y, int num_cus,
+                          int workgroups, void* workspace, size_t workspace_bytes,
+                          hipStream_t stream) {
+  if (N % 16 || K_aug % 32 || M <= 0 || num_cus <= 0) return -1;
+  const prq::StreamKConfig c = prq::choose_streamk_config(M, N, K_aug, num_cus, workgroups);
+  if (!c.ok) return -1;
+  const size_t need = c.shared ? prq::kWorkspaceStateBytes +
+                                     static_cast<size_t>(c.workgroups) * 2 * M * 16 * sizeof(float)
+                               : 0;
+  if (workspace_bytes < need) return -1;
+  return prq::launch_gemm_streamk(Aq, Asc, M, Wp, Wps, N, K_aug, Y, c, workspace, stream) ==
+                 hipSuccess
+             ? 0
+             : -3;
+}
+
+// Workspace bytes of prq_tune_gemm_streamk (0 when the kernel does not apply).
+size_t prq_tune_streamk_workspace_bytes(int M, int N, int K_aug, int num_cus, int workgroups) {
+  const prq::StreamKConfig c = prq::choose_streamk_config(M, N, K_aug, num_cus, workgroups);
+  return c.ok && c.shared ? prq::kWorkspaceStateBytes +
+                               static_cast<size_t>(c.workgroups) * 2 * M * 16 * sizeof(float)
+                         : 0;
+}
+
 // Tuning entry: the tile GEMM with an explicit tile shape (0, 1 or 2).
 int prq_tune_gemm_tile(const uint8_t* Aq, const uint8_t* Asc, int M, const int32_t* off, int E,
                        const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug, float* Y, int shape,

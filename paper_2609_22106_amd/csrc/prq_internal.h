@@ -34,6 +34,17 @@ struct DecodeConfig {
   bool ok = true;   // false: K_aug needs more LDS or steps than the kernel takes
 };
 
+// Launch parameters of the stream-K decode GEMM (gemm_streamk.hip): one
+// workgroup per CU, each an equal contiguous range of the weight's
+// (16-feature tile, 128-element K step) units.
+struct StreamKConfig {
+  int workgroups = 0;  // one per tile, or min(CUs, units)
+  bool shared = false; // some tile is covered by several workgroups (needs the workspace)
+  int groups = 1;      // 16-row activation groups (1..4)
+  int unroll = 0;      // units per wave (1, 2, 4, 7 or 10), >= ceil(units per workgroup / 8)
+  bool ok = false;     // false: M > 64, or a workgroup's range would exceed one tile
+};
+
 // act_quant.hip
 hipError_t launch_act_quant(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail,
                             const float* inv_scale, const int32_t* perm,
@@ -117,6 +128,23 @@ size_t stream_workspace_bytes(int M, int E, int N, int splits, int reduce);
 StreamConfig choose_stream_config(int M_per_group, int N, int K_aug, int grouped, int num_cus);
 bool stream_config_covers(const StreamConfig& c, int K_aug);
 int choose_variant(int M_per_group, int N, int K_aug);
+// Every GEMM workspace starts with a state head of kWorkspaceStateBytes: the
+// stream-K kernel's uint32 arrival counters, one per 16-feature tile (up to
+// kMaxStreamKTiles), zero before a workspace's first use and left zero by
+// every call.  Nothing else is written there; the scratch of every kernel
+// (partial tiles or sums, rewritten before they are read) follows it.
+constexpr size_t kWorkspaceStateBytes = 16384;
+constexpr int kMaxStreamKTiles = static_cast<int>(kWorkspaceStateBytes / 4);
+
+// gemm_streamk.hip.  Workspace: the state head, then partial tiles
+// [workgroups][2][M][16] floats.
+// workgroups 0: one per CU, or one per tile where the tiles fill at least
+// half of the CUs (no tile is then shared: no arrival protocol at all).
+StreamKConfig choose_streamk_config(int M, int N, int K_aug, int num_cus, int workgroups = 0);
+size_t streamk_workspace_bytes(int M, int N, int K_aug, int num_cus);
+hipError_t launch_gemm_streamk(const uint8_t* Aq, const uint8_t* Asc, int M, const uint8_t* Wp,
+                               const uint8_t* Wps, int N, int K_aug, float* Y,
+                               const StreamKConfig& c, void* workspace, hipStream_t stream);
 // gemm_decode.hip.  tiles / row_splits = 0 pick them from the rows.
 size_t decode_lds_bytes(int K_aug, int tiles);
 DecodeConfig choose_decode_config(int M_per_group, int N, int K_aug, int grouped, int tiles,

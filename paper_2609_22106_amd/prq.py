@@ -20,7 +20,7 @@ from . import build as _build
 
 PRQ_OK, PRQ_EINVAL, PRQ_EALIGN, PRQ_EDEVICE, PRQ_EUNSUPPORTED, PRQ_EWORKSPACE = 0, -1, -2, -3, -4, -5
 SCALE_MODES = {"smooth": 0, "act_only": 1, "none": 2}
-GEMM_AUTO, GEMM_TILE, GEMM_STREAM = 0, 1, 2
+GEMM_AUTO, GEMM_TILE, GEMM_STREAM, GEMM_STREAM_K = 0, 1, 2, 3
 HEADER = os.path.join(_build.INCLUDE, "prq.h")
 
 if not os.path.exists(_build.LIB):

@@ -207,19 +207,24 @@ def test_reference_packer_is_a_padded_permutation():
         assert np.count_nonzero(Ps == 127) == sb - sc.size
 
 
+HEAD = 16384   # every GEMM workspace: stream-K arrival counters first, scratch after
+
+
 def test_workspace_sizes():
     # the LDS-tiled kernel splits along K when its tiles would leave CUs idle:
-    # splits - 1 partial sums of M x N floats; a full round of tiles is unsplit
+    # splits - 1 partial sums of M x N floats after the state head; a full
+    # round of tiles is unsplit
     ws = prq.prq_gemm_workspace_bytes(64, 2560, 9984, prq.GEMM_TILE)
-    assert ws > 0 and ws % (64 * 2560 * 4) == 0
+    assert ws > HEAD and (ws - HEAD) % (64 * 2560 * 4) == 0
     assert prq.prq_gemm_workspace_bytes(8192, 2560, 9984, prq.GEMM_TILE) == 0
     ws = prq.prq_gemm_packed_workspace_bytes(512, 2560, 9984)
-    assert ws > 0 and ws % (512 * 2560 * 4) == 0
+    assert ws > HEAD and (ws - HEAD) % (512 * 2560 * 4) == 0
     assert prq.prq_gemm_packed_workspace_bytes(8192, 2560, 9984) == 0
     assert prq.prq_gemm_packed_workspace_bytes(512, 2560, 9980) == 0     # invalid K_aug
     assert prq.prq_gemm_workspace_bytes(64, 2560, 9984, prq.GEMM_STREAM, 1) == 0
-    ws = prq.prq_gemm_workspace_bytes(64, 2560, 9984, prq.GEMM_STREAM, 4)
-    assert ws >= 64 * 2560 * 4 + (2560 // 16) * 4     # float accumulator + arrival counters
+    # a forced split count: partial sums [splits][M][N] added in a fixed order
+    assert prq.prq_gemm_workspace_bytes(64, 2560, 9984, prq.GEMM_STREAM, 4) == HEAD + 4 * 64 * 2560 * 4
+    assert prq.prq_gemm_workspace_bytes(16, 2560, 9984, prq.GEMM_STREAM, 2) == HEAD + 2 * 16 * 2560 * 4
     assert prq.prq_packed_weight_bytes(1, 2560, 9984) == (160 * 78 * 1024, 160 * 20 * 256)
     assert prq.prq_packed_weight_bytes(128, 2048, 832) == (128 * 128 * 7 * 1024, 128 * 128 * 2 * 256)
     assert prq.prq_grouped_gemm_workspace_bytes(512, 128, 2048, 832) == 0
@@ -323,3 +328,21 @@ def test_expand_producer_matches_oracle(gate):
         bad = perm.copy()
         bad[0] = f.C
         prq.prq_expand_producer(f.W_up, None, inv, bad, 96)
+
+
+def test_streamk_workspace_sizes():
+    """Stream-K workspace (256 CUs assumed without a GPU): none where the plan
+    gives every tile its own workgroup (the down_proj's 160 tiles up to three
+    row groups), else the
+    state head and partial tiles [256][2][M][16] floats; 0 where the kernel does
+    not apply (more than 64 rows, a tile over more than four workgroups).
+    AUTO asks for no workspace at decode rows of the down_proj."""
+    for M in (1, 8, 32, 48):
+        assert prq.prq_gemm_workspace_bytes(M, 2560, 9984, prq.GEMM_STREAM_K) == 0
+    # four row groups of ten units a wave do not fit: one workgroup per CU
+    assert prq.prq_gemm_workspace_bytes(64, 2560, 9984, prq.GEMM_STREAM_K) == HEAD + 256 * 2 * 64 * 16 * 4
+    for M in (1, 8, 32, 64):
+        assert prq.prq_gemm_workspace_bytes(M, 2560, 9984) == 0
+        assert prq.prq_gemm_workspace_bytes(M, 1792, 9984, prq.GEMM_STREAM_K) == HEAD + 256 * 2 * M * 16 * 4
+    assert prq.prq_gemm_workspace_bytes(65, 2560, 9984, prq.GEMM_STREAM_K) == 0
+    assert prq.prq_gemm_workspace_bytes(31, 1024, 9984, prq.GEMM_STREAM_K) == 0
