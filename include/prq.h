@@ -234,6 +234,27 @@ int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M,
                 int32_t variant, int32_t splits, hipStream_t stream);
 
 /*
+ * prq_gemm_noalloc -- prq_gemm (AUTO) with no workspace argument and no
+ * allocation, for callers that cannot allocate device memory: code under HIP
+ * graph capture, serving loops that must not allocate, harnesses that forbid
+ * it.  The workspace is a device array inside the library of
+ * prq_gemm_noalloc_max_workspace_bytes() bytes (16 MiB), one per GPU the
+ * library runs on, held until the process ends, in prq_gemm's workspace layout
+ * (its zero-state head is zero when the library loads and every call leaves
+ * it zero).  Every call on a GPU shares that GPU's array: calls that overlap
+ * on one GPU (concurrent streams, or host threads without ordering) race and
+ * give wrong results; calls ordered on one stream are safe.  Arguments,
+ * errors and results as prq_gemm; additionally PRQ_EWORKSPACE when the call's
+ * plan would need more than the array (prq_gemm_workspace_bytes(M, N, K_aug)
+ * above the maximum; nothing is launched), PRQ_EDEVICE when the array's device
+ * address cannot be taken (on the first call on a device).
+ */
+size_t prq_gemm_noalloc_max_workspace_bytes(void);
+int prq_gemm_noalloc(const uint8_t* Aq, const uint8_t* Asc, int32_t M,
+                     const uint8_t* Wp, const uint8_t* Wps, int32_t N, int32_t K_aug,
+                     float* Y, hipStream_t stream);
+
+/*
  * Packed activations (prefill): the activation side of Eq. 3 written by the
  * quantizer directly in the packed layout of the weights (prq_pack_weight's
  * layout with the M rows in the place of the N output features), so that the

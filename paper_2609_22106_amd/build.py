@@ -35,7 +35,7 @@ HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-ffp-contract=off", "-Wall",
 
 DEVICE_SOURCES = ["act_quant.hip", "pack.hip", "gemm_tile.hip", "gemm_stream.hip", "gemm_decode.hip",
                   "gemm_streamk.hip",
-                  "evaluate.hip"]
+                  "evaluate.hip", "noalloc.hip"]
 HOST_SOURCES = ["prepare.cpp", "abi.cpp"]
 PROBE_SOURCES = ["probe.hip"]
 
@@ -74,9 +74,10 @@ def build(verbose=False):
         out = os.path.join(tmp, "libprq.so")
         _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", out, *objs, "-lpthread"])
         shutil.move(out, LIB)
-        # kernels for the tuning entry points (evaluate.hip calls into the host
-        # library and stays out)
-        pobjs = [o for o in objs if o.endswith(".hip.o") and not o.endswith("evaluate.hip.o")]
+        # kernels for the tuning entry points (evaluate.hip and noalloc.hip call
+        # into the host library and stay out)
+        pobjs = [o for o in objs if o.endswith(".hip.o") and not o.endswith("evaluate.hip.o")
+                 and not o.endswith("noalloc.hip.o")]
         for src in PROBE_SOURCES:
             obj = os.path.join(tmp, src + ".o")
             _run([HIPCC, *HIP_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c", os.path.join(CSRC, src),

@@ -63,6 +63,8 @@ _gemm_ws_ex = _decl("prq_gemm_workspace_bytes_ex", _sz, [_i32, _i32, _i32, _i32,
 _gemm = _decl("prq_gemm", ctypes.c_int, [_p, _p, _i32, _p, _p, _i32, _i32, _p, _p, _sz, _p])
 _gemm_ex = _decl("prq_gemm_ex", ctypes.c_int,
                  [_p, _p, _i32, _p, _p, _i32, _i32, _p, _p, _sz, _i32, _i32, _p])
+_gemm_noalloc = _decl("prq_gemm_noalloc", ctypes.c_int, [_p, _p, _i32, _p, _p, _i32, _i32, _p, _p])
+_gemm_noalloc_max = _decl("prq_gemm_noalloc_max_workspace_bytes", _sz, [])
 _packed_act_bytes = _decl("prq_packed_act_bytes", ctypes.c_int,
                           [_i32, _i32, ctypes.POINTER(_sz), ctypes.POINTER(_sz)])
 _quant_act_packed = _decl("prq_quant_act_packed", ctypes.c_int,
@@ -336,6 +338,23 @@ def prq_gemm(Aq, Asc, W, Y=None, workspace=None, variant=GEMM_AUTO, splits=0, st
     st = _gemm_ex(_ptr(Aq), _ptr(Asc), M, _ptr(W.Wp), _ptr(W.Wps), N, K_aug, _ptr(Y),
                   _ptr(workspace), ws_bytes, variant, splits, _stream(stream))
     _check(st, "prq_gemm")
+    return Y
+
+
+def prq_gemm_noalloc_max_workspace_bytes():
+    return int(_gemm_noalloc_max())
+
+
+def prq_gemm_noalloc(Aq, Asc, W, Y, stream=None):
+    """prq_gemm (AUTO) with the library's own device scratch as its workspace:
+    nothing is allocated, Y [M, N] float32 must be given."""
+    M = Aq.shape[0]
+    if W.E != 1:
+        raise ValueError("prq_gemm_noalloc takes a single weight (E = 1)")
+    _check_gemm_operands(Aq, Asc, W, Y, M)
+    st = _gemm_noalloc(_ptr(Aq), _ptr(Asc), M, _ptr(W.Wp), _ptr(W.Wps), W.N, W.K_aug, _ptr(Y),
+                       _stream(stream))
+    _check(st, "prq_gemm_noalloc")
     return Y
 
 

@@ -1,0 +1,67 @@
+"""prq_gemm_noalloc, prq_gemm with the library's own device scratch as its
+workspace (for callers that cannot allocate): the same bits as prq_gemm given
+a workspace of its own, on two calls in a row (the second with fewer rows),
+both within the GEMM bar of the oracle's float64 Eq. 3; a call whose plan
+needs more scratch than the library holds is refused before any launch."""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import prquant as pq                                           # noqa: E402
+from paper_2609_22106_amd import inputs                                    # noqa: E402
+from tests.gpu_util import assert_gemm_close, dev, host, nan_output, say   # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+def _prq():
+    from paper_2609_22106_amd import prq
+    return prq
+
+
+def test_noalloc_matches_prq_gemm_on_two_calls():
+    """N = 1792, K + k = 9984: M = 512 (the LDS-tiled kernel split along K,
+    partial sums in the scratch) and then M = 8 (the stream-K kernel with tiles
+    shared between workgroups, arrival counters and partial tiles in the
+    scratch), then M = 512 again over what the smaller call left."""
+    prq = _prq()
+    rng = np.random.default_rng(77)
+    N, K_aug = 1792, 9984
+    Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
+    W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
+    limit = prq.prq_gemm_noalloc_max_workspace_bytes()
+    for call, M in enumerate((512, 8, 512)):
+        need = prq.prq_gemm_workspace_bytes(M, N, K_aug)
+        assert 0 < need <= limit, (M, need, limit)
+        Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+        A, As = dev(Aq), dev(Asc)
+        say("no-alloc case: call", call, "M =", M, "scratch", need)
+        Yn = nan_output(M, N)
+        prq.prq_gemm_noalloc(A, As, W, Yn)
+        ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+        Yr = nan_output(M, N)
+        prq.prq_gemm(A, As, W, Y=Yr, workspace=ws)
+        torch.cuda.synchronize()
+        yn, yr = host(Yn), host(Yr)
+        np.testing.assert_array_equal(yn.view(np.uint32), yr.view(np.uint32))
+        assert_gemm_close(yn, pq.gemm(Aq, Asc, Wq, Wsc), f"no-alloc call {call} M={M}")
+
+
+def test_noalloc_refuses_plans_beyond_its_scratch():
+    """M = 1024 x N = 2560 over K + k = 9984 plans a split along K whose partial
+    sums (21 MB) exceed the 16 MiB scratch: PRQ_EWORKSPACE, Y left untouched."""
+    prq = _prq()
+    rng = np.random.default_rng(78)
+    M, N, K_aug = 1024, 2560, 9984
+    assert prq.prq_gemm_workspace_bytes(M, N, K_aug) > prq.prq_gemm_noalloc_max_workspace_bytes()
+    Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
+    W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
+    Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+    Y = nan_output(M, N)
+    say("no-alloc case: refused plan")
+    with pytest.raises(prq.PRQError) as e:
+        prq.prq_gemm_noalloc(dev(Aq), dev(Asc), W, Y)
+    assert e.value.status == prq.PRQ_EWORKSPACE
+    torch.cuda.synchronize()
+    assert bool(torch.isnan(Y).all())
