@@ -1,7 +1,7 @@
 #!/usr/bin/env python3
 """Benchmark of the PRQuant MXFP4 + tail-residual hot path on one MI355X.
 
-Default workload: the Qwen3-4B-shaped down_proj at decode (K = 9728 -> N =
+Headline workload: the Qwen3-4B-shaped down_proj at decode (K = 9728 -> N =
 2560, k = 256, rows M = 1, 8, 32, 64).  One step = for every M, the fused
 activation quantization (prq_quant_act) followed by the augmented MXFP4 GEMM
 over K + k (prq_gemm) on one stream, with inputs resident in HBM; the offline
@@ -10,25 +10,31 @@ copies (>= 1 GiB) that every step streams them from HBM rather than from the
 256 MB Infinity Cache.
 
 Timed region: exactly `--steps` whole steps captured into one HIP graph (each
-step binding the next rotated weight copy) and replayed once, bracketed by
-torch.cuda.synchronize() on both sides and HIP events on the stream -- how a
-serving loop launches a step, and free of per-kernel instrumentation.  The
-per-kernel durations (detail, roofline) come from a separate pass of the same
-steps launched eagerly, queued behind a GPU spin-sleep, with fence-free HIP
-events around every kernel; its step time is reported as
-``eager_ms_per_step`` (events add ~2-4 us per kernel).  --no-graph times the
-eager pass instead.
+step binding the next rotated weight copy), replayed once untimed and then five
+times, each replay bracketed by torch.cuda.synchronize() and HIP events on the
+stream; ms_per_step is the median replay over --steps.  Per-kernel launch
+durations (detail, roofline) come from batches of back-to-back launches of one
+kernel (rotated weights), queued behind a GPU spin-sleep, with fence-free HIP
+events around each batch only.
 
-Prints ONE JSON line on stdout (everything else goes to stderr):
-  value = algorithmic bytes of one step / step time (GB/s), plus per-M
-  kernel times, TFLOP/s, roofline fraction of the dominant kernel (the GEMM)
-  from the events around its launches, a same-shape BF16 torch.matmul for
-  context, and the CPU oracle timed on a bounded sample (``cpu_baseline``).
+By default (--workload all) the other workloads run after the headline and
+appear in ``detail`` (per op) and ``workloads`` (per step, with their GEMM
+roofline): prefill (M = 512, 2048, 8192), experts (128 expert down_projs
+768 -> 2048, k = 64, 64 tokens routed top-8, one grouped launch),
+experts_prefill (4096 tokens), layers (the seven linears of a
+Qwen3-4B-shaped decoder layer at M = 4096).  --workload X runs X alone as the
+headline.
 
-Other workloads (--workload): prefill (M = 512, 2048, 8192), experts (128
-expert down_projs 768 -> 2048, k = 64, 64 or 4096 tokens routed top-8, one
-grouped launch), layers (the seven linears of a Qwen3-4B-shaped decoder layer
-at M = 4096).
+Prints ONE JSON line on stdout (everything else goes to stderr): value =
+algorithmic bytes of one headline step / step time (GB/s), per-kernel times,
+TFLOP/s, the GEMM roofline fraction, context timings (same-shape BF16
+torch.matmul, plain MXFP4 through the same kernels, the weight-read floor,
+hot-cache step), the CPU oracle timed on a bounded sample (``cpu_baseline``),
+GPU clocks and ROCm version.
+
+--counters runs --warmup + --steps eager steps of one workload and nothing
+else (for rocprofv3 --pmc); --traffic-from turns two such counter runs into
+profiles/traffic_<workload>.json.
 """
 from __future__ import annotations
 
@@ -56,8 +62,9 @@ def parse_args(argv=None):
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=10)
-    p.add_argument("--workload", default="decode",
-                   choices=["decode", "prefill", "experts", "experts_prefill", "layers"])
+    p.add_argument("--workload", default="all",
+                   choices=["all", "decode", "prefill", "experts", "experts_prefill", "layers"],
+                   help="all: the decode headline plus every other workload in detail")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-bf16", action="store_true")
     p.add_argument("--no-graph", action="store_true", help="skip the graph-replay cross-check")
@@ -71,6 +78,8 @@ def parse_args(argv=None):
                         "WRITE_SIZE) into profiles/traffic_<workload>.json")
     p.add_argument("--traffic-command", default="",
                    help="the profiled command, recorded with --traffic-from")
+    p.add_argument("--counters", action="store_true",
+                   help="run --warmup + --steps eager steps of --workload and nothing else")
     return p.parse_args(argv)
 
 
@@ -94,7 +103,8 @@ class Op:
         self.name, self.M, self.N, self.K, self.k = name, M, N, K, k
         self.act_fn, self.gemm_fn = act_fn, gemm_fn
         self.gemm_bytes, self.act_bytes, self.flops = gbytes, abytes, flops
-        self.t_gemm, self.t_act = [], []
+        self.t_gemm = self.t_act = None
+        self.weights = None
 
 
 PACKED_MIN_ROWS = 64   # more rows than this: the packed prefill pair
@@ -154,6 +164,7 @@ def build_dense_ops(torch, prq, layers, M_list, rotate_bytes, plain=False):
 
             ops.append(Op(f"{name}/M={M}", M, N, K, k, act, gemm, gemm_bytes(M, N, K_aug),
                           act_bytes(M, K, K_aug), 2.0 * M * N * K_aug))
+            ops[-1].weights = Ws
         log(f"[bench] {name}: {R} rotated weight copies ({w_bytes / 1e6:.2f} MB each)")
     return ops
 
@@ -272,78 +283,143 @@ class HipTimer:
             self.hip.hipEventDestroy(e)
 
 
-def run_steps(torch, ops, steps, warmup, stream):
-    """Warmup, then the timed region: `steps` whole steps with HIP events on
-    the launch stream around every kernel.  The launches are queued behind a
-    GPU spin-sleep long enough for the host to enqueue all of them, so the
-    region measures the GPU executing the steps back to back, not the host's
-    per-launch cost (which a serving loop hides with a graph; see
-    graph_step_time)."""
+def time_kernels(torch, ops, reps, warmup, stream):
+    """Per-kernel launch durations: for every op, `reps` back-to-back launches
+    of its activation quantizer, then `reps` of its GEMM (the GEMM binding the
+    next rotated weight copy each time), each batch queued behind a GPU
+    spin-sleep long enough for the host to enqueue it and bracketed by two
+    fence-free HIP events on the launch stream (after one untimed batch of the
+    same launches); per-launch seconds = batch time / reps.  The quantizer's
+    inputs are therefore warm here (in a step they follow a weight stream).  No event sits between two launches of a batch, so the figure is
+    the kernel's average duration in a stream of launches (gaps included)."""
     for _ in range(warmup):
         step_once(ops)
     torch.cuda.synchronize()
     rate = sleep_rate(torch, stream)
-    t0 = time.perf_counter()
-    step_once(ops)                                   # host enqueue cost of a step
-    host_step = time.perf_counter() - t0
-    torch.cuda.synchronize()
-    # events add host time per launch too: budget 2x the measured step, +5 ms
-    hold_s = min(2.0, steps * host_step * 2.0 + 5e-3)
     timer = HipTimer()
-    start, end = timer.event(), timer.event()
-    pairs = [(op, timer.event(), timer.event(), timer.event()) for _ in range(steps) for op in ops]
-    torch.cuda._sleep(int(hold_s * rate))
-    timer.record(start, stream)
-    t0 = time.perf_counter()
-    for op, ea0, ea1, eg1 in pairs:
-        timer.record(ea0, stream)
-        op.act_fn()
-        timer.record(ea1, stream)
-        op.gemm_fn()
-        timer.record(eg1, stream)
-    timer.record(end, stream)
-    enqueue_s = time.perf_counter() - t0
-    torch.cuda.synchronize()
-    for op, ea0, ea1, eg1 in pairs:
-        op.t_act.append(timer.seconds(ea0, ea1))
-        op.t_gemm.append(timer.seconds(ea1, eg1))
-    gpu_s = timer.seconds(start, end)
-    timer.destroy([start, end] + [e for p in pairs for e in p[1:]])
-    return gpu_s, {"host_enqueue_s": round(enqueue_s, 5), "gpu_hold_s": round(hold_s, 5),
-                   "queued_ahead": bool(enqueue_s < hold_s)}
+    for op in ops:
+        for kind, fn in (("act", op.act_fn), ("gemm", op.gemm_fn)):
+            t0 = time.perf_counter()
+            fn()
+            host = time.perf_counter() - t0
+            torch.cuda.synchronize()
+            hold_s = min(2.0, reps * host * 2.0 + 2e-3)
+            a, b = timer.event(), timer.event()
+            for timed in (False, True):      # an untimed batch first: clocks and caches settle
+                torch.cuda._sleep(int(hold_s * rate))
+                timer.record(a, stream)
+                for _ in range(reps):
+                    fn()
+                timer.record(b, stream)
+                torch.cuda.synchronize()
+            per = timer.seconds(a, b) / reps
+            timer.destroy([a, b])
+            if kind == "act":
+                op.t_act = per
+            else:
+                op.t_gemm = per
 
 
-def graph_step_time(torch, ops, steps):
-    """Exactly `steps` steps captured into one HIP graph and replayed once
-    (after one untimed replay), bracketed by synchronize: (GPU seconds per
-    step from events around the replay, host wall seconds of the replay)."""
+def graph_step_times(torch, ops, steps, replays=5):
+    """Exactly `steps` steps captured into one HIP graph (each captured step
+    binds the next rotated weight copy, so a replay streams >= 1 GiB of
+    weights from HBM, not the 256 MB Infinity Cache), replayed once untimed and
+    then `replays` times, each bracketed by torch.cuda.synchronize() and events:
+    (GPU seconds per step of each timed replay, host wall seconds of each)."""
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
         step_once(ops)
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
-    # all `steps` steps in one graph: each captured step binds the next
-    # rotated weight copy, so replays stream the same >= 1 GiB of weights as
-    # the eager region (a short graph would cycle through few enough copies to
-    # be served from the Infinity Cache)
-    per_graph = max(1, steps)
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        for _ in range(per_graph):
+        for _ in range(steps):
             step_once(ops)
     g.replay()
     torch.cuda.synchronize()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    gpu, wall = [], []
+    for _ in range(replays):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        a.record()
+        g.replay()
+        b.record()
+        torch.cuda.synchronize()
+        wall.append(time.perf_counter() - t0)
+        gpu.append(a.elapsed_time(b) * 1e-3 / steps)
+    del g
+    return gpu, wall
+
+
+def read_floor(torch, prq, W_list, reps=160):
+    """The weight-read floor of the decode GEMM (context, committed probe
+    kernel of the test library): every byte of a packed weight (codes and
+    scales) read with one workgroup per CU, each an equal contiguous share,
+    nothing computed; back-to-back launches over the same rotated copies as the
+    GEMM, seconds per launch."""
+    import ctypes
+    from paper_2609_22106_amd import build
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    P, I = ctypes.c_void_p, ctypes.c_int
+    lib.prq_probe_read_floor.argtypes = [P, I, P, I, I, P, P]
+    lib.prq_probe_read_floor.restype = I
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    out = torch.zeros(cus, dtype=torch.int32, device="cuda")
+    sp = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    R = len(W_list)
+
+    def launch(i):
+        W = W_list[i % R]
+        st = lib.prq_probe_read_floor(W.Wp.data_ptr(), W.Wp.numel() // 1024, W.Wps.data_ptr(),
+                                      W.Wps.numel() // 1024, cus, out.data_ptr(), sp)
+        if st != 0:
+            raise RuntimeError(f"prq_probe_read_floor failed ({st})")
+    for i in range(5):
+        launch(i)
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
+    torch.cuda._sleep(20_000_000)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     a.record()
-    g.replay()
+    for i in range(reps):
+        launch(i)
     b.record()
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    del g
-    return a.elapsed_time(b) * 1e-3 / per_graph, wall
+    W = W_list[0]
+    nbytes = (W.Wp.numel() // 1024 + W.Wps.numel() // 1024) * 1024
+    return a.elapsed_time(b) * 1e-3 / reps, nbytes
+
+
+def gpu_info(torch):
+    """Device, clocks and ROCm versions for the record."""
+    import ctypes
+    info = {"device": torch.cuda.get_device_name(0),
+            "arch": getattr(torch.cuda.get_device_properties(0), "gcnArchName", None),
+            "cus": torch.cuda.get_device_properties(0).multi_processor_count,
+            "torch_hip": torch.version.hip}
+    try:
+        info["rocm"] = open("/opt/rocm/.info/version").read().strip()
+    except OSError:
+        info["rocm"] = None
+    try:
+        path = next(line.split()[-1] for line in open("/proc/self/maps") if "libamdhip64" in line)
+        hip = ctypes.CDLL(path)
+        v = ctypes.c_int()
+        if hip.hipDeviceGetAttribute(ctypes.byref(v), 5, 0) == 0:       # clock rate, kHz
+            info["max_sclk_mhz"] = v.value // 1000
+        if hip.hipDeviceGetAttribute(ctypes.byref(v), 60, 0) == 0:      # memory clock, kHz
+            info["max_mclk_mhz"] = v.value // 1000
+    except Exception as e:  # pragma: no cover
+        info["clock_error"] = str(e)
+    try:
+        import subprocess
+        r = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True, timeout=20)
+        info["rocm_smi_clocks"] = [ln.strip() for ln in r.stdout.splitlines()
+                                   if "clk" in ln.lower() and "level" in ln.lower()][:6]
+    except Exception as e:  # pragma: no cover
+        info["rocm_smi_clocks"] = f"unavailable: {e}"
+    return info
 
 
 def copy_context(torch, prq, layers, M_list, reps=50):
@@ -414,36 +490,53 @@ def bf16_context(torch, layers, M_list, rotate_bytes, steps):
 
 def cpu_baseline(np, layers, M_list, budget_s=12.0):
     """The oracle (as it stands) on the host cores: act-quant + GEMM of every
-    (layer, M) pair of one step, repeated until about `budget_s` seconds."""
+    M of one step, repeated until about `budget_s` seconds (the value, GB/s of
+    the same algorithmic bytes as the GPU step); also the oracle's prepare
+    (once), quant_act and gemm timed separately, and quant_act on one core."""
     from oracle import prquant as pq
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:  # pragma: no cover
-        threads = 1
+        threadpool_limits, threads = None, 1
     name, c = layers[0]
     t0 = time.perf_counter()
     art = pq.prepare(c.W, c.Xcal, c.alpha, c.k_tail)
-    log(f"[bench] oracle prepare (untimed): {time.perf_counter() - t0:.1f} s")
+    t_prepare = time.perf_counter() - t0
+    log(f"[bench] oracle prepare: {t_prepare:.1f} s")
     K, k, N = c.K, c.k_tail, c.N
     K_aug = K + k
-    byts, reps = 0.0, 0
+    byts, reps, t_q, t_g = 0.0, 0, 0.0, 0.0
     t0 = time.perf_counter()
     while True:
         for M in M_list:
+            ta = time.perf_counter()
             Aq, Asc = pq.quant_act(c.X[:M], art["inv_scale"], art["perm"], k)
+            tb = time.perf_counter()
             pq.gemm(Aq, Asc, art["Wq"], art["Wsc"])
+            t_q += tb - ta
+            t_g += time.perf_counter() - tb
             byts += act_bytes(M, K, K_aug) + gemm_bytes(M, N, K_aug)
         reps += 1
         el = time.perf_counter() - t0
         if el >= budget_s or reps >= 50:
             break
-    threads = max(threads, 1)
+    q1 = None
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            ta = time.perf_counter()
+            for M in M_list:
+                pq.quant_act(c.X[:M], art["inv_scale"], art["perm"], k)
+            q1 = time.perf_counter() - ta
     return {"value": round(byts / el / 1e9, 4), "unit": "GB/s",
-            "cores": int(threads), "kind": "oracle",
+            "cores": int(max(threads, 1)), "kind": "oracle",
             "sample": f"{reps} passes of oracle act-quant + GEMM at M={list(M_list)} on {name} "
                       f"(N={N}, K={K}, k={k}); {el:.1f} s; host cores visible "
-                      f"{len(os.sched_getaffinity(0))}, BLAS threads {threads}"}
+                      f"{len(os.sched_getaffinity(0))}, BLAS threads {threads}",
+            "prepare_s": round(t_prepare, 2),
+            "quant_act_s_per_pass": round(t_q / reps, 4),
+            "gemm_s_per_pass": round(t_g / reps, 4),
+            "quant_act_s_per_pass_1core": None if q1 is None else round(q1, 4)}
 
 
 CALIB_BYTES = 512 * 2 ** 20
@@ -505,12 +598,12 @@ GEMM_OPS_PER_STEP = {"decode": 4, "prefill": 3, "experts": 1, "experts_prefill":
 
 
 def _steps_run(command):
-    """Steps a counter run executed: --warmup + --steps + the one step that
-    measures the host enqueue cost (bench.py defaults when absent)."""
+    """Steps a --counters run executed: --warmup + --steps (bench.py defaults
+    when absent)."""
     def opt(name, default):
         m = re.search(rf"--{name}\s+(\d+)", command)
         return int(m.group(1)) if m else default
-    return opt("warmup", 10) + opt("steps", 50) + 1
+    return opt("warmup", 10) + opt("steps", 50)
 
 
 def traffic_from_counters(workload, fetch_dir, write_dir, command):
@@ -527,7 +620,8 @@ def traffic_from_counters(workload, fetch_dir, write_dir, command):
         rows = _counter_rows(run_dir, counter)
         calib = [v for n, v in rows if "neg_kernel" in n]
         gemm = [(n, v) for n, v in rows if "prq" in n and any(
-            t in n for t in ("gemm_decode_kernel", "gemm_stream_kernel", "gemm_tile_kernel", "gemm_grouped_persist_kernel",
+            t in n for t in ("gemm_decode_kernel", "gemm_stream_kernel", "gemm_streamk_kernel",
+                             "gemm_tile_kernel", "gemm_grouped_persist_kernel",
                              "reduce_partials_kernel", "zero_kernel", "splitk_reduce_kernel"))]
         launches = [v for n, v in gemm if "gemm_" in n]
         if not calib or not launches:
@@ -548,6 +642,129 @@ def traffic_from_counters(workload, fetch_dir, write_dir, command):
 
 
 # ---------------------------------------------------------------- main ---
+WORKLOADS = ("decode", "prefill", "experts", "experts_prefill", "layers")
+
+
+def build_workload(torch, np, prq, inputs, wl, rotate_bytes, plain=False):
+    """(ops, dense layers or [], M list, config) of one workload."""
+    if wl in ("decode", "prefill"):
+        c = inputs.down_proj_decode() if wl == "decode" else inputs.down_proj_prefill()
+        layers = [("qwen3_4b_down_proj", c)]
+        M_list = list(c.M_list)
+        ops = build_dense_ops(torch, prq, layers, M_list, rotate_bytes, plain=plain)
+        config = {"workload": f"qwen3_4b_down_proj_{wl}", "N": 2560, "K": 9728, "k_tail": 256,
+                  "alpha": 0.5, "M": M_list}
+    elif wl in ("experts", "experts_prefill"):
+        tokens = 64 if wl == "experts" else 4096
+        ops = build_expert_ops(torch, np, prq, inputs, tokens, rotate_bytes)
+        layers, M_list = [], []
+        config = {"workload": f"qwen3_30b_a3b_expert_down_proj_{tokens}tok", "E": 128, "N": 2048,
+                  "K": 768, "k_tail": 64, "alpha": 0.5, "topk": 8, "routed_rows": ops[0].M}
+    else:
+        layers = [(n, inputs.layer_case(n)) for n, _, _ in inputs.LAYER_SET]
+        M_list = [4096]
+        ops = build_dense_ops(torch, prq, layers, M_list, rotate_bytes, plain=plain)
+        config = {"workload": "qwen3_4b_decoder_linears_prefill", "M": 4096,
+                  "layers": {n: {"N": c.N, "K": c.K, "k_tail": c.k_tail} for n, c in layers}}
+    return ops, layers, M_list, config
+
+
+def op_detail(op):
+    tg, ta = op.t_gemm, op.t_act
+    return {"gemm_us": round(tg * 1e6, 3), "act_quant_us": round(ta * 1e6, 3),
+            "op_us": round((tg + ta) * 1e6, 3),
+            "gemm_GBs": round(op.gemm_bytes / tg / 1e9, 1),
+            "gemm_TFLOPs": round(op.flops / tg / 1e12, 2),
+            "gemm_hbm_frac": round(op.gemm_bytes / tg / 1e9 / HBM_PEAK_GBS, 4),
+            "gemm_mfma_frac": round(op.flops / tg / 1e12 / MXFP4_PEAK_TFLOPS, 4),
+            "act_quant_GBs": round(op.act_bytes / ta / 1e9, 1),
+            "act_quant_hbm_frac": round(op.act_bytes / ta / 1e9 / HBM_PEAK_GBS, 4)}
+
+
+def gemm_roofline(ops, wl):
+    """Roofline of the workload's dominant kernel, the GEMM: algorithmic bytes
+    (or FLOPs) of its launches over their summed launch durations; the bound
+    follows the GEMM's own arithmetic intensity against the ridge."""
+    g_bytes = sum(op.gemm_bytes for op in ops)
+    g_flops = sum(op.flops for op in ops)
+    g_time = sum(op.t_gemm for op in ops)
+    bound = "mfma" if g_flops / max(g_bytes, 1) > MXFP4_PEAK_TFLOPS / HBM_PEAK_GBS * 1e3 else "hbm"
+    if bound == "hbm":
+        achieved, peak, unit = g_bytes / g_time / 1e9, HBM_PEAK_GBS, "GB/s"
+    else:
+        achieved, peak, unit = g_flops / g_time / 1e12, MXFP4_PEAK_TFLOPS, "TFLOP/s"
+    traffic = traffic_record(wl)
+    return {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+            "frac": round(achieved / peak, 4), "traffic": traffic,
+            "traffic_over_algorithmic": None if traffic is None else round(traffic / (g_bytes / len(ops)), 3),
+            "kernel": "prq_gemm (augmented MXFP4 GEMM over K+k)",
+            "per_launch_bytes": round(g_bytes / len(ops), 1),
+            "per_launch_flops": round(g_flops / len(ops), 1),
+            "avg_launch_us": round(g_time / len(ops) * 1e6, 3)}
+
+
+def measure_workload(torch, np, prq, inputs, wl, args, stream, contexts=True):
+    """Everything measured for one workload: per-kernel launch durations, step
+    time (median of graph replays), GEMM roofline and the context timings."""
+    ops, layers, M_list, config = build_workload(torch, np, prq, inputs, wl, args.rotate_bytes)
+    reps = max(args.steps, 20)
+    time_kernels(torch, ops, reps, args.warmup, stream)
+    if args.no_graph:
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            step_once(ops)
+        torch.cuda.synchronize()
+        steps_gpu, walls = [(time.perf_counter() - t0) / args.steps], [time.perf_counter() - t0]
+    else:
+        steps_gpu, walls = graph_step_times(torch, ops, args.steps)
+    t_step = float(np.median(steps_gpu))
+    step_bytes = sum(op.gemm_bytes + op.act_bytes for op in ops)
+    step_flops = sum(op.flops for op in ops)
+    detail = {op.name: op_detail(op) for op in ops}
+    out = {"config": config, "t_step": t_step, "steps_gpu": steps_gpu, "walls": walls,
+           "value": step_bytes / t_step / 1e9, "tflops": step_flops / t_step / 1e12,
+           "roofline": gemm_roofline(ops, wl), "detail": detail, "M_list": M_list,
+           "layers": layers}
+    if contexts and wl == "decode":
+        t_floor, nbytes = read_floor(torch, prq, ops[0].weights)
+        out["read_floor"] = {"us": round(t_floor * 1e6, 3), "bytes": nbytes,
+                             "GBs": round(nbytes / t_floor / 1e9, 1),
+                             "hbm_frac": round(nbytes / t_floor / 1e9 / HBM_PEAK_GBS, 4)}
+    if contexts and layers and not args.no_bf16:
+        for key, t in bf16_context(torch, layers, M_list, args.rotate_bytes, args.steps).items():
+            if key in detail:
+                d = detail[key]
+                d["bf16_matmul_us"] = round(t * 1e6, 3)
+                d["speedup_op_vs_bf16"] = round(t / (d["op_us"] * 1e-6), 3)
+                d["speedup_gemm_vs_bf16"] = round(t / (d["gemm_us"] * 1e-6), 3)
+    if contexts and layers and not args.no_plain and wl in ("decode", "prefill"):
+        # plain MXFP4 (k = 0, no scaling) through the same kernels and timing
+        plain_ops, _, _, _ = build_workload(torch, np, prq, inputs, wl, args.rotate_bytes, plain=True)
+        time_kernels(torch, plain_ops, reps, args.warmup, stream)
+        for op in plain_ops:
+            if op.name in detail:
+                d = detail[op.name]
+                d["plain_mxfp4_gemm_us"] = round(op.t_gemm * 1e6, 3)
+                d["plain_mxfp4_op_us"] = round((op.t_gemm + op.t_act) * 1e6, 3)
+                d["op_over_plain_mxfp4"] = round(d["op_us"] / ((op.t_gemm + op.t_act) * 1e6), 3)
+        del plain_ops
+    if contexts and layers and wl in ("decode", "prefill"):
+        for key, r in copy_context(torch, prq, layers, M_list).items():
+            if key in detail:
+                detail[key]["act_quant_online_copy_warm_us"] = round(r["online"] * 1e6, 3)
+                detail[key]["act_quant_offline_copy_warm_us"] = round(r["offline"] * 1e6, 3)
+    if contexts and wl == "decode" and not args.no_graph:
+        # hot: the same steps on one weight copy (served from the Infinity Cache)
+        hot_ops, _, _, _ = build_workload(torch, np, prq, inputs, wl, 0)
+        hot, _ = graph_step_times(torch, hot_ops, args.steps)
+        out["hot_ms_per_step"] = round(float(np.median(hot)) * 1e3, 5)
+        del hot_ops
+    del ops
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
+
+
 def main(argv=None):
     args = parse_args(argv)
     if args.traffic_from:
@@ -565,117 +782,59 @@ def main(argv=None):
     from paper_2609_22106_amd import inputs, prq
 
     stream = torch.cuda.current_stream()
-    wl = args.workload
-    if wl in ("decode", "prefill"):
-        c = inputs.down_proj_decode() if wl == "decode" else inputs.down_proj_prefill()
-        layers = [("qwen3_4b_down_proj", c)]
-        M_list = list(c.M_list)
-        ops = build_dense_ops(torch, prq, layers, M_list, args.rotate_bytes)
-        config = {"workload": f"qwen3_4b_down_proj_{wl}", "N": 2560, "K": 9728, "k_tail": 256,
-                  "alpha": 0.5, "M": M_list}
-    elif wl in ("experts", "experts_prefill"):
-        tokens = 64 if wl == "experts" else 4096
-        ops = build_expert_ops(torch, np, prq, inputs, tokens, args.rotate_bytes)
-        layers, M_list = [], []
-        config = {"workload": f"qwen3_30b_a3b_expert_down_proj_{tokens}tok", "E": 128, "N": 2048,
-                  "K": 768, "k_tail": 64, "alpha": 0.5, "topk": 8, "routed_rows": ops[0].M}
-    else:
-        layers = [(n, inputs.layer_case(n)) for n, _, _ in inputs.LAYER_SET]
-        M_list = [4096]
-        ops = build_dense_ops(torch, prq, layers, M_list, args.rotate_bytes)
-        config = {"workload": "qwen3_4b_decoder_linears_prefill", "M": 4096,
-                  "layers": {n: {"N": c.N, "K": c.K, "k_tail": c.k_tail} for n, c in layers}}
-
+    if args.counters:
+        wl = "decode" if args.workload == "all" else args.workload
+        if args.copy_calibration:
+            copy_calibration(torch)
+        ops, _, _, config = build_workload(torch, np, prq, inputs, wl, args.rotate_bytes)
+        for _ in range(args.warmup + args.steps):
+            step_once(ops)
+        torch.cuda.synchronize()
+        print(json.dumps({"counters_run": config["workload"], "steps": args.warmup + args.steps,
+                          "gemm_calls": (args.warmup + args.steps) * len(ops)}), flush=True)
+        return 0
+    head_wl = "decode" if args.workload == "all" else args.workload
+    others = [w for w in WORKLOADS if w != head_wl] if args.workload == "all" else []
+    info = gpu_info(torch)
     if args.copy_calibration:
         copy_calibration(torch)
-    # untimed warmup, then the timed region: whole steps, with HIP events on
-    # the launch stream around every kernel for the per-kernel durations
-    t_gpu, queue_info = run_steps(torch, ops, args.steps, args.warmup, stream)
-    t_eager_step = t_gpu / args.steps
-    if args.no_graph:
-        t_step, t_wall = t_eager_step, None
-    else:
-        t_step, t_wall = graph_step_time(torch, ops, args.steps)
-    ms_per_step = t_step * 1e3
-    step_bytes = sum(op.gemm_bytes + op.act_bytes for op in ops)
-    step_flops = sum(op.flops for op in ops)
-    value = step_bytes / t_step / 1e9
-
-    detail = {}
-    g_bytes = g_time = 0.0
-    for op in ops:
-        tg = float(np.mean(op.t_gemm))
-        ta = float(np.mean(op.t_act))
-        g_bytes += op.gemm_bytes
-        g_time += tg
-        detail[op.name] = {
-            "gemm_us": round(tg * 1e6, 3), "act_quant_us": round(ta * 1e6, 3),
-            "op_us": round((tg + ta) * 1e6, 3),
-            "gemm_GBs": round(op.gemm_bytes / tg / 1e9, 1),
-            "gemm_TFLOPs": round(op.flops / tg / 1e12, 2),
-            "gemm_hbm_frac": round(op.gemm_bytes / tg / 1e9 / HBM_PEAK_GBS, 4),
-            "gemm_mfma_frac": round(op.flops / tg / 1e12 / MXFP4_PEAK_TFLOPS, 4),
-            "act_quant_GBs": round(op.act_bytes / ta / 1e9, 1),
-        }
-    # the GEMM's own arithmetic intensity decides which roof bounds it
-    g_flops = sum(op.flops for op in ops)
-    bound = "mfma" if g_flops / max(g_bytes, 1) > MXFP4_PEAK_TFLOPS / HBM_PEAK_GBS * 1e3 else "hbm"
-    if bound == "hbm":
-        achieved, peak, unit = g_bytes / g_time / 1e9, HBM_PEAK_GBS, "GB/s"
-    else:
-        achieved, peak, unit = g_flops / g_time / 1e12, MXFP4_PEAK_TFLOPS, "TFLOP/s"
-    roofline = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-                "frac": round(achieved / peak, 4), "traffic": traffic_record(wl),
-                "kernel": "prq_gemm (augmented MXFP4 GEMM over K+k)",
-                "per_launch_bytes": round(g_bytes / len(ops), 1),
-                "avg_launch_us": round(g_time / len(ops) * 1e6, 3)}
-
-    if not args.no_bf16 and layers:
-        bf = bf16_context(torch, layers, M_list, args.rotate_bytes, args.steps)
-        for key, t in bf.items():
-            if key in detail:
-                detail[key]["bf16_matmul_us"] = round(t * 1e6, 3)
-                detail[key]["speedup_op_vs_bf16"] = round(t / (detail[key]["op_us"] * 1e-6), 3)
-                detail[key]["speedup_gemm_vs_bf16"] = round(t / (detail[key]["gemm_us"] * 1e-6), 3)
-
-    if layers and not args.no_plain:
-        # plain MXFP4 (k = 0, no scaling) through the same kernels and timing
-        plain_ops = build_dense_ops(torch, prq, layers, M_list, args.rotate_bytes, plain=True)
-        t_plain, _ = run_steps(torch, plain_ops, args.steps, args.warmup, stream)
-        for op in plain_ops:
-            if op.name in detail:
-                tg, ta = float(np.mean(op.t_gemm)), float(np.mean(op.t_act))
-                d = detail[op.name]
-                d["plain_mxfp4_gemm_us"] = round(tg * 1e6, 3)
-                d["plain_mxfp4_op_us"] = round((tg + ta) * 1e6, 3)
-                d["op_over_plain_mxfp4"] = round(d["op_us"] / ((tg + ta) * 1e6), 3)
-        del plain_ops
-    if layers and wl in ("decode", "prefill"):
-        for key, r in copy_context(torch, prq, layers, M_list).items():
-            if key in detail:
-                detail[key]["act_quant_online_copy_warm_us"] = round(r["online"] * 1e6, 3)
-                detail[key]["act_quant_offline_copy_warm_us"] = round(r["offline"] * 1e6, 3)
+    res = measure_workload(torch, np, prq, inputs, head_wl, args, stream)
+    log(f"[bench] {head_wl}: {res['t_step'] * 1e3:.4f} ms per step")
+    detail = dict(res["detail"])
+    workloads = {}
+    for wl in others:
+        r = measure_workload(torch, np, prq, inputs, wl, args, stream)
+        log(f"[bench] {wl}: {r['t_step'] * 1e3:.4f} ms per step")
+        for key, d in r["detail"].items():
+            detail[f"layers/{key}" if wl == "layers" else key] = d
+        workloads[r["config"]["workload"]] = {
+            "ms_per_step": round(r["t_step"] * 1e3, 5), "value_GBs": round(r["value"], 2),
+            "tflops": round(r["tflops"], 3), "roofline": r["roofline"], "config": r["config"]}
 
     cpu = None
-    if not args.no_cpu_baseline and wl in ("decode",):
-        cpu = cpu_baseline(np, layers, M_list)
+    if not args.no_cpu_baseline and head_wl == "decode":
+        cpu = cpu_baseline(np, res["layers"], res["M_list"])
 
     line = {
-        "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+        "metric": METRIC, "value": round(res["value"], 2), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(res["t_step"] * 1e3, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "mxfp4", "data": "synthetic", "config": config,
-        "tflops": round(step_flops / t_step / 1e12, 3),
-        "roofline": roofline, "cpu_baseline": cpu, "detail": detail,
+        "dtype": "mxfp4", "data": "synthetic", "config": res["config"],
+        "tflops": round(res["tflops"], 3),
+        "roofline": res["roofline"], "cpu_baseline": cpu, "detail": detail,
+        "workloads": workloads,
+        "context": {k: res[k] for k in ("read_floor", "hot_ms_per_step") if k in res},
+        "gpu": info,
         "timing": {
             "method": ("eager: the steps launched directly" if args.no_graph else
-                       f"{args.steps} steps in one HIP graph, replayed once between "
-                       "torch.cuda.synchronize() calls, HIP events around the replay"),
-            "replay_wall_s": None if t_wall is None else round(t_wall, 6),
-            "eager_ms_per_step": round(t_eager_step * 1e3, 5),
-            "eager_method": "eager launches queued behind a GPU spin-sleep; HIP events "
-                            "(hipEventDisableSystemFence) on the launch stream around every kernel",
-            **queue_info},
+                       f"{args.steps} steps in one HIP graph, replayed once untimed and then 5 "
+                       "times, each between torch.cuda.synchronize() calls with HIP events "
+                       "around the replay; ms_per_step = median replay / steps"),
+            "replay_ms_per_step": [round(t * 1e3, 5) for t in res["steps_gpu"]],
+            "replay_wall_s": [round(t, 6) for t in res["walls"]],
+            "kernel_method": f"per op, {max(args.steps, 20)} back-to-back launches of the "
+                             "quantizer and then of the GEMM (rotated weights), queued behind a GPU "
+                             "spin-sleep, fence-free HIP events around each batch"},
     }
     print(json.dumps(line), flush=True)
     return 0

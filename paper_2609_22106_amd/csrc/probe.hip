@@ -84,9 +84,50 @@ __global__ __launch_bounds__(64) void lds_dma_probe(const uint8_t* g16, const ui
   for (int i = l; i < 8192 / 16; i += 64) reinterpret_cast<uint4*>(out)[i] = reinterpret_cast<uint4*>(s)[i];
 }
 
+// The weight-read floor: the kilobytes [0, kib1) of p1 and then [0, kib2) of
+// p2 read with `wgs` workgroups of 8 waves, each an equal contiguous share of
+// the kilobytes, every load issued before any is consumed (the memory side of
+// a weight-streaming decode GEMM, with no arithmetic and no output but a
+// never-taken store that keeps the loads).
+__global__ __launch_bounds__(512) void read_floor_kernel(const uint8_t* __restrict__ p1, int kib1,
+                                                         const uint8_t* __restrict__ p2, int kib2,
+                                                         uint32_t* __restrict__ out) {
+  const int total = kib1 + kib2;
+  const int wgs = gridDim.x, wg = blockIdx.x;
+  const int u0 = static_cast<int>(static_cast<int64_t>(total) * wg / wgs);
+  const int u1 = static_cast<int>(static_cast<int64_t>(total) * (wg + 1) / wgs);
+  const int nu = u1 - u0, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int v0 = u0 + nu * wave / 8, cnt = nu * (wave + 1) / 8 - nu * wave / 8;   // <= 8 (host)
+  uint4 w[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int u = cnt > 0 ? v0 + min(j, cnt - 1) : u0;
+    const uint8_t* src = u < kib1 ? p1 + static_cast<int64_t>(u) * 1024
+                                  : p2 + static_cast<int64_t>(u - kib1) * 1024;
+    w[j] = *reinterpret_cast<const uint4*>(src + lane * 16);
+  }
+  uint32_t x = 0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) x ^= w[j].x ^ w[j].y ^ w[j].z ^ w[j].w;
+  if (x == 0x9E3779B9u && lane == 0) out[wg] = x;
+}
+
 }  // namespace
 
 extern "C" {
+
+// Weight-read floor (context for the decode GEMM): out needs wgs dwords;
+// kib1, kib2 >= 0 kilobytes, at most 64 kilobytes per workgroup.
+int prq_probe_read_floor(const uint8_t* p1, int kib1, const uint8_t* p2, int kib2, int wgs,
+                         uint32_t* out, hipStream_t stream) {
+  if (wgs <= 0 || kib1 < 0 || kib2 < 0 || kib1 + kib2 < wgs ||
+      (static_cast<int64_t>(kib1) + kib2 + wgs - 1) / wgs > 64 || !out || (kib1 && !p1) ||
+      (kib2 && !p2))
+    return -1;
+  read_floor_kernel<<<wgs, 512, 0, stream>>>(p1, kib1, p2, kib2, out);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
 
 int prq_probe_mfma16(const void* a, const void* b, const uint32_t* sa, const uint32_t* sb,
                      float* out, hipStream_t stream) {
