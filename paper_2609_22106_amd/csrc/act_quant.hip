@@ -14,9 +14,9 @@
 // nibbles (a wave writes 256 contiguous bytes) and lane 0 of the quad the scale.
 // Two kernels:
 //   * rows kernel (few rows, decode): a thread per unit across many
-//     workgroups; perm and d of its 8 positions live in registers (no
-//     dependent gather: d is given in position order) and the row values are
-//     gathered straight from global memory (rows of a few KB stay in L2).
+//     workgroups; perm and d of its 8 positions live in registers (d is given
+//     in position order); the workgroup's rows are copied whole into LDS
+//     while those entries load, and gathered from LDS.
 //   * LDS kernel (many rows, prefill): a workgroup takes a contiguous range of
 //     rows; a thread keeps the perm and d of its units in registers; each row
 //     is staged into LDS with coalesced 16-byte loads (double-buffered, the
@@ -25,6 +25,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "mx_device.hpp"
 #include "prq_internal.h"
@@ -164,28 +165,65 @@ __device__ __forceinline__ void pad_row_tail(const Sink& out, int u0, int units,
   }
 }
 
+#define PRQ_ROWS_GPTR(p) ((const __attribute__((address_space(1))) void*)(p))
+#define PRQ_ROWS_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
+
+// Few rows (decode).  A workgroup owns kRowsThreads units (quarter blocks) of
+// `rows_per_wg` rows.  Its rows are copied whole into LDS by direct
+// global->LDS copies issued at once, in flight together with the units'
+// permutation entries and inverse scales (the copies do not depend on them),
+// so a cold call pays one memory round trip before the gather instead of
+// two (permutation, then the rows at the permuted channels); the gather then
+// reads LDS.
 template <bool kGrouped>
 __global__ __launch_bounds__(kRowsThreads) void act_quant_rows_kernel(
     const uint16_t* __restrict__ X, int64_t ld_x, int M, int K, int k_tail,
     const float* __restrict__ inv, const int32_t* __restrict__ perm,
     const int32_t* __restrict__ offsets, int G, int rows_per_wg, uint8_t* __restrict__ Aq,
     uint8_t* __restrict__ Asc) {
+  extern __shared__ __align__(16) unsigned char rows_lds[];   // [rows_per_wg][pitch]
+  const int units = K >> 3;
   const int u = blockIdx.x * kRowsThreads + threadIdx.x;
-  if (u >= (K >> 3)) return;   // K/8 is a multiple of 4: quads leave together
   const int r0 = blockIdx.y * rows_per_wg;
   const int r1 = min(M, r0 + rows_per_wg);
+  const int n = r1 - r0;
   const int k_aug = K + k_tail;
   const int64_t row_bytes = k_aug >> 1;
   const int nb = k_aug >> 5;
+  const int xb = 2 * K;                               // bytes of a row of X
+  const int chunks = (xb + 1023) >> 10;
+  const int pitch = chunks * 1024;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int lane = threadIdx.x & 63;
+  // 1. The rows, 1 KB per wave copy (lanes past the row copy its start into
+  //    the pad, never read).
+  for (int i = wave; i < n * chunks; i += kRowsThreads / 64) {
+    const int rr = i / chunks, c = i - rr * chunks;
+    const int off = c * 1024 + lane * 16;
+    const uint8_t* src = reinterpret_cast<const uint8_t*>(X + static_cast<int64_t>(r0 + rr) * ld_x);
+    __builtin_amdgcn_global_load_lds(PRQ_ROWS_GPTR(src + (off < xb ? off : 0)),
+                                     PRQ_ROWS_LPTR(rows_lds + rr * pitch + c * 1024), 16, 0, 0);
+  }
+  // 2. The unit's permutation entries and inverse scales meanwhile.
+  const bool active = u < units;                      // K/8 is a multiple of 4: quads agree
+  const int uc = active ? u : units - 1;
   Unit un;
-  int cur_g = -1;
-  for (int r = r0; r < r1; ++r) {
-    const int g = kGrouped ? dev::find_group(offsets, G, r) : 0;
-    if (g != cur_g) {
-      load_unit(perm, inv, g, K, u, &un);
-      cur_g = g;
+  int cur_g = kGrouped ? dev::find_group(offsets, G, r0) : 0;
+  load_unit(perm, inv, cur_g, K, uc, &un);
+  __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));   // vmcnt(0): copies and entries
+  __syncthreads();
+  if (!active) return;
+  // 3. Gather from LDS, quantize, store.
+  for (int rr = 0; rr < n; ++rr) {
+    const int r = r0 + rr;
+    if (kGrouped) {
+      const int g = dev::find_group(offsets, G, r);
+      if (g != cur_g) {
+        load_unit(perm, inv, g, K, uc, &un);
+        cur_g = g;
+      }
     }
-    const uint16_t* xr = X + static_cast<int64_t>(r) * ld_x;
+    const uint16_t* xr = reinterpret_cast<const uint16_t*>(rows_lds + rr * pitch);
     float z[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j)
@@ -628,6 +666,18 @@ hipError_t launch_act_quant(const uint16_t* X, int64_t ld_x, int M, int K, int k
                                  Asc, num_cus, 0, stream);
 }
 
+// Dynamic LDS of the few-rows kernel above the 64 KiB default (up to four
+// staged rows of K = 16384), set once per instantiation.
+template <bool kGrouped>
+void set_rows_lds_limit() {
+  static std::once_flag once;
+  std::call_once(once, [] {
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&act_quant_rows_kernel<kGrouped>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, 4 * 32768);
+    (void)hipGetLastError();
+  });
+}
+
 hipError_t launch_act_quant_kernel(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail,
                                    const float* inv_scale_pos, const int32_t* perm,
                                    const int32_t* group_offsets, int G, uint8_t* Aq, uint8_t* Asc,
@@ -635,15 +685,21 @@ hipError_t launch_act_quant_kernel(const uint16_t* X, int64_t ld_x, int M, int K
   const bool grouped = group_offsets && G > 1;
   const int units = K >> 3;
   if (kernel == 1 || (kernel == 0 && M <= 64)) {
-    // Few rows: spread the positions over workgroups, at most ~16 row chunks.
-    const int rows_per_wg = std::max(1, (M + 15) / 16);
+    // Few rows: spread the positions over workgroups, at most ~16 row chunks,
+    // each workgroup's rows staged whole in LDS (at most 4 rows of 32 KiB).
+    const int pitch = (2 * K + 1023) / 1024 * 1024;
+    const int rows_per_wg = std::max(1, std::min((M + 15) / 16, 4 * 32768 / pitch));
     const dim3 grid((units + kRowsThreads - 1) / kRowsThreads, (M + rows_per_wg - 1) / rows_per_wg);
-    if (grouped)
-      act_quant_rows_kernel<true><<<grid, kRowsThreads, 0, stream>>>(
+    const size_t lds = static_cast<size_t>(std::min(rows_per_wg, M)) * pitch;
+    if (grouped) {
+      set_rows_lds_limit<true>();
+      act_quant_rows_kernel<true><<<grid, kRowsThreads, lds, stream>>>(
           X, ld_x, M, K, k_tail, inv_scale_pos, perm, group_offsets, G, rows_per_wg, Aq, Asc);
-    else
-      act_quant_rows_kernel<false><<<grid, kRowsThreads, 0, stream>>>(
+    } else {
+      set_rows_lds_limit<false>();
+      act_quant_rows_kernel<false><<<grid, kRowsThreads, lds, stream>>>(
           X, ld_x, M, K, k_tail, inv_scale_pos, perm, nullptr, 1, rows_per_wg, Aq, Asc);
+    }
     return hipGetLastError();
   }
   const int32_t* goff = grouped ? group_offsets : nullptr;

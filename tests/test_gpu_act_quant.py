@@ -136,6 +136,23 @@ def test_random_permutation_and_scales():
     _check(X, K, 96, inv, perm, "random perm")
 
 
+@pytest.mark.parametrize("K,M", [(96, 2), (1056, 31), (4192, 64), (9728, 17)])
+def test_few_row_kernel_staged_row_pads(K, M):
+    """The few-rows kernel copies each row whole into LDS in 1 KiB pieces: rows
+    whose byte length is not a multiple of 1 KiB (the last piece partly past
+    the row), strided rows (ld = K + 32), 1 to 4 rows per workgroup."""
+    rng = np.random.default_rng(K + M)
+    X = inputs.f32_to_bf16_bits((rng.standard_normal((M, K)) * 3).astype(np.float32))
+    perm = rng.permutation(K).astype(np.int32)
+    inv = rng.uniform(0.05, 8.0, K).astype(np.float32)
+    k = 32
+    say("act_quant case: staged row pads", K, M)
+    Aq, Asc = _gpu_quant(X, K, k, inv, perm, ld=K + 32)
+    rq, rs = pq.quant_act(X, inv, perm, k)
+    np.testing.assert_array_equal(Asc, rs)
+    np.testing.assert_array_equal(Aq, rq)
+
+
 def test_strided_rows():
     c = inputs.tiny_case()
     art = pq.prepare(c.W, c.Xcal, 0.5, 64)
