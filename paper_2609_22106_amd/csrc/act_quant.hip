@@ -599,17 +599,21 @@ int lds_rows_per_wg(int M, int units, int num_cus) {
 // Stage classes of the copy kernel by row length (2K bytes): stage bytes, stages,
 // units per compute thread (K/8 units over 512 threads), LDS bytes of the packed
 // output window (each workgroup's LDS within 160 KiB / workgroups per CU; the
-// window holds K + k up to 2K in the first three classes, up to 15360 in the
-// fourth, never in the last).  window: 0 = where it pays, 1 = where it fits,
-// 2 = never (packed output stored directly).  It pays on long rows with many
-// rows per workgroup: a row block's lines then stay partial in L2 too long
-// (cold, M = 8192 x 9728: 56.5 -> 42.5 us, M = 4096: 29.5 -> 23.7); with short
-// rows they complete in L2 anyway and the window's last flush is pure latency
-// (M = 4096 x 2560: 8.5 -> 12.3 us; M = 512 x 9728, two rows each: 6.8 -> 8.1).
+// window holds K + k up to 2K in the first three classes, up to 14336 in the
+// fourth, 15360 in the fifth, never in the last).  window: 0 = where it pays,
+// 1 = where it fits, 2 = never (packed output stored directly).  It pays on
+// rows long enough for one workgroup per CU with many rows per workgroup: a
+// row block's lines then stay partial in L2 too long (cold, M = 8192 x 9728:
+// 56.5 -> 42.5 us, M = 4096: 29.5 -> 23.7; M = 8192 x 6144: 32.3 -> 28.7);
+// with short rows they complete in L2 anyway and the window's last flush is
+// pure latency (M = 4096 x 2560: 8.5 -> 12.3 us, x 4096: 10.4 -> 13.9; M =
+// 512 x 9728, two rows each: 6.8 -> 8.1).  The 20480-byte class (five stages)
+// fits the 19456-byte down_proj row; against 24576-byte stages (four) it
+// measured the same.
 static_assert(kComputeThreads == 512, "stage classes assume 512 compute threads");
-constexpr int kWindowBytes[5] = {17408, 34816, 69632, 65536, 0};
+constexpr int kWindowBytes[6] = {17408, 34816, 69632, 61440, 65536, 0};
 constexpr int cls_of(int stage) {
-  return stage <= 4096 ? 0 : stage <= 8192 ? 1 : stage <= 16384 ? 2 : stage <= 24576 ? 3 : 4;
+  return stage <= 4096 ? 0 : stage <= 8192 ? 1 : stage <= 16384 ? 2 : stage <= 20480 ? 3 : stage <= 24576 ? 4 : 5;
 }
 
 int packed_window_bytes(int K_aug) {
@@ -626,8 +630,8 @@ hipError_t launch_dma(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail,
   const int target = std::max(1, num_cus * per_cu);
   const int rows_per_wg = std::max(1, (M + target - 1) / target);
   const dim3 grid((M + rows_per_wg - 1) / rows_per_wg);
-  const int cls = rb <= 4096 ? 0 : rb <= 8192 ? 1 : rb <= 16384 ? 2 : rb <= 24576 ? 3 : 4;
-  const bool pays = K > 8192 && rows_per_wg >= 16;
+  const int cls = cls_of(rb);
+  const bool pays = per_cu == 1 && rows_per_wg >= 16;
   const bool win = kPacked && window != 2 && (window == 1 || pays) &&
                    packed_window_bytes(K + k_tail) <= kWindowBytes[cls];
 #define PRQ_DMA_OUT(STAGE, NS, U, OUT)                                                            \
@@ -641,7 +645,7 @@ hipError_t launch_dma(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail,
       PRQ_DMA_OUT(STAGE, NS, U, 0);                                                               \
   } while (0)
   // kUnits = ceil(K / 8 / 512) exactly: every unit but the last exists.
-  // Four stages in every class: with all of a
+  // Four stages in every class but 20480 bytes (five): with all of a
   // workgroup's rows requested at once (up to 8 stages) the copies of the
   // whole launch exceed X itself and the short-row cases ran a third slower
   // (M = 4096: K = 2560 11.8 -> 8.4 us, K = 4096 14.4 -> 11.1 us packed; K =
@@ -649,6 +653,7 @@ hipError_t launch_dma(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail,
   if (rb <= 4096) PRQ_DMA(4096, 4, 1);
   else if (rb <= 8192) PRQ_DMA(8192, 4, 1);
   else if (rb <= 16384) PRQ_DMA(16384, 4, 2);
+  else if (rb <= 20480) PRQ_DMA(20480, 5, 3);
   else if (rb <= 24576) PRQ_DMA(24576, 4, 3);
   else PRQ_DMA_OUT(32768, 4, 4, 0);
 #undef PRQ_DMA

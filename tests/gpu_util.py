@@ -53,3 +53,17 @@ def rows_per_block(M, rng, block=16):
     starts = np.arange(0, M, block)
     picks = starts + rng.integers(0, block, starts.size)
     return np.unique(np.concatenate([np.minimum(picks, M - 1), [0, M - 1]]))
+
+
+def tail_permutation(rng, K, k, swaps=0):
+    """A permutation of the form Algorithm 1 exports: K - k channels in
+    increasing order, then k randomly chosen channels in increasing order
+    (the head then reads runs of consecutive channels at every alignment);
+    `swaps` random transpositions inside the head break some runs."""
+    sel = np.sort(rng.choice(K, k, replace=False))
+    head = np.setdiff1d(np.arange(K), sel)
+    perm = np.concatenate([head, sel]).astype(np.int32)
+    for _ in range(swaps):
+        i, j = rng.integers(0, K - k, 2)
+        perm[i], perm[j] = perm[j], perm[i]
+    return perm

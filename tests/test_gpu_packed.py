@@ -95,10 +95,14 @@ def _tune_quant_packed(X, K, k, inv_pos, perm, off, G, kernel, num_cus):
 # (M, K, k, num_cus): row ranges of several rows that start and end inside
 # 8-row windows (a CU count that makes them so), ragged M, K + k not a whole
 # number of 128-element steps, the largest K + k each stage class takes through
-# the window (2K in the first three classes, 17408 and 65280 window bytes) and
-# sizes past it (stored directly), the largest class (always direct).
+# the window (2K in the first three classes, 14336 = 60928 window bytes in the
+# 20480-byte class, 15360 = 65280 bytes in the 24576-byte class) and sizes past
+# it (stored directly), the largest class (always direct).
 WINDOW_QUANT = [(1000, 2560, 64, 13),     # 39 rows per workgroup, 8192-byte stages
-                (517, 9728, 256, 7),      # 74 rows, the down_proj row, 24576-byte stages
+                (517, 9728, 256, 7),      # 74 rows, the down_proj row, 20480-byte stages
+                (60, 10240, 4096, 2),     # 20480-byte stages, K + k = 14336 (60928 bytes)
+                (60, 10240, 4224, 2),     # K + k = 14464: past the window, stored directly
+                (45, 8320, 96, 3),        # the shortest row of the 20480-byte class
                 (300, 4096, 1024, 5),     # 30 rows
                 (260, 8192, 2048, 3),     # 87 rows, 16384-byte stages
                 (77, 2048, 2048, 2),      # 4096-byte stages, window exactly full
