@@ -80,6 +80,9 @@ def parse_args(argv=None):
                    help="the profiled command, recorded with --traffic-from")
     p.add_argument("--counters", action="store_true",
                    help="run --warmup + --steps eager steps of --workload and nothing else")
+    p.add_argument("--lds-patterns", action="store_true",
+                   help="first run the LDS read-pattern probe kernels (reference points for "
+                        "the bank-conflict counters); alone, nothing else")
     return p.parse_args(argv)
 
 
@@ -556,6 +559,27 @@ def copy_calibration(torch, nbytes=CALIB_BYTES, reps=5):
     log(f"[bench] copy calibration: {reps} x neg over {nbytes} bytes")
 
 
+def lds_patterns(torch, blocks=1024, iters=2048):
+    """One launch of each LDS read-pattern probe kernel (the tile GEMM's
+    operand reads, its scale reads without and with the staging swap, one
+    dword per bank, the quantizer's 2-byte gather): the same bank-conflict
+    counters over them give reference points for the kernels' own ratios."""
+    import ctypes
+    from paper_2609_22106_amd import build
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    lib.prq_probe_lds_pattern.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                          ctypes.c_void_p, ctypes.c_void_p]
+    lib.prq_probe_lds_pattern.restype = ctypes.c_int
+    out = torch.zeros(blocks * 256, dtype=torch.int32, device="cuda")
+    sp = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    for mode in range(5):
+        st = lib.prq_probe_lds_pattern(mode, blocks, iters, out.data_ptr(), sp)
+        if st != 0:
+            raise RuntimeError(f"prq_probe_lds_pattern({mode}) failed ({st})")
+    torch.cuda.synchronize()
+    log(f"[bench] LDS read patterns: 5 kernels x {blocks} workgroups x {iters} reads per wave")
+
+
 def gemm_source_hash():
     h = hashlib.sha256()
     for name in GEMM_SOURCES:
@@ -782,6 +806,11 @@ def main(argv=None):
     from paper_2609_22106_amd import inputs, prq
 
     stream = torch.cuda.current_stream()
+    if args.lds_patterns:
+        lds_patterns(torch)
+        if not args.counters:
+            print(json.dumps({"lds_patterns_run": 5}), flush=True)
+            return 0
     if args.counters:
         wl = "decode" if args.workload == "all" else args.workload
         if args.copy_calibration:

@@ -290,7 +290,15 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   // Per-lane byte offsets of this wave's loads from uniform bases (fixed over
   // the K loop; rows and tiles clamped into the operands; the host checks that
   // the operands fit 32-bit offsets).
+  // Scale kilobytes (four 256-byte blocks of 64 dwords, dword = row + 16 K
+  // part) land in LDS with the K parts of every odd block swapped in pairs
+  // (0 <-> 1, 2 <-> 3).  A wave's scale read covers two blocks, 16 lanes per
+  // (block, K part); the LDS serves dword reads half a wave at a time over 32
+  // banks, so without the swap lanes 0-15 and 16-31 (same K part, two blocks)
+  // hit the same 16 banks; with it they take the other 16.  A lane's global
+  // source is its own piece's swap partner.
   uint32_t a_off[kAPer], as_off[kAsPer], b_off[kBPer], bs_off[kBsPer], sc_off[kScPer];
+  const int swz = ((lane & 15) ^ (((lane >> 4) & 1) << 2)) * 16;
 #pragma unroll
   for (int i = 0; i < kAPer; ++i) {
     if constexpr (kPackedA) {
@@ -306,14 +314,14 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
     const int c = (wave + i * kWaves) % kAsChunks;
     const int m = kScaleDword ? min(row_begin + c * 64 + lane, row_end - 1)
                               : min(row_begin + c * 16 + lr, row_end - 1);
-    as_off[i] = static_cast<uint32_t>(m) * nb + (kScaleDword ? 0 : lk);
+    as_off[i] = static_cast<uint32_t>(m) * nb;
   }
 #pragma unroll
   for (int i = 0; i < kScPer; ++i) {   // packed: A chunks first, then B chunks
     const int c = (wave + i * kWaves) % kScChunks;
     const int blk = c < kAsChunks ? min((row_begin >> 4) + c * 4 + (lane >> 4), nblk - 1)
                                   : min(t0 + (c - kAsChunks) * 4 + (lane >> 4), ntiles - 1);
-    sc_off[i] = static_cast<uint32_t>(blk) * sgroups * 256 + (lane & 15) * 16;
+    sc_off[i] = static_cast<uint32_t>(blk) * sgroups * 256 + swz;
   }
 #pragma unroll
   for (int i = 0; i < kBPer; ++i) {
@@ -324,7 +332,7 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   for (int i = 0; i < kBsPer; ++i) {
     const int c = (wave + i * kWaves) % kBsChunks;
     const int t = min(t0 + c * 4 + (lane >> 4), ntiles - 1);
-    bs_off[i] = static_cast<uint32_t>(t) * sgroups * 256 + (lane & 15) * 16;
+    bs_off[i] = static_cast<uint32_t>(t) * sgroups * 256 + swz;
   }
 
   // Step s into stage `st`.  Every source address is valid: with K_aug not a
@@ -363,10 +371,12 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
         if constexpr (kScaleDword)   // K_aug % 128 == 0: the row's 4 bytes of step s, aligned
           __builtin_amdgcn_global_load_lds(PRQ_GPTR(Asc + (as_off[i] + s * 4)),
                                            PRQ_LPTR(st + L::kOffAs + c * 256), 4, 0, 0);
-        else
+        else {   // block c: the lane's K part (swapped in odd blocks); past K_aug the row start
+          const int kp = lk ^ (c & 1);
           __builtin_amdgcn_global_load_lds(
-              PRQ_GPTR(Asc + (kok ? as_off[i] + s * 4 : as_off[i] - lk)),
+              PRQ_GPTR(Asc + (as_off[i] + (s * kStepK + kp * 32 < K_aug ? s * 4 + kp : 0))),
               PRQ_LPTR(st + L::kOffAs + c * 256), 1, 0, 0);
+        }
       }
 #pragma unroll
       for (int i = 0; i < kBsPer; ++i) {
@@ -400,9 +410,13 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   const int lib0 = (lane & 15) + 16 * (lane >> 5);
   const uint32_t a_lb = (wm * (kTM / 16) + blk_sel) * 1024 + lib0 * 16;
   const uint32_t b_lb = L::kOffB + (wn * (kTN / 16) + blk_sel) * 1024 + lib0 * 16;
+  // Scale dwords: half h of a step reads K part 2h + l / 32, found in an odd
+  // block (blk_sel = 1) at part 2h + (l / 32 ^ 1).
+  static_assert((kTM / 16) % 2 == 0 && (kTN / 16) % 2 == 0, "blk_sel is the block parity");
+  const uint32_t lsc = (lane & 15) * 4 + (((lane >> 5) ^ blk_sel) * 64);
   const uint32_t as_lb = kScaleDword ? L::kOffAs + (wm * kTM + (lane & 31)) * 4
-                                     : L::kOffAs + (wm * (kTM / 16) + blk_sel) * 256 + lib0 * 4;
-  const uint32_t bs_lb = L::kOffBs + (wn * (kTN / 16) + blk_sel) * 256 + lib0 * 4;
+                                     : L::kOffAs + (wm * (kTM / 16) + blk_sel) * 256 + lsc;
+  const uint32_t bs_lb = L::kOffBs + (wn * (kTN / 16) + blk_sel) * 256 + lsc;
   const uint32_t a_shift = 8 * (lane >> 5);   // row dword: part l / 32 to byte 0, 2 + l / 32 to byte 2
   auto read = [&](const uint8_t* st, auto hc, Half& o) {
     constexpr int h = decltype(hc)::value;
@@ -612,6 +626,7 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_grouped_persist_kernel(
   struct Offs {
     uint32_t a[kAPer], b[kBPer], sc[kScPer];
   };
+  const int swz = ((lane & 15) ^ (((lane >> 4) & 1) << 2)) * 16;
   auto offsets = [&](const Tile& t) {
     Offs o;
 #pragma unroll
@@ -629,7 +644,7 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_grouped_persist_kernel(
       const int c = (wave + i * kWaves) % kScChunks;
       const int blk = c < kAsChunks ? min((t.row_begin >> 4) + c * 4 + (lane >> 4), nblk - 1)
                                     : min(t.t0 + (c - kAsChunks) * 4 + (lane >> 4), ntiles - 1);
-      o.sc[i] = static_cast<uint32_t>(blk) * sgroups * 256 + (lane & 15) * 16;
+      o.sc[i] = static_cast<uint32_t>(blk) * sgroups * 256 + swz;   // odd blocks' K parts swapped in pairs
     }
     return o;
   };
@@ -676,8 +691,10 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_grouped_persist_kernel(
   const int lib0 = (lane & 15) + 16 * (lane >> 5);
   const uint32_t a_lb = (wm * (kTM / 16) + blk_sel) * 1024 + lib0 * 16;
   const uint32_t b_lb = L::kOffB + (wn * (kTN / 16) + blk_sel) * 1024 + lib0 * 16;
-  const uint32_t as_lb = L::kOffAs + (wm * (kTM / 16) + blk_sel) * 256 + lib0 * 4;
-  const uint32_t bs_lb = L::kOffBs + (wn * (kTN / 16) + blk_sel) * 256 + lib0 * 4;
+  static_assert((kTM / 16) % 2 == 0 && (kTN / 16) % 2 == 0, "blk_sel is the block parity");
+  const uint32_t lsc = (lane & 15) * 4 + (((lane >> 5) ^ blk_sel) * 64);   // odd blocks swapped
+  const uint32_t as_lb = L::kOffAs + (wm * (kTM / 16) + blk_sel) * 256 + lsc;
+  const uint32_t bs_lb = L::kOffBs + (wn * (kTN / 16) + blk_sel) * 256 + lsc;
   auto read = [&](const uint8_t* st, auto hc, Half& o) {
     constexpr int h = decltype(hc)::value;
 #pragma unroll

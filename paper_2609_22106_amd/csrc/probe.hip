@@ -112,6 +112,51 @@ __global__ __launch_bounds__(512) void read_floor_kernel(const uint8_t* __restri
   if (x == 0x9E3779B9u && lane == 0) out[wg] = x;
 }
 
+// LDS read patterns (reference points for the bank-conflict counters): each
+// workgroup of 4 waves fills 16 KiB of LDS, then every wave reads, `iters`
+// times, one kilobyte (rotating over the 16) in pattern kMode:
+//   0  16 bytes per lane at 16 l: the tile GEMM's operand reads;
+//   1  4 bytes per lane at 256 ((l / 16) % 2) + 4 ((l % 16) + 16 (l / 32)):
+//      the tile GEMM's scale reads (two 16-row blocks, half a step each);
+//   2  4 bytes per lane at 4 l (one dword per bank);
+//   4  pattern 1 with the tile GEMM's staging swap: lanes of the odd block
+//      (l / 16 odd) read K part (l / 32) ^ 1, 4 ((l % 16) + 16 ((l / 32) ^ 1));
+//   3  eight 2-byte reads per lane at 16 l + 2 j: the quantizer's gather of a
+//      unit of 8 consecutive channels (the element stride `elem` = 2 is a
+//      run-time value, so the reads stay eight separate 2-byte reads as in
+//      the quantizer, whose addresses come from the permutation).
+// Every address is inside the 16 KiB; lane results are folded and stored.
+template <int kMode>
+__global__ __launch_bounds__(256) void lds_pattern_kernel(int iters, int elem, uint32_t* __restrict__ out) {
+  __shared__ __align__(16) uint8_t s[16384];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int i = tid; i < 16384 / 4; i += 256) reinterpret_cast<uint32_t*>(s)[i] = i * 2654435761u;
+  __syncthreads();
+  uint32_t acc = 0;
+  for (int it = 0; it < iters; ++it) {
+    const int base = ((it + wave) & 15) * 1024;
+    if constexpr (kMode == 0) {
+      const uint4 v = *reinterpret_cast<const uint4*>(s + base + lane * 16);
+      acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    } else if constexpr (kMode == 1) {
+      acc ^= *reinterpret_cast<const uint32_t*>(
+          s + base + ((lane >> 4) & 1) * 256 + ((lane & 15) + 16 * (lane >> 5)) * 4);
+    } else if constexpr (kMode == 2) {
+      acc ^= *reinterpret_cast<const uint32_t*>(s + base + lane * 4);
+    } else if constexpr (kMode == 4) {
+      const int odd = (lane >> 4) & 1;
+      acc ^= *reinterpret_cast<const uint32_t*>(
+          s + base + odd * 256 + ((lane & 15) + 16 * ((lane >> 5) ^ odd)) * 4);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        acc += *reinterpret_cast<const uint16_t*>(s + base + lane * 16 + elem * j);
+    }
+    asm volatile("" ::: "memory");   // one read (set) per iteration, none hoisted
+  }
+  out[blockIdx.x * 256 + tid] = acc;
+}
+
 }  // namespace
 
 extern "C" {
@@ -128,6 +173,21 @@ int prq_probe_read_floor(const uint8_t* p1, int kib1, const uint8_t* p2, int kib
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
+
+// The LDS read-pattern kernel of `mode` (0-4): `blocks` workgroups, `iters`
+// reads per wave; out holds blocks * 256 uint32 (their folded values).
+int prq_probe_lds_pattern(int mode, int blocks, int iters, uint32_t* out, hipStream_t stream) {
+  if (mode < 0 || mode > 4 || blocks <= 0 || iters < 0 || !out) return -1;
+  const int elem = 2;   // mode 3: 8 reads of 2 bytes, 16 l + 14 + 2 < 1024
+  switch (mode) {
+    case 0: lds_pattern_kernel<0><<<blocks, 256, 0, stream>>>(iters, elem, out); break;
+    case 1: lds_pattern_kernel<1><<<blocks, 256, 0, stream>>>(iters, elem, out); break;
+    case 2: lds_pattern_kernel<2><<<blocks, 256, 0, stream>>>(iters, elem, out); break;
+    case 4: lds_pattern_kernel<4><<<blocks, 256, 0, stream>>>(iters, elem, out); break;
+    default: lds_pattern_kernel<3><<<blocks, 256, 0, stream>>>(iters, elem, out); break;
+  }
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
 
 int prq_probe_mfma16(const void* a, const void* b, const uint32_t* sa, const uint32_t* sb,
                      float* out, hipStream_t stream) {

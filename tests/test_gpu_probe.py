@@ -185,3 +185,51 @@ def test_fp4_convert_destination_byte_select():
             want = (old & ~(0xFF << (8 * sel))) | (pair << (8 * sel))
             assert int(got[l, sel]) == want, (l, sel, hex(int(got[l, sel])), hex(want))
 
+
+
+def _lds_pattern_expected(mode, iters):
+    """The folded value of every thread of the LDS read-pattern kernel (the
+    LDS word i holds i * 2654435761 mod 2^32), computed on the host."""
+    words = (np.arange(4096, dtype=np.uint64) * 2654435761) & 0xFFFFFFFF
+    halves = words.astype(np.uint32).view(np.uint16)   # little-endian 2-byte pieces
+    out = np.zeros(256, dtype=np.uint64)
+    for tid in range(256):
+        lane, wave = tid & 63, tid >> 6
+        acc = 0
+        for it in range(iters):
+            base = ((it + wave) & 15) * 1024
+            if mode == 0:
+                w = (base + 16 * lane) // 4
+                acc ^= int(words[w] ^ words[w + 1] ^ words[w + 2] ^ words[w + 3])
+            elif mode == 1:
+                acc ^= int(words[(base + ((lane >> 4) & 1) * 256 + ((lane & 15) + 16 * (lane >> 5)) * 4) // 4])
+            elif mode == 2:
+                acc ^= int(words[(base + 4 * lane) // 4])
+            elif mode == 4:
+                odd = (lane >> 4) & 1
+                acc ^= int(words[(base + odd * 256 + ((lane & 15) + 16 * ((lane >> 5) ^ odd)) * 4) // 4])
+            else:
+                acc = (acc + sum(int(halves[(base + 16 * lane + 2 * j) // 2]) for j in range(8))) & 0xFFFFFFFF
+        out[tid] = acc
+    return out.astype(np.uint32)
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2, 3, 4])
+def test_lds_read_pattern_probe(mode):
+    """The LDS read-pattern kernels (reference points for the bank-conflict
+    counters: the tile GEMM's operand reads, its scale reads without and with
+    the staging swap, one dword per bank, the quantizer's 2-byte gather) read
+    what their patterns name."""
+    from paper_2609_22106_amd import build
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    lib.prq_probe_lds_pattern.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                          ctypes.c_void_p]
+    blocks, iters = 3, 37
+    out = torch.zeros(blocks * 256, dtype=torch.int32, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+    assert lib.prq_probe_lds_pattern(mode, blocks, iters, out.data_ptr(), s) == 0
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().view(np.uint32).reshape(blocks, 256)
+    exp = _lds_pattern_expected(mode, iters)
+    for b in range(blocks):
+        np.testing.assert_array_equal(got[b], exp)
