@@ -100,17 +100,20 @@ struct PackedSink {
 };
 
 // One row of an 8-row window of the packed layout staged in LDS: the window's
-// codes as [S][4 K parts][8 rows][16 bytes] and then its scales as
+// codes as [S][4 K parts][8 slots][16 bytes] and then its scales as
 // [ceil(S/4)][4 K parts][8 rows][4 bytes] -- the packed layout with the row
 // block cut to the window's 8 rows, so that every (step, K part) of the window
 // is 128 contiguous bytes in LDS and in global memory (its 32-byte scale runs
-// likewise).
+// likewise).  Row j's 16 bytes of code line L = 4 step + K part sit in slot
+// (j + L) % 8: the 32 words a half wave writes (8 lines x 4 words of one row)
+// then fall on 32 distinct banks instead of the row's 4.
 struct LdsPackedSink {
-  uint8_t* code;    // window codes + j 16 (j = the row's place in the window)
+  uint8_t* code;    // window codes
   uint8_t* sc;      // window scales + j 4
+  int j;            // the row's place in the window
   __device__ void word(int v, uint32_t w) const {
-    const int b = v >> 2;
-    *reinterpret_cast<uint32_t*>(code + (b >> 2) * 512 + (b & 3) * 128 + (v & 3) * 4) = w;
+    const int line = v >> 2;
+    *reinterpret_cast<uint32_t*>(code + line * 128 + (((j + line) & 7) << 4) + (v & 3) * 4) = w;
   }
   __device__ void scale(int b, uint32_t c) const {
     const int s = b >> 2;
@@ -125,9 +128,12 @@ struct LdsPackedSink {
 // code comes from the hardware converter at scale 1, which rounds to nearest
 // even and saturates at 6 exactly like the software rule on every float32
 // (checked exhaustively on the GPU).
+// rs: z holds the unit's values with their pairs rotated by 4 - rs (pair j =
+// pair (j + 4 - rs) % 4); the code word is rotated back by rs bytes.
 template <class Sink>
 __device__ __forceinline__ void quantize_store(const float (&z)[8], int u, int tail_unit0,
-                                               int copy_units, int copy_blocks, const Sink& out) {
+                                               int copy_units, int copy_blocks, const Sink& out,
+                                               int rs = 0) {
   float amax = 0.0f;
 #pragma unroll
   for (int j = 0; j < 8; ++j) amax = fmaxf(amax, fabsf(z[j]));
@@ -139,6 +145,7 @@ __device__ __forceinline__ void quantize_store(const float (&z)[8], int u, int t
   w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, z[2] * mul, z[3] * mul, 1.0f, 1);
   w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, z[4] * mul, z[5] * mul, 1.0f, 2);
   w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, z[6] * mul, z[7] * mul, 1.0f, 3);
+  if (rs) w = __builtin_amdgcn_alignbyte(w, w, rs);   // byte i -> byte (i - rs) mod 4
   out.word(u, w);
   if ((u & 3) == 0) out.scale(u >> 2, code);
   if (u >= tail_unit0) {  // online copy of the quantized tail and its scales
@@ -240,16 +247,31 @@ struct PackedUnit {
   float d[8];
 };
 
+// rot (0-3): the pairs stored rotated, pair j = the unit's pair (j + rot) % 4
+// (selects only: a run-time index into a private array would be moved to
+// memory by the compiler).
 __device__ __forceinline__ void load_packed_unit(const int32_t* __restrict__ perm,
                                                  const float* __restrict__ inv, int g, int K,
-                                                 int u, PackedUnit* out) {
+                                                 int u, PackedUnit* out, int rot = 0) {
   Unit t;
   load_unit(perm, inv, g, K, u, &t);
+  uint32_t p[4];
+  float2 q[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
-    out->src2[j] = static_cast<uint32_t>(t.src[2 * j]) | (static_cast<uint32_t>(t.src[2 * j + 1]) << 16);
-#pragma unroll
-  for (int j = 0; j < 8; ++j) out->d[j] = t.d[j];
+  for (int j = 0; j < 4; ++j) {
+    p[j] = static_cast<uint32_t>(t.src[2 * j]) | (static_cast<uint32_t>(t.src[2 * j + 1]) << 16);
+    q[j] = make_float2(t.d[2 * j], t.d[2 * j + 1]);
+  }
+  const bool r2 = rot & 2, r1 = rot & 1;
+  const uint32_t a0 = r2 ? p[2] : p[0], a1 = r2 ? p[3] : p[1], a2 = r2 ? p[0] : p[2], a3 = r2 ? p[1] : p[3];
+  const float2 b0 = r2 ? q[2] : q[0], b1 = r2 ? q[3] : q[1], b2 = r2 ? q[0] : q[2], b3 = r2 ? q[1] : q[3];
+  out->src2[0] = r1 ? a1 : a0;
+  out->src2[1] = r1 ? a2 : a1;
+  out->src2[2] = r1 ? a3 : a2;
+  out->src2[3] = r1 ? a0 : a3;
+  const float2 c0 = r1 ? b1 : b0, c1 = r1 ? b2 : b1, c2 = r1 ? b3 : b2, c3 = r1 ? b0 : b3;
+  out->d[0] = c0.x; out->d[1] = c0.y; out->d[2] = c1.x; out->d[3] = c1.y;
+  out->d[4] = c2.x; out->d[5] = c2.y; out->d[6] = c3.x; out->d[7] = c3.y;
 }
 
 // Rows handled together by one pass of the LDS kernel: one when a row has at
@@ -475,13 +497,23 @@ __global__ __launch_bounds__(kDmaThreads) void act_quant_dma_kernel(
 
   PackedUnit un[kUnits];
   int cur_g = -1;
+  // A unit's 8 values are gathered two bytes at a time from its 16-byte
+  // stretch of the row; the LDS serves half a wave per pass over 32 banks, so
+  // lanes 8 units apart (128 bytes) would hit the same banks (4 lanes per
+  // bank).  Each lane instead takes its pairs rotated by rot = (lane / 8) % 4
+  // dwords (fixed when the units are loaded; the code word rotated back by one
+  // byte-align): a half wave's reads then cover 32 distinct banks.  (Rotating
+  // by the unit's first channel instead, which follows the shifts the
+  // selected channels cause, measured no better.)
+  const int rot = (lane >> 3) & 3;
+  const int rs = (4 - rot) & 3;
   // (Re)load the units' permutation entries and inverse scales, then wait for
   // them right here: later uses then see nothing outstanding.
   auto load_units = [&](int g) {
 #pragma unroll
     for (int j = 0; j < kUnits; ++j) {
       const int u = min(tid + j * kComputeThreads, units - 1);
-      load_packed_unit(perm, inv, g, K, u, &un[j]);
+      load_packed_unit(perm, inv, g, K, u, &un[j], rot);
     }
     __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));   // vmcnt(0)
     cur_g = g;
@@ -497,9 +529,9 @@ __global__ __launch_bounds__(kDmaThreads) void act_quant_dma_kernel(
     const int j = tid & 7;                          // the thread's row in the window, fixed
     if (j < lo - w0 || j >= hi - w0) return;
     uint8_t* const gcode = Aq + static_cast<int64_t>(w0 >> 4) * steps * 1024 + (w0 & 8) * 16;
-    for (int c = tid; c < steps * 32; c += kComputeThreads)
+    for (int c = tid; c < steps * 32; c += kComputeThreads)   // line c / 8, row j (slot rotated)
       *reinterpret_cast<uint4*>(gcode + (c >> 3) * 256 + j * 16) =
-          *reinterpret_cast<const uint4*>(win + c * 16);
+          *reinterpret_cast<const uint4*>(win + (c >> 3) * 128 + (((j + (c >> 3)) & 7) << 4));
     uint8_t* const gsc = Asc + static_cast<int64_t>(w0 >> 4) * sgroups * 256 + (w0 & 8) * 4;
     for (int e = tid; e < sgroups * 32; e += kComputeThreads)
       *reinterpret_cast<uint32_t*>(gsc + (e >> 3) * 64 + j * 4) =
@@ -532,7 +564,7 @@ __global__ __launch_bounds__(kDmaThreads) void act_quant_dma_kernel(
     const uint16_t* row = reinterpret_cast<const uint16_t*>(stg + (i % kNS) * kStage);
     const RowSink rsink{Aq + static_cast<int64_t>(r) * row_bytes, Asc + static_cast<int64_t>(r) * nb};
     const PackedSink psink(Aq, Asc, r, steps, sgroups);
-    const LdsPackedSink wsink{win + (r & 7) * 16, win_sc + (r & 7) * 4};
+    const LdsPackedSink wsink{win, win_sc + (r & 7) * 4, r & 7};
     if constexpr (kWindow) pad_row_tail(wsink, tid, units, nb, steps, sgroups);
     else if constexpr (kPacked) pad_row_tail(psink, tid, units, nb, steps, sgroups);
     // Units below the last always exist (the host picks kUnits = ceil(units /
@@ -550,11 +582,11 @@ __global__ __launch_bounds__(kDmaThreads) void act_quant_dma_kernel(
           z[2 * e + 1] = __uint_as_float(static_cast<uint32_t>(row[sp >> 16]) << 16) * un[j].d[2 * e + 1];
         }
         if constexpr (kWindow)
-          quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, wsink);
+          quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, wsink, rs);
         else if constexpr (kPacked)
-          quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, psink);
+          quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, psink, rs);
         else
-          quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, rsink);
+          quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, rsink, rs);
       }
     }
   }
