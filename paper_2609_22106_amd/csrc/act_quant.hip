@@ -347,6 +347,11 @@ __global__ __launch_bounds__(kLdsThreads) void act_quant_lds_kernel(
 
   const int ro = tid / units;                     // this thread's row within a pass
   const int u0 = tid - ro * units;                // its first unit
+  // Pairs rotated by (lane / 8) % 4 dwords against LDS bank conflicts (the
+  // rows of a pass lie back to back: lanes still read consecutive 16-byte
+  // stretches), as in the copy kernel below.
+  const int rot = (tid >> 3) & 3;
+  const int rs = (4 - rot) & 3;
   PackedUnit un[kUnits];
   int cur_g = -1;
   dev::GroupCursor gc;   // this thread's rows only increase
@@ -367,7 +372,7 @@ __global__ __launch_bounds__(kLdsThreads) void act_quant_lds_kernel(
 #pragma unroll
         for (int j = 0; j < kUnits; ++j) {
           const int u = u0 + j * kLdsThreads;
-          if (u < units) load_packed_unit(perm, inv, g, K, u, &un[j]);
+          if (u < units) load_packed_unit(perm, inv, g, K, u, &un[j], rot);
         }
         cur_g = g;
       }
@@ -387,9 +392,9 @@ __global__ __launch_bounds__(kLdsThreads) void act_quant_lds_kernel(
             z[2 * e + 1] = __uint_as_float(static_cast<uint32_t>(row[sp >> 16]) << 16) * un[j].d[2 * e + 1];
           }
           if constexpr (kPacked)
-            quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, psink);
+            quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, psink, rs);
           else
-            quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, rsink);
+            quantize_store(z, u, tail_unit0, k_tail >> 3, k_tail >> 5, rsink, rs);
         }
       }
     }
