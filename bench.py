@@ -142,7 +142,7 @@ def build_dense_ops(torch, prq, layers, M_list, rotate_bytes, plain=False):
                 # tile GEMM copies in whole kilobytes)
                 A = prq.prq_quant_act_packed(Xm, K, k, inv, perm)
                 ws_n = prq.prq_gemm_packed_workspace_bytes(M, N, K_aug)   # split along K
-                ws = torch.empty(ws_n, dtype=torch.uint8, device="cuda") if ws_n else None
+                ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda") if ws_n else None
 
                 def act(Xm=Xm, A=A, K=K, k=k, inv=inv, perm=perm):
                     prq.prq_quant_act_packed(Xm, K, k, inv, perm, out=A)

@@ -216,7 +216,7 @@ def test_packed_pair_down_proj(M):
     say("packed pair case:", M)
     A = prq.prq_quant_act_packed(dev(X), K, k, dev(_pos(inv, perm)), dev(perm))
     ws_n = prq.prq_gemm_packed_workspace_bytes(M, N, K + k)
-    ws = torch.empty(ws_n, dtype=torch.uint8, device="cuda") if ws_n else None
+    ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda") if ws_n else None
     Yd, Yd0 = nan_output(M, N), nan_output(M, N)     # both live: no reuse of one block
     prq.prq_gemm_packed(A, W, Y=Yd, workspace=ws)
     prq.prq_gemm_packed(A, W, Y=Yd0)
@@ -246,7 +246,7 @@ def test_full_prefill_gemm_every_element(entry):
     if entry == "packed":
         ap, aps = pack_rows(Aq, Asc)
         ws_n = prq.prq_gemm_packed_workspace_bytes(M, N, K_aug)
-        ws = torch.empty(ws_n, dtype=torch.uint8, device="cuda") if ws_n else None
+        ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda") if ws_n else None
         prq.prq_gemm_packed(prq.PackedAct(dev(ap), dev(aps), M, K_aug), W, Y=Yd, workspace=ws)
     else:
         prq.prq_gemm(dev(Aq), dev(Asc), W, Y=Yd)
@@ -512,7 +512,7 @@ def test_packed_pair_layer_shapes(name, N, K):
     say("layer shape case:", name, M, N, K, k)
     A = prq.prq_quant_act_packed(dev(X), K, k, dev(_pos(inv, perm)), dev(perm))
     ws_n = prq.prq_gemm_packed_workspace_bytes(M, N, K + k)
-    ws = torch.empty(ws_n, dtype=torch.uint8, device="cuda") if ws_n else None
+    ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda") if ws_n else None
     Yd = nan_output(M, N)
     prq.prq_gemm_packed(A, W, Y=Yd, workspace=ws)
     Y = host(Yd)
