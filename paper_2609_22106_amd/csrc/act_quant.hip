@@ -68,6 +68,40 @@ __device__ __forceinline__ void load_unit(const int32_t* __restrict__ perm,
   }
 }
 
+// Positions of a unit with their source channels packed two per register
+// (K <= 16384 fits 16 bits) and their inverse scales.
+struct PackedUnit {
+  uint32_t src2[4];
+  float d[8];
+};
+
+// rot (0-3): the pairs stored rotated, pair j = the unit's pair (j + rot) % 4
+// (selects only: a run-time index into a private array would be moved to
+// memory by the compiler).
+__device__ __forceinline__ void load_packed_unit(const int32_t* __restrict__ perm,
+                                                 const float* __restrict__ inv, int g, int K,
+                                                 int u, PackedUnit* out, int rot = 0) {
+  Unit t;
+  load_unit(perm, inv, g, K, u, &t);
+  uint32_t p[4];
+  float2 q[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    p[j] = static_cast<uint32_t>(t.src[2 * j]) | (static_cast<uint32_t>(t.src[2 * j + 1]) << 16);
+    q[j] = make_float2(t.d[2 * j], t.d[2 * j + 1]);
+  }
+  const bool r2 = rot & 2, r1 = rot & 1;
+  const uint32_t a0 = r2 ? p[2] : p[0], a1 = r2 ? p[3] : p[1], a2 = r2 ? p[0] : p[2], a3 = r2 ? p[1] : p[3];
+  const float2 b0 = r2 ? q[2] : q[0], b1 = r2 ? q[3] : q[1], b2 = r2 ? q[0] : q[2], b3 = r2 ? q[1] : q[3];
+  out->src2[0] = r1 ? a1 : a0;
+  out->src2[1] = r1 ? a2 : a1;
+  out->src2[2] = r1 ? a3 : a2;
+  out->src2[3] = r1 ? a0 : a3;
+  const float2 c0 = r1 ? b1 : b0, c1 = r1 ? b2 : b1, c2 = r1 ? b3 : b2, c3 = r1 ? b0 : b3;
+  out->d[0] = c0.x; out->d[1] = c0.y; out->d[2] = c1.x; out->d[3] = c1.y;
+  out->d[4] = c2.x; out->d[5] = c2.y; out->d[6] = c3.x; out->d[7] = c3.y;
+}
+
 // Where a row's codes and scales go.  Row-major: Aq [M][K_aug/2], Asc
 // [M][K_aug/32].  Packed: the MFMA-ordered layout of the packed weights with the
 // rows in the place of the output features -- Ap [ceil(M/16)][S][64][16] bytes,
@@ -214,9 +248,13 @@ __global__ __launch_bounds__(kRowsThreads) void act_quant_rows_kernel(
   // 2. The unit's permutation entries and inverse scales meanwhile.
   const bool active = u < units;                      // K/8 is a multiple of 4: quads agree
   const int uc = active ? u : units - 1;
-  Unit un;
+  // Pairs rotated by (lane / 8) % 4 dwords against LDS bank conflicts, as in
+  // the copy kernel below.
+  const int rot = (threadIdx.x >> 3) & 3;
+  const int rs = (4 - rot) & 3;
+  PackedUnit un;
   int cur_g = kGrouped ? dev::find_group(offsets, G, r0) : 0;
-  load_unit(perm, inv, cur_g, K, uc, &un);
+  load_packed_unit(perm, inv, cur_g, K, uc, &un, rot);
   __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));   // vmcnt(0): copies and entries
   __syncthreads();
   if (!active) return;
@@ -226,52 +264,22 @@ __global__ __launch_bounds__(kRowsThreads) void act_quant_rows_kernel(
     if (kGrouped) {
       const int g = dev::find_group(offsets, G, r);
       if (g != cur_g) {
-        load_unit(perm, inv, g, K, uc, &un);
+        load_packed_unit(perm, inv, g, K, uc, &un, rot);
         cur_g = g;
       }
     }
     const uint16_t* xr = reinterpret_cast<const uint16_t*>(rows_lds + rr * pitch);
     float z[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
-      z[j] = __uint_as_float(static_cast<uint32_t>(xr[un.src[j]]) << 16) * un.d[j];
+    for (int e = 0; e < 4; ++e) {
+      const uint32_t sp = un.src2[e];
+      z[2 * e] = __uint_as_float(static_cast<uint32_t>(xr[sp & 0xFFFFu]) << 16) * un.d[2 * e];
+      z[2 * e + 1] = __uint_as_float(static_cast<uint32_t>(xr[sp >> 16]) << 16) * un.d[2 * e + 1];
+    }
     quantize_store(z, u, (K - k_tail) >> 3, k_tail >> 3, k_tail >> 5,
-                   RowSink{Aq + static_cast<int64_t>(r) * row_bytes, Asc + static_cast<int64_t>(r) * nb});
+                   RowSink{Aq + static_cast<int64_t>(r) * row_bytes, Asc + static_cast<int64_t>(r) * nb},
+                   rs);
   }
-}
-
-// Positions of a unit with their source channels packed two per register
-// (K <= 16384 fits 16 bits) and their inverse scales.
-struct PackedUnit {
-  uint32_t src2[4];
-  float d[8];
-};
-
-// rot (0-3): the pairs stored rotated, pair j = the unit's pair (j + rot) % 4
-// (selects only: a run-time index into a private array would be moved to
-// memory by the compiler).
-__device__ __forceinline__ void load_packed_unit(const int32_t* __restrict__ perm,
-                                                 const float* __restrict__ inv, int g, int K,
-                                                 int u, PackedUnit* out, int rot = 0) {
-  Unit t;
-  load_unit(perm, inv, g, K, u, &t);
-  uint32_t p[4];
-  float2 q[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    p[j] = static_cast<uint32_t>(t.src[2 * j]) | (static_cast<uint32_t>(t.src[2 * j + 1]) << 16);
-    q[j] = make_float2(t.d[2 * j], t.d[2 * j + 1]);
-  }
-  const bool r2 = rot & 2, r1 = rot & 1;
-  const uint32_t a0 = r2 ? p[2] : p[0], a1 = r2 ? p[3] : p[1], a2 = r2 ? p[0] : p[2], a3 = r2 ? p[1] : p[3];
-  const float2 b0 = r2 ? q[2] : q[0], b1 = r2 ? q[3] : q[1], b2 = r2 ? q[0] : q[2], b3 = r2 ? q[1] : q[3];
-  out->src2[0] = r1 ? a1 : a0;
-  out->src2[1] = r1 ? a2 : a1;
-  out->src2[2] = r1 ? a3 : a2;
-  out->src2[3] = r1 ? a0 : a3;
-  const float2 c0 = r1 ? b1 : b0, c1 = r1 ? b2 : b1, c2 = r1 ? b3 : b2, c3 = r1 ? b0 : b3;
-  out->d[0] = c0.x; out->d[1] = c0.y; out->d[2] = c1.x; out->d[3] = c1.y;
-  out->d[4] = c2.x; out->d[5] = c2.y; out->d[6] = c3.x; out->d[7] = c3.y;
 }
 
 // Rows handled together by one pass of the LDS kernel: one when a row has at
