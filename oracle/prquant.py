@@ -367,3 +367,60 @@ def gated_ffn(X_hidden_bf16, W_up_bf16, W_gate_bf16):
     up = X @ bf16_bits_to_f32(np.asarray(W_up_bf16, dtype=np.uint16)).astype(np.float64).T
     g = X @ bf16_bits_to_f32(np.asarray(W_gate_bf16, dtype=np.uint16)).astype(np.float64).T
     return up * (g / (1.0 + np.exp(-g)))
+
+
+# --------------------------------------------------------------------------- #
+# Offline copy, producer side: the gated activation quantized as it is formed
+# (Sec. Method, "Activation tail construction", offline copy; Eq. 1 with
+# sigma = SiLU).  The expanded up/gate projections (expand_producer) emit
+# gate and up outputs C + k wide whose product is already [Z~, Z~_tail]; the
+# down-projection's MXFP4 input is Q(SiLU(gate) * up) over those C + k
+# columns.  Reading: gate and up are the producer GEMMs' bf16 outputs; the
+# product is formed in float32 and quantized without rounding it to bf16; the
+# paper fixes no precision for SiLU, so it is computed by the fixed float32
+# sequence below, one IEEE float32 operation per step (no fused multiply-add),
+# which a kernel can repeat bit for bit.
+# --------------------------------------------------------------------------- #
+# e^x = 2^n e^r with n = rint(x log2 e) and r = x - n ln 2 (|r| <= ln 2 / 2);
+# ln 2 is split into a head with 15 significant bits (n * head exact for
+# |n| <= 256) and a tail; e^r by its degree-6 Taylor polynomial (truncation
+# below 2^-23 relative on |r| <= 0.35) in Horner form; x is first clamped to
+# [-104, 89], where e^x is 0 or inf in float32 anyway.
+EXP_LOG2E = np.float32(1.4426950408889634)
+EXP_LN2_HI = np.float32(0.693145751953125)
+EXP_LN2_LO = np.float32(1.4286067653301870e-06)
+EXP_TAYLOR = tuple(np.float32(1.0 / math.factorial(i)) for i in range(6, -1, -1))   # c6 .. c0
+EXP_X_MIN, EXP_X_MAX = np.float32(-104.0), np.float32(89.0)
+
+
+def exp_f32(x):
+    """e^x in float32 by the fixed sequence above (elementwise)."""
+    x = np.minimum(np.maximum(np.asarray(x, dtype=np.float32), EXP_X_MIN), EXP_X_MAX)
+    n = np.rint(x * EXP_LOG2E).astype(np.float32)
+    r = ((x - n * EXP_LN2_HI).astype(np.float32) - n * EXP_LN2_LO).astype(np.float32)
+    p = np.full_like(r, EXP_TAYLOR[0])
+    for c in EXP_TAYLOR[1:]:
+        p = ((p * r).astype(np.float32) + c).astype(np.float32)
+    with np.errstate(over="ignore"):   # e^x past float32's range is inf, as intended
+        return np.ldexp(p, n.astype(np.int32)).astype(np.float32)
+
+
+def silu_f32(g):
+    """SiLU(g) = g / (1 + e^-g) in float32 (one rounding per operation)."""
+    g = np.asarray(g, dtype=np.float32)
+    d = (np.float32(1.0) + exp_f32(-g)).astype(np.float32)
+    return (g / d).astype(np.float32)
+
+
+def swiglu_f32(gate_bf16, up_bf16):
+    """SiLU(gate) * up in float32 from the producers' bf16 outputs."""
+    g = bf16_bits_to_f32(np.asarray(gate_bf16, dtype=np.uint16))
+    u = bf16_bits_to_f32(np.asarray(up_bf16, dtype=np.uint16))
+    return (silu_f32(g) * u).astype(np.float32)
+
+
+def swiglu_quant(gate_bf16, up_bf16):
+    """Q(SiLU(gate) * up) packed: (Aq uint8 [M, K_aug/2], Asc uint8 [M, K_aug/32])
+    for gate/up [M, K_aug] (K_aug = C + k from the expanded producers)."""
+    codes, scales = mx_quantize(swiglu_f32(gate_bf16, up_bf16))
+    return pack_codes(codes), scales

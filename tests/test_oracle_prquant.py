@@ -530,3 +530,96 @@ def test_ablation_variants_match_their_definitions():
     # the five values are distinct, so no two names can trade places unnoticed
     vals = [g[n] for n in want]
     assert len(set(vals)) == len(vals), g
+
+
+# --------------------------------------------------------------------------- #
+# Offline copy, producer side: SiLU(gate) * up quantized as it is formed
+# --------------------------------------------------------------------------- #
+def _ulps(got, want):
+    got = np.asarray(got, np.float32)
+    return np.abs(got.astype(np.float64) - want) / np.spacing(np.abs(got)).astype(np.float64)
+
+
+def test_exp_f32_against_float64():
+    """The fixed float32 exponential stays within 3 ulp of the float64 exp on
+    a dense sweep of its finite range; e^0 = 1 exactly; past the clamp it is
+    0 or inf."""
+    x = np.linspace(-87.0, 88.0, 350001, dtype=np.float32)
+    e = pq.exp_f32(x)
+    assert np.all(np.isfinite(e)) and np.all(e > 0)
+    assert _ulps(e, np.exp(x.astype(np.float64))).max() <= 3.0
+    assert pq.exp_f32(np.float32(0.0)) == np.float32(1.0)
+    assert pq.exp_f32(np.float32(1.0)) == np.float32(math.e)
+    big = pq.exp_f32(np.array([89.0, 1e30, np.finfo(np.float32).max], np.float32))
+    assert np.all(np.isinf(big)) and np.all(big > 0)
+    assert np.all(pq.exp_f32(np.array([-104.0, -1e30, -np.finfo(np.float32).max], np.float32)) == 0)
+
+
+def test_silu_f32_against_float64():
+    """SiLU(g) = g / (1 + e^-g) within 5 ulp of its float64 value while 1 + e^-g
+    is finite in float32 (g >= -85); SiLU(0) = 0; SiLU(g) = g exactly once e^-g
+    is below half an ulp of 1 (g >= 17); -0 far left, where e^-g overflows
+    float32 (the float64 value there is below 1e-35)."""
+    g = np.linspace(-85.0, 100.0, 400001, dtype=np.float32)
+    s = pq.silu_f32(g)
+    ref = g.astype(np.float64) / (1.0 + np.exp(-g.astype(np.float64)))
+    keep = np.abs(ref) > 0
+    assert _ulps(s[keep], ref[keep]).max() <= 5.0
+    assert pq.silu_f32(np.float32(0.0)) == 0.0
+    big = np.array([17.0, 100.0, 3.0e38], np.float32)
+    np.testing.assert_array_equal(pq.silu_f32(big), big)
+    far = pq.silu_f32(np.array([-104.0, -1e20], np.float32))
+    assert np.all(far == 0) and np.all(np.signbit(far))
+
+
+def test_swiglu_quant_definition():
+    """The gate gets the SiLU, the up output multiplies it (against the float64
+    formula with the roles written out: a swap fails); where SiLU is exact
+    (gate >= 17) the codes are those of Q(gate * up) formed directly; a zero
+    gate gives zeros carrying the up output's sign and the all-zero scale."""
+    rng = np.random.default_rng(41)
+    M, K = 5, 96
+    gate = rng.standard_normal((M, K)).astype(np.float32) * 3
+    up = rng.standard_normal((M, K)).astype(np.float32) * 2
+    gb, ub = pq.bf16_round_bits(gate), pq.bf16_round_bits(up)
+    g64 = pq.bf16_bits_to_f32(gb).astype(np.float64)
+    u64 = pq.bf16_bits_to_f32(ub).astype(np.float64)
+    z = pq.swiglu_f32(gb, ub)
+    want = u64 * g64 / (1.0 + np.exp(-g64))
+    assert _ulps(z[np.abs(want) > 1e-30], want[np.abs(want) > 1e-30]).max() <= 5.0
+    swapped = g64 * u64 / (1.0 + np.exp(-u64))
+    assert np.max(np.abs(z - swapped)) > 1e-2
+    # exact SiLU: gate >= 17
+    gate_hi = pq.bf16_round_bits(17.0 + np.abs(rng.standard_normal((M, K))).astype(np.float32) * 40)
+    Aq, Asc = pq.swiglu_quant(gate_hi, ub)
+    direct = (pq.bf16_bits_to_f32(gate_hi) * pq.bf16_bits_to_f32(ub)).astype(np.float32)
+    c, sc = mx.mx_quantize(direct)
+    np.testing.assert_array_equal(Aq, mx.pack_codes(c))
+    np.testing.assert_array_equal(Asc, sc)
+    Aq0, Asc0 = pq.swiglu_quant(np.zeros((M, K), np.uint16), ub)   # 0 * up: signed zeros
+    c0 = mx.unpack_codes(Aq0)
+    assert not (c0 & 7).any() and not Asc0.any()
+    np.testing.assert_array_equal(c0 >> 3, np.signbit(pq.bf16_bits_to_f32(ub)).astype(np.uint8))
+
+
+def test_swiglu_quant_of_expanded_producers_is_the_augmented_activation():
+    """Offline copy end to end on the oracle: the expanded producers' outputs
+    (bf16) through SiLU(gate) * up give, column for column, the permuted and
+    scaled gated activation with its last k channels repeated -- the
+    [Z~, Z~_tail] layout of Eq. 3 -- so the quantized result has its tail
+    blocks equal to the copied ones."""
+    rng = np.random.default_rng(43)
+    H, C, k, M = 64, 128, 32, 6
+    Wup = pq.bf16_round_bits((rng.standard_normal((C, H)) * 0.1).astype(np.float32))
+    Wg = pq.bf16_round_bits((rng.standard_normal((C, H)) * 0.1).astype(np.float32))
+    X = pq.bf16_round_bits(rng.standard_normal((M, H)).astype(np.float32))
+    inv = (np.float32(1.0) / rng.uniform(0.5, 2.0, C).astype(np.float32)).astype(np.float32)
+    perm = rng.permutation(C)
+    up_aug, gate_aug = pq.expand_producer(Wup, Wg, inv, perm, k)
+    Xf = pq.bf16_bits_to_f32(X).astype(np.float64)
+    up_out = pq.bf16_round_bits((Xf @ pq.bf16_bits_to_f32(up_aug).astype(np.float64).T).astype(np.float32))
+    g_out = pq.bf16_round_bits((Xf @ pq.bf16_bits_to_f32(gate_aug).astype(np.float64).T).astype(np.float32))
+    Aq, Asc = pq.swiglu_quant(g_out, up_out)
+    assert Aq.shape == (M, (C + k) // 2) and Asc.shape == (M, (C + k) // 32)
+    np.testing.assert_array_equal(Aq[:, (C + k) // 2 - k // 2:], Aq[:, C // 2 - k // 2:C // 2])
+    np.testing.assert_array_equal(Asc[:, -(k // 32):], Asc[:, C // 32 - k // 32:C // 32])
