@@ -428,8 +428,11 @@ def gpu_info(torch):
 def copy_context(torch, prq, layers, M_list, reps=50):
     """Activation side, online copy (gather by perm, scale, quantize, copy the
     tail blocks) against offline copy (the expanded producer already emitted
-    [Z~, Z~_tail]: a plain quantizer over K + k), both launched back to back
-    on warm inputs (seconds per launch)."""
+    [Z~, Z~_tail]: a plain quantizer over K + k), and the offline copy's
+    producer side from the expanded gate/up outputs: the fused SiLU(gate) * up
+    quantization against torch's SiLU and product (bf16 Z) followed by the
+    plain quantizer; all launched back to back on warm inputs (seconds per
+    launch)."""
     out = {}
     for name, c in layers:
         K, k = c.K, c.k_tail
@@ -439,17 +442,32 @@ def copy_context(torch, prq, layers, M_list, reps=50):
         X = torch.from_numpy(c.X.view("int16")).cuda()
         g = torch.Generator(device="cpu").manual_seed(0)
         Zaug = (torch.randn((max(M_list), K + k), generator=g) * 2).to(torch.bfloat16).cuda()
+        Gaug = (torch.randn((max(M_list), K + k), generator=g) * 4).to(torch.bfloat16).cuda()
+        Uaug = torch.randn((max(M_list), K + k), generator=g).to(torch.bfloat16).cuda()
+        Zb = torch.empty_like(Zaug)
+
+        def swiglu_then(M, quant):
+            torch.mul(torch.nn.functional.silu(Gaug[:M]), Uaug[:M], out=Zb[:M])
+            quant(Zb[:M])
         for M in M_list:
             res = {}
             if M > PACKED_MIN_ROWS:     # the quantizer the step uses: packed output
                 A = prq.prq_quant_act_packed(X[:M], K, k, inv, perm)
                 fns = (("online", lambda: prq.prq_quant_act_packed(X[:M], K, k, inv, perm, out=A)),
-                       ("offline", lambda: prq.prq_quant_act_packed(Zaug[:M], K + k, 0, out=A)))
+                       ("offline", lambda: prq.prq_quant_act_packed(Zaug[:M], K + k, 0, out=A)),
+                       ("fused", lambda: prq.prq_swiglu_quant(Gaug[:M], Uaug[:M], K + k, packed=True,
+                                                              out=A)),
+                       ("unfused", lambda: swiglu_then(M, lambda Z: prq.prq_quant_act_packed(
+                           Z, K + k, 0, out=A))))
             else:
                 Aq = torch.empty((M, (K + k) // 2), dtype=torch.uint8, device="cuda")
                 Asc = torch.empty((M, (K + k) // 32), dtype=torch.uint8, device="cuda")
                 fns = (("online", lambda: prq.prq_quant_act(X[:M], K, k, inv, perm, Aq=Aq, Asc=Asc)),
-                       ("offline", lambda: prq.prq_quant_act(Zaug[:M], K + k, 0, Aq=Aq, Asc=Asc)))
+                       ("offline", lambda: prq.prq_quant_act(Zaug[:M], K + k, 0, Aq=Aq, Asc=Asc)),
+                       ("fused", lambda: prq.prq_swiglu_quant(Gaug[:M], Uaug[:M], K + k,
+                                                              out=(Aq, Asc))),
+                       ("unfused", lambda: swiglu_then(M, lambda Z: prq.prq_quant_act(
+                           Z, K + k, 0, Aq=Aq, Asc=Asc))))
             for label, fn in fns:
                 for _ in range(3):
                     fn()
@@ -777,6 +795,8 @@ def measure_workload(torch, np, prq, inputs, wl, args, stream, contexts=True):
             if key in detail:
                 detail[key]["act_quant_online_copy_warm_us"] = round(r["online"] * 1e6, 3)
                 detail[key]["act_quant_offline_copy_warm_us"] = round(r["offline"] * 1e6, 3)
+                detail[key]["producer_swiglu_quant_fused_warm_us"] = round(r["fused"] * 1e6, 3)
+                detail[key]["producer_swiglu_then_quant_warm_us"] = round(r["unfused"] * 1e6, 3)
     if contexts and wl == "decode" and not args.no_graph:
         # hot: the same steps on one weight copy (served from the Infinity Cache)
         hot_ops, _, _, _ = build_workload(torch, np, prq, inputs, wl, 0)

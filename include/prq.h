@@ -354,6 +354,35 @@ int prq_expand_producer(const uint16_t* W_up_bf16, const uint16_t* W_gate_bf16,
                         int32_t k_tail, uint16_t* W_up_aug, uint16_t* W_gate_aug);
 
 /*
+ * prq_swiglu_quant / prq_swiglu_quant_packed -- offline copy, producer side
+ * (Sec. Method, "Activation tail construction"; Eq. 1 with sigma = SiLU): the
+ * gated activation of the expanded producers quantized as it is formed.
+ *   gate_bf16, up_bf16 [M, ld] device, bf16 bit patterns: the outputs of the
+ *       up/gate projections expanded by prq_expand_producer (first K_aug =
+ *       C + k columns used; row stride ld elements, ld % 8 == 0, 16-byte
+ *       aligned), so that SiLU(gate) * up is [Z~, Z~_tail]
+ *   Aq [M, K_aug/2], Asc [M, K_aug/32] (row-major, as prq_quant_act), or
+ *   Ap / Aps in the packed activation layout below (16-byte aligned, sizes
+ *   from prq_packed_act_bytes; rows past M and K positions past K_aug written
+ *   as zero codes and scale byte 127)
+ * Output: Q(SiLU(gate) * up), the product in float32 (never rounded to bf16),
+ * SiLU(g) = g / (1 + e^-g) with e^x by a fixed float32 sequence -- x clamped
+ * to [-104, 89], n = rint(x log2 e), r = (x - n ln2_hi) - n ln2_lo with ln 2
+ * split into a 15-bit head and a tail, e^r by its degree-6 Taylor polynomial
+ * in Horner form, scaled by 2^n -- one IEEE float32 operation per step, so
+ * the codes do not depend on the device's exp.  Finite inputs whose product
+ * is finite; the quantized value of a non-finite product is unspecified.
+ * Device, asynchronous on `stream`, allocates nothing.  Returns PRQ_OK,
+ * PRQ_EINVAL (null pointer, M < 0, ld < K_aug), PRQ_EALIGN (K_aug % 32,
+ * alignment), PRQ_EUNSUPPORTED (K_aug > 65536), PRQ_EDEVICE.  M == 0 is a
+ * no-op.
+ */
+int prq_swiglu_quant(const void* gate_bf16, const void* up_bf16, int64_t ld, int32_t M,
+                     int32_t K_aug, uint8_t* Aq, uint8_t* Asc, hipStream_t stream);
+int prq_swiglu_quant_packed(const void* gate_bf16, const void* up_bf16, int64_t ld, int32_t M,
+                            int32_t K_aug, uint8_t* Ap, uint8_t* Aps, hipStream_t stream);
+
+/*
  * prq_evaluate_nrmse -- offline: the normalized reconstruction error of one
  * configuration, ||Y_hat - X W^T||_F / ||X W^T||_F, where Y_hat is Eq. 3
  * evaluated on the rows X with the device path (prq_prepare_ex on the

@@ -311,6 +311,37 @@ int prq_quant_act_packed(const void* X_bf16, int64_t ld_x, int32_t M, int32_t K,
                                                     G, Ap, Aps, dev.num_cus, stream));
 }
 
+namespace {
+
+int swiglu_quant_common(const void* gate, const void* up, int64_t ld, int32_t M, int32_t K_aug,
+                        uint8_t* A, uint8_t* As, bool packed, hipStream_t stream) {
+  if (M < 0 || K_aug <= 0 || ld < K_aug) return PRQ_EINVAL;
+  if (K_aug % PRQ_BLOCK) return PRQ_EALIGN;
+  if (K_aug > kMaxKAug) return PRQ_EUNSUPPORTED;
+  if (M == 0) return PRQ_OK;
+  if (!gate || !up || !A || !As) return PRQ_EINVAL;
+  if (!aligned16(gate) || !aligned16(up) || ld % 8) return PRQ_EALIGN;
+  if (packed && (!aligned16(A) || !aligned16(As))) return PRQ_EALIGN;
+  DeviceInfo dev;
+  const int st = current_device(&dev);
+  if (st != PRQ_OK) return st;
+  return launch_status(prq::launch_swiglu_quant(static_cast<const uint16_t*>(gate),
+                                                static_cast<const uint16_t*>(up), ld, M, K_aug, A,
+                                                As, packed, dev.num_cus, stream));
+}
+
+}  // namespace
+
+int prq_swiglu_quant(const void* gate_bf16, const void* up_bf16, int64_t ld, int32_t M,
+                     int32_t K_aug, uint8_t* Aq, uint8_t* Asc, hipStream_t stream) {
+  return swiglu_quant_common(gate_bf16, up_bf16, ld, M, K_aug, Aq, Asc, false, stream);
+}
+
+int prq_swiglu_quant_packed(const void* gate_bf16, const void* up_bf16, int64_t ld, int32_t M,
+                            int32_t K_aug, uint8_t* Ap, uint8_t* Aps, hipStream_t stream) {
+  return swiglu_quant_common(gate_bf16, up_bf16, ld, M, K_aug, Ap, Aps, true, stream);
+}
+
 size_t prq_gemm_packed_workspace_bytes(int32_t M, int32_t N, int32_t K_aug) {
   if (M <= 0 || N <= 0 || K_aug <= 0 || N % 16 || K_aug % PRQ_BLOCK || K_aug > kMaxKAug) return 0;
   return with_head(prq::tile_workspace_bytes(M, N, K_aug, true, device_cus()));

@@ -835,4 +835,106 @@ hipError_t launch_act_quant_packed_kernel(const uint16_t* X, int64_t ld_x, int M
   return hipGetLastError();
 }
 
+namespace {
+
+// Offline copy, producer side (Sec. Method, "Activation tail construction";
+// Eq. 1 with sigma = SiLU): the expanded up/gate projections emit gate and up
+// outputs K_aug = C + k wide whose product SiLU(gate) * up is already
+// [Z~, Z~_tail], so the down-projection's MXFP4 input is that product
+// quantized -- no gather, no scaling, no tail copy.  The product is formed in
+// float32 and never rounded to bf16.  SiLU(g) = g / (1 + e^-g) with e^x by a
+// fixed sequence, one IEEE float32 operation per step (contraction off), so
+// the result does not depend on the device's own exp: x clamped to [-104, 89];
+// n = rint(x log2 e); r = (x - n ln2_hi) - n ln2_lo with ln 2 split into a
+// 15-bit head (n ln2_hi exact) and a tail; e^r by its degree-6 Taylor
+// polynomial in Horner form; e^x = r's polynomial scaled by 2^n (exact).
+__device__ __forceinline__ float silu_seq(float g) {
+#pragma clang fp contract(off)
+  const float x = fminf(fmaxf(-g, -104.0f), 89.0f);
+  const float n = rintf(x * 0x1.715476p+0f);                // log2 e
+  const float r = (x - n * 0x1.62e4p-1f) - n * 0x1.7f7d1cp-20f;   // ln 2 head, tail
+  float p = 0x1.6c16c2p-10f;                                // 1/6!
+  p = p * r + 0x1.111112p-7f;                               // 1/5!
+  p = p * r + 0x1.555556p-5f;                               // 1/4!
+  p = p * r + 0x1.555556p-3f;                               // 1/3!
+  p = p * r + 0.5f;
+  p = p * r + 1.0f;
+  p = p * r + 1.0f;
+  const float e = ldexpf(p, static_cast<int>(n));
+  return __fdiv_rn(g, 1.0f + e);
+}
+
+// One thread per unit (8 consecutive outputs of a row); the 4 units of a
+// 32-block are consecutive lanes (K_aug % 32 == 0).  Packed output: the rows of
+// the last 16-row block past M and the K positions past K_aug get zero codes
+// and scale byte 127, as the packed quantizer writes them.
+template <bool kPacked>
+__global__ __launch_bounds__(256) void swiglu_quant_kernel(const uint16_t* __restrict__ G,
+                                                           const uint16_t* __restrict__ U,
+                                                           int64_t ld, int M, int K_aug,
+                                                           uint8_t* __restrict__ Aq,
+                                                           uint8_t* __restrict__ Asc) {
+#pragma clang fp contract(off)
+  const int units = K_aug >> 3;
+  const int nb = K_aug >> 5;
+  const int64_t row_bytes = K_aug >> 1;
+  const int steps = (K_aug + 127) >> 7;
+  const int sgroups = (steps + 3) >> 2;
+  const int rows = kPacked ? (M + 15) & ~15 : M;
+  const int64_t total = static_cast<int64_t>(rows) * units;   // a multiple of 4: whole quads
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < total;
+       i += static_cast<int64_t>(gridDim.x) * 256) {
+    const int r = static_cast<int>(i / units);
+    const int u = static_cast<int>(i - static_cast<int64_t>(r) * units);
+    if (kPacked && r >= M) {                       // quad-uniform
+      const PackedSink psink(Aq, Asc, r, steps, sgroups);
+      psink.word(u, 0u);
+      if ((u & 3) == 0) psink.scale(u >> 2, 127u);
+      pad_row_tail(psink, u, units, nb, steps, sgroups);
+      continue;
+    }
+    const int64_t at = static_cast<int64_t>(r) * ld + u * 8;
+    const uint4 gv = *reinterpret_cast<const uint4*>(G + at);
+    const uint4 uv = *reinterpret_cast<const uint4*>(U + at);
+    const uint32_t gw[4] = {gv.x, gv.y, gv.z, gv.w};
+    const uint32_t uw[4] = {uv.x, uv.y, uv.z, uv.w};
+    float z[8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float g0 = __uint_as_float(gw[j] << 16), g1 = __uint_as_float(gw[j] & 0xFFFF0000u);
+      const float u0 = __uint_as_float(uw[j] << 16), u1 = __uint_as_float(uw[j] & 0xFFFF0000u);
+      z[2 * j] = silu_seq(g0) * u0;
+      z[2 * j + 1] = silu_seq(g1) * u1;
+    }
+    if constexpr (kPacked) {
+      const PackedSink psink(Aq, Asc, r, steps, sgroups);
+      quantize_store(z, u, units, 0, 0, psink);
+      pad_row_tail(psink, u, units, nb, steps, sgroups);
+    } else {
+      quantize_store(z, u, units, 0, 0,
+                     RowSink{Aq + static_cast<int64_t>(r) * row_bytes, Asc + static_cast<int64_t>(r) * nb});
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_swiglu_quant(const uint16_t* G, const uint16_t* U, int64_t ld, int M, int K_aug,
+                               uint8_t* Aq, uint8_t* Asc, bool packed, int num_cus,
+                               hipStream_t stream) {
+  // One thread per unit (a thread's two 16-byte loads are its only memory
+  // round trip; with a grid capped at a few workgroups per CU each thread
+  // looped over ~20 units, one round trip after another: 132 against 64 us at
+  // M = 8192 x 9984); the loop only covers grids past the launch limit.
+  (void)num_cus;
+  const int rows = packed ? (M + 15) & ~15 : M;
+  const int64_t total = static_cast<int64_t>(rows) * (K_aug >> 3);
+  const dim3 grid(static_cast<unsigned>(std::max<int64_t>(1, std::min<int64_t>((total + 255) / 256, int64_t{1} << 30))));
+  if (packed)
+    swiglu_quant_kernel<true><<<grid, 256, 0, stream>>>(G, U, ld, M, K_aug, Aq, Asc);
+  else
+    swiglu_quant_kernel<false><<<grid, 256, 0, stream>>>(G, U, ld, M, K_aug, Aq, Asc);
+  return hipGetLastError();
+}
+
 }  // namespace prq

@@ -67,6 +67,12 @@ hipError_t launch_act_quant_packed(const uint16_t* X, int64_t ld_x, int M, int K
 // kernel: 0 = automatic, 2 = register-staged rows, 3 = rows copied into LDS stages
 // with the output through an 8-row LDS window wherever it fits (automatic: only
 // where it pays), 4 = as 3 with the output stored directly.
+// Q(SiLU(G) * U) of bf16 gate/up outputs [M, K_aug] (row stride ld elements,
+// 16-byte aligned rows) into row-major Aq / Asc or, with `packed`, the packed
+// activation layout (offline copy, producer side).
+hipError_t launch_swiglu_quant(const uint16_t* G, const uint16_t* U, int64_t ld, int M, int K_aug,
+                               uint8_t* Aq, uint8_t* Asc, bool packed, int num_cus,
+                               hipStream_t stream);
 hipError_t launch_act_quant_packed_kernel(const uint16_t* X, int64_t ld_x, int M, int K,
                                           int k_tail, const float* inv_scale_pos,
                                           const int32_t* perm, const int32_t* group_offsets,

@@ -69,6 +69,9 @@ _packed_act_bytes = _decl("prq_packed_act_bytes", ctypes.c_int,
                           [_i32, _i32, ctypes.POINTER(_sz), ctypes.POINTER(_sz)])
 _quant_act_packed = _decl("prq_quant_act_packed", ctypes.c_int,
                           [_p, _i64, _i32, _i32, _i32, _p, _p, _p, _i32, _p, _p, _p])
+_swiglu_quant = _decl("prq_swiglu_quant", ctypes.c_int, [_p, _p, _i64, _i32, _i32, _p, _p, _p])
+_swiglu_quant_packed = _decl("prq_swiglu_quant_packed", ctypes.c_int,
+                             [_p, _p, _i64, _i32, _i32, _p, _p, _p])
 _gemm_packed_ws = _decl("prq_gemm_packed_workspace_bytes", _sz, [_i32, _i32, _i32])
 _gemm_packed = _decl("prq_gemm_packed", ctypes.c_int,
                      [_p, _p, _i32, _p, _p, _i32, _i32, _p, _p, _sz, _p])
@@ -411,6 +414,44 @@ def prq_quant_act_packed(X, K, k_tail, inv_scale_pos=None, perm=None, out=None, 
                            _ptr(group_offsets) if G > 1 else None, G, _ptr(out.Ap), _ptr(out.Aps),
                            _stream(stream))
     _check(st, "prq_quant_act_packed")
+    return out
+
+
+def prq_swiglu_quant(gate, up, K_aug, packed=False, out=None, stream=None):
+    """Q(SiLU(gate) * up) of the expanded producers' bf16 outputs [M, >= K_aug]
+    (offline copy, producer side): row-major (Aq, Asc) or, with packed=True, a
+    PackedAct.  out: (Aq, Asc) or a PackedAct to write into (else allocated)."""
+    for name, t in (("gate", gate), ("up", up)):
+        if not isinstance(t, torch.Tensor) or t.dim() != 2 or t.dtype not in _BF16_LIKE:
+            raise ValueError(f"{name} must be a 2-D tensor of bf16 values (or their int16 bit patterns)")
+        if t.shape[1] < K_aug or t.stride(1) != 1:
+            raise ValueError(f"{name} rows must hold K_aug={K_aug} contiguous values "
+                             f"(shape {tuple(t.shape)}, strides {t.stride()})")
+    if gate.shape != up.shape or gate.stride() != up.stride():
+        raise ValueError(f"gate {tuple(gate.shape)} / {gate.stride()} and up {tuple(up.shape)} / "
+                         f"{up.stride()} must have the same shape and strides")
+    M = gate.shape[0]
+    ld = gate.stride(0) if M > 1 else K_aug
+    if packed:
+        if out is None:
+            cb, sb = prq_packed_act_bytes(M, K_aug)
+            out = PackedAct(torch.empty(cb, dtype=torch.uint8, device=gate.device),
+                            torch.empty(sb, dtype=torch.uint8, device=gate.device), M, K_aug)
+        if out.M != M or out.K_aug != K_aug:
+            raise ValueError(f"out holds {out.M} rows of K_aug {out.K_aug}, expected {M} x {K_aug}")
+        out.check_sizes()
+        A, As = out.Ap, out.Aps
+    else:
+        if out is None:
+            out = (torch.empty((M, K_aug // 2), dtype=torch.uint8, device=gate.device),
+                   torch.empty((M, K_aug // 32), dtype=torch.uint8, device=gate.device))
+        A, As = out
+        _need(A, "Aq", torch.uint8, (M, K_aug // 2))
+        _need(As, "Asc", torch.uint8, (M, K_aug // 32))
+    _on_gpu(gate=gate, up=up, A=A, As=As)
+    fn = _swiglu_quant_packed if packed else _swiglu_quant
+    st = fn(_ptr(gate), _ptr(up), ld, M, K_aug, _ptr(A), _ptr(As), _stream(stream))
+    _check(st, "prq_swiglu_quant_packed" if packed else "prq_swiglu_quant")
     return out
 
 

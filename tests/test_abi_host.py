@@ -346,3 +346,21 @@ def test_streamk_workspace_sizes():
         assert prq.prq_gemm_workspace_bytes(M, 1792, 9984, prq.GEMM_STREAM_K) == HEAD + 256 * 2 * M * 16 * 4
     assert prq.prq_gemm_workspace_bytes(65, 2560, 9984, prq.GEMM_STREAM_K) == 0
     assert prq.prq_gemm_workspace_bytes(31, 1024, 9984, prq.GEMM_STREAM_K) == 0
+
+
+def test_swiglu_quant_rejects_bad_arguments_before_the_gpu():
+    """prq_swiglu_quant(_packed): argument errors are reported before any
+    device work (null, negative M, ld below K_aug, K_aug not a multiple of 32,
+    unaligned rows or outputs, K_aug past the limit); M == 0 is a no-op."""
+    for fn in (prq._swiglu_quant, prq._swiglu_quant_packed):
+        a = 256                                          # a 16-byte aligned stand-in address
+        assert fn(a, a, 64, 0, 64, a, a, None) == prq.PRQ_OK
+        assert fn(a, a, 64, -1, 64, a, a, None) == prq.PRQ_EINVAL
+        assert fn(a, a, 32, 4, 64, a, a, None) == prq.PRQ_EINVAL
+        assert fn(None, a, 64, 4, 64, a, a, None) == prq.PRQ_EINVAL
+        assert fn(a, a, 64, 4, 64, None, a, None) == prq.PRQ_EINVAL
+        assert fn(a, a, 96, 4, 80, a, a, None) == prq.PRQ_EALIGN
+        assert fn(a + 2, a, 64, 4, 64, a, a, None) == prq.PRQ_EALIGN
+        assert fn(a, a, 68, 4, 64, a, a, None) == prq.PRQ_EALIGN
+        assert fn(a, a, 70000, 4, 65568, a, a, None) == prq.PRQ_EUNSUPPORTED
+    assert prq._swiglu_quant_packed(256, 256, 64, 4, 64, 256, 260, None) == prq.PRQ_EALIGN
