@@ -173,7 +173,7 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
     const int32_t* __restrict__ off, int E, int n_mtiles, int tile_base, int region_tiles,
     const uint8_t* __restrict__ Wp,
     const uint8_t* __restrict__ Wps, int N, int K_aug, float* __restrict__ Y, int splits,
-    int split_steps, float* __restrict__ ws) {
+    int split_steps, float* __restrict__ ws, int group_rows) {
   using L = TileStage<kBM, kBN, kAMode>;
   constexpr bool kScaleDword = kAMode == kARowDword;
   constexpr bool kPackedA = kAMode == kAPacked;
@@ -240,17 +240,14 @@ __global__ __launch_bounds__(kWM * kWN * 64) void gemm_tile_kernel(
   const int split = logical / n_tiles;
   const int tl = logical - split * n_tiles;
   // Tile order within a launch: row-major (an XCD's contiguous range is a band
-  // of row tiles), or for 256 x 320 tiles groups of four row tiles, column-major
-  // inside each group, so that an XCD's range is a block of row and column
-  // tiles and its L2 holds fewer operand bytes per step (4096 x 9728 x 2624:
-  // 77.0 -> 73.6 us; 8192 x 2560 unchanged; the 128 x 128 tiles of 2048 x 2560
-  // ran slower in that order, 42.3 -> 49.8 us).
-  constexpr int kGroupRows = kBN == 320 && !kGrouped ? 4 : 0;
+  // of row tiles), or groups of group_rows row tiles, column-major inside each
+  // group, so that an XCD's range is a block of row and column tiles and its
+  // L2 holds fewer operand bytes per step (the host's choice per launch).
   int mt, nt;
-  if constexpr (kGroupRows > 0) {
-    const int grp = tl / (kGroupRows * n_ntiles), first_m = grp * kGroupRows;
-    const int gm = min(n_mtiles - first_m, kGroupRows);
-    const int in_g = tl - grp * kGroupRows * n_ntiles;
+  if (!kGrouped && group_rows > 0) {                  // uniform
+    const int grp = tl / (group_rows * n_ntiles), first_m = grp * group_rows;
+    const int gm = min(n_mtiles - first_m, group_rows);
+    const int in_g = tl - grp * group_rows * n_ntiles;
     mt = first_m + in_g % gm;
     nt = in_g / gm;
   } else {
@@ -836,11 +833,18 @@ hipError_t launch_shape_scales(const uint8_t* Aq, const uint8_t* Asc, int M, con
   if (off) {
     gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, true, kAMode><<<grid, kWM * kWN * 64, 0, stream>>>(
         Aq, Asc, M, off, E, n_mtiles, tile_base, region_tiles, Wp, Wps, N, K_aug, Y, 1,
-        split_steps, nullptr);
+        split_steps, nullptr, 0);
   } else {
+    // Grouped tile order (measured, weights rotated, M x N x (K + k)): for 256-row
+    // tiles always -- 4096 x 9728 x 2624 in 256 x 320, 77.0 -> 73.6 us; 4096 x
+    // 2560 x 4192 in 256 x 256, 40.3 -> 35.0; 2048 x 2560 x 9984 in 256 x 128,
+    // 52.5 -> 44.8 -- and for 128 x 128 tiles up to 8 row tiles (1024 x 2560 x
+    // 9984: 31.6 -> 28.8 us; 2048 x 2560 went 44.4 -> 51.5, 512 and 4096 x 1024
+    // unchanged).
+    const int group_rows = kBM == 256 || n_mtiles <= 8 ? 4 : 0;
     gemm_tile_kernel<kBM, kBN, kWM, kWN, kNS, false, kAMode><<<grid, kWM * kWN * 64, 0, stream>>>(
         Aq, Asc, M, nullptr, 1, n_mtiles, tile_base, region_tiles, Wp, Wps, N, K_aug, Y, splits,
-        split_steps, ws);
+        split_steps, ws, group_rows);
   }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess || splits == 1) return err;
