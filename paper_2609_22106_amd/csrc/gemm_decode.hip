@@ -12,13 +12,20 @@
 //     issues the loads of its chunk of the packed weight (the MFMA A operand,
 //     one contiguous kilobyte per step) first, with clamped unconditional
 //     addresses; the tiles' weight scale dwords go straight to LDS.
-//   * The activation operand of every K step is then copied straight into LDS
-//     in MFMA lane order by direct global->LDS loads (lane l: row l % 16, K
-//     part l / 16, 16 bytes at LDS offset 16 l; its scale byte into dword slot
-//     l), spread over the waves -- no registers, one round trip for all of K.
-//     It is read back with one conflict-free 16-byte LDS read per MFMA.
-//   * One wait for all loads, one barrier, kU MFMAs per wave, and a fixed-order
-//     sum of the K chunks through LDS; Y is written once.
+//   * The group's activation rows (contiguous in the row-major quantizer
+//     output) are then copied straight into LDS by direct global->LDS loads,
+//     whole kilobytes of one row per copy, and its scale bytes as one
+//     contiguous run -- no registers, one round trip for all of K.  Rows sit
+//     at a pitch of a whole number of kilobytes plus 32 bytes, at which the
+//     MFMA's operand read (lane l: row l % 16, 16 bytes of K part l / 16) is
+//     free of LDS bank conflicts (measured; a pitch that is a multiple of
+//     256 bytes conflicts 4- to 8-way).  Gathering the operand in MFMA lane
+//     order instead (16 rows x 64 bytes and 64 scale bytes per copy) costs
+//     ~2 us more per pass.
+//   * One wait for all loads, one barrier; each wave reads all of its steps'
+//     operands from LDS before its kU MFMAs (steps past its chunk meet zero
+//     weight codes, so the reads need no branches), and a fixed-order sum of
+//     the K chunks through LDS; Y is written once.
 // K parts past K_aug read the row start (a valid address) and meet zero weight
 // codes; rows past the group's end are zeroed at the MFMA.
 // Grouped (MoE) mode: blockIdx.z is the expert; a workgroup loops over the
@@ -45,6 +52,15 @@ constexpr size_t kMaxDecodeLds = 160 * 1024;
 
 #define PRQ_GPTR(p) ((const __attribute__((address_space(1))) void*)(p))
 #define PRQ_LPTR(p) ((__attribute__((address_space(3))) void*)(p))
+
+// Pitch, in 16-byte pieces, of a staged activation row of nb pieces: whole
+// kilobyte copies plus two pieces (32 bytes past a multiple of 1 KB).
+__host__ __device__ inline int staged_row_pitch(int nb) { return ((nb + 63) & ~63) + 2; }
+
+// LDS bytes of 16 staged rows, rounded up to whole kilobytes.
+__host__ __device__ inline size_t staged_rows_bytes(int nb) {
+  return (static_cast<size_t>(16) * staged_row_pitch(nb) * 16 + 1023) & ~static_cast<size_t>(1023);
+}
 
 __device__ __forceinline__ void wait_all_vm() {
   // vmcnt = 0, expcnt and lgkmcnt left at their maxima
@@ -90,11 +106,13 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_decode_kernel(
     w[j] = *reinterpret_cast<const uint4*>(Wt + static_cast<int64_t>(st) * 1024);
   }
 
-  // LDS: weight scales (kept for every pass), then the staged activation,
-  // which the reduction buffer of a pass reuses.
-  uint8_t* const sWs = smem;                         // [kT][sgroups][64 dwords] weight scales
-  uint8_t* const sA = smem + kT * sgroups * 256;     // [steps][1024] activation codes
-  uint8_t* const sAs = sA + steps * 1024;            // [steps][64 dwords] activation scales
+  // LDS: weight scales (kept for every pass), then the staged activation
+  // rows, then their scale bytes; the reduction buffer of a pass reuses the rows.
+  const int pitch = staged_row_pitch(nb);             // 16-byte pieces
+  const int copies = (nb + 63) >> 6;                  // kilobyte copies per row
+  uint8_t* const sWs = smem;                          // [kT][sgroups][64 dwords] weight scales
+  uint8_t* const sA = smem + kT * sgroups * 256;      // [16][pitch][16 bytes] activation rows
+  uint8_t* const sAs = sA + staged_rows_bytes(nb);    // the rows' scale bytes (after `shift`)
   float* const s_red = reinterpret_cast<float*>(sA);
 
   // The weight scale dwords of the workgroup's tiles, straight into LDS
@@ -109,34 +127,79 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_decode_kernel(
   for (int pass_row = row_begin + static_cast<int>(blockIdx.y) * 16; pass_row < row_end;
        pass_row += static_cast<int>(gridDim.y) * 16) {
     const int rows = min(16, row_end - pass_row);
-    const int m = pass_row + min(lr, rows - 1);
-    // 2. The activation operand of every step, straight into LDS.
-    for (int s = wave; s < steps; s += kWaves) {
-      const bool kin = s * kStepK + lk * 32 < K_aug;
+    // 2. The group's rows, a kilobyte of one row per copy (lanes past the row
+    //    read its start into the pad past the row's pieces, never read back),
+    //    and their scale bytes as one run of 16-byte pieces from the aligned
+    //    address below it (each piece holds at least one byte of the run).
+    const uint8_t* const ablk = Aq + static_cast<int64_t>(pass_row) * row_bytes;
+    for (int i = wave; i < rows * copies; i += kWaves) {
+      const int r = i / copies, c = i - r * copies;
+      const int piece = c * 64 + lane;
       __builtin_amdgcn_global_load_lds(
-          PRQ_GPTR(Aq + m * row_bytes + (kin ? static_cast<int64_t>(s) * kStepBytes + lk * 16 : 0)),
-          PRQ_LPTR(sA + s * 1024), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(
-          PRQ_GPTR(Asc + static_cast<int64_t>(m) * nb + (kin ? s * 4 + lk : 0)),
-          PRQ_LPTR(sAs + s * 256), 1, 0, 0);
+          PRQ_GPTR(ablk + r * row_bytes + (piece < nb ? piece : 0) * 16),
+          PRQ_LPTR(sA + (r * pitch + c * 64) * 16), 16, 0, 0);
+    }
+    const uint8_t* const sblk = Asc + static_cast<int64_t>(pass_row) * nb;
+    const int shift = static_cast<int>(reinterpret_cast<uintptr_t>(sblk) & 15u);
+    const int spieces = (rows * nb + shift + 15) >> 4;
+    for (int i = wave; i < ((spieces + 63) >> 6); i += kWaves) {
+      __builtin_amdgcn_global_load_lds(PRQ_GPTR(sblk - shift + min(i * 64 + lane, spieces - 1) * 16),
+                                       PRQ_LPTR(sAs + i * 1024), 16, 0, 0);
     }
     wait_all_vm();
     __syncthreads();
 
-    // 3. MFMAs of the wave's chunk.
-    v4f acc = {0.f, 0.f, 0.f, 0.f};
-    const bool row_ok = lr < rows;
+    // 3. The wave's operands from LDS, then its MFMAs, in batches of at most
+    //    five steps (ten steps' operands at once do not fit beside the 40
+    //    registers of weight).  Lane (lr, lk) of step s0 + j reads K part
+    //    4 (s0 + j) + lk of row lr at a fixed offset from one base address per
+    //    operand; the base is recomputed every pass (the empty asm), which
+    //    keeps the compiler from holding ten steps' addresses in registers
+    //    across passes.  Steps past the wave's chunk, rows past the group and
+    //    tiles past N meet a zero activation operand, K parts past K_aug the
+    //    neutral scale (their weight codes are zero), so no step branches;
+    //    reads past a row land in the pad, the next row or the LDS tail.
+    int part0 = s0 * 4 + lk;
+    asm volatile("" : "+v"(part0));
+    const uint8_t* const a_at = sA + (lr * pitch + part0) * 16;
+    const uint8_t* const sa_at = sAs + shift + lr * nb + part0;
+    // The weight scale bytes of the wave's steps: the scale dwords of steps
+    // 4 (s0 / 4) .. +4 nd - 1, realigned so that byte j % 4 of ws[j / 4] is
+    // step s0 + j's (bytes past the tile's steps are never used).
+    constexpr int nd = (kU + 6) / 4;
+    uint32_t ws[nd + 1];
+    {
+      const uint32_t* const ws_at = reinterpret_cast<const uint32_t*>(
+          sWs + (t_in * sgroups + (part0 >> 4)) * 256 + lane * 4);
 #pragma unroll
-    for (int j = 0; j < kU; ++j) {
-      const int st = s0 + j;
-      if (tile_ok && st < s1) {                       // wave-uniform
-        const uint4 a = *reinterpret_cast<const uint4*>(sA + st * 1024 + lane * 16);
-        const uint32_t sa = *reinterpret_cast<const uint32_t*>(sAs + st * 256 + lane * 4) & 0xFFu;
-        const uint32_t sw =
-            (*reinterpret_cast<const uint32_t*>(sWs + (t_in * sgroups + (st >> 2)) * 256 + lane * 4) >>
-             (8 * (st & 3))) & 0xFFu;
-        acc = dev::mfma_fp4_16x16x128(w[j], row_ok ? a : make_uint4(0, 0, 0, 0), sw,
-                                      row_ok ? sa : kNeutralScale, acc);
+      for (int i = 0; i < nd; ++i) ws[i] = ws_at[i * 64];
+      ws[nd] = 0;
+      const int o = (part0 >> 2) & 3;   // s0 % 4
+#pragma unroll
+      for (int i = 0; i < nd; ++i) ws[i] = __builtin_amdgcn_alignbyte(ws[i + 1], ws[i], o);
+    }
+    const bool row_ok = lr < rows && tile_ok;
+    v4f acc = {0.f, 0.f, 0.f, 0.f};
+    constexpr int kBatch = kU < 5 ? kU : 5;
+#pragma unroll
+    for (int j0 = 0; j0 < kU; j0 += kBatch) {
+      uint4 a[kBatch];
+      uint32_t sa[kBatch];
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        a[j] = *reinterpret_cast<const uint4*>(a_at + (j0 + j) * 64);
+        sa[j] = sa_at[(j0 + j) * 4];
+      }
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        const int jj = j0 + j;
+        const bool step_ok = s0 + jj < s1;             // wave-uniform
+        const bool use = row_ok && step_ok;
+        // lane l's weight scale is feature l % 16's: masked by the step only
+        const uint32_t sw = (ws[jj >> 2] >> (8 * (jj & 3))) & 0xFFu;
+        acc = dev::mfma_fp4_16x16x128(w[jj], use ? a[j] : make_uint4(0, 0, 0, 0),
+                                      step_ok ? sw : kNeutralScale,
+                                      use && part0 + 4 * jj < nb ? sa[j] : kNeutralScale, acc);
       }
     }
     __syncthreads();   // the staged operand becomes the reduction buffer
@@ -200,8 +263,14 @@ int round_decode_unroll(int per) {
 
 size_t decode_lds_bytes(int K_aug, int tiles) {
   const int steps = (K_aug + kStepK - 1) / kStepK;
+  const int nb = K_aug / 32;
+  // the scale run of 16 rows: 16 nb bytes after a shift of up to 15, copied
+  // in whole kilobytes of 16-byte pieces
+  const size_t scale_bytes = static_cast<size_t>((((16 * nb + 15 + 15) >> 4) + 63) >> 6) * 1024;
+  // + 2 KiB for the operand reads of steps past a wave's chunk beyond the
+  // last row: at most (kWaves + 10) steps of 64 bytes past K_aug
   return static_cast<size_t>(tiles) * ((steps + 3) / 4) * 256 +
-         std::max(static_cast<size_t>(steps) * 1280, static_cast<size_t>(kWaves) * 64 * 4 * 4);
+         std::max(staged_rows_bytes(nb) + scale_bytes + 2048, static_cast<size_t>(kWaves) * 64 * 4 * 4);
 }
 
 DecodeConfig choose_decode_config(int M_per_group, int N, int K_aug, int grouped, int tiles,

@@ -103,6 +103,45 @@ def test_decode_kernel_configs(M, N, K_aug, tiles, row_splits):
     assert_gemm_close(Y, pq.gemm(Aq, Asc, Wq, Wsc), f"decode {M}x{N}x{K_aug} t{tiles} r{row_splits}")
 
 
+@pytest.mark.parametrize("M,shift", [(1, 3), (9, 1), (33, 4), (40, 7), (64, 15)])
+def test_decode_scale_rows_at_any_byte_offset(M, shift):
+    """Asc carries no alignment requirement: the decode kernels read a row
+    group's scale bytes as one run of 16-byte pieces from the aligned address
+    below it.  Asc at offsets 1..15 from a 16-byte boundary, rows of
+    K_aug / 32 = 82 bytes (not a multiple of 16), K_aug not a multiple of
+    128 (the last step's K parts past K_aug); Y starts as NaN."""
+    prq = _prq()
+    rng = np.random.default_rng(M * 16 + shift)
+    N, K_aug = 160, 2624
+    Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+    Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
+    buf = torch.zeros(Asc.size + 64, dtype=torch.uint8, device="cuda")
+    S = buf[shift:shift + Asc.size].view(M, K_aug // 32)
+    S.copy_(dev(Asc))
+    assert S.data_ptr() % 16 == shift % 16
+    say("gemm case: decode scale offset", M, shift)
+    Y = nan_output(M, N)
+    prq.prq_gemm(dev(Aq), S, _packed(Wq, Wsc), Y=Y, variant=prq.GEMM_STREAM)
+    torch.cuda.synchronize()
+    assert_gemm_close(host(Y), pq.gemm(Aq, Asc, Wq, Wsc), f"decode scale offset {M} {shift}")
+
+
+def test_decode_kernel_longest_rows():
+    """K_aug = 16384 (512 scale blocks a row): 16 staged rows take 129 KB of
+    LDS at one tile per workgroup; two tiles per workgroup need 16 weight
+    steps per wave and are refused."""
+    rng = np.random.default_rng(5)
+    M, N, K_aug = 20, 64, 16384
+    Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+    Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
+    say("gemm case: decode K_aug 16384")
+    st, Y = _tune_decode(Aq, Asc, Wq, Wsc, 1, 2)
+    assert st == 0
+    assert_gemm_close(Y, pq.gemm(Aq, Asc, Wq, Wsc), "decode K_aug 16384")
+    st, _ = _tune_decode(Aq, Asc, Wq, Wsc, 2, 2)
+    assert st == -1
+
+
 @pytest.mark.parametrize("M,splits", [(8, 1), (24, 0), (24, 2), (24, 3), (24, 7), (24, 19), (64, 6)])
 def test_stream_split_counts(M, splits):
     prq = _prq()
