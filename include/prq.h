@@ -213,11 +213,11 @@ int prq_pack_weight(const uint8_t* Wq, const uint8_t* Wsc, int32_t E, int32_t N,
  *   LDS-tiled kernel's split along K, splits - 1 partial sums [M][N] (Y
  *   16-byte aligned).  One buffer may therefore serve calls of any shape in
  *   turn, as long as it is large enough for each; calls that share it must be
- *   ordered (same stream).  AUTO runs the stream-K kernel up to 8 rows, the
- *   whole-K decode kernel up to 64, the LDS-tiled kernel above; a call whose
- *   plan would use more workspace than it is given (or NULL) runs without it
- *   (the whole-K decode kernel instead of a stream-K plan that shares tiles,
- *   the LDS-tiled kernel unsplit; same result up to float rounding).
+ *   ordered (same stream).  AUTO runs the whole-K decode kernel up to 64
+ *   rows (no workspace) and the LDS-tiled kernel above; the stream-K kernel
+ *   runs only when asked for (PRQ_GEMM_STREAM_K).  A call whose plan would
+ *   use more workspace than it is given (or NULL) runs without it (the
+ *   LDS-tiled kernel unsplit; same result up to float rounding).
  * Limits: N % 16 == 0, K_aug <= 65536.  M == 0 is a no-op.
  */
 size_t prq_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K_aug);

@@ -185,25 +185,15 @@ int device_cus() {
   return current_device(&dev) == PRQ_OK ? dev.num_cus : 256;
 }
 
-// Rows up to which AUTO runs the stream-K kernel.  Measured on the 9728 ->
-// 2560 down_proj (one workgroup per tile, weights rotated, back-to-back
-// launches): M = 1 5.3 vs 6.1 us for the whole-K decode kernel, M = 8 6.3 vs
-// 7.0, M = 16 8.0 vs 7.8; from two 16-row groups on, each workgroup reading
-// the activation of all K steps costs more than the whole-K kernel's staging.
-constexpr int kStreamKMaxRows = 8;
-
-// The variant an AUTO call runs when given `workspace_bytes` of workspace:
-// the stream-K kernel for up to kStreamKMaxRows rows wherever it applies (and
-// its workspace, if its plan shares tiles, is there), else the shape's default
-// (whole-K decode kernel up to 64 rows, LDS-tiled kernel above).
-int auto_variant(int M, int N, int K_aug, size_t workspace_bytes, int num_cus) {
-  const int v = prq::choose_variant(M, N, K_aug);
-  if (v == PRQ_GEMM_STREAM && M <= kStreamKMaxRows &&
-      prq::choose_streamk_config(M, N, K_aug, num_cus).ok &&
-      workspace_bytes >= prq::streamk_workspace_bytes(M, N, K_aug, num_cus))
-    return PRQ_GEMM_STREAM_K;
-  return v;
-}
+// The variant an AUTO call runs: the whole-K decode kernel up to 64 rows, the
+// LDS-tiled kernel above.  The stream-K kernel (PRQ_GEMM_STREAM_K) is not an
+// AUTO choice: since the decode kernel stages each row group's activation in
+// whole-row copies it is as fast or faster at every measured shape (weights
+// rotated, back-to-back launches, decode / stream-K): 9728 -> 2560 M = 1 5.1 /
+// 5.3 us, M = 8 5.5 / 6.3; 9728 -> 1792 (112 tiles, stream-K sharing tiles
+// over all CUs) M = 1 5.1 / 8.2, M = 8 5.2 / 8.7; 2560 -> 4096 M = 8 3.9 /
+// 4.0; 4096 -> 2560 M = 8 4.5 / 4.8.
+int auto_variant(int M, int N, int K_aug) { return prq::choose_variant(M, N, K_aug); }
 
 }  // namespace
 
@@ -212,7 +202,7 @@ extern "C" {
 size_t prq_gemm_workspace_bytes_ex(int32_t M, int32_t N, int32_t K_aug, int32_t variant,
                                    int32_t splits) {
   if (M <= 0 || N <= 0 || K_aug <= 0 || N % 16 || K_aug % PRQ_BLOCK || splits < 0) return 0;
-  if (variant == PRQ_GEMM_AUTO) variant = auto_variant(M, N, K_aug, SIZE_MAX, device_cus());
+  if (variant == PRQ_GEMM_AUTO) variant = auto_variant(M, N, K_aug);
   if (variant == PRQ_GEMM_STREAM_K) return prq::streamk_workspace_bytes(M, N, K_aug, device_cus());
   if (variant == PRQ_GEMM_TILE)
     return with_head(prq::tile_workspace_bytes(M, N, K_aug, false, device_cus()));
@@ -236,8 +226,7 @@ int prq_gemm_ex(const uint8_t* Aq, const uint8_t* Asc, int32_t M, const uint8_t*
   DeviceInfo dev;
   st = current_device(&dev);
   if (st != PRQ_OK) return st;
-  if (variant == PRQ_GEMM_AUTO)
-    variant = auto_variant(M, N, K_aug, workspace ? workspace_bytes : 0, dev.num_cus);
+  if (variant == PRQ_GEMM_AUTO) variant = auto_variant(M, N, K_aug);
   if (variant == PRQ_GEMM_STREAM_K) {
     const prq::StreamKConfig c = prq::choose_streamk_config(M, N, K_aug, dev.num_cus);
     if (!c.ok) return PRQ_EUNSUPPORTED;

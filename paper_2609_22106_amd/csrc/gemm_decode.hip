@@ -278,17 +278,19 @@ DecodeConfig choose_decode_config(int M_per_group, int N, int K_aug, int grouped
   DecodeConfig c;
   const int steps = (K_aug + kStepK - 1) / kStepK;
   const int groups = (std::max(M_per_group, 1) + 15) / 16;
-  // Dense (measured on the 9728 -> 2560 down_proj): one tile per workgroup
-  // for one row group; from two row groups on, two tiles per workgroup, and
-  // each row group its own workgroup row while the launch still fits the CUs
-  // in one round (a workgroup at this LDS size holds a CU) -- a second pass
-  // over another row group costs ~4 us more than a workgroup of its own --
-  // else two workgroup rows, each looping over its row groups with the weight
-  // still in registers.  Grouped: one tile per workgroup, the expert's row
-  // groups in one workgroup (the experts multiply the workgroups).
-  c.tiles = tiles > 0 ? tiles : (grouped || groups <= 1 ? 1 : 2);
+  // Dense (measured on the 9728 -> 2560 down_proj, weights rotated,
+  // back-to-back launches): one tile per workgroup up to two row groups (two
+  // passes of one workgroup row, M = 17 / 24 / 32 7.1 / 7.5 / 8.1 us, against
+  // 7.7 / 7.8 / 8.0 for two tiles and a workgroup row per group), two tiles
+  // per workgroup from three row groups on; then as many workgroup rows as
+  // the launch fits in one round of the CUs (a workgroup at this LDS size
+  // holds a CU), the row groups dealt to them in turn (M = 64: three rows
+  // 10.6 us, two 10.7, four -- two rounds -- 12.3).  Grouped: one tile per
+  // workgroup, the expert's row groups in one workgroup (the experts multiply
+  // the workgroups).
+  c.tiles = tiles > 0 ? tiles : (grouped || groups <= 2 ? 1 : 2);
   const int cols = (N / 16 + c.tiles - 1) / c.tiles;
-  const int auto_rows = cols * groups <= std::max(num_cus, 1) ? groups : std::min(groups, 2);
+  const int auto_rows = std::min(groups, std::max(1, std::max(num_cus, 1) / std::max(cols, 1)));
   c.row_splits = grouped ? 1 : std::min(row_splits > 0 ? row_splits : auto_rows, groups);
   if (c.tiles != 1 && c.tiles != 2 && c.tiles != 4) c.ok = false;
   c.unroll = round_decode_unroll((steps + kWaves / c.tiles - 1) / (kWaves / c.tiles));

@@ -336,13 +336,14 @@ def test_streamk_workspace_sizes():
     row groups), else the
     state head and partial tiles [256][2][M][16] floats; 0 where the kernel does
     not apply (more than 64 rows, a tile over more than four workgroups).
-    AUTO asks for no workspace at decode rows of the down_proj."""
+    AUTO (the whole-K decode kernel at decode rows) asks for none."""
     for M in (1, 8, 32, 48):
         assert prq.prq_gemm_workspace_bytes(M, 2560, 9984, prq.GEMM_STREAM_K) == 0
     # four row groups of ten units a wave do not fit: one workgroup per CU
     assert prq.prq_gemm_workspace_bytes(64, 2560, 9984, prq.GEMM_STREAM_K) == HEAD + 256 * 2 * 64 * 16 * 4
     for M in (1, 8, 32, 64):
         assert prq.prq_gemm_workspace_bytes(M, 2560, 9984) == 0
+        assert prq.prq_gemm_workspace_bytes(M, 1792, 9984) == 0
         assert prq.prq_gemm_workspace_bytes(M, 1792, 9984, prq.GEMM_STREAM_K) == HEAD + 256 * 2 * M * 16 * 4
     assert prq.prq_gemm_workspace_bytes(65, 2560, 9984, prq.GEMM_STREAM_K) == 0
     assert prq.prq_gemm_workspace_bytes(31, 1024, 9984, prq.GEMM_STREAM_K) == 0

@@ -96,27 +96,29 @@ def test_streamk_is_reproducible_and_reuses_its_workspace():
     assert not np.any(_counters(big, N))
 
 
-def test_auto_runs_streamk_up_to_eight_rows():
-    """prq_gemm (AUTO) runs the stream-K kernel up to 8 rows (one workgroup per
-    tile on the down_proj shape: no workspace needed) and the whole-K decode
-    kernel from 9 to 64 rows: the same bits as forcing either."""
+def test_auto_runs_the_whole_k_decode_kernel():
+    """prq_gemm (AUTO) runs the whole-K decode kernel at every M up to 64, with
+    many output tiles (N = 2560: 160) or few (N = 1792: 112), and needs no
+    workspace: the same bits as forcing it; the stream-K kernel runs only when
+    asked for (it gives the same result within the GEMM bar)."""
     prq = _prq()
     rng = np.random.default_rng(12)
-    N, K_aug = 2560, 9984
-    Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
-    W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
-    for M in (1, 8, 9, 64):
-        Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
-        A, As = dev(Aq), dev(Asc)
-        assert prq.prq_gemm_workspace_bytes(M, N, K_aug) == 0
-        say("stream-K case: auto, M =", M)
-        Ya = host(prq.prq_gemm(A, As, W))
-        if M <= 8:
-            Yf = host(prq.prq_gemm(A, As, W, variant=prq.GEMM_STREAM_K))
-        else:
+    K_aug = 9984
+    for N, cases in ((2560, (1, 8, 9, 64)), (1792, (1, 8, 9))):
+        Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
+        W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
+        for M in cases:
+            Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+            A, As = dev(Aq), dev(Asc)
+            assert prq.prq_gemm_workspace_bytes(M, N, K_aug) == 0
+            say("decode case: auto, N =", N, "M =", M)
+            Ya = host(prq.prq_gemm(A, As, W))
             Yf = host(prq.prq_gemm(A, As, W, variant=prq.GEMM_STREAM, splits=1))
-        np.testing.assert_array_equal(Ya.view(np.uint32), Yf.view(np.uint32))
-        assert_gemm_close(Ya, pq.gemm(Aq, Asc, Wq, Wsc), f"auto M={M}")
+            np.testing.assert_array_equal(Ya.view(np.uint32), Yf.view(np.uint32))
+            assert_gemm_close(Ya, pq.gemm(Aq, Asc, Wq, Wsc), f"auto N={N} M={M}")
+            if M <= 8:
+                Ys = host(prq.prq_gemm(A, As, W, variant=prq.GEMM_STREAM_K))
+                assert_gemm_close(Ys, pq.gemm(Aq, Asc, Wq, Wsc), f"stream-K N={N} M={M}")
 
 
 def _tune(lib, A, As, M, W, N, K_aug, Y, cus, wgs, ws):

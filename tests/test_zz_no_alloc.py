@@ -22,16 +22,16 @@ def _prq():
 
 def test_noalloc_matches_prq_gemm_on_two_calls():
     """N = 1792, K + k = 9984: M = 512 (the LDS-tiled kernel split along K,
-    partial sums in the scratch) and then M = 8 (the stream-K kernel with tiles
-    shared between workgroups, arrival counters and partial tiles in the
-    scratch), then M = 512 again over what the smaller call left."""
+    partial sums in the scratch) and then M = 128 (split along K into more
+    ranges over fewer rows), then M = 512 again over what the smaller call
+    left."""
     prq = _prq()
     rng = np.random.default_rng(77)
     N, K_aug = 1792, 9984
     Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
     W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
     limit = prq.prq_gemm_noalloc_max_workspace_bytes()
-    for call, M in enumerate((512, 8, 512)):
+    for call, M in enumerate((512, 128, 512)):
         need = prq.prq_gemm_workspace_bytes(M, N, K_aug)
         assert 0 < need <= limit, (M, need, limit)
         Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
