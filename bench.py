@@ -99,6 +99,14 @@ def grouped_gemm_bytes(M, E_active, N, K_aug):
     return (E_active * N + M) * K_aug * 17 / 32 + 4 * M * N
 
 
+# Rows from which a dense op runs the packed pair: one 16-row group or fewer
+# run row-major (the packed layout would stage and store a whole 16-row block;
+# measured on the down_proj decode rows, back to back, quantizer + GEMM: M = 1
+# 7.7 us row-major vs 8.5 packed, M = 8 8.2 vs 8.6, M = 32 10.8 vs 10.5, M = 64
+# 14.0 vs 13.5).
+PACKED_MIN_ROWS = 17
+
+
 class Op:
     """One act-quant + GEMM pair of a step (launch closures bound to buffers)."""
 
@@ -110,12 +118,14 @@ class Op:
         self.weights = None
 
 
-PACKED_MIN_ROWS = 64   # more rows than this: the packed prefill pair
 PACKED_MIN_EXPERT_ROWS = 64   # mean routed rows per expert from which experts use it
 
 
-def build_dense_ops(torch, prq, layers, M_list, rotate_bytes, plain=False):
+def build_dense_ops(torch, prq, layers, M_list, rotate_bytes, plain=False, rowmajor=False):
     """layers: list of (name, DenseCase).  Weights rotated, activations per M.
+    From PACKED_MIN_ROWS rows the packed pair (activation written in the layout
+    the GEMM copies in whole kilobytes: the whole-K decode kernel up to 64 rows,
+    the tile GEMM above), else (or with rowmajor) prq_quant_act + prq_gemm.
     plain: the plain MXFP4 baseline (no scaling, no tail: k = 0)."""
     ops = []
     for name, c in layers:
@@ -137,9 +147,7 @@ def build_dense_ops(torch, prq, layers, M_list, rotate_bytes, plain=False):
             state = {"r": 0}
             # every per-layer buffer is bound here: a name captured from the
             # enclosing loop would see the last layer's buffers in every op
-            if M > PACKED_MIN_ROWS:
-                # prefill: the packed pair (activation written in the layout the
-                # tile GEMM copies in whole kilobytes)
+            if M >= PACKED_MIN_ROWS and not rowmajor:
                 A = prq.prq_quant_act_packed(Xm, K, k, inv, perm)
                 ws_n = prq.prq_gemm_packed_workspace_bytes(M, N, K_aug)   # split along K
                 ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda") if ws_n else None
@@ -451,7 +459,7 @@ def copy_context(torch, prq, layers, M_list, reps=50):
             quant(Zb[:M])
         for M in M_list:
             res = {}
-            if M > PACKED_MIN_ROWS:     # the quantizer the step uses: packed output
+            if M >= PACKED_MIN_ROWS:     # the quantizer the step uses: packed output
                 A = prq.prq_quant_act_packed(X[:M], K, k, inv, perm)
                 fns = (("online", lambda: prq.prq_quant_act_packed(X[:M], K, k, inv, perm, out=A)),
                        ("offline", lambda: prq.prq_quant_act_packed(Zaug[:M], K + k, 0, out=A)),
@@ -687,13 +695,13 @@ def traffic_from_counters(workload, fetch_dir, write_dir, command):
 WORKLOADS = ("decode", "prefill", "experts", "experts_prefill", "layers")
 
 
-def build_workload(torch, np, prq, inputs, wl, rotate_bytes, plain=False):
+def build_workload(torch, np, prq, inputs, wl, rotate_bytes, plain=False, rowmajor=False):
     """(ops, dense layers or [], M list, config) of one workload."""
     if wl in ("decode", "prefill"):
         c = inputs.down_proj_decode() if wl == "decode" else inputs.down_proj_prefill()
         layers = [("qwen3_4b_down_proj", c)]
         M_list = list(c.M_list)
-        ops = build_dense_ops(torch, prq, layers, M_list, rotate_bytes, plain=plain)
+        ops = build_dense_ops(torch, prq, layers, M_list, rotate_bytes, plain=plain, rowmajor=rowmajor)
         config = {"workload": f"qwen3_4b_down_proj_{wl}", "N": 2560, "K": 9728, "k_tail": 256,
                   "alpha": 0.5, "M": M_list}
     elif wl in ("experts", "experts_prefill"):
@@ -790,6 +798,17 @@ def measure_workload(torch, np, prq, inputs, wl, args, stream, contexts=True):
                 d["plain_mxfp4_op_us"] = round((op.t_gemm + op.t_act) * 1e6, 3)
                 d["op_over_plain_mxfp4"] = round(d["op_us"] / ((op.t_gemm + op.t_act) * 1e6), 3)
         del plain_ops
+    if contexts and layers and wl == "decode":
+        # the row-major pair (prq_quant_act + prq_gemm) at every M, same timing
+        rm_ops, _, _, _ = build_workload(torch, np, prq, inputs, wl, args.rotate_bytes, rowmajor=True)
+        time_kernels(torch, rm_ops, reps, args.warmup, stream)
+        for op in rm_ops:
+            if op.name in detail:
+                d = detail[op.name]
+                d["rowmajor_gemm_us"] = round(op.t_gemm * 1e6, 3)
+                d["rowmajor_act_quant_us"] = round(op.t_act * 1e6, 3)
+                d["rowmajor_op_us"] = round((op.t_gemm + op.t_act) * 1e6, 3)
+        del rm_ops
     if contexts and layers and wl in ("decode", "prefill"):
         for key, r in copy_context(torch, prq, layers, M_list).items():
             if key in detail:

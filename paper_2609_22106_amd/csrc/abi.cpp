@@ -333,6 +333,9 @@ int prq_swiglu_quant_packed(const void* gate_bf16, const void* up_bf16, int64_t 
 
 size_t prq_gemm_packed_workspace_bytes(int32_t M, int32_t N, int32_t K_aug) {
   if (M <= 0 || N <= 0 || K_aug <= 0 || N % 16 || K_aug % PRQ_BLOCK || K_aug > kMaxKAug) return 0;
+  if (prq::choose_variant(M, N, K_aug) == PRQ_GEMM_STREAM &&
+      prq::choose_decode_config(M, N, K_aug, 0, 0, 0, device_cus()).ok)
+    return 0;   // the decode kernel: no workspace
   return with_head(prq::tile_workspace_bytes(M, N, K_aug, true, device_cus()));
 }
 
@@ -346,6 +349,14 @@ int prq_gemm_packed(const uint8_t* Ap, const uint8_t* Aps, int32_t M, const uint
   DeviceInfo dev;
   st = current_device(&dev);
   if (st != PRQ_OK) return st;
+  // decode rows: the whole-K decode kernel on the packed operand (each row
+  // group's operand one contiguous kilobyte per K step)
+  if (prq::choose_variant(M, N, K_aug) == PRQ_GEMM_STREAM) {
+    const prq::DecodeConfig d = prq::choose_decode_config(M, N, K_aug, 0, 0, 0, dev.num_cus);
+    if (d.ok)
+      return launch_status(prq::launch_gemm_decode(Ap, Aps, M, nullptr, 1, Wp, Wps, N, K_aug, Y, d,
+                                                   stream, true));
+  }
   return launch_status(prq::launch_gemm_tile_planned(
       Ap, Aps, M, Wp, Wps, N, K_aug, Y, true, dev.num_cus, scratch_of(workspace, workspace_bytes),
       scratch_bytes(workspace, workspace_bytes), stream));

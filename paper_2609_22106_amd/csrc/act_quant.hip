@@ -216,7 +216,7 @@ __device__ __forceinline__ void pad_row_tail(const Sink& out, int u0, int units,
 // so a cold call pays one memory round trip before the gather instead of
 // two (permutation, then the rows at the permuted channels); the gather then
 // reads LDS.
-template <bool kGrouped>
+template <bool kGrouped, bool kPacked>
 __global__ __launch_bounds__(kRowsThreads) void act_quant_rows_kernel(
     const uint16_t* __restrict__ X, int64_t ld_x, int M, int K, int k_tail,
     const float* __restrict__ inv, const int32_t* __restrict__ perm,
@@ -231,6 +231,24 @@ __global__ __launch_bounds__(kRowsThreads) void act_quant_rows_kernel(
   const int k_aug = K + k_tail;
   const int64_t row_bytes = k_aug >> 1;
   const int nb = k_aug >> 5;
+  const int steps = (k_aug + 127) >> 7;
+  const int sgroups = (steps + 3) >> 2;
+  if (kPacked && n <= 0) {
+    // Workgroup rows past M (packed output, up to the end of the last 16-row
+    // block): zero codes and scale byte 127 over the whole padded row.
+    if (u >= units) return;
+    for (int r = r0; r < r0 + rows_per_wg; ++r) {
+      const PackedSink ps(Aq, Asc, r, steps, sgroups);
+      ps.word(u, 0u);
+      if ((u & 3) == 0) ps.scale(u >> 2, 127u);
+      if (u >= (K - k_tail) >> 3) {
+        ps.word(u + (k_tail >> 3), 0u);
+        if ((u & 3) == 0) ps.scale((u >> 2) + (k_tail >> 5), 127u);
+      }
+      pad_row_tail(ps, u, units, nb, steps, sgroups);
+    }
+    return;
+  }
   const int xb = 2 * K;                               // bytes of a row of X
   const int chunks = (xb + 1023) >> 10;
   const int pitch = chunks * 1024;
@@ -276,9 +294,15 @@ __global__ __launch_bounds__(kRowsThreads) void act_quant_rows_kernel(
       z[2 * e] = __uint_as_float(static_cast<uint32_t>(xr[sp & 0xFFFFu]) << 16) * un.d[2 * e];
       z[2 * e + 1] = __uint_as_float(static_cast<uint32_t>(xr[sp >> 16]) << 16) * un.d[2 * e + 1];
     }
-    quantize_store(z, u, (K - k_tail) >> 3, k_tail >> 3, k_tail >> 5,
-                   RowSink{Aq + static_cast<int64_t>(r) * row_bytes, Asc + static_cast<int64_t>(r) * nb},
-                   rs);
+    if constexpr (kPacked) {
+      const PackedSink ps(Aq, Asc, r, steps, sgroups);
+      quantize_store(z, u, (K - k_tail) >> 3, k_tail >> 3, k_tail >> 5, ps, rs);
+      pad_row_tail(ps, u, units, nb, steps, sgroups);
+    } else {
+      quantize_store(z, u, (K - k_tail) >> 3, k_tail >> 3, k_tail >> 5,
+                     RowSink{Aq + static_cast<int64_t>(r) * row_bytes, Asc + static_cast<int64_t>(r) * nb},
+                     rs);
+    }
   }
 }
 
@@ -718,14 +742,34 @@ hipError_t launch_act_quant(const uint16_t* X, int64_t ld_x, int M, int K, int k
 
 // Dynamic LDS of the few-rows kernel above the 64 KiB default (up to four
 // staged rows of K = 16384), set once per instantiation.
-template <bool kGrouped>
+template <bool kGrouped, bool kPacked>
 void set_rows_lds_limit() {
   static std::once_flag once;
   std::call_once(once, [] {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&act_quant_rows_kernel<kGrouped>),
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&act_quant_rows_kernel<kGrouped, kPacked>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, 4 * 32768);
     (void)hipGetLastError();
   });
+}
+
+// Few rows into the packed layout: one row per workgroup row, and workgroup
+// rows up to the end of the last 16-row block that write its padding rows.
+hipError_t launch_rows_packed(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail,
+                              const float* inv, const int32_t* perm, const int32_t* off, int G,
+                              uint8_t* Ap, uint8_t* Aps, hipStream_t stream) {
+  const int units = K >> 3;
+  const int pitch = (2 * K + 1023) / 1024 * 1024;
+  const dim3 grid((units + kRowsThreads - 1) / kRowsThreads, (M + 15) / 16 * 16);
+  if (off) {
+    set_rows_lds_limit<true, true>();
+    act_quant_rows_kernel<true, true><<<grid, kRowsThreads, pitch, stream>>>(
+        X, ld_x, M, K, k_tail, inv, perm, off, G, 1, Ap, Aps);
+  } else {
+    set_rows_lds_limit<false, true>();
+    act_quant_rows_kernel<false, true><<<grid, kRowsThreads, pitch, stream>>>(
+        X, ld_x, M, K, k_tail, inv, perm, nullptr, 1, 1, Ap, Aps);
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_act_quant_kernel(const uint16_t* X, int64_t ld_x, int M, int K, int k_tail,
@@ -746,12 +790,12 @@ hipError_t launch_act_quant_kernel(const uint16_t* X, int64_t ld_x, int M, int K
     const dim3 grid((units + kRowsThreads - 1) / kRowsThreads, (M + rows_per_wg - 1) / rows_per_wg);
     const size_t lds = static_cast<size_t>(std::min(rows_per_wg, M)) * pitch;
     if (grouped) {
-      set_rows_lds_limit<true>();
-      act_quant_rows_kernel<true><<<grid, kRowsThreads, lds, stream>>>(
+      set_rows_lds_limit<true, false>();
+      act_quant_rows_kernel<true, false><<<grid, kRowsThreads, lds, stream>>>(
           X, ld_x, M, K, k_tail, inv_scale_pos, perm, group_offsets, G, rows_per_wg, Aq, Asc);
     } else {
-      set_rows_lds_limit<false>();
-      act_quant_rows_kernel<false><<<grid, kRowsThreads, lds, stream>>>(
+      set_rows_lds_limit<false, false>();
+      act_quant_rows_kernel<false, false><<<grid, kRowsThreads, lds, stream>>>(
           X, ld_x, M, K, k_tail, inv_scale_pos, perm, nullptr, 1, rows_per_wg, Aq, Asc);
     }
     return hipGetLastError();
@@ -808,6 +852,11 @@ hipError_t launch_act_quant_packed_kernel(const uint16_t* X, int64_t ld_x, int M
                                           int kernel, hipStream_t stream) {
   const bool grouped = group_offsets && G > 1;
   const int32_t* off = grouped ? group_offsets : nullptr;
+  // Few rows (decode): the few-rows kernel, as for the row-major output (the
+  // whole-K decode GEMM then copies each 16-row group's operand in whole
+  // kilobytes).
+  if (kernel == 1 || (kernel == 0 && M <= 64))
+    return launch_rows_packed(X, ld_x, M, K, k_tail, inv_scale_pos, perm, off, G, Ap, Aps, stream);
   if (kernel == 3 || kernel == 4 || (kernel == 0 && K >= 2048)) {
     const int window = kernel == 3 ? 1 : kernel == 4 ? 2 : 0;
     if (grouped)

@@ -67,7 +67,7 @@ __device__ __forceinline__ void wait_all_vm() {
   __builtin_amdgcn_s_waitcnt((0x7 << 4) | (0xF << 8));
 }
 
-template <bool kGrouped, int kT, int kU>
+template <bool kGrouped, bool kPackedA, int kT, int kU>
 __global__ __launch_bounds__(kWaves * 64) void gemm_decode_kernel(
     const uint8_t* __restrict__ Aq, const uint8_t* __restrict__ Asc, int M,
     const int32_t* __restrict__ off, const uint8_t* __restrict__ Wp,
@@ -127,24 +127,38 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_decode_kernel(
   for (int pass_row = row_begin + static_cast<int>(blockIdx.y) * 16; pass_row < row_end;
        pass_row += static_cast<int>(gridDim.y) * 16) {
     const int rows = min(16, row_end - pass_row);
-    // 2. The group's rows, a kilobyte of one row per copy (lanes past the row
-    //    read its start into the pad past the row's pieces, never read back),
-    //    and their scale bytes as one run of 16-byte pieces from the aligned
-    //    address below it (each piece holds at least one byte of the run).
-    const uint8_t* const ablk = Aq + static_cast<int64_t>(pass_row) * row_bytes;
-    for (int i = wave; i < rows * copies; i += kWaves) {
-      const int r = i / copies, c = i - r * copies;
-      const int piece = c * 64 + lane;
-      __builtin_amdgcn_global_load_lds(
-          PRQ_GPTR(ablk + r * row_bytes + (piece < nb ? piece : 0) * 16),
-          PRQ_LPTR(sA + (r * pitch + c * 64) * 16), 16, 0, 0);
-    }
-    const uint8_t* const sblk = Asc + static_cast<int64_t>(pass_row) * nb;
-    const int shift = static_cast<int>(reinterpret_cast<uintptr_t>(sblk) & 15u);
-    const int spieces = (rows * nb + shift + 15) >> 4;
-    for (int i = wave; i < ((spieces + 63) >> 6); i += kWaves) {
-      __builtin_amdgcn_global_load_lds(PRQ_GPTR(sblk - shift + min(i * 64 + lane, spieces - 1) * 16),
-                                       PRQ_LPTR(sAs + i * 1024), 16, 0, 0);
+    // 2. The group's activation, straight into LDS.  Packed: the group's
+    //    16-row block is one contiguous kilobyte per K step in MFMA lane
+    //    order, plus its scale dwords.  Row-major: its rows, a kilobyte of one
+    //    row per copy (lanes past the row read its start into the pad past the
+    //    row's pieces, never read back), and their scale bytes as one run of
+    //    16-byte pieces from the aligned address below it (each piece holds at
+    //    least one byte of the run).
+    int shift = 0;
+    if constexpr (kPackedA) {
+      const int64_t blk = pass_row >> 4;   // pass_row is a multiple of 16 (dense)
+      for (int st = wave; st < steps; st += kWaves)
+        __builtin_amdgcn_global_load_lds(PRQ_GPTR(Aq + (blk * steps + st) * 1024 + lane * 16),
+                                         PRQ_LPTR(sA + st * 1024), 16, 0, 0);
+      for (int q = wave; q < sgroups; q += kWaves)
+        __builtin_amdgcn_global_load_lds(PRQ_GPTR(Asc + (blk * sgroups + q) * 256 + lane * 4),
+                                         PRQ_LPTR(sAs + q * 256), 4, 0, 0);
+    } else {
+      const uint8_t* const ablk = Aq + static_cast<int64_t>(pass_row) * row_bytes;
+      for (int i = wave; i < rows * copies; i += kWaves) {
+        const int r = i / copies, c = i - r * copies;
+        const int piece = c * 64 + lane;
+        __builtin_amdgcn_global_load_lds(
+            PRQ_GPTR(ablk + r * row_bytes + (piece < nb ? piece : 0) * 16),
+            PRQ_LPTR(sA + (r * pitch + c * 64) * 16), 16, 0, 0);
+      }
+      const uint8_t* const sblk = Asc + static_cast<int64_t>(pass_row) * nb;
+      shift = static_cast<int>(reinterpret_cast<uintptr_t>(sblk) & 15u);
+      const int spieces = (rows * nb + shift + 15) >> 4;
+      for (int i = wave; i < ((spieces + 63) >> 6); i += kWaves) {
+        __builtin_amdgcn_global_load_lds(PRQ_GPTR(sblk - shift + min(i * 64 + lane, spieces - 1) * 16),
+                                         PRQ_LPTR(sAs + i * 1024), 16, 0, 0);
+      }
     }
     wait_all_vm();
     __syncthreads();
@@ -159,24 +173,36 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_decode_kernel(
     //    tiles past N meet a zero activation operand, K parts past K_aug the
     //    neutral scale (their weight codes are zero), so no step branches;
     //    reads past a row land in the pad, the next row or the LDS tail.
-    int part0 = s0 * 4 + lk;
+    // (A wave with no steps reads from step 0: its operands are all masked.)
+    int part0 = (s0 < steps ? s0 : 0) * 4 + lk;
     asm volatile("" : "+v"(part0));
-    const uint8_t* const a_at = sA + (lr * pitch + part0) * 16;
+    const int o = (part0 >> 2) & 3;   // s0 % 4
+    // Packed: step s0 + j's operand is a kilobyte further on; row-major: 64
+    // bytes (four K parts) further along the lane's row.
+    const uint8_t* const a_at =
+        kPackedA ? sA + (part0 >> 2) * 1024 + lane * 16 : sA + (lr * pitch + part0) * 16;
     const uint8_t* const sa_at = sAs + shift + lr * nb + part0;
-    // The weight scale bytes of the wave's steps: the scale dwords of steps
-    // 4 (s0 / 4) .. +4 nd - 1, realigned so that byte j % 4 of ws[j / 4] is
-    // step s0 + j's (bytes past the tile's steps are never used).
+    // Scale bytes held as dwords (four steps a dword, as in the packed
+    // layouts) of steps 4 (s0 / 4) .. +4 nd - 1, realigned so that byte j % 4
+    // of x[j / 4] is step s0 + j's (bytes past the tile's steps are never used).
     constexpr int nd = (kU + 6) / 4;
-    uint32_t ws[nd + 1];
+    uint32_t ws[nd + 1], xs[nd + 1];
     {
       const uint32_t* const ws_at = reinterpret_cast<const uint32_t*>(
           sWs + (t_in * sgroups + (part0 >> 4)) * 256 + lane * 4);
+      const uint32_t* const xs_at =
+          reinterpret_cast<const uint32_t*>(sAs + (part0 >> 4) * 256 + lane * 4);
 #pragma unroll
-      for (int i = 0; i < nd; ++i) ws[i] = ws_at[i * 64];
-      ws[nd] = 0;
-      const int o = (part0 >> 2) & 3;   // s0 % 4
+      for (int i = 0; i < nd; ++i) {
+        ws[i] = ws_at[i * 64];
+        xs[i] = kPackedA ? xs_at[i * 64] : 0u;
+      }
+      ws[nd] = xs[nd] = 0;
 #pragma unroll
-      for (int i = 0; i < nd; ++i) ws[i] = __builtin_amdgcn_alignbyte(ws[i + 1], ws[i], o);
+      for (int i = 0; i < nd; ++i) {
+        ws[i] = __builtin_amdgcn_alignbyte(ws[i + 1], ws[i], o);
+        xs[i] = __builtin_amdgcn_alignbyte(xs[i + 1], xs[i], o);
+      }
     }
     const bool row_ok = lr < rows && tile_ok;
     v4f acc = {0.f, 0.f, 0.f, 0.f};
@@ -187,8 +213,14 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_decode_kernel(
       uint32_t sa[kBatch];
 #pragma unroll
       for (int j = 0; j < kBatch; ++j) {
-        a[j] = *reinterpret_cast<const uint4*>(a_at + (j0 + j) * 64);
-        sa[j] = sa_at[(j0 + j) * 4];
+        const int jj = j0 + j;
+        if constexpr (kPackedA) {
+          a[j] = *reinterpret_cast<const uint4*>(a_at + jj * 1024);
+          sa[j] = (xs[jj >> 2] >> (8 * (jj & 3))) & 0xFFu;
+        } else {
+          a[j] = *reinterpret_cast<const uint4*>(a_at + jj * 64);
+          sa[j] = sa_at[jj * 4];
+        }
       }
 #pragma unroll
       for (int j = 0; j < kBatch; ++j) {
@@ -223,30 +255,36 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_decode_kernel(
   }
 }
 
-template <bool kGrouped, int kT, int kU>
+template <bool kGrouped, bool kPackedA, int kT, int kU>
 hipError_t launch_cfg(dim3 grid, size_t lds, const uint8_t* Aq, const uint8_t* Asc, int M,
                       const int32_t* off, const uint8_t* Wp, const uint8_t* Wps, int N,
                       int K_aug, float* Y, hipStream_t stream) {
   static std::once_flag attr_once;   // dynamic LDS above the 64 KiB default
   std::call_once(attr_once, [] {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_decode_kernel<kGrouped, kT, kU>),
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_decode_kernel<kGrouped, kPackedA, kT, kU>),
                               hipFuncAttributeMaxDynamicSharedMemorySize,
                               static_cast<int>(kMaxDecodeLds));
     (void)hipGetLastError();
   });
-  gemm_decode_kernel<kGrouped, kT, kU><<<grid, kWaves * 64, lds, stream>>>(Aq, Asc, M, off, Wp, Wps,
-                                                                         N, K_aug, Y);
+  gemm_decode_kernel<kGrouped, kPackedA, kT, kU><<<grid, kWaves * 64, lds, stream>>>(
+      Aq, Asc, M, off, Wp, Wps, N, K_aug, Y);
   return hipGetLastError();
 }
 
-template <bool kGrouped, int kT>
+template <bool kGrouped, bool kPackedA, int kT>
 hipError_t launch_u(int U, dim3 grid, size_t lds, const uint8_t* Aq, const uint8_t* Asc, int M,
                     const int32_t* off, const uint8_t* Wp, const uint8_t* Wps, int N, int K_aug,
                     float* Y, hipStream_t stream) {
   switch (U) {
-    case 2: return launch_cfg<kGrouped, kT, 2>(grid, lds, Aq, Asc, M, off, Wp, Wps, N, K_aug, Y, stream);
-    case 5: return launch_cfg<kGrouped, kT, 5>(grid, lds, Aq, Asc, M, off, Wp, Wps, N, K_aug, Y, stream);
-    default: return launch_cfg<kGrouped, kT, 10>(grid, lds, Aq, Asc, M, off, Wp, Wps, N, K_aug, Y, stream);
+    case 2:
+      return launch_cfg<kGrouped, kPackedA, kT, 2>(grid, lds, Aq, Asc, M, off, Wp, Wps, N, K_aug, Y,
+                                                   stream);
+    case 5:
+      return launch_cfg<kGrouped, kPackedA, kT, 5>(grid, lds, Aq, Asc, M, off, Wp, Wps, N, K_aug, Y,
+                                                   stream);
+    default:
+      return launch_cfg<kGrouped, kPackedA, kT, 10>(grid, lds, Aq, Asc, M, off, Wp, Wps, N, K_aug, Y,
+                                                    stream);
   }
 }
 
@@ -267,10 +305,13 @@ size_t decode_lds_bytes(int K_aug, int tiles) {
   // the scale run of 16 rows: 16 nb bytes after a shift of up to 15, copied
   // in whole kilobytes of 16-byte pieces
   const size_t scale_bytes = static_cast<size_t>((((16 * nb + 15 + 15) >> 4) + 63) >> 6) * 1024;
-  // + 2 KiB for the operand reads of steps past a wave's chunk beyond the
-  // last row: at most (kWaves + 10) steps of 64 bytes past K_aug
+  // + 10 KiB for the operand reads of steps past a wave's chunk (a wave reads
+  // 10 steps from its first, or from step 0): in the row-major layout at most
+  // 10 steps of 64 bytes past the last row, in the packed one 10 kilobyte
+  // steps past the last step (the packed block of steps x 1 KB and its
+  // sgroups x 256 scale bytes fit the row-major layout's room)
   return static_cast<size_t>(tiles) * ((steps + 3) / 4) * 256 +
-         std::max(staged_rows_bytes(nb) + scale_bytes + 2048, static_cast<size_t>(kWaves) * 64 * 4 * 4);
+         std::max(staged_rows_bytes(nb) + scale_bytes + 10240, static_cast<size_t>(kWaves) * 64 * 4 * 4);
 }
 
 DecodeConfig choose_decode_config(int M_per_group, int N, int K_aug, int grouped, int tiles,
@@ -302,22 +343,30 @@ DecodeConfig choose_decode_config(int M_per_group, int N, int K_aug, int grouped
 hipError_t launch_gemm_decode(const uint8_t* Aq, const uint8_t* Asc, int M,
                               const int32_t* group_offsets, int E, const uint8_t* Wp,
                               const uint8_t* Wps, int N, int K_aug, float* Y,
-                              const DecodeConfig& cfg, hipStream_t stream) {
+                              const DecodeConfig& cfg, hipStream_t stream, bool packed_a) {
+  if (packed_a && group_offsets) return hipErrorInvalidValue;   // dense only
   const int ntiles = N >> 4;
   const bool grouped = group_offsets != nullptr;
   const dim3 grid((ntiles + cfg.tiles - 1) / cfg.tiles, grouped ? 1 : cfg.row_splits,
                   grouped ? E : 1);
   const size_t lds = decode_lds_bytes(K_aug, cfg.tiles);
-#define PRQ_DECODE_T(G, T)                                                                   \
-  return launch_u<G, T>(cfg.unroll, grid, lds, Aq, Asc, M, group_offsets, Wp, Wps, N, K_aug, Y, \
-                        stream)
+#define PRQ_DECODE_T(G, P, T)                                                                   \
+  return launch_u<G, P, T>(cfg.unroll, grid, lds, Aq, Asc, M, group_offsets, Wp, Wps, N, K_aug, Y, \
+                           stream)
   if (grouped) {
-    PRQ_DECODE_T(true, 1);
+    PRQ_DECODE_T(true, false, 1);
+  }
+  if (packed_a) {
+    switch (cfg.tiles) {
+      case 1: PRQ_DECODE_T(false, true, 1);
+      case 2: PRQ_DECODE_T(false, true, 2);
+      default: PRQ_DECODE_T(false, true, 4);
+    }
   }
   switch (cfg.tiles) {
-    case 1: PRQ_DECODE_T(false, 1);
-    case 2: PRQ_DECODE_T(false, 2);
-    default: PRQ_DECODE_T(false, 4);
+    case 1: PRQ_DECODE_T(false, false, 1);
+    case 2: PRQ_DECODE_T(false, false, 2);
+    default: PRQ_DECODE_T(false, false, 4);
   }
 #undef PRQ_DECODE_T
 }

@@ -282,7 +282,8 @@ int prq_tune_act_quant(const void* X, int64_t ld_x, int M, int K, int k_tail, co
              : -3;
 }
 
-// The same into the packed activation layout (0 automatic, 2 register-staged, 3 LDS stages
+// The same into the packed activation layout (0 automatic, 1 one row per workgroup row,
+// 2 register-staged, 3 LDS stages
 // with the output through an LDS window where it fits, 4 LDS stages with the
 // output stored directly), its workgroups sized for num_cus CUs.
 int prq_tune_act_quant_packed(const void* X, int64_t ld_x, int M, int K, int k_tail,
@@ -290,7 +291,7 @@ int prq_tune_act_quant_packed(const void* X, int64_t ld_x, int M, int K, int k_t
                               uint8_t* Ap, uint8_t* Aps, int kernel, int num_cus,
                               hipStream_t stream) {
   if (M <= 0 || K <= 0 || K % 32 || k_tail % 32 || k_tail > K || K > 16384 || ld_x < K ||
-      (kernel != 0 && (kernel < 2 || kernel > 4)) || num_cus <= 0)
+      kernel < 0 || kernel > 4 || num_cus <= 0)
     return -1;
   return prq::launch_act_quant_packed_kernel(static_cast<const uint16_t*>(X), ld_x, M, K, k_tail,
                                              inv, perm, off, G, Ap, Aps, num_cus, kernel,

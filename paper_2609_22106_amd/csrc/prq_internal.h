@@ -155,9 +155,10 @@ hipError_t launch_gemm_streamk(const uint8_t* Aq, const uint8_t* Asc, int M, con
 size_t decode_lds_bytes(int K_aug, int tiles);
 DecodeConfig choose_decode_config(int M_per_group, int N, int K_aug, int grouped, int tiles,
                                   int row_splits, int num_cus);
+// packed_a: Aq / Asc in the packed activation layout (dense calls only).
 hipError_t launch_gemm_decode(const uint8_t* Aq, const uint8_t* Asc, int M,
                               const int32_t* group_offsets, int E, const uint8_t* Wp,
                               const uint8_t* Wps, int N, int K_aug, float* Y,
-                              const DecodeConfig& cfg, hipStream_t stream);
+                              const DecodeConfig& cfg, hipStream_t stream, bool packed_a = false);
 
 }  // namespace prq

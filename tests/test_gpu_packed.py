@@ -229,6 +229,76 @@ def test_packed_pair_down_proj(M):
     assert_gemm_close(Y0[rows], Yo, f"packed pair M={M} without workspace")
 
 
+@pytest.mark.parametrize("M", [1, 8, 17, 32, 64])
+def test_packed_pair_decode_rows(M):
+    """Decode rows through the packed pair on the down_proj shape: the
+    quantizer's few-rows kernel writes the packed layout (codes, scales and the
+    padding of the last 16-row block, byte for byte the oracle's), and the
+    whole-K decode kernel reads it: every element written (Y starts as NaN),
+    within the GEMM bar of the oracle, and bit for bit the row-major pair's Y
+    (the same operands reach the same MFMAs in the same order)."""
+    prq = _prq()
+    rng = np.random.default_rng(M + 1000)
+    K, k, N = 9728, 256, 2560
+    X = inputs.f32_to_bf16_bits((rng.standard_normal((M, K)) *
+                                 rng.uniform(0.01, 30.0, K)).astype(np.float32))
+    inv = rng.uniform(0.25, 4.0, K).astype(np.float32)
+    perm = rng.permutation(K).astype(np.int32)
+    Wq, Wsc = inputs.random_mxfp4(rng, N, K + k)
+    W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
+    say("packed decode pair case:", M)
+    assert prq.prq_gemm_packed_workspace_bytes(M, N, K + k) == 0
+    cb, sb = prq.prq_packed_act_bytes(M, K + k)
+    A = prq.PackedAct(torch.full((cb,), 0xAB, dtype=torch.uint8, device="cuda"),
+                      torch.full((sb,), 0xCD, dtype=torch.uint8, device="cuda"), M, K + k)
+    prq.prq_quant_act_packed(dev(X), K, k, dev(_pos(inv, perm)), dev(perm), out=A)
+    Yp = nan_output(M, N)
+    prq.prq_gemm_packed(A, W, Y=Yp)
+    Aq, Asc = prq.prq_quant_act(dev(X), K, k, dev(_pos(inv, perm)), dev(perm))
+    Yr = nan_output(M, N)
+    prq.prq_gemm(Aq, Asc, W, Y=Yr)
+    torch.cuda.synchronize()
+    rq, rs = pq.quant_act(X, inv, perm, k)
+    ep, es = pack_rows(rq, rs)
+    np.testing.assert_array_equal(host(A.Aps), es, err_msg="packed scales")
+    np.testing.assert_array_equal(host(A.Ap), ep, err_msg="packed codes")
+    yp = host(Yp)
+    assert np.all(np.isfinite(yp)), "an output element was not written"
+    np.testing.assert_array_equal(yp.view(np.uint32), host(Yr).view(np.uint32))
+    assert_gemm_close(yp, pq.gemm(rq, rs, Wq, Wsc), f"packed decode pair M={M}")
+
+
+@pytest.mark.parametrize("M,K,k,counts", [(1, 1024, 64, None), (40, 2080, 32, None),
+                                          (100, 768, 64, None), (50, 1088, 0, [3, 0, 30, 17])])
+def test_quant_act_packed_few_rows_kernel(M, K, k, counts):
+    """The few-rows kernel forced (tuning entry, kernel 1) into the packed
+    layout: one row per workgroup row and padding rows up to the end of the last
+    16-row block, ragged K + k (2112 = 16.5 steps), more rows than AUTO gives
+    it, and groups of sorted rows that share 16-row blocks."""
+    rng = np.random.default_rng(M * 3 + K)
+    X = inputs.f32_to_bf16_bits((rng.standard_normal((M, K)) *
+                                 rng.uniform(0.01, 30.0, K)).astype(np.float32))
+    if counts is None:
+        inv = rng.uniform(0.25, 4.0, K).astype(np.float32)
+        perm = rng.permutation(K).astype(np.int32)
+        say("packed few-rows quant case:", M, K, k)
+        ap, aps = _tune_quant_packed(X, K, k, _pos(inv, perm), perm, None, 1, 1, 256)
+        rq, rs = pq.quant_act(X, inv, perm, k)
+    else:
+        G = len(counts)
+        off = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+        assert off[-1] == M
+        inv = rng.uniform(0.25, 4.0, (G, K)).astype(np.float32)
+        perm = np.stack([rng.permutation(K) for _ in range(G)]).astype(np.int32)
+        inv_pos = np.stack([inv[g][perm[g]] for g in range(G)])
+        say("packed few-rows quant case: grouped", counts)
+        ap, aps = _tune_quant_packed(X, K, k, inv_pos, perm, off, G, 1, 256)
+        rq, rs = pq.quant_act_grouped(X, inv, perm, off, k)
+    ep, es = pack_rows(rq, rs)
+    np.testing.assert_array_equal(aps, es, err_msg="packed scales")
+    np.testing.assert_array_equal(ap, ep, err_msg="packed codes")
+
+
 @pytest.mark.parametrize("entry", ["packed", "rowmajor"])
 def test_full_prefill_gemm_every_element(entry):
     """The largest down_proj prefill GEMM (8192 x 2560 over K + k = 9984) with
