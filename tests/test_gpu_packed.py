@@ -143,7 +143,11 @@ def _tune_packed(shape, A, W, Y):
 
 
 GEMM = [(300, 384, 1024), (513, 272, 1152), (40, 512, 9984), (257, 272, 1088), (130, 144, 4192),
-        (17, 48, 96), (64, 256, 256), (1, 16, 32)]
+        (17, 48, 96), (64, 256, 256), (1, 16, 32),
+        # decode rows (AUTO: the whole-K decode kernel on the packed operand): two
+        # tiles per workgroup over an odd tile count, one tile for two-tile
+        # workgroups, three row groups, ragged K + k
+        (49, 80, 1088), (64, 16, 2624), (33, 272, 4192)]
 
 
 @pytest.mark.parametrize("M,N,K_aug", GEMM)
