@@ -69,8 +69,8 @@ enum {
   PRQ_GEMM_TILE = 1,   /* LDS-tiled block-scaled MFMA kernel (prefill shapes) */
   PRQ_GEMM_STREAM = 2, /* weight-streaming decode kernels: whole-K workgroups
                           (splits 0 or 1), split-K for a forced split count > 1 */
-  PRQ_GEMM_STREAM_K = 3 /* stream-K decode kernel (up to 64 rows; AUTO's choice up
-                          to 8): equal contiguous ranges of the weight's
+  PRQ_GEMM_STREAM_K = 3 /* stream-K decode kernel (up to 64 rows; never AUTO's
+                          choice): equal contiguous ranges of the weight's
                           (16-feature tile, 128-element K step) units, one
                           workgroup per tile where the tiles fill at least half
                           of the CUs, else one per CU; a tile shared by several
