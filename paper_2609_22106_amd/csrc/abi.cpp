@@ -352,7 +352,7 @@ int prq_gemm_packed(const uint8_t* Ap, const uint8_t* Aps, int32_t M, const uint
   // decode rows: the whole-K decode kernel on the packed operand (each row
   // group's operand one contiguous kilobyte per K step)
   if (prq::choose_variant(M, N, K_aug) == PRQ_GEMM_STREAM) {
-    const prq::DecodeConfig d = prq::choose_decode_config(M, N, K_aug, 0, 0, 0, dev.num_cus);
+    const prq::DecodeConfig d = prq::choose_decode_config(M, N, K_aug, 0, 0, 0, dev.num_cus, true);
     if (d.ok)
       return launch_status(prq::launch_gemm_decode(Ap, Aps, M, nullptr, 1, Wp, Wps, N, K_aug, Y, d,
                                                    stream, true));

@@ -31,6 +31,13 @@
 // Grouped (MoE) mode: blockIdx.z is the expert; a workgroup loops over the
 // expert's 16-row groups reusing its weight registers; experts without rows
 // return before reading their weight.
+//
+// Direct variant (packed activation, two or four row groups): one tile per
+// workgroup and all row groups in it, every operand loaded straight into
+// registers.  With one tile per workgroup each activation kilobyte is used by
+// exactly one wave, so staging it in LDS only adds a barrier per group; here
+// each wave loads its chunk of the next group's block while its MFMAs run on
+// the current one, and the waves meet once, for the K-chunk sum of all groups.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -255,6 +262,130 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_decode_kernel(
   }
 }
 
+// Lane (l % 16, l / 16) of step s0 + j: the packed block's kilobyte of step
+// s0 + j (clamped to the last step; steps past the chunk are masked at the
+// MFMA) and the nd scale dwords of steps 4 (s0 / 4) .. (clamped likewise).
+template <int kU>
+__device__ __forceinline__ void load_block(const uint8_t* __restrict__ Ap,
+                                           const uint8_t* __restrict__ Aps, int64_t blk, int steps,
+                                           int sgroups, int sbase, int lane, uint4 (&a)[kU],
+                                           uint32_t (&xs)[(kU + 6) / 4 + 1]) {
+  constexpr int nd = (kU + 6) / 4;
+  const uint8_t* const ab = Ap + blk * steps * 1024 + lane * 16;
+#pragma unroll
+  for (int j = 0; j < kU; ++j)
+    a[j] = *reinterpret_cast<const uint4*>(ab + static_cast<int64_t>(min(sbase + j, steps - 1)) * 1024);
+  const uint32_t* const xg = reinterpret_cast<const uint32_t*>(Aps + blk * sgroups * 256) + lane;
+#pragma unroll
+  for (int i = 0; i < nd; ++i) xs[i] = xg[min((sbase >> 2) + i, sgroups - 1) * 64];
+}
+
+// The kU MFMAs of one row group (xs realigned in place, as the weight's ws).
+template <int kU>
+__device__ __forceinline__ v4f block_mfmas(const uint4 (&w)[kU], const uint32_t (&ws)[(kU + 6) / 4 + 1],
+                                           const uint4 (&a)[kU], uint32_t (&xs)[(kU + 6) / 4 + 1],
+                                           int o, int s0, int s1, int part0, int nb) {
+  constexpr int nd = (kU + 6) / 4;
+  xs[nd] = 0;
+#pragma unroll
+  for (int i = 0; i < nd; ++i) xs[i] = __builtin_amdgcn_alignbyte(xs[i + 1], xs[i], o);
+  v4f acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int jj = 0; jj < kU; ++jj) {
+    const bool step_ok = s0 + jj < s1;   // wave-uniform
+    const uint32_t sw = (ws[jj >> 2] >> (8 * (jj & 3))) & 0xFFu;
+    const uint32_t sa = (xs[jj >> 2] >> (8 * (jj & 3))) & 0xFFu;
+    acc = dev::mfma_fp4_16x16x128(w[jj], step_ok ? a[jj] : make_uint4(0, 0, 0, 0),
+                                  step_ok ? sw : kNeutralScale,
+                                  step_ok && part0 + 4 * jj < nb ? sa : kNeutralScale, acc);
+  }
+  return acc;
+}
+
+// Dense, packed activation, one 16-feature tile per workgroup (blockIdx.x)
+// and kP row groups (blockIdx.y + p gridDim.y), 16 waves of contiguous K
+// chunks.  Rows past M sit in the packed block as zero codes and only reach
+// output rows that are not stored.  The bits equal the staged kernel's with
+// one tile per workgroup (same chunks, MFMA order and K-chunk sum).
+template <int kU, int kP>
+__global__ __launch_bounds__(kWaves * 64) void gemm_decode_direct_kernel(
+    const uint8_t* __restrict__ Ap, const uint8_t* __restrict__ Aps, int M,
+    const uint8_t* __restrict__ Wp, const uint8_t* __restrict__ Wps, int N, int K_aug,
+    float* __restrict__ Y) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  constexpr int nd = (kU + 6) / 4;
+  const int steps = (K_aug + kStepK - 1) / kStepK;
+  const int sgroups = (steps + 3) >> 2;
+  const int nb = K_aug >> 5;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lk = lane >> 4;
+  const int tile = blockIdx.x;
+  const int per = (steps + kWaves - 1) / kWaves;   // <= kU (checked on the host)
+  const int s0 = wave * per, s1 = min(steps, s0 + per);
+  const int sbase = s0 < steps ? s0 : 0;          // a wave without steps reads step 0, masked
+  const int o = sbase & 3;
+  const int part0 = sbase * 4 + lk;
+
+  // The weight chunk and its scale dwords (realigned after the first loads
+  // of the activation are issued, so that no wait comes before them).
+  const uint8_t* const wt = Wp + static_cast<int64_t>(tile) * steps * 1024 + lane * 16;
+  uint4 w[kU];
+#pragma unroll
+  for (int j = 0; j < kU; ++j)
+    w[j] = *reinterpret_cast<const uint4*>(wt + static_cast<int64_t>(min(sbase + j, steps - 1)) * 1024);
+  uint32_t ws[nd + 1];
+  {
+    const uint32_t* const wg = reinterpret_cast<const uint32_t*>(Wps + static_cast<int64_t>(tile) * sgroups * 256) + lane;
+#pragma unroll
+    for (int i = 0; i < nd; ++i) ws[i] = wg[min((sbase >> 2) + i, sgroups - 1) * 64];
+    ws[nd] = 0;
+  }
+
+  // Row group p's operands are loaded while group p - 1's MFMAs run (two
+  // register sets); the scheduling barriers keep the compiler from sinking
+  // the loads next to their MFMAs.  Groups past this workgroup's count
+  // (only where the launch's rows do not divide evenly) reload the last block
+  // and are not stored.
+  const int nblk = (M + 15) >> 4;
+  const int gy = static_cast<int>(gridDim.y), by = static_cast<int>(blockIdx.y);
+  const int ngroups = (nblk - by + gy - 1) / gy;   // <= kP
+  uint4 a[2][kU];
+  uint32_t xs[2][nd + 1];
+  load_block<kU>(Ap, Aps, by, steps, sgroups, sbase, lane, a[0], xs[0]);
+  __builtin_amdgcn_sched_barrier(0);
+  v4f acc[kP];
+#pragma unroll
+  for (int p = 0; p < kP; ++p) {
+    if (p + 1 < kP)
+      load_block<kU>(Ap, Aps, min(by + (p + 1) * gy, nblk - 1), steps, sgroups, sbase, lane,
+                     a[(p + 1) & 1], xs[(p + 1) & 1]);
+    __builtin_amdgcn_sched_barrier(0);
+    if (p == 0) {
+#pragma unroll
+      for (int i = 0; i < nd; ++i) ws[i] = __builtin_amdgcn_alignbyte(ws[i + 1], ws[i], o);
+    }
+    acc[p] = block_mfmas<kU>(w, ws, a[p & 1], xs[p & 1], o, s0, s1, part0, nb);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  // The K chunks of every group summed in a fixed order.  acc[p][q] of this
+  // lane is Y[16 (by + p gy) + l % 16][16 tile + 4 (l / 16) + q].
+  float* const s_red = reinterpret_cast<float*>(smem);   // [kP][16 waves][64][4]
+#pragma unroll
+  for (int p = 0; p < kP; ++p)
+    *reinterpret_cast<v4f*>(s_red + ((p * kWaves + wave) * 64 + lane) * 4) = acc[p];
+  __syncthreads();
+  for (int idx = tid; idx < ngroups * 256; idx += kWaves * 64) {
+    const int p = idx >> 8, l = (idx >> 2) & 63, q = idx & 3;
+    const int row = (by + p * gy) * 16 + (l & 15);
+    if (row < M) {
+      float v = 0.0f;
+#pragma unroll
+      for (int c = 0; c < kWaves; ++c) v += s_red[((p * kWaves + c) * 64 + l) * 4 + q];
+      Y[static_cast<int64_t>(row) * N + tile * 16 + 4 * (l >> 4) + q] = v;
+    }
+  }
+}
+
 template <bool kGrouped, bool kPackedA, int kT, int kU>
 hipError_t launch_cfg(dim3 grid, size_t lds, const uint8_t* Aq, const uint8_t* Asc, int M,
                       const int32_t* off, const uint8_t* Wp, const uint8_t* Wps, int N,
@@ -315,7 +446,7 @@ size_t decode_lds_bytes(int K_aug, int tiles) {
 }
 
 DecodeConfig choose_decode_config(int M_per_group, int N, int K_aug, int grouped, int tiles,
-                                  int row_splits, int num_cus) {
+                                  int row_splits, int num_cus, bool packed) {
   DecodeConfig c;
   const int steps = (K_aug + kStepK - 1) / kStepK;
   const int groups = (std::max(M_per_group, 1) + 15) / 16;
@@ -337,7 +468,25 @@ DecodeConfig choose_decode_config(int M_per_group, int N, int K_aug, int grouped
   c.unroll = round_decode_unroll((steps + kWaves / c.tiles - 1) / (kWaves / c.tiles));
   c.ok = c.ok && c.unroll > 0 && decode_lds_bytes(K_aug, c.tiles) <= kMaxDecodeLds &&
          (N % 16) == 0 && (!grouped || c.tiles == 1);
+  // Packed activation, two or four row groups: the direct variant, one tile
+  // and every row group per workgroup (down_proj, weights rotated, back to
+  // back: 17-32 rows 6.8 against 7.4 us, 49-64 rows 8.8 against 9.8).  Three
+  // groups stay staged: two tiles and one group per workgroup in a single
+  // round of the CUs, 7.7 against 7.85 direct.
+  const int per16 = (steps + kWaves - 1) / kWaves;
+  if (packed && !grouped && tiles <= 0 && row_splits <= 0 && (groups == 2 || groups == 4) &&
+      per16 <= 5 && (N % 16) == 0) {
+    c.direct = true;
+    c.tiles = 1;
+    c.row_splits = 1;
+    c.unroll = per16 <= 2 ? 2 : 5;
+    c.ok = true;
+  }
   return c;
+}
+
+size_t decode_direct_lds_bytes(int M) {
+  return static_cast<size_t>((std::max(M, 1) + 15) / 16) * kWaves * 64 * 4 * sizeof(float);
 }
 
 hipError_t launch_gemm_decode(const uint8_t* Aq, const uint8_t* Asc, int M,
@@ -346,6 +495,33 @@ hipError_t launch_gemm_decode(const uint8_t* Aq, const uint8_t* Asc, int M,
                               const DecodeConfig& cfg, hipStream_t stream, bool packed_a) {
   if (packed_a && group_offsets) return hipErrorInvalidValue;   // dense only
   const int ntiles = N >> 4;
+  if (cfg.direct) {
+    const int groups = (M + 15) / 16;
+    if (!packed_a || cfg.row_splits != 1 || groups < 1 || groups > 4 || (N % 16) != 0)
+      return hipErrorInvalidValue;
+    const dim3 grid(ntiles, 1, 1);
+    const size_t lds = decode_direct_lds_bytes(M);   // <= 64 KiB, the default limit
+#define PRQ_DECODE_D(U, P)                                                                   \
+  gemm_decode_direct_kernel<U, P><<<grid, kWaves * 64, lds, stream>>>(Aq, Asc, M, Wp, Wps, N, \
+                                                                      K_aug, Y);             \
+  return hipGetLastError()
+    if (cfg.unroll == 2) {
+      switch (groups) {
+        case 1: PRQ_DECODE_D(2, 1);
+        case 2: PRQ_DECODE_D(2, 2);
+        case 3: PRQ_DECODE_D(2, 3);
+        default: PRQ_DECODE_D(2, 4);
+      }
+    }
+    if (cfg.unroll != 5) return hipErrorInvalidValue;
+    switch (groups) {
+      case 1: PRQ_DECODE_D(5, 1);
+      case 2: PRQ_DECODE_D(5, 2);
+      case 3: PRQ_DECODE_D(5, 3);
+      default: PRQ_DECODE_D(5, 4);
+    }
+#undef PRQ_DECODE_D
+  }
   const bool grouped = group_offsets != nullptr;
   const dim3 grid((ntiles + cfg.tiles - 1) / cfg.tiles, grouped ? 1 : cfg.row_splits,
                   grouped ? E : 1);
