@@ -32,12 +32,12 @@
 // expert's 16-row groups reusing its weight registers; experts without rows
 // return before reading their weight.
 //
-// Direct variant (packed activation, two or four row groups): one tile per
-// workgroup and all row groups in it, every operand loaded straight into
-// registers.  With one tile per workgroup each activation kilobyte is used by
-// exactly one wave, so staging it in LDS only adds a barrier per group; here
-// each wave loads its chunk of the next group's block while its MFMAs run on
-// the current one, and the waves meet once, for the K-chunk sum of all groups.
+// Direct variant (packed activation, two to four row groups): every operand
+// loaded straight into registers, no LDS staging.  Each wave holds its K chunk
+// of the weight of one or two tiles, so each activation kilobyte it loads
+// feeds one or two MFMAs and no other wave needs it; the wave loads its chunk
+// of the next row group's block while its MFMAs run on the current one, and
+// the waves meet once, for the K-chunk sum of all groups and tiles.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -280,34 +280,15 @@ __device__ __forceinline__ void load_block(const uint8_t* __restrict__ Ap,
   for (int i = 0; i < nd; ++i) xs[i] = xg[min((sbase >> 2) + i, sgroups - 1) * 64];
 }
 
-// The kU MFMAs of one row group (xs realigned in place, as the weight's ws).
-template <int kU>
-__device__ __forceinline__ v4f block_mfmas(const uint4 (&w)[kU], const uint32_t (&ws)[(kU + 6) / 4 + 1],
-                                           const uint4 (&a)[kU], uint32_t (&xs)[(kU + 6) / 4 + 1],
-                                           int o, int s0, int s1, int part0, int nb) {
-  constexpr int nd = (kU + 6) / 4;
-  xs[nd] = 0;
-#pragma unroll
-  for (int i = 0; i < nd; ++i) xs[i] = __builtin_amdgcn_alignbyte(xs[i + 1], xs[i], o);
-  v4f acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int jj = 0; jj < kU; ++jj) {
-    const bool step_ok = s0 + jj < s1;   // wave-uniform
-    const uint32_t sw = (ws[jj >> 2] >> (8 * (jj & 3))) & 0xFFu;
-    const uint32_t sa = (xs[jj >> 2] >> (8 * (jj & 3))) & 0xFFu;
-    acc = dev::mfma_fp4_16x16x128(w[jj], step_ok ? a[jj] : make_uint4(0, 0, 0, 0),
-                                  step_ok ? sw : kNeutralScale,
-                                  step_ok && part0 + 4 * jj < nb ? sa : kNeutralScale, acc);
-  }
-  return acc;
-}
-
-// Dense, packed activation, one 16-feature tile per workgroup (blockIdx.x)
-// and kP row groups (blockIdx.y + p gridDim.y), 16 waves of contiguous K
-// chunks.  Rows past M sit in the packed block as zero codes and only reach
-// output rows that are not stored.  The bits equal the staged kernel's with
-// one tile per workgroup (same chunks, MFMA order and K-chunk sum).
-template <int kU, int kP>
+// Dense, packed activation: kTW 16-feature tiles per workgroup (2 blockIdx.x,
+// + 1) and kP row groups (blockIdx.y + p gridDim.y), 16 waves of contiguous K
+// chunks; each wave holds its chunk of the weight of every tile, so one load
+// of its activation operand feeds kTW MFMAs.  Rows past M sit in the packed
+// block as zero codes and only reach output rows that are not stored; a
+// second tile past N reloads the last one and is not stored.  The bits equal
+// the staged kernel's with one tile per workgroup (same chunks, MFMA order
+// and K-chunk sum).
+template <int kU, int kP, int kTW>
 __global__ __launch_bounds__(kWaves * 64) void gemm_decode_direct_kernel(
     const uint8_t* __restrict__ Ap, const uint8_t* __restrict__ Aps, int M,
     const uint8_t* __restrict__ Wp, const uint8_t* __restrict__ Wps, int N, int K_aug,
@@ -317,27 +298,30 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_decode_direct_kernel(
   const int steps = (K_aug + kStepK - 1) / kStepK;
   const int sgroups = (steps + 3) >> 2;
   const int nb = K_aug >> 5;
+  const int ntiles = N >> 4;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lk = lane >> 4;
-  const int tile = blockIdx.x;
+  const int tile0 = static_cast<int>(blockIdx.x) * kTW;
   const int per = (steps + kWaves - 1) / kWaves;   // <= kU (checked on the host)
   const int s0 = wave * per, s1 = min(steps, s0 + per);
   const int sbase = s0 < steps ? s0 : 0;          // a wave without steps reads step 0, masked
   const int o = sbase & 3;
   const int part0 = sbase * 4 + lk;
 
-  // The weight chunk and its scale dwords (realigned after the first loads
-  // of the activation are issued, so that no wait comes before them).
-  const uint8_t* const wt = Wp + static_cast<int64_t>(tile) * steps * 1024 + lane * 16;
-  uint4 w[kU];
+  // The weight chunks and their scale dwords (realigned after the first
+  // loads of the activation are issued, so that no wait comes before them).
+  uint4 w[kTW][kU];
+  uint32_t ws[kTW][nd + 1];
 #pragma unroll
-  for (int j = 0; j < kU; ++j)
-    w[j] = *reinterpret_cast<const uint4*>(wt + static_cast<int64_t>(min(sbase + j, steps - 1)) * 1024);
-  uint32_t ws[nd + 1];
-  {
-    const uint32_t* const wg = reinterpret_cast<const uint32_t*>(Wps + static_cast<int64_t>(tile) * sgroups * 256) + lane;
+  for (int tt = 0; tt < kTW; ++tt) {
+    const int t = min(tile0 + tt, ntiles - 1);
+    const uint8_t* const wt = Wp + static_cast<int64_t>(t) * steps * 1024 + lane * 16;
 #pragma unroll
-    for (int i = 0; i < nd; ++i) ws[i] = wg[min((sbase >> 2) + i, sgroups - 1) * 64];
-    ws[nd] = 0;
+    for (int j = 0; j < kU; ++j)
+      w[tt][j] = *reinterpret_cast<const uint4*>(wt + static_cast<int64_t>(min(sbase + j, steps - 1)) * 1024);
+    const uint32_t* const wg = reinterpret_cast<const uint32_t*>(Wps + static_cast<int64_t>(t) * sgroups * 256) + lane;
+#pragma unroll
+    for (int i = 0; i < nd; ++i) ws[tt][i] = wg[min((sbase >> 2) + i, sgroups - 1) * 64];
+    ws[tt][nd] = 0;
   }
 
   // Row group p's operands are loaded while group p - 1's MFMAs run (two
@@ -352,7 +336,7 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_decode_direct_kernel(
   uint32_t xs[2][nd + 1];
   load_block<kU>(Ap, Aps, by, steps, sgroups, sbase, lane, a[0], xs[0]);
   __builtin_amdgcn_sched_barrier(0);
-  v4f acc[kP];
+  v4f acc[kP][kTW];
 #pragma unroll
   for (int p = 0; p < kP; ++p) {
     if (p + 1 < kP)
@@ -361,27 +345,49 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_decode_direct_kernel(
     __builtin_amdgcn_sched_barrier(0);
     if (p == 0) {
 #pragma unroll
-      for (int i = 0; i < nd; ++i) ws[i] = __builtin_amdgcn_alignbyte(ws[i + 1], ws[i], o);
+      for (int tt = 0; tt < kTW; ++tt)
+#pragma unroll
+        for (int i = 0; i < nd; ++i) ws[tt][i] = __builtin_amdgcn_alignbyte(ws[tt][i + 1], ws[tt][i], o);
     }
-    acc[p] = block_mfmas<kU>(w, ws, a[p & 1], xs[p & 1], o, s0, s1, part0, nb);
+    uint32_t* const x = xs[p & 1];
+    x[nd] = 0;
+#pragma unroll
+    for (int i = 0; i < nd; ++i) x[i] = __builtin_amdgcn_alignbyte(x[i + 1], x[i], o);
+#pragma unroll
+    for (int tt = 0; tt < kTW; ++tt) {
+      v4f c = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int jj = 0; jj < kU; ++jj) {
+        const bool step_ok = s0 + jj < s1;   // wave-uniform
+        const uint32_t sw = (ws[tt][jj >> 2] >> (8 * (jj & 3))) & 0xFFu;
+        const uint32_t sa = (x[jj >> 2] >> (8 * (jj & 3))) & 0xFFu;
+        c = dev::mfma_fp4_16x16x128(w[tt][jj], step_ok ? a[p & 1][jj] : make_uint4(0, 0, 0, 0),
+                                    step_ok ? sw : kNeutralScale,
+                                    step_ok && part0 + 4 * jj < nb ? sa : kNeutralScale, c);
+      }
+      acc[p][tt] = c;
+    }
     __builtin_amdgcn_sched_barrier(0);
   }
 
-  // The K chunks of every group summed in a fixed order.  acc[p][q] of this
-  // lane is Y[16 (by + p gy) + l % 16][16 tile + 4 (l / 16) + q].
-  float* const s_red = reinterpret_cast<float*>(smem);   // [kP][16 waves][64][4]
+  // The K chunks of every group and tile summed in a fixed order.
+  // acc[p][tt][q] of this lane is Y[16 (by + p gy) + l % 16][16 (tile0 + tt) + 4 (l / 16) + q].
+  float* const s_red = reinterpret_cast<float*>(smem);   // [kP][kTW][16 waves][64][4]
 #pragma unroll
   for (int p = 0; p < kP; ++p)
-    *reinterpret_cast<v4f*>(s_red + ((p * kWaves + wave) * 64 + lane) * 4) = acc[p];
+#pragma unroll
+    for (int tt = 0; tt < kTW; ++tt)
+      *reinterpret_cast<v4f*>(s_red + (((p * kTW + tt) * kWaves + wave) * 64 + lane) * 4) = acc[p][tt];
   __syncthreads();
-  for (int idx = tid; idx < ngroups * 256; idx += kWaves * 64) {
-    const int p = idx >> 8, l = (idx >> 2) & 63, q = idx & 3;
+  for (int idx = tid; idx < ngroups * kTW * 256; idx += kWaves * 64) {
+    const int pt = idx >> 8, l = (idx >> 2) & 63, q = idx & 3;
+    const int p = pt / kTW, t = tile0 + (pt - p * kTW);
     const int row = (by + p * gy) * 16 + (l & 15);
-    if (row < M) {
+    if (row < M && t < ntiles) {
       float v = 0.0f;
 #pragma unroll
-      for (int c = 0; c < kWaves; ++c) v += s_red[((p * kWaves + c) * 64 + l) * 4 + q];
-      Y[static_cast<int64_t>(row) * N + tile * 16 + 4 * (l >> 4) + q] = v;
+      for (int c = 0; c < kWaves; ++c) v += s_red[((pt * kWaves + c) * 64 + l) * 4 + q];
+      Y[static_cast<int64_t>(row) * N + t * 16 + 4 * (l >> 4) + q] = v;
     }
   }
 }
@@ -468,25 +474,39 @@ DecodeConfig choose_decode_config(int M_per_group, int N, int K_aug, int grouped
   c.unroll = round_decode_unroll((steps + kWaves / c.tiles - 1) / (kWaves / c.tiles));
   c.ok = c.ok && c.unroll > 0 && decode_lds_bytes(K_aug, c.tiles) <= kMaxDecodeLds &&
          (N % 16) == 0 && (!grouped || c.tiles == 1);
-  // Packed activation, two or four row groups: the direct variant, one tile
-  // and every row group per workgroup (down_proj, weights rotated, back to
-  // back: 17-32 rows 6.8 against 7.4 us, 49-64 rows 8.8 against 9.8).  Three
-  // groups stay staged: two tiles and one group per workgroup in a single
-  // round of the CUs, 7.7 against 7.85 direct.
+  // Packed activation from two row groups on: the direct variant.  Measured
+  // on the down_proj (9728 -> 2560, weights rotated, back to back) against
+  // the staged kernel's plan: two groups, one tile per wave and workgroup and
+  // both groups in it, 6.8 against 7.4 us (two tiles per wave 7.0); three,
+  // two tiles per wave and one group per workgroup row (240 workgroups), 6.9
+  // against 7.7 (one tile per wave 7.3-7.8); four, two tiles per wave in three
+  // workgroup rows, 7.9 against 9.8 (one tile, one row: 8.8).  Two tiles per
+  // wave take at most two groups per workgroup (registers).
   const int per16 = (steps + kWaves - 1) / kWaves;
-  if (packed && !grouped && tiles <= 0 && row_splits <= 0 && (groups == 2 || groups == 4) &&
+  if (packed && !grouped && tiles <= 0 && row_splits <= 0 && groups >= 2 && groups <= 4 &&
       per16 <= 5 && (N % 16) == 0) {
+    const int cus = std::max(num_cus, 1);
+    int tw = groups >= 3 ? 2 : 1;
+    int cols = (N / 16 + tw - 1) / tw;
+    int rows = std::min(groups, std::max(1, cus / cols));
+    if (tw == 2 && (groups + rows - 1) / rows > 2) {
+      tw = 1;
+      cols = N / 16;
+      rows = std::min(groups, std::max(1, cus / cols));
+    }
     c.direct = true;
-    c.tiles = 1;
-    c.row_splits = 1;
+    c.tiles = tw;
+    c.row_splits = rows;
     c.unroll = per16 <= 2 ? 2 : 5;
     c.ok = true;
   }
   return c;
 }
 
-size_t decode_direct_lds_bytes(int M) {
-  return static_cast<size_t>((std::max(M, 1) + 15) / 16) * kWaves * 64 * 4 * sizeof(float);
+size_t decode_direct_lds_bytes(int M, int tiles, int row_splits) {
+  const int groups = (std::max(M, 1) + 15) / 16;
+  const int kp = (groups + std::max(row_splits, 1) - 1) / std::max(row_splits, 1);
+  return static_cast<size_t>(kp) * tiles * kWaves * 64 * 4 * sizeof(float);
 }
 
 hipError_t launch_gemm_decode(const uint8_t* Aq, const uint8_t* Asc, int M,
@@ -497,29 +517,33 @@ hipError_t launch_gemm_decode(const uint8_t* Aq, const uint8_t* Asc, int M,
   const int ntiles = N >> 4;
   if (cfg.direct) {
     const int groups = (M + 15) / 16;
-    if (!packed_a || cfg.row_splits != 1 || groups < 1 || groups > 4 || (N % 16) != 0)
+    const int kp = cfg.row_splits >= 1 ? (groups + cfg.row_splits - 1) / cfg.row_splits : 0;
+    if (!packed_a || groups < 1 || cfg.row_splits < 1 || cfg.row_splits > groups || kp > 4 ||
+        (cfg.tiles == 2 && kp > 2) || (cfg.tiles != 1 && cfg.tiles != 2) ||
+        (cfg.unroll != 2 && cfg.unroll != 5) || (N % 16) != 0)
       return hipErrorInvalidValue;
-    const dim3 grid(ntiles, 1, 1);
-    const size_t lds = decode_direct_lds_bytes(M);   // <= 64 KiB, the default limit
-#define PRQ_DECODE_D(U, P)                                                                   \
-  gemm_decode_direct_kernel<U, P><<<grid, kWaves * 64, lds, stream>>>(Aq, Asc, M, Wp, Wps, N, \
-                                                                      K_aug, Y);             \
+    const dim3 grid((ntiles + cfg.tiles - 1) / cfg.tiles, cfg.row_splits, 1);
+    const size_t lds = decode_direct_lds_bytes(M, cfg.tiles, cfg.row_splits);   // <= 64 KiB
+#define PRQ_DECODE_D(U, P, T)                                                                   \
+  gemm_decode_direct_kernel<U, P, T><<<grid, kWaves * 64, lds, stream>>>(Aq, Asc, M, Wp, Wps, N, \
+                                                                         K_aug, Y);             \
   return hipGetLastError()
+#define PRQ_DECODE_DU(U)                       \
+  if (cfg.tiles == 2) {                        \
+    if (kp == 1) { PRQ_DECODE_D(U, 1, 2); }    \
+    PRQ_DECODE_D(U, 2, 2);                     \
+  }                                            \
+  switch (kp) {                                \
+    case 1: PRQ_DECODE_D(U, 1, 1);             \
+    case 2: PRQ_DECODE_D(U, 2, 1);             \
+    case 3: PRQ_DECODE_D(U, 3, 1);             \
+    default: PRQ_DECODE_D(U, 4, 1);            \
+  }
     if (cfg.unroll == 2) {
-      switch (groups) {
-        case 1: PRQ_DECODE_D(2, 1);
-        case 2: PRQ_DECODE_D(2, 2);
-        case 3: PRQ_DECODE_D(2, 3);
-        default: PRQ_DECODE_D(2, 4);
-      }
+      PRQ_DECODE_DU(2)
     }
-    if (cfg.unroll != 5) return hipErrorInvalidValue;
-    switch (groups) {
-      case 1: PRQ_DECODE_D(5, 1);
-      case 2: PRQ_DECODE_D(5, 2);
-      case 3: PRQ_DECODE_D(5, 3);
-      default: PRQ_DECODE_D(5, 4);
-    }
+    PRQ_DECODE_DU(5)
+#undef PRQ_DECODE_DU
 #undef PRQ_DECODE_D
   }
   const bool grouped = group_offsets != nullptr;

@@ -32,8 +32,8 @@ struct DecodeConfig {
   int row_splits = 1;  // workgroup rows the 16-row groups are dealt to (dense)
   int unroll = 5;   // K steps per wave (2, 5 or 10), >= ceil(steps / (16 / tiles))
   bool ok = true;   // false: K_aug needs more LDS or steps than the kernel takes
-  bool direct = false;  // packed dense only: the register-direct variant, one
-                        // tile and every row group per workgroup (unroll 2 or 5)
+  bool direct = false;  // packed dense only: the register-direct variant
+                        // (tiles = tiles per wave, 1 or 2; unroll 2 or 5)
 };
 
 // Launch parameters of the stream-K decode GEMM (gemm_streamk.hip): one
@@ -158,7 +158,7 @@ size_t decode_lds_bytes(int K_aug, int tiles);
 // packed: the activation is in the packed layout (may pick the direct variant).
 DecodeConfig choose_decode_config(int M_per_group, int N, int K_aug, int grouped, int tiles,
                                   int row_splits, int num_cus, bool packed = false);
-size_t decode_direct_lds_bytes(int M);
+size_t decode_direct_lds_bytes(int M, int tiles, int row_splits);
 // packed_a: Aq / Asc in the packed activation layout (dense calls only).
 hipError_t launch_gemm_decode(const uint8_t* Aq, const uint8_t* Asc, int M,
                               const int32_t* group_offsets, int E, const uint8_t* Wp,
