@@ -126,7 +126,7 @@ __global__ __launch_bounds__(kWaves * 64) void gemm_stream_kernel(
 #pragma unroll
     for (int j = 0; j < kU; ++j) {
       const int st = min(st0 + j, nst - 1);
-      w[tw][j] = *reinterpret_cast<const uint4*>(Wt + static_cast<int64_t>(st) * 1024);
+      w[tw][j] = dev::load_stream16(Wt + static_cast<int64_t>(st) * 1024);   // read once
     }
   }
 #pragma unroll
