@@ -670,7 +670,8 @@ def traffic_from_counters(workload, fetch_dir, write_dir, command):
         rows = _counter_rows(run_dir, counter)
         calib = [v for n, v in rows if "neg_kernel" in n]
         gemm = [(n, v) for n, v in rows if "prq" in n and any(
-            t in n for t in ("gemm_decode_kernel", "gemm_stream_kernel", "gemm_streamk_kernel",
+            t in n for t in ("gemm_decode_kernel", "gemm_decode_direct_kernel", "gemm_stream_kernel",
+                             "gemm_streamk_kernel",
                              "gemm_tile_kernel", "gemm_grouped_persist_kernel",
                              "reduce_partials_kernel", "zero_kernel", "splitk_reduce_kernel"))]
         launches = [v for n, v in gemm if "gemm_" in n]
