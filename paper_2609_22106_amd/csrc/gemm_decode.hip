@@ -280,12 +280,13 @@ __device__ __forceinline__ void load_block(const uint8_t* __restrict__ Ap,
   for (int i = 0; i < nd; ++i) xs[i] = xg[min((sbase >> 2) + i, sgroups - 1) * 64];
 }
 
-// Dense, packed activation: kTW 16-feature tiles per workgroup (2 blockIdx.x,
-// + 1) and kP row groups (blockIdx.y + p gridDim.y), 16 waves of contiguous K
-// chunks; each wave holds its chunk of the weight of every tile, so one load
-// of its activation operand feeds kTW MFMAs.  Rows past M sit in the packed
-// block as zero codes and only reach output rows that are not stored; a
-// second tile past N reloads the last one and is not stored.  The bits equal
+// Dense, packed activation: kTW 16-feature tiles per workgroup (tiles
+// kTW blockIdx.x onward) and kP row groups (blockIdx.y + p gridDim.y), 16 waves
+// of contiguous K chunks; each wave holds its chunk of the weight of every
+// tile, so one load of its activation operand feeds kTW MFMAs.  Rows past M
+// in the last block (zero codes as the packed quantizer writes them; whatever
+// they hold only reaches their own output rows) are not stored; a second tile
+// past N reloads the last one and is not stored.  The bits equal
 // the staged kernel's with one tile per workgroup (same chunks, MFMA order
 // and K-chunk sum).
 template <int kU, int kP, int kTW>
