@@ -190,7 +190,8 @@ def _staged_decode_one_tile(Aq, Asc, W):
 
 @pytest.mark.parametrize("M,N,K_aug", [(64, 2560, 9984), (17, 2560, 9984), (40, 2560, 9984),
                                        (32, 160, 9984), (49, 80, 1088), (64, 16, 2624),
-                                       (20, 272, 4192), (33, 272, 4192), (30, 48, 2080)])
+                                       (20, 272, 4192), (33, 272, 4192), (30, 48, 2080),
+                                       (48, 80, 2624), (40, 48, 10240)])
 def test_packed_decode_direct_variant(M, N, K_aug):
     """prq_gemm_packed at two to four 16-row blocks runs the decode kernel's
     register-direct variant (operands loaded straight into registers; one tile
@@ -200,7 +201,8 @@ def test_packed_decode_direct_variant(M, N, K_aug):
     sum).  Shapes: the down_proj at 17, 40 and 64 rows, a single tile (its
     second tile past N), an odd tile count with two tiles per wave, waves
     without K steps (1088 = 9 steps), a ragged last step (2080), rows past M
-    in the last block, workgroup rows with unequal group counts."""
+    in the last block, workgroup rows with unequal group counts, three whole
+    blocks, and the longest K it takes (10240: 80 steps, five per wave)."""
     prq = _prq()
     rng = np.random.default_rng(M * 7 + N + K_aug)
     Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
