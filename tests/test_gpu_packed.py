@@ -326,6 +326,39 @@ def test_packed_pair_decode_rows(M):
     assert_gemm_close(host(Yr), pq.gemm(rq, rs, Wq, Wsc), f"row-major decode pair M={M}")
 
 
+def _random_decode_shapes(n, seed=7):
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        M = int(rng.integers(17, 65))
+        N = 16 * int(rng.integers(1, 41))
+        K_aug = 32 * int(rng.integers(4, 321))          # up to 10240: at most 5 steps per wave
+        out.append((M, N, K_aug))
+    return out
+
+
+@pytest.mark.parametrize("M,N,K_aug", _random_decode_shapes(12))
+def test_packed_decode_direct_random_shapes(M, N, K_aug):
+    """Seeded random decode shapes through prq_gemm_packed (17-64 rows: the
+    direct variant): every element written, within the GEMM bar of the oracle,
+    bit for bit the staged one-tile kernel."""
+    prq = _prq()
+    rng = np.random.default_rng(M * 131 + N * 7 + K_aug)
+    Aq, Asc = inputs.random_mxfp4(rng, M, K_aug)
+    Wq, Wsc = inputs.random_mxfp4(rng, N, K_aug)
+    ap, aps = pack_rows(Aq, Asc)
+    A = prq.PackedAct(dev(ap), dev(aps), M, K_aug)
+    W = prq.prq_pack_weight(dev(Wq), dev(Wsc))
+    say("packed decode random case:", M, N, K_aug)
+    Y = nan_output(M, N)
+    prq.prq_gemm_packed(A, W, Y=Y)
+    torch.cuda.synchronize()
+    y = host(Y)
+    assert np.all(np.isfinite(y)), "an output element was not written"
+    np.testing.assert_array_equal(y.view(np.uint32), _staged_decode_one_tile(Aq, Asc, W).view(np.uint32))
+    assert_gemm_close(y, pq.gemm(Aq, Asc, Wq, Wsc), f"packed decode random {M}x{N}x{K_aug}")
+
+
 @pytest.mark.parametrize("M,K,k,counts", [(1, 1024, 64, None), (40, 2080, 32, None),
                                           (100, 768, 64, None), (50, 1088, 0, [3, 0, 30, 17])])
 def test_quant_act_packed_few_rows_kernel(M, K, k, counts):
