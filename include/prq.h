@@ -275,10 +275,10 @@ int prq_gemm_noalloc(const uint8_t* Aq, const uint8_t* Asc, int32_t M,
  *   rows of K in perm / inv_scale_pos).  Rows of different groups may share a
  *   16-row block.  Limits and errors as prq_quant_act.  M == 0 is a no-op.
  * prq_gemm_packed -- prq_gemm on a packed activation (the whole-K decode
- *   kernel up to 64 rows, which needs no workspace: at two or four 16-row
- *   blocks one tile and every block per workgroup, the operands loaded
- *   straight into registers; otherwise each block's operand copied into LDS
- *   in whole kilobytes; the LDS-tiled kernel above):
+ *   kernel up to 64 rows, which needs no workspace: from two to four 16-row
+ *   blocks the operands loaded straight into registers, one or two tiles per
+ *   wave; at one block the block's operand copied into LDS in whole
+ *   kilobytes; the LDS-tiled kernel above):
  *   Y [M, N] float32 = Eq. 3 over K_aug; Ap / Aps from prq_quant_act_packed,
  *   Wp / Wps from prq_pack_weight (E = 1).  workspace: at least
  *   prq_gemm_packed_workspace_bytes(M, N, K_aug) bytes, 16-byte aligned, in
